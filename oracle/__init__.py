@@ -1,0 +1,128 @@
+"""Float64 CPU oracle for the Blurry Window Attention forward operator.
+
+TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the CPU
+baseline leg of ``bench.py`` may import this package; the product package never
+does.  The oracle shares no code with the HIP library.
+
+``bla_oracle.c`` runs the paper's naive recurrent algorithm (Appendix C, Alg. 2:
+the mode-state recurrence of Sec. 3.1 Eq. recurrence, the blurry slots of
+Eq. compressed and the masked slot softmax of Eq. output) token by token in
+double precision.  ``interp`` exposes its interpolation matrices (Eq. translated
+evaluated on the dilated slot grid) so the tests can pin them.
+
+Parity status of each function (what pins it) is listed in the tests
+(``tests/test_oracle_pins.py``); every function here is pinned.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "bla_oracle.c")
+_LIB = os.path.join(_HERE, "libbla_oracle.so")
+_lib = None
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_ip = ctypes.POINTER(ctypes.c_int64)
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc (-O2, OpenMP, strict IEEE double)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+                        "-fno-fast-math", "-ffp-contract=off", _SRC, "-o", tmp, "-lm"],
+                       check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        lib.bla_oracle_interp.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                          _dp, _dp, _ip]
+        lib.bla_oracle_interp.restype = None
+        lib.bla_oracle_forward.argtypes = [ctypes.c_int] * 7 + [
+            _dp, ctypes.c_int64, ctypes.c_double, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp,
+            ctypes.c_int, ctypes.c_int]
+        lib.bla_oracle_forward.restype = ctypes.c_int
+        lib.bla_oracle_step.argtypes = [ctypes.c_int] * 6 + [
+            _dp, _ip, ctypes.c_double, _dp, _dp, _dp, _dp, _dp, _dp, ctypes.c_int]
+        lib.bla_oracle_step.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(_dp)
+
+
+def _f64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float64)
+
+
+def interp(M: int, S: int, T: float):
+    """Interpolation matrices A, B [S, M] and mask thresholds theta [S] for one head."""
+    lib = _load()
+    A = np.zeros((S, M), np.float64)
+    B = np.zeros((S, M), np.float64)
+    th = np.zeros((S,), np.int64)
+    lib.bla_oracle_interp(M, S, float(T), _ptr(A), _ptr(B), th.ctypes.data_as(_ip))
+    return A, B, th
+
+
+def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale=None, state_k=None,
+            state_v=None, literal: bool = False, nthreads: int = 0):
+    """Alg. 2 over q,k [B,H,L,dk], v [B,H,L,dv]; T is a per-head sequence of periods.
+
+    Returns (o [B,H,L,dv], state_k [B,H,2,M,dk], state_v [B,H,2,M,dv]) in float64.
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    Bn, H, L, dk = q.shape
+    dv = v.shape[-1]
+    assert k.shape == q.shape and v.shape[:3] == (Bn, H, L)
+    T = np.ascontiguousarray(np.broadcast_to(np.asarray(T, np.float64), (H,)))
+    if scale is None:
+        scale = 1.0 / np.sqrt(dk)
+    sk_in, sv_in = _f64(state_k), _f64(state_v)
+    o = np.zeros((Bn, H, L, dv), np.float64)
+    sk = np.zeros((Bn, H, 2, M, dk), np.float64)
+    sv = np.zeros((Bn, H, 2, M, dv), np.float64)
+    rc = _load().bla_oracle_forward(Bn, H, L, dk, dv, M, S, _ptr(T), int(t0), float(scale),
+                                    _ptr(q), _ptr(k), _ptr(v), _ptr(sk_in), _ptr(sv_in),
+                                    _ptr(o), _ptr(sk), _ptr(sv), 1 if literal else 0,
+                                    int(nthreads))
+    if rc != 0:
+        raise ValueError("bla_oracle_forward rejected its arguments")
+    return o, sk, sv
+
+
+def step(q, k, v, T, M: int, S: int, state_k, state_v, pos, scale=None, nthreads: int = 0):
+    """One recurrent decode step at absolute positions pos [B]; q,k [B,H,dk], v [B,H,dv].
+
+    Returns (o [B,H,dv], new state_k, new state_v) without modifying the inputs.
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    Bn, H, dk = q.shape
+    dv = v.shape[-1]
+    T = np.ascontiguousarray(np.broadcast_to(np.asarray(T, np.float64), (H,)))
+    if scale is None:
+        scale = 1.0 / np.sqrt(dk)
+    sk = np.array(state_k, dtype=np.float64, copy=True, order="C")
+    sv = np.array(state_v, dtype=np.float64, copy=True, order="C")
+    pos = np.ascontiguousarray(np.broadcast_to(np.asarray(pos, np.int64), (Bn,)))
+    o = np.zeros((Bn, H, dv), np.float64)
+    rc = _load().bla_oracle_step(Bn, H, dk, dv, M, S, _ptr(T), pos.ctypes.data_as(_ip),
+                                 float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(sk), _ptr(sv),
+                                 _ptr(o), int(nthreads))
+    if rc != 0:
+        raise ValueError("bla_oracle_step rejected its arguments")
+    return o, sk, sv
