@@ -1,0 +1,117 @@
+/*
+ * bla.h -- C ABI of the MI355X (gfx950) library for the forward operator of
+ * Blurry Window Attention (BLA).
+ *
+ * The operator (Sec. 3.1; Appendix C, Alg. 2).  Per batch row b and head h the
+ * layer keeps complex mode states Z_k[m] = Kcos[m] + i Ksin[m] (d_k wide) and
+ * Z_v[m] = Vcos[m] + i Vsin[m] (d_v wide) for m = 0..M-1.  With the period
+ * T_h clamped to at least 2M-1 and w = 2 pi / T_h, each token at absolute
+ * position p does, in order:
+ *   1. rotate and add (Eq. recurrence):  Z[m] <- exp(i m w) Z[m] + x_t   (x = k or v)
+ *   2. rebuild S blurry slots (Eq. compressed, coefficients of Eq. translated at
+ *      the slot lags tau_s = s T_h / S):
+ *        K~[s] = sum_m c_m (cos(m w tau_s) Kcos[m] + sin(m w tau_s) Ksin[m]),
+ *        c_0 = 1/(2M-1), c_m = 2/(2M-1);  V~ likewise
+ *   3. attend over the slots (Eq. output) with the start-of-sequence mask:
+ *        z_s = scale <q_t, K~[s]> if p >= rint(tau_s) else -inf,
+ *        o_t = sum_s softmax(z)_s V~[s].
+ * The paper's own slot count is S = 2M-1; any S >= 1 is accepted and places the
+ * slots on the grid tau_s = s T / S (at S = 2M-1 this is the paper's dilated grid).
+ *
+ * Conventions shared by every entry point:
+ *   - All tensors are row-major and contiguous, in device memory, 16-byte aligned:
+ *       q, k: [B, H, L, d_k]   v, o: [B, H, L, d_v]   (bla_step: L is absent)
+ *       states: float32 [B, H, 2, M, d] -- plane 0 = cos accumulator, plane 1 = sin.
+ *   - io_dtype selects float32 or bfloat16 for q, k, v, o; states are float32.
+ *   - T is a HOST array of H periods (double).  Each is clamped to >= 2M-1, as the
+ *     paper's algorithms do; NaN, infinite, non-positive or > 1e9 is an error.
+ *   - Every device buffer is owned by the caller.  The library allocates no
+ *     device memory: scratch space (tables, per-block partial states) lives in the
+ *     caller's workspace, sized by bla_workspace_size / bla_step_workspace_size.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream).
+ *     Argument errors are reported synchronously before anything is launched;
+ *     launch failures are reported as BLA_ERR_HIP.  Buffers must stay valid until
+ *     the stream has executed the call.  Calls that share a workspace race unless
+ *     they are ordered on one stream.
+ *   - Supported shapes: d_k == d_v in {32, 64, 128}; 1 <= M <= 128; 1 <= S <= 256
+ *     and S <= max(32, 2 P(M)) where P(M) is M rounded up to 16, 32, 64 or 128 (so
+ *     the paper's S = 2M-1 is always accepted); chunk in {0, 64}; float32 I/O also
+ *     needs the kernel's LDS tiles to fit (d = 128 with M > 64 does not).  Anything
+ *     else returns BLA_ERR_UNSUPPORTED; bla_supported() answers without launching.
+ */
+#ifndef BLA_H
+#define BLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BLA_OK = 0,
+    BLA_ERR_INVALID_ARG = 1, /* a null/misaligned pointer, a negative size, a bad period */
+    BLA_ERR_UNSUPPORTED = 2, /* a valid shape this build has no kernel for            */
+    BLA_ERR_WORKSPACE = 3,   /* workspace pointer null or smaller than required       */
+    BLA_ERR_HIP = 4          /* the HIP runtime reported an error while launching     */
+} bla_status;
+
+typedef enum { BLA_F32 = 0, BLA_BF16 = 1 } bla_dtype;
+
+typedef struct {
+    int32_t B, H, L;     /* batch rows, heads, tokens in this call (L >= 0)              */
+    int32_t d_k, d_v;    /* head widths of keys/queries and of values                    */
+    int32_t M;           /* Fourier modes (Sec. 3.1), >= 1                               */
+    int32_t S;           /* blurry slots, >= 1 (the paper's value is 2M-1)               */
+    int32_t chunk;       /* tokens per chunk of the parallel form; 0 = default (64)      */
+    int64_t t0;          /* absolute position of token 0 (start mask only), >= 0         */
+    float scale;         /* softmax scale; 0 selects 1/sqrt(d_k) (Eq. output)            */
+    int32_t io_dtype;    /* bla_dtype of q, k, v, o                                      */
+} bla_params;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* bla_status_string(bla_status s);
+
+/* BLA_OK if the shape in *p has a kernel in this build, else the error it would get. */
+bla_status bla_supported(const bla_params* p);
+
+/*
+ * Bytes of device workspace bla_forward needs for *p on the current device
+ * (0 if *p is invalid or unsupported).  The value depends on B, H, L, d, M, S
+ * and the device's compute-unit count, not on the data.
+ */
+size_t bla_workspace_size(const bla_params* p);
+
+/*
+ * Chunked-parallel forward over L tokens (Sec. 3.2's chunk mode; the operator is
+ * Alg. 2's recurrence).  Writes o [B,H,L,d_v].  state_k_in / state_v_in
+ * [B,H,2,M,d] give the states before token 0 (NULL = zero, a fresh sequence);
+ * state_k_out / state_v_out receive the states after token L-1 (NULL = not
+ * wanted).  The outputs must not alias the inputs.  L = 0 copies the input
+ * states (or zeros) to the outputs.
+ */
+bla_status bla_forward(const bla_params* p, const double* T, const void* q, const void* k,
+                       const void* v, const float* state_k_in, const float* state_v_in, void* o,
+                       float* state_k_out, float* state_v_out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace bla_step needs for *p (L is ignored). */
+size_t bla_step_workspace_size(const bla_params* p);
+
+/*
+ * One recurrent decode step (one iteration of Alg. 2's loop) for every (b,h):
+ * q, k [B,H,d_k], v, o [B,H,d_v].  The token of row b sits at absolute position
+ * pos[b] (device int64 [B]; NULL = p->t0 for every row); the start mask uses it.
+ * state_k / state_v [B,H,2,M,d] hold the states before the token and are updated
+ * in place.  p->L is ignored.
+ */
+bla_status bla_step(const bla_params* p, const double* T, const void* q, const void* k,
+                    const void* v, const int64_t* pos, float* state_k, float* state_v, void* o,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BLA_H */

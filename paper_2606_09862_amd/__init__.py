@@ -1,0 +1,169 @@
+"""Blurry Window Attention forward operator on MI355X (gfx950).
+
+A thin ctypes binding over ``libbla.so`` (the C ABI in ``include/bla.h``).  It
+only marshals arguments: every step of the operator runs in the library's HIP
+kernels.  torch is used for device buffers and the current stream.  If the
+library has not been built, importing works but every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbla.so")
+
+BLA_F32, BLA_BF16 = 0, 1
+STATUS = {0: "BLA_OK", 1: "BLA_ERR_INVALID_ARG", 2: "BLA_ERR_UNSUPPORTED", 3: "BLA_ERR_WORKSPACE",
+          4: "BLA_ERR_HIP"}
+
+
+class BlaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what} failed: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    """Mirror of ``bla_params``."""
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("L", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("M", ctypes.c_int32),
+                ("S", ctypes.c_int32), ("chunk", ctypes.c_int32), ("t0", ctypes.c_int64),
+                ("scale", ctypes.c_float), ("io_dtype", ctypes.c_int32)]
+
+
+_lib = None
+_dp = ctypes.POINTER(ctypes.c_double)
+_vp = ctypes.c_void_p
+
+
+def lib():
+    """The loaded library; raises if it is missing (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_09862_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER(Params)
+        L.bla_status_string.argtypes = [ctypes.c_int]
+        L.bla_status_string.restype = ctypes.c_char_p
+        L.bla_supported.argtypes = [P]
+        L.bla_supported.restype = ctypes.c_int
+        L.bla_workspace_size.argtypes = [P]
+        L.bla_workspace_size.restype = ctypes.c_size_t
+        L.bla_step_workspace_size.argtypes = [P]
+        L.bla_step_workspace_size.restype = ctypes.c_size_t
+        L.bla_forward.argtypes = [P, _dp] + [_vp] * 9 + [ctypes.c_size_t, _vp]
+        L.bla_forward.restype = ctypes.c_int
+        L.bla_step.argtypes = [P, _dp] + [_vp] * 8 + [ctypes.c_size_t, _vp]
+        L.bla_step.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def make_params(B, H, L, d, M, S, dtype, t0=0, scale=0.0, chunk=0) -> Params:
+    io = BLA_BF16 if dtype == torch.bfloat16 else BLA_F32
+    return Params(B, H, L, d, d, M, S, chunk, int(t0), float(scale), io)
+
+
+def _periods(T, H):
+    arr = (ctypes.c_double * max(H, 1))()
+    vals = list(T) if hasattr(T, "__len__") else [T] * H
+    if len(vals) != H:
+        raise ValueError("T must have one period per head")
+    for i, x in enumerate(vals):
+        arr[i] = float(x)
+    return arr
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def supported(p: Params) -> int:
+    return lib().bla_supported(ctypes.byref(p))
+
+
+def workspace_size(p: Params) -> int:
+    return lib().bla_workspace_size(ctypes.byref(p))
+
+
+def step_workspace_size(p: Params) -> int:
+    return lib().bla_step_workspace_size(ctypes.byref(p))
+
+
+def _check(t, shape, dtype, name):
+    if t.shape != tuple(shape) or t.dtype != dtype or not t.is_contiguous() or not t.is_cuda:
+        raise ValueError(f"{name}: expected contiguous {dtype} cuda tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
+            state_k=None, state_v=None, want_state: bool = True, workspace=None, out=None):
+    """bla_forward on q, k, v [B,H,L,d] (float32 or bfloat16 cuda tensors).
+
+    Returns (o, state_k_out, state_v_out); the states are float32 [B,H,2,M,d]
+    (None when want_state is False).
+    """
+    B, H, L, d = q.shape
+    dt = q.dtype
+    for name, t in (("k", k), ("v", v)):
+        _check(t, (B, H, L, d), dt, name)
+    _check(q, (B, H, L, d), dt, "q")
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    for name, t in (("state_k", state_k), ("state_v", state_v)):
+        if t is not None:
+            _check(t, (B, H, 2, M, d), torch.float32, name)
+    dev = q.device
+    o = torch.empty_like(q) if out is None else out
+    sk = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
+    sv = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
+    need = workspace_size(p)
+    if need == 0 and supported(p) != 0:
+        raise BlaError(supported(p), "bla_forward (shape check)")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib().bla_forward(ctypes.byref(p), _periods(T, H), _ptr(q), _ptr(k), _ptr(v), _ptr(state_k),
+                           _ptr(state_v), _ptr(o), _ptr(sk), _ptr(sv), _ptr(workspace),
+                           workspace.numel(), _stream(dev))
+    if st != 0:
+        raise BlaError(st, "bla_forward")
+    return o, sk, sv
+
+
+def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
+         scale: float | None = None, workspace=None, out=None):
+    """bla_step: one decode token per row; q,k,v [B,H,d]; updates state_k/state_v in place."""
+    B, H, d = q.shape
+    dt = q.dtype
+    _check(q, (B, H, d), dt, "q")
+    _check(k, (B, H, d), dt, "k")
+    _check(v, (B, H, d), dt, "v")
+    _check(state_k, (B, H, 2, M, d), torch.float32, "state_k")
+    _check(state_v, (B, H, 2, M, d), torch.float32, "state_v")
+    if pos is not None:
+        _check(pos, (B,), torch.int64, "pos")
+    p = make_params(B, H, 1, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    dev = q.device
+    o = torch.empty_like(q) if out is None else out
+    need = step_workspace_size(p)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib().bla_step(ctypes.byref(p), _periods(T, H), _ptr(q), _ptr(k), _ptr(v), _ptr(pos),
+                        _ptr(state_k), _ptr(state_v), _ptr(o), _ptr(workspace), workspace.numel(),
+                        _stream(dev))
+    if st != 0:
+        raise BlaError(st, "bla_step")
+    return o
+
+
+def default_scale(d: int) -> float:
+    return 1.0 / math.sqrt(d)

@@ -1,0 +1,329 @@
+// Host side of the C ABI declared in include/bla.h: argument validation, the
+// launch plan (segments, summarised blocks, workspace layout) and the launches.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <hip/hip_runtime.h>
+
+#include "bla.h"
+#include "bla_plan.h"
+
+namespace bla {
+hipError_t launch_forward_bf16(const Plan& p, const FwdArgs& a, hipStream_t s);
+hipError_t launch_forward_f32(const Plan& p, const FwdArgs& a, hipStream_t s);
+hipError_t launch_summary_bf16(const Plan& p, const FwdArgs& a, hipStream_t s);
+hipError_t launch_summary_f32(const Plan& p, const FwdArgs& a, hipStream_t s);
+bool forward_supported_bf16(int D, int MP, int SP);
+bool forward_supported_f32(int D, int MP, int SP);
+
+hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s)
+{
+    return p.bf16 ? launch_forward_bf16(p, a, s) : launch_forward_f32(p, a, s);
+}
+hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s)
+{
+    return p.bf16 ? launch_summary_bf16(p, a, s) : launch_summary_f32(p, a, s);
+}
+bool forward_supported(int bf16, int D, int MP, int SP)
+{
+    return bf16 ? forward_supported_bf16(D, MP, SP) : forward_supported_f32(D, MP, SP);
+}
+}  // namespace bla
+
+namespace {
+
+using namespace bla;
+
+constexpr size_t kAlign = 256;
+constexpr size_t kMaxSummaryBytes = size_t(256) << 20;  // cap on per-block summary scratch
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int pad_modes(int M) { return M <= 16 ? 16 : M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : -1; }
+int pad_slots(int S) { return S <= 32 ? 32 : S <= 64 ? 64 : S <= 128 ? 128 : S <= 256 ? 256 : -1; }
+
+int device_cu_count()
+{
+    static int cache[128] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 128) return 256;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+
+// Shape checks shared by every entry point (no pointers).
+bla_status check_shape(const bla_params* p, bool step)
+{
+    if (!p) return BLA_ERR_INVALID_ARG;
+    if (p->B < 0 || p->H < 0 || (!step && p->L < 0)) return BLA_ERR_INVALID_ARG;
+    if (p->d_k <= 0 || p->d_v <= 0 || p->M <= 0 || p->S <= 0 || p->t0 < 0) return BLA_ERR_INVALID_ARG;
+    if (p->io_dtype != BLA_F32 && p->io_dtype != BLA_BF16) return BLA_ERR_INVALID_ARG;
+    if (!isfinite(p->scale)) return BLA_ERR_INVALID_ARG;
+    if (p->chunk != 0 && p->chunk != kChunk) return BLA_ERR_UNSUPPORTED;
+    if (p->d_k != p->d_v) return BLA_ERR_UNSUPPORTED;
+    if (p->d_k != 32 && p->d_k != 64 && p->d_k != 128) return BLA_ERR_UNSUPPORTED;
+    const int MP = pad_modes(p->M), SP = pad_slots(p->S);
+    if (MP < 0 || SP < 0) return BLA_ERR_UNSUPPORTED;
+    if (SP > (2 * MP > 32 ? 2 * MP : 32)) return BLA_ERR_UNSUPPORTED;
+    if (!step && !forward_supported(p->io_dtype == BLA_BF16, p->d_k, MP, SP)) return BLA_ERR_UNSUPPORTED;
+    if ((long long)p->B * p->H > (1ll << 31) / 4) return BLA_ERR_UNSUPPORTED;
+    return BLA_OK;
+}
+
+bla_status check_periods(const bla_params* p, const double* T)
+{
+    if (p->H > 0 && !T) return BLA_ERR_INVALID_ARG;
+    for (int h = 0; h < p->H; ++h)
+        if (!isfinite(T[h]) || T[h] <= 0.0 || T[h] > 1e9) return BLA_ERR_INVALID_ARG;
+    return BLA_OK;
+}
+
+void make_plan(const bla_params* p, bool step, Plan* pl)
+{
+    memset(pl, 0, sizeof(*pl));
+    pl->B = p->B;
+    pl->H = p->H;
+    pl->L = step ? 1 : p->L;
+    pl->D = p->d_k;
+    pl->M = p->M;
+    pl->S = p->S;
+    pl->MP = pad_modes(p->M);
+    pl->SP = pad_slots(p->S);
+    pl->C = kChunk;
+    pl->bf16 = p->io_dtype == BLA_BF16;
+    pl->t0 = p->t0;
+    pl->scale = p->scale != 0.f ? p->scale : 1.f / sqrtf((float)p->d_k);
+    pl->unit_floats = (size_t)4 * pl->MP * pl->D;
+    const long long units = (long long)p->B * p->H;
+    pl->nch = step ? 1 : (p->L + kChunk - 1) / kChunk;
+    pl->nseg = 1;
+    pl->cps = pl->nch;
+    pl->cpb = pl->nch;
+    pl->nbs = 0;
+    if (!step && units > 0 && pl->nch > 1) {
+        const int cus = device_cu_count();
+        if (units < cus) {
+            long long want = (cus + units - 1) / units;
+            int nseg = (int)(want < pl->nch ? want : pl->nch);
+            int cps = (pl->nch + nseg - 1) / nseg;
+            nseg = (pl->nch + cps - 1) / cps;
+            pl->nseg = nseg;
+            pl->cps = cps;
+            if (nseg > 1) {
+                // Blocks per segment: enough summary workgroups to fill the device, within
+                // the scratch cap; always a divisor of cps.
+                int bps = 1;
+                const size_t unit_bytes = pl->unit_floats * sizeof(float);
+                while (units * (nseg - 1) * bps < 2 * cus && cps % (2 * bps) == 0 &&
+                       (size_t)units * (nseg - 1) * (2 * bps) * unit_bytes <= kMaxSummaryBytes)
+                    bps *= 2;
+                pl->cpb = cps / bps;
+                pl->nbs = (nseg - 1) * bps;
+            }
+        }
+    }
+    const size_t esz = pl->bf16 ? 2 : 4;
+    const size_t H = (size_t)p->H, C = kChunk, MP2 = 2 * (size_t)pl->MP, SP = (size_t)pl->SP;
+    size_t off = 0;
+    pl->off_E32 = off;    off = align_up(off + H * (C + 1) * MP2 * 4);
+    pl->off_EbarT = off;  off = align_up(off + H * MP2 * C * esz);
+    pl->off_ErevT = off;  off = align_up(off + H * MP2 * C * esz);
+    pl->off_Etab = off;   off = align_up(off + H * C * MP2 * esz);
+    pl->off_ABs = off;    off = align_up(off + SP * MP2 * esz);
+    pl->off_ABm = off;    off = align_up(off + MP2 * SP * esz);
+    pl->off_AB32 = off;   off = align_up(off + SP * MP2 * 4);
+    pl->off_theta = off;  off = align_up(off + H * SP * 4);
+    pl->off_rotblk = off; off = align_up(off + H * MP2 * 4);
+    pl->off_summ = off;   off = align_up(off + (size_t)units * pl->nbs * pl->unit_floats * 4);
+    pl->off_carry = off;  off = align_up(off + (size_t)units * (pl->nseg - 1) * pl->unit_floats * 4);
+    pl->total = off;
+}
+
+bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s)
+{
+    for (int h0 = 0; h0 < pl.H; h0 += kMaxHeadsPerTableLaunch) {
+        TableArgs a;
+        memset(&a, 0, sizeof(a));
+        a.E32 = (float*)(ws + pl.off_E32);
+        a.EbarT = ws + pl.off_EbarT;
+        a.ErevT = ws + pl.off_ErevT;
+        a.Etab = ws + pl.off_Etab;
+        a.ABs = ws + pl.off_ABs;
+        a.ABm = ws + pl.off_ABm;
+        a.AB32 = (float*)(ws + pl.off_AB32);
+        a.theta = (int*)(ws + pl.off_theta);
+        a.rotblk = (float*)(ws + pl.off_rotblk);
+        a.M = pl.M;
+        a.S = pl.S;
+        a.MP = pl.MP;
+        a.SP = pl.SP;
+        a.C = kChunk;
+        a.Lblk = pl.cpb * kChunk;
+        a.h0 = h0;
+        a.nh = pl.H - h0 < kMaxHeadsPerTableLaunch ? pl.H - h0 : kMaxHeadsPerTableLaunch;
+        a.with_shared = h0 == 0;
+        a.scale = pl.scale;
+        for (int i = 0; i < a.nh; ++i) {
+            const double tmin = 2.0 * pl.M - 1.0;
+            a.T[i] = T[h0 + i] < tmin ? tmin : T[h0 + i];  // clamp, as Alg. 1 and Alg. 3 do
+        }
+        if (launch_tables(a, pl.bf16, s) != hipSuccess) return BLA_ERR_HIP;
+    }
+    return BLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bla_status_string(bla_status s)
+{
+    switch (s) {
+    case BLA_OK: return "BLA_OK";
+    case BLA_ERR_INVALID_ARG: return "BLA_ERR_INVALID_ARG: invalid argument";
+    case BLA_ERR_UNSUPPORTED: return "BLA_ERR_UNSUPPORTED: shape not supported by this build";
+    case BLA_ERR_WORKSPACE: return "BLA_ERR_WORKSPACE: workspace missing or too small";
+    case BLA_ERR_HIP: return "BLA_ERR_HIP: HIP runtime error";
+    }
+    return "BLA_ERR_UNKNOWN";
+}
+
+bla_status bla_supported(const bla_params* p) { return check_shape(p, false); }
+
+size_t bla_workspace_size(const bla_params* p)
+{
+    if (check_shape(p, false) != BLA_OK) return 0;
+    Plan pl;
+    make_plan(p, false, &pl);
+    return pl.total;
+}
+
+size_t bla_step_workspace_size(const bla_params* p)
+{
+    if (check_shape(p, true) != BLA_OK) return 0;
+    Plan pl;
+    make_plan(p, true, &pl);
+    return pl.total;
+}
+
+bla_status bla_forward(const bla_params* p, const double* T, const void* q, const void* k,
+                       const void* v, const float* state_k_in, const float* state_v_in, void* o,
+                       float* state_k_out, float* state_v_out, void* workspace,
+                       size_t workspace_bytes, void* stream)
+{
+    bla_status st = check_shape(p, false);
+    if (st != BLA_OK) return st;
+    if ((st = check_periods(p, T)) != BLA_OK) return st;
+    const long long units = (long long)p->B * p->H;
+    if (units == 0) return BLA_OK;
+    if (p->L > 0) {
+        if (!q || !k || !v || !o) return BLA_ERR_INVALID_ARG;
+        if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return BLA_ERR_INVALID_ARG;
+    }
+    const float* sptr[4] = {state_k_in, state_v_in, state_k_out, state_v_out};
+    for (int i = 0; i < 4; ++i)
+        if (sptr[i] && !aligned16(sptr[i])) return BLA_ERR_INVALID_ARG;
+    if ((state_k_out && state_k_out == state_k_in) || (state_v_out && state_v_out == state_v_in))
+        return BLA_ERR_INVALID_ARG;
+    Plan pl;
+    make_plan(p, false, &pl);
+    if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const size_t n_state = (size_t)units * 2 * p->M * p->d_k;
+
+    if (p->L == 0) {
+        if (launch_state_copy(state_k_in, state_k_out, n_state, s) != hipSuccess) return BLA_ERR_HIP;
+        if (launch_state_copy(state_v_in, state_v_out, n_state, s) != hipSuccess) return BLA_ERR_HIP;
+        return BLA_OK;
+    }
+    if ((st = build_tables(pl, T, ws, s)) != BLA_OK) return st;
+
+    FwdArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.sk_in = state_k_in;
+    a.sv_in = state_v_in;
+    a.sk_out = state_k_out;
+    a.sv_out = state_v_out;
+    a.E32 = (const float*)(ws + pl.off_E32);
+    a.EbarT = ws + pl.off_EbarT;
+    a.ErevT = ws + pl.off_ErevT;
+    a.Etab = ws + pl.off_Etab;
+    a.ABs = ws + pl.off_ABs;
+    a.ABm = ws + pl.off_ABm;
+    a.theta = (const int*)(ws + pl.off_theta);
+    a.summ = (float*)(ws + pl.off_summ);
+    a.carry = (float*)(ws + pl.off_carry);
+    a.rotblk = (const float*)(ws + pl.off_rotblk);
+    a.B = pl.B;
+    a.H = pl.H;
+    a.L = pl.L;
+    a.M = pl.M;
+    a.nch = pl.nch;
+    a.nseg = pl.nseg;
+    a.cps = pl.cps;
+    a.cpb = pl.cpb;
+    a.nbs = pl.nbs;
+    a.t0 = pl.t0;
+    if (pl.nseg > 1) {
+        if (launch_summary(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+        if (launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    }
+    if (launch_forward(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    return BLA_OK;
+}
+
+bla_status bla_step(const bla_params* p, const double* T, const void* q, const void* k,
+                    const void* v, const int64_t* pos, float* state_k, float* state_v, void* o,
+                    void* workspace, size_t workspace_bytes, void* stream)
+{
+    bla_status st = check_shape(p, true);
+    if (st != BLA_OK) return st;
+    if ((st = check_periods(p, T)) != BLA_OK) return st;
+    const long long units = (long long)p->B * p->H;
+    if (units == 0) return BLA_OK;
+    if (!q || !k || !v || !o || !state_k || !state_v) return BLA_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(state_k) ||
+        !aligned16(state_v))
+        return BLA_ERR_INVALID_ARG;
+    if (pos && ((uintptr_t)pos & 7u)) return BLA_ERR_INVALID_ARG;
+    Plan pl;
+    make_plan(p, true, &pl);
+    if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if ((st = build_tables(pl, T, ws, s)) != BLA_OK) return st;
+    StepArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.pos = pos;
+    a.sk = state_k;
+    a.sv = state_v;
+    a.E32 = (const float*)(ws + pl.off_E32);
+    a.AB32 = (const float*)(ws + pl.off_AB32);
+    a.theta = (const int*)(ws + pl.off_theta);
+    a.B = pl.B;
+    a.H = pl.H;
+    a.M = pl.M;
+    a.t0 = pl.t0;
+    a.scale = pl.scale;
+    if (launch_step(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    return BLA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+// Device-side building blocks shared by the BLA kernels (gfx950 / CDNA4).
+//
+// Matrix-core convention used everywhere.  Every contraction is computed with
+// 16x16 output tiles on the matrix cores: bf16 operands use
+// v_mfma_f32_16x16x32_bf16, float32 operands use eight v_mfma_f32_16x16x4_f32.
+// For a 64-lane wave, lane l has group g = l / 16 and index r = l % 16.
+//
+//  * Accumulator tile (floatx4): lane (g, r) holds rows 4g+0..3 of column r.
+//  * Operand fragment for reduction block kb (32 reduction indices): lane (g, r)
+//    holds 8 values for row r (A operand) or column r (B operand), element e at
+//    reduction index  k(e) = 32 kb + 16 (e / 4) + 4 g + (e % 4).
+//    The same k(e) is used for A and B, so the products pair up correctly
+//    whatever order the hardware walks the reduction in.
+//  * With this k(e), two stacked accumulator tiles (rows 32kb..32kb+15 and
+//    32kb+16..32kb+31) ARE the B fragment of the next contraction over those
+//    rows (and, for a transposed state, the A fragment), so chains of
+//    contractions pass their intermediates in registers without a shuffle.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bla {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+typedef int intx4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Frag;
+template <> struct Frag<bf16> { typedef bf16x8 type; typedef bf16x4 half; };
+template <> struct Frag<float> { typedef floatx8 type; typedef floatx4 half; };
+
+__device__ __forceinline__ floatx4 mma(bf16x8 a, bf16x8 b, floatx4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ floatx4 mma(floatx8 a, floatx8 b, floatx4 c)
+{
+#pragma unroll
+    for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
+    return c;
+}
+
+__device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
+
+template <typename T> __device__ __forceinline__ typename Frag<T>::type zero_frag()
+{
+    typename Frag<T>::type f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = (T)0.f;
+    return f;
+}
+
+template <typename T> __device__ __forceinline__ typename Frag<T>::half zero_half()
+{
+    typename Frag<T>::half f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = (T)0.f;
+    return f;
+}
+
+__device__ __forceinline__ bf16x8 join(bf16x4 a, bf16x4 b)
+{
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+__device__ __forceinline__ floatx8 join(floatx4 a, floatx4 b)
+{
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Four consecutive elements as a vector (pointer 4-element aligned).
+template <typename T> __device__ __forceinline__ typename Frag<T>::half ld4(const T* p)
+{
+    return *reinterpret_cast<const typename Frag<T>::half*>(p);
+}
+
+// Fragment of a row-major matrix whose reduction index is contiguous in memory:
+// `row` points at the lane's row (A) or column (B); k0 = 32 kb.
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type ld_frag(const T* row, int k0, int g)
+{
+    return join(ld4<T>(row + k0 + 4 * g), ld4<T>(row + k0 + 16 + 4 * g));
+}
+
+// Same, with the upper half (reduction indices k0+16..k0+31) replaced by zeros.
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type ld_frag_lo(const T* row, int k0, int g)
+{
+    return join(ld4<T>(row + k0 + 4 * g), zero_half<T>());
+}
+
+__device__ __forceinline__ bf16x4 cvt4(floatx4 x, bf16)
+{
+    bf16x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = (bf16)x[e];
+    return r;
+}
+__device__ __forceinline__ floatx4 cvt4(floatx4 x, float) { return x; }
+
+// Two stacked accumulator tiles -> operand fragment (see the header comment).
+template <typename T>
+__device__ __forceinline__ typename Frag<T>::type frag_from_acc(floatx4 lo, floatx4 hi)
+{
+    return join(cvt4(lo, T()), cvt4(hi, T()));
+}
+
+// Store four floats as four consecutive elements of type T.
+template <typename T> __device__ __forceinline__ void st4(T* p, floatx4 x)
+{
+    *reinterpret_cast<typename Frag<T>::half*>(p) = cvt4(x, T());
+}
+
+__device__ __forceinline__ floatx4 ld4f(const float* p) { return *reinterpret_cast<const floatx4*>(p); }
+__device__ __forceinline__ void st4f(float* p, floatx4 x) { *reinterpret_cast<floatx4*>(p) = x; }
+
+// Up-convert a 4-vector of T to float.
+__device__ __forceinline__ floatx4 to_f4(bf16x4 x)
+{
+    floatx4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = (float)x[e];
+    return r;
+}
+__device__ __forceinline__ floatx4 to_f4(floatx4 x) { return x; }
+
+}  // namespace bla

@@ -1,0 +1,571 @@
+// Chunked-parallel BLA forward kernels for gfx950 (templated; instantiated in
+// bla_forward_bf16.hip and bla_forward_f32.hip).
+//
+// The operator is the mode-state recurrence (Sec. 3.1 Eq. recurrence) read out
+// through blurry slots (Eq. compressed) with a masked slot softmax (Eq. output),
+// i.e. Alg. 2.  The kernels compute it in chunks of C = 64 tokens with the state
+// carried in registers.  Per chunk (local token j, key i, mode m), with
+// rho_m = exp(i m w), E[j,m] = rho_m^j, G = tril(Q K^T) and the pre-rotated state
+// Z' = rho Z (so every phase is a local power rho^j, j <= C):
+//
+//   (1+3)  U   = E o (Q Z'_k^T + G conj(E))            query-mode projection
+//   (4)    z   = scale (Re U A^T + Im U B^T)            slot scores
+//   (5)    P   = softmax(z masked where pos < theta)    start mask (Alg. 2)
+//   (6)    W'' = (P A - i P B) o E                      readout weights per mode
+//   (7-9)  O   = Re(W'' Z'_v) + tril(Re(W'' conj(E)^T)) V
+//   (10)   Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i]
+//
+// Work split inside a 256-thread workgroup (4 waves): contractions that produce
+// per-mode rows (1+3, 10) are split by mode tiles, the Gram tile (2) by key
+// tiles, and the per-token chain (4-9) by token tiles, so that the chain passes
+// its intermediates in registers (see bla_device.h).  The fp32 state of the
+// wave's own mode tiles lives in registers for the whole segment; its bf16 copy
+// of Z'_v goes through LDS for (7).
+//
+// A sequence is split into nseg segments processed by separate workgroups.  The
+// state entering segment g >= 1 comes from a scan over per-block summaries
+// (summary_kernel: step 10 alone, from a zero state) -- the recurrence is
+// linear, so carry_g = sum of block summaries rotated to the segment start.
+#pragma once
+
+#include <math.h>
+
+#include "bla_device.h"
+#include "bla_plan.h"
+
+namespace bla {
+
+template <typename T, int D, int MP> struct Geo {
+    static constexpr int C = kChunk;
+    static constexpr int NT = C / 16;           // token tiles per chunk
+    static constexpr int NW = kThreads / 64;    // waves
+    static constexpr int NMT = MP / 16;         // mode tiles
+    static constexpr int NDT = D / 16;          // head-dim tiles
+    static constexpr int KBD = D / 32;          // reduction blocks over d
+    static constexpr int KBM = 2 * MP / 32;     // reduction blocks over [Re | Im] modes
+    static constexpr int KBC = C / 32;          // reduction blocks over chunk tokens
+    static constexpr int OWN = (NMT + NW - 1) / NW;  // mode tiles owned per wave
+    static constexpr int PAD = 16 / (int)sizeof(T);  // 16-byte row padding in LDS
+    static constexpr int LDK = C + PAD;         // Kt, Vt: [D][LDK]
+    static constexpr int LDZ = 2 * MP + PAD;    // ZvT: [D][LDZ]
+    static constexpr size_t KT_ELEMS = (size_t)D * LDK;
+    static_assert(NT == NW, "one token tile per wave");
+    static_assert(D % 32 == 0 && MP % 16 == 0, "tile shapes");
+};
+
+template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
+    using G = Geo<T, D, MP>;
+    static constexpr int NST = SP / 16;
+    static constexpr int KBS = SP / 32;
+    static constexpr int LDG = G::C + G::PAD;   // GT: [C tokens][LDG]
+    static constexpr int LDU = 2 * MP + G::PAD; // UT: [C tokens][LDU]
+    static constexpr size_t LDS_ELEMS =
+        2 * G::KT_ELEMS + (size_t)G::C * LDG + (size_t)G::C * LDU + (size_t)D * G::LDZ;
+    static constexpr size_t LDS_BYTES = LDS_ELEMS * sizeof(T);
+    static_assert(SP % 32 == 0, "slot padding");
+};
+
+constexpr size_t kMaxLds = 160 * 1024;
+
+// The wave's fp32 state tiles: [owned mode tile][Re, Im][head-dim tile].
+template <typename T, int D, int MP> using StateTiles = floatx4[Geo<T, D, MP>::OWN][2][D / 16];
+
+// ---------------------------------------------------------------------------------
+// Stage one chunk of K and V transposed into LDS: Kt[d][i], Vt[d][i] (zero past c).
+template <typename T, int D, int MP>
+__device__ __forceinline__ void stage_kv(T* Kt, T* Vt, const T* kc, const T* vc, int c, int tid)
+{
+    using GG = Geo<T, D, MP>;
+    constexpr int DO = D / 8;
+    constexpr int UNITS = (GG::C / 4) * DO;
+#pragma unroll
+    for (int u0 = 0; u0 < 2 * UNITS; u0 += kThreads) {
+        const int u = u0 + tid;
+        if (u < 2 * UNITS) {
+            const int which = u / UNITS, uu = u % UNITS, tq = uu / DO, dq = uu % DO;
+            const T* src = (which ? vc : kc) + (size_t)(4 * tq) * D + 8 * dq;
+            T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
+            typename Frag<T>::half lo[4], hi[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                if (4 * tq + t < c) {
+                    lo[t] = ld4<T>(src + (size_t)t * D);
+                    hi[t] = ld4<T>(src + (size_t)t * D + 4);
+                } else {
+                    lo[t] = zero_half<T>();
+                    hi[t] = zero_half<T>();
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                typename Frag<T>::half a{lo[0][e], lo[1][e], lo[2][e], lo[3][e]};
+                typename Frag<T>::half b{hi[0][e], hi[1][e], hi[2][e], hi[3][e]};
+                *reinterpret_cast<typename Frag<T>::half*>(dst + e * GG::LDK) = a;
+                *reinterpret_cast<typename Frag<T>::half*>(dst + (e + 4) * GG::LDK) = b;
+            }
+        }
+    }
+}
+
+// Fragment of rho^{c-i} (i < c, zero past c) for a ragged last chunk, built from E32.
+template <typename T, int MP>
+__device__ __forceinline__ typename Frag<T>::type erev_frag(const float* E32h, int c, int p, int mt,
+                                                            int kb, int g, int r)
+{
+    typename Frag<T>::type f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int i = 32 * kb + 16 * (e / 4) + 4 * g + (e % 4);
+        float val = 0.f;
+        if (i < c) val = E32h[(size_t)(c - i) * 2 * MP + p * MP + 16 * mt + r];
+        f[e] = (T)val;
+    }
+    return f;
+}
+
+// Write the bf16/fp32 copy of Z'_v as ZvT[d][Re m | Im m] with the Im part negated
+// (the A operand of O += Re(W'' Z'_v)).
+template <typename T, int D, int MP>
+__device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP>& Zv, int w, int g, int r)
+{
+    using GG = Geo<T, D, MP>;
+#pragma unroll
+    for (int o = 0; o < GG::OWN; ++o) {
+        const int mt = w + GG::NW * o;
+        if (mt < GG::NMT) {
+#pragma unroll
+            for (int dt = 0; dt < GG::NDT; ++dt) {
+                st4<T>(ZvT + (size_t)(16 * dt + r) * GG::LDZ + 16 * mt + 4 * g, Zv[o][0][dt]);
+                st4<T>(ZvT + (size_t)(16 * dt + r) * GG::LDZ + MP + 16 * mt + 4 * g, -Zv[o][1][dt]);
+            }
+        }
+    }
+}
+
+// Step 10: Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i] on the wave's own mode tiles.
+template <typename T, int D, int MP>
+__device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTiles<T, D, MP>& Zv,
+                                              const T* Kt, const T* Vt, const float* E32h,
+                                              const T* ErevTh, int c, int w, int g, int r)
+{
+    using GG = Geo<T, D, MP>;
+    using F = typename Frag<T>::type;
+    const float* Ec = E32h + (size_t)c * 2 * MP;
+#pragma unroll
+    for (int o = 0; o < GG::OWN; ++o) {
+        const int mt = w + GG::NW * o;
+        if (mt < GG::NMT) {
+            const float cc = Ec[16 * mt + r], ss = Ec[MP + 16 * mt + r];
+#pragma unroll
+            for (int dt = 0; dt < GG::NDT; ++dt) {
+                const floatx4 re = Zk[o][0][dt], im = Zk[o][1][dt];
+                Zk[o][0][dt] = cc * re - ss * im;
+                Zk[o][1][dt] = ss * re + cc * im;
+            }
+            const floatx4 cv = ld4f(Ec + 16 * mt + 4 * g), sv = ld4f(Ec + MP + 16 * mt + 4 * g);
+#pragma unroll
+            for (int dt = 0; dt < GG::NDT; ++dt) {
+                const floatx4 re = Zv[o][0][dt], im = Zv[o][1][dt];
+                Zv[o][0][dt] = cv * re - sv * im;
+                Zv[o][1][dt] = sv * re + cv * im;
+            }
+        }
+    }
+#pragma unroll
+    for (int kb = 0; kb < GG::KBC; ++kb) {
+        F kf[GG::NDT], vf[GG::NDT];
+#pragma unroll
+        for (int dt = 0; dt < GG::NDT; ++dt) {
+            kf[dt] = ld_frag<T>(Kt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
+            vf[dt] = ld_frag<T>(Vt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
+        }
+#pragma unroll
+        for (int o = 0; o < GG::OWN; ++o) {
+            const int mt = w + GG::NW * o;
+            if (mt < GG::NMT) {
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    F ef = (c == GG::C)
+                               ? ld_frag<T>(ErevTh + (size_t)(16 * (p * GG::NMT + mt) + r) * GG::C,
+                                            32 * kb, g)
+                               : erev_frag<T, MP>(E32h, c, p, mt, kb, g, r);
+#pragma unroll
+                    for (int dt = 0; dt < GG::NDT; ++dt) {
+                        Zk[o][p][dt] = mma(kf[dt], ef, Zk[o][p][dt]);
+                        Zv[o][p][dt] = mma(ef, vf[dt], Zv[o][p][dt]);
+                    }
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// Block summaries: the pre-rotated state after cpb full chunks, from zero.
+template <typename T, int D, int MP>
+__global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
+{
+    using GG = Geo<T, D, MP>;
+    __shared__ __attribute__((aligned(16))) T lds[2 * GG::KT_ELEMS];
+    T* Kt = lds;
+    T* Vt = lds + GG::KT_ELEMS;
+    const int tid = threadIdx.x, w = tid >> 6, g = (tid & 63) >> 4, r = tid & 15;
+    const int blk = blockIdx.x % a.nbs, bh = blockIdx.x / a.nbs, h = bh % a.H;
+    const T* kb = (const T*)a.k + (size_t)bh * a.L * D;
+    const T* vb = (const T*)a.v + (size_t)bh * a.L * D;
+    const float* E32h = a.E32 + (size_t)h * (GG::C + 1) * 2 * MP;
+    const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C;
+
+    floatx4 Zk[GG::OWN][2][GG::NDT], Zv[GG::OWN][2][GG::NDT];
+#pragma unroll
+    for (int o = 0; o < GG::OWN; ++o)
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int dt = 0; dt < GG::NDT; ++dt) Zk[o][p][dt] = Zv[o][p][dt] = zero4();
+
+    for (int n = 0; n < a.cpb; ++n) {
+        const size_t tok0 = (size_t)(blk * a.cpb + n) * GG::C;
+        __syncthreads();
+        stage_kv<T, D, MP>(Kt, Vt, kb + tok0 * D, vb + tok0 * D, GG::C, tid);
+        __syncthreads();
+        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, ErevTh, GG::C, w, g, r);
+    }
+    float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
+#pragma unroll
+    for (int o = 0; o < GG::OWN; ++o) {
+        const int mt = w + GG::NW * o;
+        if (mt < GG::NMT) {
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int dt = 0; dt < GG::NDT; ++dt) {
+                    st4f(S + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[o][p][dt]);
+                    st4f(S + (size_t)2 * MP * D + ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
+                         Zv[o][p][dt]);
+                }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// One workgroup per (b, h, segment): the chunk loop over the segment.
+template <typename T, int D, int MP, int SP>
+__global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
+{
+    using P = Fwd<T, D, MP, SP>;
+    using GG = Geo<T, D, MP>;
+    using F = typename Frag<T>::type;
+    constexpr int C = GG::C, NT = GG::NT, NW = GG::NW, NMT = GG::NMT, NDT = GG::NDT, OWN = GG::OWN;
+    __shared__ __attribute__((aligned(16))) T lds[P::LDS_ELEMS];
+    T* Kt = lds;
+    T* Vt = Kt + GG::KT_ELEMS;
+    T* GT = Vt + GG::KT_ELEMS;
+    T* UT = GT + (size_t)C * P::LDG;
+    T* ZvT = UT + (size_t)C * P::LDU;
+
+    const int tid = threadIdx.x, w = tid >> 6, g = (tid & 63) >> 4, r = tid & 15;
+    const int seg = blockIdx.x % a.nseg, bh = blockIdx.x / a.nseg, h = bh % a.H;
+    const int ch0 = seg * a.cps;
+    const int nch = min(a.cps, a.nch - ch0);
+    const T* qb = (const T*)a.q + (size_t)bh * a.L * D;
+    const T* kb_ = (const T*)a.k + (size_t)bh * a.L * D;
+    const T* vb = (const T*)a.v + (size_t)bh * a.L * D;
+    T* ob = (T*)a.o + (size_t)bh * a.L * D;
+    const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
+    const T* EbarTh = (const T*)a.EbarT + (size_t)h * 2 * MP * C;
+    const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * C;
+    const T* Etabh = (const T*)a.Etab + (size_t)h * C * 2 * MP;
+    const T* ABs = (const T*)a.ABs;
+    const T* ABm = (const T*)a.ABm;
+    const int* thh = a.theta + (size_t)h * SP;
+
+    // ---- state entering the segment (pre-rotated: Z' = rho Z)
+    floatx4 Zk[OWN][2][NDT], Zv[OWN][2][NDT];
+    if (seg == 0) {
+        const float* E1 = E32h + 2 * MP;
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = w + NW * o;
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                floatx4 kr = zero4(), ki = zero4(), vr = zero4(), vi = zero4();
+                if (mt < NMT) {
+                    const int m = 16 * mt + r;
+                    if (a.sk_in && m < a.M) {
+                        kr = ld4f(a.sk_in + (((size_t)bh * 2 + 0) * a.M + m) * D + 16 * dt + 4 * g);
+                        ki = ld4f(a.sk_in + (((size_t)bh * 2 + 1) * a.M + m) * D + 16 * dt + 4 * g);
+                    }
+                    if (a.sv_in) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int mv = 16 * mt + 4 * g + e;
+                            if (mv < a.M) {
+                                vr[e] = a.sv_in[(((size_t)bh * 2 + 0) * a.M + mv) * D + 16 * dt + r];
+                                vi[e] = a.sv_in[(((size_t)bh * 2 + 1) * a.M + mv) * D + 16 * dt + r];
+                            }
+                        }
+                    }
+                    const float c1 = E1[m], s1 = E1[MP + m];
+                    Zk[o][0][dt] = c1 * kr - s1 * ki;
+                    Zk[o][1][dt] = s1 * kr + c1 * ki;
+                    const floatx4 cv = ld4f(E1 + 16 * mt + 4 * g), sv = ld4f(E1 + MP + 16 * mt + 4 * g);
+                    Zv[o][0][dt] = cv * vr - sv * vi;
+                    Zv[o][1][dt] = sv * vr + cv * vi;
+                } else {
+                    Zk[o][0][dt] = Zk[o][1][dt] = Zv[o][0][dt] = Zv[o][1][dt] = zero4();
+                }
+            }
+        }
+    } else {
+        const float* cy = a.carry + ((size_t)bh * (a.nseg - 1) + (seg - 1)) * 4 * MP * D;
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = w + NW * o;
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    if (mt < NMT) {
+                        Zk[o][p][dt] = ld4f(cy + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
+                        Zv[o][p][dt] = ld4f(cy + (size_t)2 * MP * D +
+                                            ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+                    } else {
+                        Zk[o][p][dt] = Zv[o][p][dt] = zero4();
+                    }
+                }
+        }
+    }
+    write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
+
+    for (int n = 0; n < nch; ++n) {
+        const int tok0 = (ch0 + n) * C;
+        const int c = min(C, a.L - tok0);
+        __syncthreads();
+        stage_kv<T, D, MP>(Kt, Vt, kb_ + (size_t)tok0 * D, vb + (size_t)tok0 * D, c, tid);
+        __syncthreads();
+
+        // ---- phase A: Gram tile (key tile w) and Q Z'_k^T on owned mode tiles
+        floatx4 U[OWN][2][NT];
+#pragma unroll
+        for (int o = 0; o < OWN; ++o)
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int ct = 0; ct < NT; ++ct) U[o][p][ct] = zero4();
+#pragma unroll
+        for (int ct = 0; ct < NT; ++ct) {
+            const int j = 16 * ct + r;
+            F qf[GG::KBD];
+#pragma unroll
+            for (int kb = 0; kb < GG::KBD; ++kb)
+                qf[kb] = j < c ? ld_frag<T>(qb + (size_t)(tok0 + j) * D, 32 * kb, g) : zero_frag<T>();
+            if (ct >= w) {
+                const int i = 16 * w + r;
+                floatx4 acc = zero4();
+#pragma unroll
+                for (int kb = 0; kb < GG::KBD; ++kb) {
+                    F kf = i < c ? ld_frag<T>(kb_ + (size_t)(tok0 + i) * D, 32 * kb, g) : zero_frag<T>();
+                    acc = mma(kf, qf[kb], acc);
+                }
+                if (ct == w) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (4 * g + e > r) acc[e] = 0.f;
+                }
+                st4<T>(GT + (size_t)j * P::LDG + 16 * w + 4 * g, acc);
+            }
+#pragma unroll
+            for (int o = 0; o < OWN; ++o) {
+                if (w + NW * o < NMT) {
+#pragma unroll
+                    for (int p = 0; p < 2; ++p)
+#pragma unroll
+                        for (int kb = 0; kb < GG::KBD; ++kb)
+                            U[o][p][ct] = mma(frag_from_acc<T>(Zk[o][p][2 * kb], Zk[o][p][2 * kb + 1]),
+                                              qf[kb], U[o][p][ct]);
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- phase B: + G conj(E), twiddle by E, publish U to LDS
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = w + NW * o;
+            if (mt < NMT) {
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    F ef[GG::KBC];
+#pragma unroll
+                    for (int kb = 0; kb < GG::KBC; ++kb)
+                        ef[kb] = ld_frag<T>(EbarTh + (size_t)(16 * (p * NMT + mt) + r) * C, 32 * kb, g);
+#pragma unroll
+                    for (int ct = 0; ct < NT; ++ct) {
+#pragma unroll
+                        for (int kb = 0; kb < GG::KBC; ++kb) {
+                            if (2 * kb <= ct) {
+                                const T* grow = GT + (size_t)(16 * ct + r) * P::LDG;
+                                F gf = (2 * kb + 1 <= ct) ? ld_frag<T>(grow, 32 * kb, g)
+                                                          : ld_frag_lo<T>(grow, 32 * kb, g);
+                                U[o][p][ct] = mma(ef[kb], gf, U[o][p][ct]);
+                            }
+                        }
+                    }
+                }
+#pragma unroll
+                for (int ct = 0; ct < NT; ++ct) {
+                    const int j = 16 * ct + r;
+                    const floatx4 cs = ld4f(E32h + (size_t)j * 2 * MP + 16 * mt + 4 * g);
+                    const floatx4 sn = ld4f(E32h + (size_t)j * 2 * MP + MP + 16 * mt + 4 * g);
+                    const floatx4 re = U[o][0][ct], im = U[o][1][ct];
+                    st4<T>(UT + (size_t)j * P::LDU + 16 * mt + 4 * g, cs * re - sn * im);
+                    st4<T>(UT + (size_t)j * P::LDU + MP + 16 * mt + 4 * g, sn * re + cs * im);
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- per-token chain on token tile w: scores, softmax, readout, output
+        {
+            const int j = 16 * w + r;
+            const long long pos = a.t0 + tok0 + j;
+            F uf[GG::KBM];
+#pragma unroll
+            for (int kb = 0; kb < GG::KBM; ++kb) uf[kb] = ld_frag<T>(UT + (size_t)j * P::LDU, 32 * kb, g);
+            floatx4 sc[P::NST];
+#pragma unroll
+            for (int st = 0; st < P::NST; ++st) {
+                sc[st] = zero4();
+#pragma unroll
+                for (int kb = 0; kb < GG::KBM; ++kb)
+                    sc[st] = mma(ld_frag<T>(ABs + (size_t)(16 * st + r) * 2 * MP, 32 * kb, g), uf[kb], sc[st]);
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int st = 0; st < P::NST; ++st) {
+                const intx4 th = *reinterpret_cast<const intx4*>(thh + 16 * st + 4 * g);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (pos < (long long)th[e]) sc[st][e] = -INFINITY;
+                    mx = fmaxf(mx, sc[st][e]);
+                }
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            float sum = 0.f;
+#pragma unroll
+            for (int st = 0; st < P::NST; ++st)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float ex = __expf(sc[st][e] - mx);
+                    sc[st][e] = ex;
+                    sum += ex;
+                }
+            sum += __shfl_xor(sum, 16);
+            sum += __shfl_xor(sum, 32);
+            const float inv = 1.f / sum;
+            F pf[P::KBS];
+#pragma unroll
+            for (int kb = 0; kb < P::KBS; ++kb) pf[kb] = frag_from_acc<T>(sc[2 * kb] * inv, sc[2 * kb + 1] * inv);
+
+            floatx4 wa[2 * NMT];
+#pragma unroll
+            for (int t = 0; t < 2 * NMT; ++t) {
+                wa[t] = zero4();
+#pragma unroll
+                for (int kb = 0; kb < P::KBS; ++kb)
+                    wa[t] = mma(ld_frag<T>(ABm + (size_t)(16 * t + r) * SP, 32 * kb, g), pf[kb], wa[t]);
+            }
+#pragma unroll
+            for (int mt = 0; mt < NMT; ++mt) {
+                const floatx4 cs = ld4f(E32h + (size_t)j * 2 * MP + 16 * mt + 4 * g);
+                const floatx4 sn = ld4f(E32h + (size_t)j * 2 * MP + MP + 16 * mt + 4 * g);
+                const floatx4 am = wa[mt], bm = wa[NMT + mt];
+                wa[mt] = am * cs + bm * sn;
+                wa[NMT + mt] = am * sn - bm * cs;
+            }
+            F wf[GG::KBM];
+#pragma unroll
+            for (int kb = 0; kb < GG::KBM; ++kb) wf[kb] = frag_from_acc<T>(wa[2 * kb], wa[2 * kb + 1]);
+
+            floatx4 oa[NDT];
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                oa[dt] = zero4();
+#pragma unroll
+                for (int kb = 0; kb < GG::KBM; ++kb)
+                    oa[dt] = mma(ld_frag<T>(ZvT + (size_t)(16 * dt + r) * GG::LDZ, 32 * kb, g), wf[kb], oa[dt]);
+            }
+            floatx4 hh[NT];
+#pragma unroll
+            for (int kt = 0; kt < NT; ++kt) {
+                hh[kt] = zero4();
+                if (kt <= w) {
+#pragma unroll
+                    for (int kb = 0; kb < GG::KBM; ++kb)
+                        hh[kt] = mma(ld_frag<T>(Etabh + (size_t)(16 * kt + r) * 2 * MP, 32 * kb, g), wf[kb],
+                                     hh[kt]);
+                    if (kt == w) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (4 * g + e > r) hh[kt][e] = 0.f;
+                    }
+                }
+            }
+#pragma unroll
+            for (int kb = 0; kb < GG::KBC; ++kb) {
+                if (2 * kb <= w) {
+                    const F hf = frag_from_acc<T>(hh[2 * kb], hh[2 * kb + 1]);
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt)
+                        oa[dt] = mma(ld_frag<T>(Vt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g), hf, oa[dt]);
+                }
+            }
+            if (j < c) {
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) st4<T>(ob + (size_t)(tok0 + j) * D + 16 * dt + 4 * g, oa[dt]);
+            }
+        }
+        __syncthreads();
+
+        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, ErevTh, c, w, g, r);
+        write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
+    }
+
+    // ---- final state (last segment): Z = conj(rho) Z'
+    if (seg == a.nseg - 1) {
+        const float* E1 = E32h + 2 * MP;
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = w + NW * o;
+            if (mt < NMT) {
+                const int m = 16 * mt + r;
+                const float c1 = E1[m], s1 = E1[MP + m];
+                const floatx4 cv = ld4f(E1 + 16 * mt + 4 * g), sv = ld4f(E1 + MP + 16 * mt + 4 * g);
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    if (a.sk_out && m < a.M) {
+                        const floatx4 re = Zk[o][0][dt], im = Zk[o][1][dt];
+                        st4f(a.sk_out + (((size_t)bh * 2 + 0) * a.M + m) * D + 16 * dt + 4 * g, c1 * re + s1 * im);
+                        st4f(a.sk_out + (((size_t)bh * 2 + 1) * a.M + m) * D + 16 * dt + 4 * g, c1 * im - s1 * re);
+                    }
+                    if (a.sv_out) {
+                        const floatx4 re = Zv[o][0][dt], im = Zv[o][1][dt];
+                        const floatx4 nr = cv * re + sv * im, ni = cv * im - sv * re;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int mv = 16 * mt + 4 * g + e;
+                            if (mv < a.M) {
+                                a.sv_out[(((size_t)bh * 2 + 0) * a.M + mv) * D + 16 * dt + r] = nr[e];
+                                a.sv_out[(((size_t)bh * 2 + 1) * a.M + mv) * D + 16 * dt + r] = ni[e];
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+}  // namespace bla

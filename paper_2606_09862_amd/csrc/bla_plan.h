@@ -1,0 +1,98 @@
+// Launch plan and kernel argument blocks shared by the host API and the kernels.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace bla {
+
+constexpr int kChunk = 64;      // tokens per chunk of the parallel form
+constexpr int kThreads = 256;   // 4 waves of 64 lanes per workgroup
+constexpr int kMaxHeadsPerTableLaunch = 64;
+
+// Sizes and workspace layout of one forward / step call.
+struct Plan {
+    int B, H, L, D, M, S;
+    int MP, SP;          // M padded to 16/32/64/128, S padded to 32/64/128/256
+    int C;               // chunk length
+    int bf16;            // 1 if q,k,v,o are bfloat16
+    int64_t t0;
+    float scale;
+    int nch;             // chunks per sequence
+    int nseg, cps;       // segments per sequence, chunks per segment
+    int cpb, nbs;        // chunks per summarised block, summarised blocks per sequence
+    size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
+    // workspace byte offsets
+    size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_AB32, off_theta,
+        off_rotblk, off_summ, off_carry, total;
+};
+
+struct TableArgs {
+    float* E32;     // [H][C+1][2MP]  cos | sin of m w j, j = 0..C
+    void* EbarT;    // [H][2MP][C]    cos(m w i) | -sin(m w i)       (operand type)
+    void* ErevT;    // [H][2MP][C]    cos(m w (C-i)) | sin(m w (C-i)) (operand type)
+    void* Etab;     // [H][C][2MP]    cos(m w i) | sin(m w i)        (operand type)
+    void* ABs;      // [SP][2MP]      scale * (A | B)                (operand type)
+    void* ABm;      // [2MP][SP]      (A | B) transposed             (operand type)
+    float* AB32;    // [SP][2MP]      A | B in float32
+    int* theta;     // [H][SP]        start-mask thresholds (INT32_MAX for padded slots)
+    float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
+    int M, S, MP, SP, C, Lblk, h0, nh, with_shared;
+    float scale;
+    double T[kMaxHeadsPerTableLaunch];  // clamped periods of heads h0..h0+nh-1
+};
+
+struct FwdArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    const float* sk_in;
+    const float* sv_in;
+    float* sk_out;
+    float* sv_out;
+    const float* E32;
+    const void* EbarT;
+    const void* ErevT;
+    const void* Etab;
+    const void* ABs;
+    const void* ABm;
+    const int* theta;
+    float* summ;
+    float* carry;
+    const float* rotblk;
+    int B, H, L, M;
+    int nch, nseg, cps, cpb, nbs;
+    long long t0;
+};
+
+struct StepArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    const int64_t* pos;
+    float* sk;
+    float* sv;
+    const float* E32;
+    const float* AB32;
+    const int* theta;
+    int B, H, M;
+    long long t0;
+    float scale;
+};
+
+// Launchers (defined in the .hip translation units).  They return a HIP error.
+hipError_t launch_tables(const TableArgs& a, int bf16, hipStream_t s);
+hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s);
+hipError_t launch_scan(const Plan& p, const FwdArgs& a, hipStream_t s);
+hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s);
+hipError_t launch_state_copy(const float* src, float* dst, size_t n, hipStream_t s);
+hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
+
+// Whether a forward kernel exists for (bf16, D, MP, SP); LDS bytes it needs.
+bool forward_supported(int bf16, int D, int MP, int SP);
+
+}  // namespace bla

@@ -1,0 +1,161 @@
+"""The C ABI on the host (no GPU needed): exports, shape rules, workspace sizes, and every
+argument error path, which must return before any kernel is launched."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2606_09862_amd as bla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bla.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bla.LIB_PATH):
+        from paper_2606_09862_amd import build
+        build.build()
+    return bla.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bla_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"bla_forward", "bla_step", "bla_workspace_size"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"libbla.so does not export {n}"
+
+
+def test_params_struct_layout():
+    # int32 x8, then int64 t0 (8-aligned), float, int32 -> 48 bytes as in bla.h
+    assert ctypes.sizeof(bla.Params) == 48
+    assert bla.Params.t0.offset == 32 and bla.Params.io_dtype.offset == 44
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.bla_status_string(s).decode().startswith(bla.STATUS[s])
+    assert lib.bla_status_string(99) == b"BLA_ERR_UNKNOWN"
+
+
+def P(**kw):
+    base = dict(B=2, H=2, L=100, d=64, M=16, S=16, dtype=None, t0=0, scale=0.0, chunk=0)
+    base.update(kw)
+    import torch
+    dt = torch.bfloat16 if base.pop("dtype") in (None, "bf16") else torch.float32
+    return bla.make_params(base["B"], base["H"], base["L"], base["d"], base["M"], base["S"], dt,
+                           base["t0"], base["scale"], base["chunk"])
+
+
+@pytest.mark.parametrize("kw,expect", [
+    ({}, OK),
+    (dict(d=32, M=16, S=16, dtype="f32"), OK),
+    (dict(d=128, M=128, S=128), OK),
+    (dict(M=64, S=127), OK),                 # S = 2M-1
+    (dict(M=1, S=1), OK),
+    (dict(M=128, S=255), OK),
+    (dict(d=48), UNSUPPORTED),
+    (dict(M=129), UNSUPPORTED),
+    (dict(M=16, S=33), UNSUPPORTED),        # S beyond 2 * padded M
+    (dict(S=257), UNSUPPORTED),
+    (dict(chunk=32), UNSUPPORTED),
+    (dict(d=128, M=128, S=128, dtype="f32"), UNSUPPORTED),  # float32 tiles exceed the LDS
+    (dict(M=0), INVALID),
+    (dict(S=0), INVALID),
+    (dict(L=-1), INVALID),
+    (dict(B=-1), INVALID),
+    (dict(t0=-5), INVALID),
+    (dict(scale=float("nan")), INVALID),
+])
+def test_supported(lib, kw, expect):
+    p = P(**kw)
+    assert bla.supported(p) == expect
+
+
+def test_dk_dv_mismatch_unsupported(lib):
+    p = P()
+    p.d_v = 32
+    assert bla.supported(p) == UNSUPPORTED
+    p = P()
+    p.io_dtype = 7
+    assert bla.supported(p) == INVALID
+
+
+def test_workspace_sizes(lib):
+    small = bla.workspace_size(P(B=64, H=4, L=512, d=64, M=32, S=32))
+    assert small > 0
+    assert bla.workspace_size(P(M=0)) == 0
+    assert bla.step_workspace_size(P(B=512, H=16, L=1, d=64, M=64, S=64)) > 0
+    # workloads that split sequences into segments need room for the block summaries
+    seg = bla.workspace_size(P(B=1, H=16, L=65536, d=128, M=128, S=128))
+    assert seg > 16 * 4 * 128 * 128 * 4
+
+
+def _fake(addr):
+    return ctypes.c_void_p(addr)
+
+
+def call_forward(lib, p, T=None, q=0x10000, k=0x20000, v=0x30000, o=0x40000, ski=None, svi=None,
+                 sko=None, svo=None, ws=0x100000, nbytes=1 << 40):
+    H = max(p.H, 1)
+    arr = (ctypes.c_double * H)(*([31.0] * H if T is None else T))
+    return lib.bla_forward(ctypes.byref(p), arr, _fake(q), _fake(k), _fake(v), _fake(ski), _fake(svi),
+                           _fake(o), _fake(sko), _fake(svo), _fake(ws), nbytes, None)
+
+
+@pytest.mark.parametrize("T", [[float("nan"), 31.0], [0.0, 31.0], [-3.0, 31.0], [float("inf"), 31.0],
+                               [1e10, 31.0]])
+def test_bad_periods(lib, T):
+    assert call_forward(lib, P(), T=T) == INVALID
+
+
+def test_pointer_errors(lib):
+    assert call_forward(lib, P(), q=0) == INVALID
+    assert call_forward(lib, P(), o=0) == INVALID
+    assert call_forward(lib, P(), v=0x30008) == INVALID            # misaligned
+    assert call_forward(lib, P(), ski=0x50004) == INVALID          # misaligned state
+    assert call_forward(lib, P(), ski=0x50000, sko=0x50000) == INVALID  # output aliases input
+    assert call_forward(lib, P(), ws=0) == WORKSPACE
+    assert call_forward(lib, P(), nbytes=16) == WORKSPACE
+    assert call_forward(lib, P(), ws=0x100004) == WORKSPACE        # misaligned workspace
+    assert lib.bla_forward(None, None, *([None] * 9), 0, None) == INVALID
+
+
+def test_empty_batch_is_a_noop(lib):
+    # B = 0: nothing to compute, null data pointers are fine, no workspace needed
+    p = P(B=0)
+    assert call_forward(lib, p, q=0, k=0, v=0, o=0, ws=0, nbytes=0) == OK
+
+
+def test_step_errors(lib):
+    p = P(L=1)
+    H = 2
+    arr = (ctypes.c_double * H)(31.0, 62.0)
+    args = [_fake(0x10000), _fake(0x20000), _fake(0x30000), None, _fake(0x40000), _fake(0x50000),
+            _fake(0x60000)]
+    assert lib.bla_step(ctypes.byref(p), arr, *args, _fake(0x100000), 16, None) == WORKSPACE
+    bad = list(args)
+    bad[3] = _fake(0x70004)   # pos not 8-byte aligned
+    assert lib.bla_step(ctypes.byref(p), arr, *bad, _fake(0x100000), 1 << 40, None) == INVALID
+    bad = list(args)
+    bad[4] = None             # state_k missing
+    assert lib.bla_step(ctypes.byref(p), arr, *bad, _fake(0x100000), 1 << 40, None) == INVALID
+    nan = (ctypes.c_double * H)(math.nan, 1.0)
+    assert lib.bla_step(ctypes.byref(p), nan, *args, _fake(0x100000), 1 << 40, None) == INVALID
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(bla, "LIB_PATH", str(tmp_path / "nope.so"))
+    monkeypatch.setattr(bla, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        bla.lib()

@@ -1,0 +1,211 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Bar (from the operator's specification): relative L2 error <= 1e-4 for float32
+inputs and <= 2e-2 for bfloat16 inputs, on the outputs and on the final states.
+A looser per-element check (max |err| <= 25 x bar x RMS) guards against errors
+confined to a few tokens that an L2 norm would dilute.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import bla_inputs as bi
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+TOL = {torch.float32: 1e-4, torch.bfloat16: 2e-2}
+
+
+def _bla():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    import paper_2606_09862_amd as bla
+    bla.lib()  # raises if the library is not built
+    return bla
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def relerr(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def assert_close(got, ref, tol, what):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite values"
+    e = relerr(got, ref)
+    rms = math.sqrt(float(np.mean(ref ** 2))) if ref.size else 0.0
+    emax = float(np.max(np.abs(got - ref))) if ref.size else 0.0
+    _say(f"  {what}: rel-L2 {e:.3e} (bar {tol:.0e}), max-abs {emax:.3e}, rms {rms:.3e}")
+    assert e <= tol, f"{what}: rel-L2 {e:.3e} > {tol:.0e}"
+    assert emax <= 25 * tol * max(rms, 1e-30), f"{what}: max-abs {emax:.3e}"
+
+
+def to_dev(x, dtype):
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to("cuda").to(dtype)
+
+
+def run_case(q, k, v, T, M, S, dtype, t0=0, sk=None, sv=None, literal=False, label=""):
+    """q,k,v float32 numpy holding dtype-representable values; returns errors dict."""
+    bla = _bla()
+    _say(f"case {label}: shape {q.shape} M={M} S={S} T={list(T)} t0={t0} dtype={dtype}")
+    tq, tk, tv = (to_dev(x, dtype) for x in (q, k, v))
+    tsk = None if sk is None else torch.from_numpy(np.ascontiguousarray(sk, np.float32)).cuda()
+    tsv = None if sv is None else torch.from_numpy(np.ascontiguousarray(sv, np.float32)).cuda()
+    o, ok, ov = bla.forward(tq, tk, tv, T, M, S, t0=t0, state_k=tsk, state_v=tsv)
+    torch.cuda.synchronize()
+    ref_o, ref_k, ref_v = oracle.forward(q, k, v, T, M, S, t0=t0,
+                                         state_k=None if sk is None else np.asarray(sk, np.float64),
+                                         state_v=None if sv is None else np.asarray(sv, np.float64),
+                                         literal=literal)
+    tol = TOL[dtype]
+    assert_close(o.float().cpu().numpy(), ref_o, tol, "O")
+    assert_close(ok.cpu().numpy(), ref_k, tol, "state_k")
+    assert_close(ov.cpu().numpy(), ref_v, tol, "state_v")
+    return o, ok, ov
+
+
+def gauss(seed, B, H, L, d, dtype):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(3):
+        x = (rng.standard_normal((B, H, L, d)) / math.sqrt(d)).astype(np.float32)
+        out.append(bi.round_bf16(x) if dtype == torch.bfloat16 else x)
+    return out
+
+
+# ------------------------------------------------------------------ the tiny workload (id 1)
+def test_workload1_tiny_fp32():
+    w = bi.WORKLOADS[1]
+    q, k, v = bi.generate(1)
+    run_case(q, k, v, bi.periods(w.M, w.H), w.M, w.S, torch.float32, literal=True, label="workload 1")
+
+
+# ------------------------------------------------------------------ small shapes, ragged, edge cases
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,H,L,d,M,S,T", [
+    (2, 3, 100, 32, 16, 16, (31.0, 62.0, 40.5)),     # ragged last chunk, non-integer T
+    (1, 2, 64, 64, 8, 15, (15.0, 30.0)),              # exactly one chunk, S = 2M-1
+    (2, 2, 7, 32, 5, 9, (9.0, 9.0)),                  # L < chunk, T = S = 2M-1 (SWA limit)
+    (1, 2, 200, 64, 24, 40, (47.0, 94.0)),            # padded modes (24 -> 32) and slots (40 -> 64)
+    (3, 1, 130, 32, 32, 63, (3.0,)),                  # T below 2M-1 is clamped
+    (1, 1, 1, 64, 4, 4, (7.0,)),                      # a single token
+])
+def test_small_shapes(dtype, B, H, L, d, M, S, T):
+    q, k, v = gauss(L * 7 + M, B, H, L, d, dtype)
+    run_case(q, k, v, T, M, S, dtype, label=f"small {B}x{H}x{L}x{d}")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_state_in_and_offset(dtype):
+    """Continue a sequence: state_in from the oracle, t0 > 0 (start mask at absolute positions)."""
+    B, H, L, d, M, S, T = 2, 2, 150, 64, 16, 20, (31.0, 77.25)
+    q, k, v = gauss(11, B, H, 2 * L, d, dtype)
+    _, sk, sv = oracle.forward(q[:, :, :L], k[:, :, :L], v[:, :, :L], T, M, S)
+    run_case(q[:, :, L:], k[:, :, L:], v[:, :, L:], T, M, S, dtype, t0=L, sk=sk, sv=sv,
+             label="continuation")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_many_segments(dtype):
+    """Few sequences and many chunks: the sequence is split into segments whose entering
+    states come from per-block summaries and the scan; ragged tail included."""
+    B, H, L, d, M, S, T = 1, 2, 64 * 37 + 5, 32, 16, 31, (31.0, 62.0)
+    q, k, v = gauss(12, B, H, L, d, dtype)
+    run_case(q, k, v, T, M, S, dtype, label="segments")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_segments_with_state_in(dtype):
+    B, H, L, d, M, S, T = 1, 1, 64 * 20, 64, 16, 16, (50.0,)
+    q, k, v = gauss(13, B, H, L, d, dtype)
+    rng = np.random.default_rng(14)
+    sk = rng.standard_normal((B, H, 2, M, d)).astype(np.float32)
+    sv = rng.standard_normal((B, H, 2, M, d)).astype(np.float32)
+    sk[:, :, 1, 0] = 0.0
+    sv[:, :, 1, 0] = 0.0
+    run_case(q, k, v, T, M, S, dtype, t0=1000, sk=sk, sv=sv, label="segments+state_in")
+
+
+def test_empty_and_degenerate():
+    bla = _bla()
+    M, d = 8, 32
+    # L = 0 passes the state through
+    sk = torch.randn(2, 3, 2, M, d, device="cuda")
+    sv = torch.randn(2, 3, 2, M, d, device="cuda")
+    z = torch.zeros(2, 3, 0, d, device="cuda")
+    o, ok, ov = bla.forward(z, z, z, [15.0] * 3, M, 15, state_k=sk, state_v=sv)
+    torch.cuda.synchronize()
+    assert o.shape == (2, 3, 0, d)
+    assert torch.equal(ok, sk) and torch.equal(ov, sv)
+    # L = 0 without a state gives zeros
+    _, ok, ov = bla.forward(z, z, z, [15.0] * 3, M, 15)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(ok) == 0 and torch.count_nonzero(ov) == 0
+    # B = 0: nothing to do
+    e = torch.zeros(0, 3, 10, d, device="cuda")
+    o, _, _ = bla.forward(e, e, e, [15.0] * 3, M, 15)
+    assert o.shape == (0, 3, 10, d)
+
+
+def test_deterministic():
+    """No atomics in any reduction: two runs give bitwise-identical results."""
+    bla = _bla()
+    q, k, v = gauss(15, 2, 4, 64 * 9 + 3, 64, torch.bfloat16)
+    tq, tk, tv = (to_dev(x, torch.bfloat16) for x in (q, k, v))
+    a = bla.forward(tq, tk, tv, [63.0, 126.0] * 2, 32, 32)
+    b = bla.forward(tq, tk, tv, [63.0, 126.0] * 2, 32, 32)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+# ------------------------------------------------------------------ the full workloads
+def test_workload2_recall_bf16():
+    w = bi.WORKLOADS[2]
+    q, k, v = bi.generate(2)
+    run_case(q, k, v, bi.periods(w.M, w.H), w.M, w.S, torch.bfloat16, label="workload 2")
+
+
+def test_workload3_lm_layer_sampled_rows():
+    """Full LM-layer workload on the GPU (the benchmark's launch configuration); the oracle
+    checks every head of two batch rows, first and last."""
+    bla = _bla()
+    w = bi.WORKLOADS[3]
+    T = bi.periods(w.M, w.H)
+    q, k, v = bi.generate(3)
+    _say(f"workload 3 full size {q.shape}")
+    tq, tk, tv = (to_dev(x, torch.bfloat16) for x in (q, k, v))
+    o, sk, sv = bla.forward(tq, tk, tv, T, w.M, w.S)
+    torch.cuda.synchronize()
+    for b in (0, w.B - 1):
+        ref_o, ref_k, ref_v = oracle.forward(q[b:b + 1], k[b:b + 1], v[b:b + 1], T, w.M, w.S)
+        assert_close(o[b:b + 1].float().cpu().numpy(), ref_o, 2e-2, f"O row {b}")
+        assert_close(sk[b:b + 1].cpu().numpy(), ref_k, 2e-2, f"state_k row {b}")
+        assert_close(sv[b:b + 1].cpu().numpy(), ref_v, 2e-2, f"state_v row {b}")
+
+
+def test_workload4_long_context():
+    """B=1, H=16, L=65536, d=M=S=128: every head against the oracle (threads over heads)."""
+    bla = _bla()
+    w = bi.WORKLOADS[4]
+    T = bi.periods(w.M, w.H)
+    q, k, v = bi.generate(4)
+    _say(f"workload 4 full size {q.shape}")
+    tq, tk, tv = (to_dev(x, torch.bfloat16) for x in (q, k, v))
+    o, sk, sv = bla.forward(tq, tk, tv, T, w.M, w.S)
+    torch.cuda.synchronize()
+    ref_o, ref_k, ref_v = oracle.forward(q, k, v, T, w.M, w.S)
+    assert_close(o.float().cpu().numpy(), ref_o, 2e-2, "O")
+    assert_close(sk.cpu().numpy(), ref_k, 2e-2, "state_k")
+    assert_close(sv.cpu().numpy(), ref_v, 2e-2, "state_v")
