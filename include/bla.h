@@ -96,6 +96,20 @@ bla_status bla_forward(const bla_params* p, const double* T, const void* q, cons
                        float* state_k_out, float* state_v_out, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/*
+ * bla_forward with phase timing, for measurement tools: events[0..4] are
+ * hipEvent_t handles created by the caller (any entry may be NULL; the array may
+ * be NULL) and are recorded on `stream` before the table kernel, after it, after
+ * the block-summary kernel, after the summary scan, and after the chunked forward
+ * kernel (a phase that does not run for this shape still gets its event).  The
+ * computation and every other convention are exactly those of bla_forward;
+ * BLA_ERR_HIP is also returned if an event cannot be recorded.
+ */
+bla_status bla_forward_timed(const bla_params* p, const double* T, const void* q, const void* k,
+                             const void* v, const float* state_k_in, const float* state_v_in, void* o,
+                             float* state_k_out, float* state_v_out, void* workspace,
+                             size_t workspace_bytes, void* stream, void* const* events);
+
 /* Bytes of device workspace bla_step needs for *p (L is ignored). */
 size_t bla_step_workspace_size(const bla_params* p);
 

@@ -214,10 +214,10 @@ size_t bla_step_workspace_size(const bla_params* p)
     return pl.total;
 }
 
-bla_status bla_forward(const bla_params* p, const double* T, const void* q, const void* k,
-                       const void* v, const float* state_k_in, const float* state_v_in, void* o,
-                       float* state_k_out, float* state_v_out, void* workspace,
-                       size_t workspace_bytes, void* stream)
+static bla_status forward_impl(const bla_params* p, const double* T, const void* q, const void* k,
+                               const void* v, const float* state_k_in, const float* state_v_in,
+                               void* o, float* state_k_out, float* state_v_out, void* workspace,
+                               size_t workspace_bytes, void* stream, void* const* events)
 {
     bla_status st = check_shape(p, false);
     if (st != BLA_OK) return st;
@@ -245,7 +245,12 @@ bla_status bla_forward(const bla_params* p, const double* T, const void* q, cons
         if (launch_state_copy(state_v_in, state_v_out, n_state, s) != hipSuccess) return BLA_ERR_HIP;
         return BLA_OK;
     }
+    auto mark = [&](int i) -> bool {
+        return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
+    };
+    if (!mark(0)) return BLA_ERR_HIP;
     if ((st = build_tables(pl, T, ws, s)) != BLA_OK) return st;
+    if (!mark(1)) return BLA_ERR_HIP;
 
     FwdArgs a;
     memset(&a, 0, sizeof(a));
@@ -277,12 +282,31 @@ bla_status bla_forward(const bla_params* p, const double* T, const void* q, cons
     a.cpb = pl.cpb;
     a.nbs = pl.nbs;
     a.t0 = pl.t0;
-    if (pl.nseg > 1) {
-        if (launch_summary(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
-        if (launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
-    }
+    if (pl.nseg > 1 && launch_summary(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    if (!mark(2)) return BLA_ERR_HIP;
+    if (pl.nseg > 1 && launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    if (!mark(3)) return BLA_ERR_HIP;
     if (launch_forward(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    if (!mark(4)) return BLA_ERR_HIP;
     return BLA_OK;
+}
+
+bla_status bla_forward(const bla_params* p, const double* T, const void* q, const void* k,
+                       const void* v, const float* state_k_in, const float* state_v_in, void* o,
+                       float* state_k_out, float* state_v_out, void* workspace,
+                       size_t workspace_bytes, void* stream)
+{
+    return forward_impl(p, T, q, k, v, state_k_in, state_v_in, o, state_k_out, state_v_out, workspace,
+                        workspace_bytes, stream, nullptr);
+}
+
+bla_status bla_forward_timed(const bla_params* p, const double* T, const void* q, const void* k,
+                             const void* v, const float* state_k_in, const float* state_v_in, void* o,
+                             float* state_k_out, float* state_v_out, void* workspace,
+                             size_t workspace_bytes, void* stream, void* const* events)
+{
+    return forward_impl(p, T, q, k, v, state_k_in, state_v_in, o, state_k_out, state_v_out, workspace,
+                        workspace_bytes, stream, events);
 }
 
 bla_status bla_step(const bla_params* p, const double* T, const void* q, const void* k,
