@@ -16,89 +16,84 @@ __device__ __forceinline__ double mode_phase(long long mj, double T)
     return 2.0 * M_PI * fmod((double)mj, T) / T;
 }
 
+// One thread per angle: a (head, j, m) phase with j = 0..C for the per-head tables,
+// an (s, m) phase for the slot matrices, plus the per-head mask thresholds and
+// block rotations.  Each sincos result is written to every table that uses it.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
 {
-    const int MP2 = 2 * a.MP;
-    const int C = a.C;
-    if ((int)blockIdx.x < a.nh) {
-        const int h = a.h0 + blockIdx.x;
-        const double Tp = a.T[blockIdx.x];
-        // E32: (C+1) x 2MP
+    const int MP = a.MP, MP2 = 2 * MP, C = a.C;
+    const long long n_head = (long long)a.nh * (C + 1) * MP;   // (h, j, m)
+    const long long n_misc = (long long)a.nh * (a.SP + MP);     // theta, rotblk
+    const long long n_ab = a.with_shared ? (long long)a.SP * MP : 0;
+    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid < n_head) {
+        const int hl = (int)(gid / ((C + 1) * MP));
+        const int rem = (int)(gid % ((C + 1) * MP));
+        const int j = rem / MP, m = rem % MP, h = a.h0 + hl;
+        double sn = 0.0, cs = 0.0;
+        if (m < a.M) sincos(mode_phase((long long)m * j, a.T[hl]), &sn, &cs);
         float* E32 = a.E32 + (size_t)h * (C + 1) * MP2;
-        for (int idx = threadIdx.x; idx < (C + 1) * MP2; idx += blockDim.x) {
-            int j = idx / MP2, col = idx % MP2, m = col % a.MP;
-            float val = 0.f;
-            if (m < a.M) {
-                double sn, cs;
-                sincos(mode_phase((long long)m * j, Tp), &sn, &cs);
-                val = (float)(col < a.MP ? cs : sn);
-            }
-            E32[idx] = val;
-        }
+        E32[(size_t)j * MP2 + m] = (float)cs;
+        E32[(size_t)j * MP2 + MP + m] = (float)sn;
         T* EbarT = (T*)a.EbarT + (size_t)h * MP2 * C;
         T* ErevT = (T*)a.ErevT + (size_t)h * MP2 * C;
-        for (int idx = threadIdx.x; idx < MP2 * C; idx += blockDim.x) {
-            int row = idx / C, i = idx % C, m = row % a.MP;
-            float eb = 0.f, er = 0.f;
-            if (m < a.M) {
-                double sn, cs, sr, cr;
-                sincos(mode_phase((long long)m * i, Tp), &sn, &cs);
-                sincos(mode_phase((long long)m * (C - i), Tp), &sr, &cr);
-                eb = (float)(row < a.MP ? cs : -sn);
-                er = (float)(row < a.MP ? cr : sr);
-            }
-            EbarT[idx] = (T)eb;
-            ErevT[idx] = (T)er;
-        }
         T* Etab = (T*)a.Etab + (size_t)h * C * MP2;
-        for (int idx = threadIdx.x; idx < C * MP2; idx += blockDim.x) {
-            int i = idx / MP2, col = idx % MP2, m = col % a.MP;
-            float val = 0.f;
-            if (m < a.M) {
-                double sn, cs;
-                sincos(mode_phase((long long)m * i, Tp), &sn, &cs);
-                val = (float)(col < a.MP ? cs : sn);
-            }
-            Etab[idx] = (T)val;
+        if (j < C) {
+            EbarT[(size_t)m * C + j] = (T)(float)cs;           // conj(rho^j)
+            EbarT[(size_t)(MP + m) * C + j] = (T)(float)(-sn);
+            Etab[(size_t)j * MP2 + m] = (T)(float)cs;
+            Etab[(size_t)j * MP2 + MP + m] = (T)(float)sn;
         }
-        for (int s = threadIdx.x; s < a.SP; s += blockDim.x)
-            a.theta[(size_t)h * a.SP + s] =
-                s < a.S ? (int)rint((double)s * Tp / (double)a.S) : INT32_MAX;
-        for (int col = threadIdx.x; col < MP2; col += blockDim.x) {
-            int m = col % a.MP;
-            float val = 0.f;
-            if (m < a.M) {
-                double sn, cs;
-                sincos(mode_phase((long long)m * a.Lblk, Tp), &sn, &cs);
-                val = (float)(col < a.MP ? cs : sn);
-            }
-            a.rotblk[(size_t)h * MP2 + col] = val;
+        if (j >= 1) {                                          // rho^{C-i} at i = C - j
+            ErevT[(size_t)m * C + (C - j)] = (T)(float)cs;
+            ErevT[(size_t)(MP + m) * C + (C - j)] = (T)(float)sn;
         }
-    } else if (a.with_shared) {
+        return;
+    }
+    if (gid < n_head + n_misc) {
+        const long long e = gid - n_head;
+        const int hl = (int)(e / (a.SP + MP)), k = (int)(e % (a.SP + MP)), h = a.h0 + hl;
+        const double Tp = a.T[hl];
+        if (k < a.SP) {
+            a.theta[(size_t)h * a.SP + k] = k < a.S ? (int)rint((double)k * Tp / (double)a.S) : INT32_MAX;
+        } else {
+            const int m = k - a.SP;
+            double sn = 0.0, cs = 0.0;
+            if (m < a.M) sincos(mode_phase((long long)m * a.Lblk, Tp), &sn, &cs);
+            a.rotblk[(size_t)h * MP2 + m] = (float)cs;
+            a.rotblk[(size_t)h * MP2 + MP + m] = (float)sn;
+        }
+        return;
+    }
+    if (gid < n_head + n_misc + n_ab) {
         // Interpolation matrices (Eq. translated at tau_s = s T / S): the phase
         // m w tau_s = 2 pi m s / S does not depend on the head's period.
-        const double inv = 1.0 / (2.0 * a.M - 1.0);
-        for (int idx = threadIdx.x; idx < a.SP * MP2; idx += blockDim.x) {
-            int s = idx / MP2, col = idx % MP2, m = col % a.MP;
-            float val = 0.f;
-            if (s < a.S && m < a.M) {
-                double cm = (m == 0 ? 1.0 : 2.0) * inv;
-                double ph = 2.0 * M_PI * (double)(((long long)m * s) % a.S) / (double)a.S;
-                double sn, cs;
-                sincos(ph, &sn, &cs);
-                val = (float)(cm * (col < a.MP ? cs : sn));
-            }
-            a.AB32[idx] = val;
-            ((T*)a.ABs)[idx] = (T)(val * a.scale);
-            ((T*)a.ABm)[(size_t)col * a.SP + s] = (T)val;
+        const long long e = gid - n_head - n_misc;
+        const int s = (int)(e / MP), m = (int)(e % MP);
+        float ca = 0.f, sa = 0.f;
+        if (s < a.S && m < a.M) {
+            const double cm = (m == 0 ? 1.0 : 2.0) / (2.0 * a.M - 1.0);
+            const double ph = 2.0 * M_PI * (double)(((long long)m * s) % a.S) / (double)a.S;
+            double sn, cs;
+            sincos(ph, &sn, &cs);
+            ca = (float)(cm * cs);
+            sa = (float)(cm * sn);
         }
+        a.AB32[(size_t)s * MP2 + m] = ca;
+        a.AB32[(size_t)s * MP2 + MP + m] = sa;
+        ((T*)a.ABs)[(size_t)s * MP2 + m] = (T)(ca * a.scale);
+        ((T*)a.ABs)[(size_t)s * MP2 + MP + m] = (T)(sa * a.scale);
+        ((T*)a.ABm)[(size_t)m * a.SP + s] = (T)ca;
+        ((T*)a.ABm)[(size_t)(MP + m) * a.SP + s] = (T)sa;
     }
 }
 
 hipError_t launch_tables(const TableArgs& a, int is_bf16, hipStream_t s)
 {
-    dim3 grid(a.nh + (a.with_shared ? 1 : 0));
+    const long long n = (long long)a.nh * (a.C + 1) * a.MP + (long long)a.nh * (a.SP + a.MP) +
+                        (a.with_shared ? (long long)a.SP * a.MP : 0);
+    dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
     if (is_bf16)
         hipLaunchKernelGGL(tables_kernel<bf16>, grid, dim3(kThreads), 0, s, a);
     else

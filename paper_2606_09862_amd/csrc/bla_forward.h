@@ -22,6 +22,13 @@
 // wave's own mode tiles lives in registers for the whole segment; its bf16 copy
 // of Z'_v goes through LDS for (7).
 //
+// Data movement: the next chunk's Q, K, V are loaded into registers while the
+// current chunk computes, and written to LDS (Q row-major, K and V transposed)
+// at the top of the next iteration.  The head's tables (slot matrices, phase
+// tables) are copied into LDS once per workgroup when they fit next to the
+// per-chunk tiles; the wave's own rows of conj(E) and rho^{C-i} stay in
+// registers for the whole segment.
+//
 // A sequence is split into nseg segments processed by separate workgroups.  The
 // state entering segment g >= 1 comes from a scan over per-block summaries
 // (summary_kernel: step 10 alone, from a zero state) -- the recurrence is
@@ -35,6 +42,8 @@
 
 namespace bla {
 
+constexpr size_t kMaxLds = 160 * 1024;
+
 template <typename T, int D, int MP> struct Geo {
     static constexpr int C = kChunk;
     static constexpr int NT = C / 16;           // token tiles per chunk
@@ -47,8 +56,15 @@ template <typename T, int D, int MP> struct Geo {
     static constexpr int OWN = (NMT + NW - 1) / NW;  // mode tiles owned per wave
     static constexpr int PAD = 16 / (int)sizeof(T);  // 16-byte row padding in LDS
     static constexpr int LDK = C + PAD;         // Kt, Vt: [D][LDK]
+    static constexpr int LDQ = D + PAD;         // Qs: [C][LDQ]
     static constexpr int LDZ = 2 * MP + PAD;    // ZvT: [D][LDZ]
     static constexpr size_t KT_ELEMS = (size_t)D * LDK;
+    static constexpr size_t Q_ELEMS = (size_t)C * LDQ;
+    // staging units: Q rows in pieces of 8 elements, K/V in 4-token x 8-element blocks
+    static constexpr int QU = C * D / 8;
+    static constexpr int KVU = 2 * (C / 4) * (D / 8);
+    static constexpr int QPT = (QU + kThreads - 1) / kThreads;
+    static constexpr int KVPT = (KVU + kThreads - 1) / kThreads;
     static_assert(NT == NW, "one token tile per wave");
     static_assert(D % 32 == 0 && MP % 16 == 0, "tile shapes");
 };
@@ -57,70 +73,155 @@ template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
     using G = Geo<T, D, MP>;
     static constexpr int NST = SP / 16;
     static constexpr int KBS = SP / 32;
-    static constexpr int LDG = G::C + G::PAD;   // GT: [C tokens][LDG]
-    static constexpr int LDU = 2 * MP + G::PAD; // UT: [C tokens][LDU]
-    static constexpr size_t LDS_ELEMS =
-        2 * G::KT_ELEMS + (size_t)G::C * LDG + (size_t)G::C * LDU + (size_t)D * G::LDZ;
-    static constexpr size_t LDS_BYTES = LDS_ELEMS * sizeof(T);
+    static constexpr int LDG = G::C + G::PAD;    // GT:   [C tokens][LDG]
+    static constexpr int LDU = 2 * MP + G::PAD;  // UT:   [C tokens][LDU]
+    static constexpr int LDAS = 2 * MP + G::PAD; // ABs:  [SP][LDAS]
+    static constexpr int LDAM = SP + G::PAD;     // ABm:  [2MP][LDAM]
+    static constexpr int LDE = 2 * MP + G::PAD;  // Etab: [C][LDE]
+    static constexpr int LDE32 = 2 * MP + 4;     // E32:  [C+1][LDE32] floats
+    // Qs (read in phase A) and UT (written after the next barrier) share one buffer.
+    static constexpr int LDQU = LDU > G::LDQ ? LDU : G::LDQ;
+    static constexpr size_t BASE_ELEMS = 2 * G::KT_ELEMS + (size_t)G::C * LDQU + (size_t)G::C * LDG +
+                                         (size_t)D * G::LDZ;
+    static constexpr size_t TAB_ELEMS = (size_t)SP * LDAS + (size_t)2 * MP * LDAM + (size_t)G::C * LDE;
+    static constexpr size_t E32_FLOATS = (size_t)(G::C + 1) * LDE32;
+    static constexpr size_t BASE_BYTES = BASE_ELEMS * sizeof(T);
+    static constexpr size_t FULL_BYTES = BASE_BYTES + TAB_ELEMS * sizeof(T) + E32_FLOATS * 4;
+    static constexpr bool TL = FULL_BYTES <= kMaxLds;  // tables live in LDS
+    static constexpr size_t LDS_BYTES = TL ? FULL_BYTES : BASE_BYTES;
     static_assert(SP % 32 == 0, "slot padding");
 };
 
-constexpr size_t kMaxLds = 160 * 1024;
-
 // The wave's fp32 state tiles: [owned mode tile][Re, Im][head-dim tile].
 template <typename T, int D, int MP> using StateTiles = floatx4[Geo<T, D, MP>::OWN][2][D / 16];
+// Per-wave register copies of table rows: [owned mode tile][Re, Im][reduction block].
+template <typename T, int D, int MP>
+using OwnFrags = typename Frag<T>::type[Geo<T, D, MP>::OWN][2][kChunk / 32];
 
 // ---------------------------------------------------------------------------------
-// Stage one chunk of K and V transposed into LDS: Kt[d][i], Vt[d][i] (zero past c).
-template <typename T, int D, int MP>
-__device__ __forceinline__ void stage_kv(T* Kt, T* Vt, const T* kc, const T* vc, int c, int tid)
+// Chunk staging: global -> registers (issued a chunk ahead) -> LDS.
+template <typename T, int D, int MP> struct Stage {
+    using GG = Geo<T, D, MP>;
+    using H = typename Frag<T>::half;
+    H q[GG::QPT][2];
+    H kv[GG::KVPT][4][2];
+};
+
+// WQ: also stage the query rows.  c: valid tokens of the chunk (zero-filled past c).
+template <typename T, int D, int MP, bool WQ>
+__device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, const T* kc, const T* vc,
+                                           int c, int tid)
 {
     using GG = Geo<T, D, MP>;
     constexpr int DO = D / 8;
-    constexpr int UNITS = (GG::C / 4) * DO;
 #pragma unroll
-    for (int u0 = 0; u0 < 2 * UNITS; u0 += kThreads) {
-        const int u = u0 + tid;
-        if (u < 2 * UNITS) {
-            const int which = u / UNITS, uu = u % UNITS, tq = uu / DO, dq = uu % DO;
-            const T* src = (which ? vc : kc) + (size_t)(4 * tq) * D + 8 * dq;
-            T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
-            typename Frag<T>::half lo[4], hi[4];
+    for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
+        const int u = tid + i * kThreads;
+        const int t = u / DO, dq = u % DO;
+        if (u < GG::QU && t < c) {
+            st.q[i][0] = ld4<T>(qc + (size_t)t * D + 8 * dq);
+            st.q[i][1] = ld4<T>(qc + (size_t)t * D + 8 * dq + 4);
+        } else {
+            st.q[i][0] = st.q[i][1] = zero_half<T>();
+        }
+    }
+    constexpr int UNITS = GG::KVU / 2;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                if (4 * tq + t < c) {
-                    lo[t] = ld4<T>(src + (size_t)t * D);
-                    hi[t] = ld4<T>(src + (size_t)t * D + 4);
-                } else {
-                    lo[t] = zero_half<T>();
-                    hi[t] = zero_half<T>();
-                }
-            }
+    for (int i = 0; i < GG::KVPT; ++i) {
+        const int u = tid + i * kThreads;
+        const int which = u / UNITS, uu = u % UNITS, tq = uu / DO, dq = uu % DO;
+        const T* src = (which ? vc : kc) + (size_t)(4 * tq) * D + 8 * dq;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                typename Frag<T>::half a{lo[0][e], lo[1][e], lo[2][e], lo[3][e]};
-                typename Frag<T>::half b{hi[0][e], hi[1][e], hi[2][e], hi[3][e]};
-                *reinterpret_cast<typename Frag<T>::half*>(dst + e * GG::LDK) = a;
-                *reinterpret_cast<typename Frag<T>::half*>(dst + (e + 4) * GG::LDK) = b;
+        for (int t = 0; t < 4; ++t) {
+            if (u < GG::KVU && 4 * tq + t < c) {
+                st.kv[i][t][0] = ld4<T>(src + (size_t)t * D);
+                st.kv[i][t][1] = ld4<T>(src + (size_t)t * D + 4);
+            } else {
+                st.kv[i][t][0] = st.kv[i][t][1] = zero_half<T>();
             }
         }
     }
 }
 
+template <typename T, int D, int MP, bool WQ>
+__device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T* Kt, T* Vt, int tid)
+{
+    using GG = Geo<T, D, MP>;
+    using H = typename Frag<T>::half;
+    constexpr int DO = D / 8;
+#pragma unroll
+    for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
+        const int u = tid + i * kThreads;
+        if (u < GG::QU) {
+            const int t = u / DO, dq = u % DO;
+            *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq) = st.q[i][0];
+            *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq + 4) = st.q[i][1];
+        }
+    }
+    constexpr int UNITS = GG::KVU / 2;
+#pragma unroll
+    for (int i = 0; i < GG::KVPT; ++i) {
+        const int u = tid + i * kThreads;
+        if (u < GG::KVU) {
+            const int which = u / UNITS, uu = u % UNITS, tq = uu / DO, dq = uu % DO;
+            T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                H a{st.kv[i][0][0][e], st.kv[i][1][0][e], st.kv[i][2][0][e], st.kv[i][3][0][e]};
+                H b{st.kv[i][0][1][e], st.kv[i][1][1][e], st.kv[i][2][1][e], st.kv[i][3][1][e]};
+                *reinterpret_cast<H*>(dst + e * GG::LDK) = a;
+                *reinterpret_cast<H*>(dst + (e + 4) * GG::LDK) = b;
+            }
+        }
+    }
+}
+
+// Copy rows x cols elements (cols * sizeof(E) a multiple of 16 bytes) in 16-byte pieces.
+template <typename E>
+__device__ __forceinline__ void copy_rows(E* dst, int dstride, const E* src, int sstride, int rows,
+                                          int cols, int tid)
+{
+    constexpr int PER = 16 / sizeof(E);
+    const int pieces = cols / PER;
+    for (int u = tid; u < rows * pieces; u += kThreads) {
+        const int rr = u / pieces, cc = (u % pieces) * PER;
+        *reinterpret_cast<intx4*>(dst + (size_t)rr * dstride + cc) =
+            *reinterpret_cast<const intx4*>(src + (size_t)rr * sstride + cc);
+    }
+}
+
 // Fragment of rho^{c-i} (i < c, zero past c) for a ragged last chunk, built from E32.
 template <typename T, int MP>
-__device__ __forceinline__ typename Frag<T>::type erev_frag(const float* E32h, int c, int p, int mt,
-                                                            int kb, int g, int r)
+__device__ __forceinline__ typename Frag<T>::type erev_frag(const float* E32, int ldE, int c, int p,
+                                                            int mt, int kb, int g, int r)
 {
     typename Frag<T>::type f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int i = 32 * kb + 16 * (e / 4) + 4 * g + (e % 4);
         float val = 0.f;
-        if (i < c) val = E32h[(size_t)(c - i) * 2 * MP + p * MP + 16 * mt + r];
+        if (i < c) val = E32[(size_t)(c - i) * ldE + p * MP + 16 * mt + r];
         f[e] = (T)val;
     }
     return f;
+}
+
+// Register rows of a [2MP][C] table for the wave's own mode tiles.
+template <typename T, int D, int MP>
+__device__ __forceinline__ void load_own_frags(OwnFrags<T, D, MP>& f, const T* tab, int w, int g, int r)
+{
+    using GG = Geo<T, D, MP>;
+#pragma unroll
+    for (int o = 0; o < GG::OWN; ++o) {
+        const int mt = w + GG::NW * o;
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int kb = 0; kb < GG::KBC; ++kb)
+                f[o][p][kb] = mt < GG::NMT ? ld_frag<T>(tab + (size_t)(16 * (p * GG::NMT + mt) + r) * GG::C,
+                                                        32 * kb, g)
+                                           : zero_frag<T>();
+    }
 }
 
 // Write the bf16/fp32 copy of Z'_v as ZvT[d][Re m | Im m] with the Im part negated
@@ -143,14 +244,15 @@ __device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP>& Zv
 }
 
 // Step 10: Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i] on the wave's own mode tiles.
+// E32 / ldE: phase table (rows 0..C); erf: rho^{C-i} fragments for full chunks.
 template <typename T, int D, int MP>
 __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTiles<T, D, MP>& Zv,
-                                              const T* Kt, const T* Vt, const float* E32h,
-                                              const T* ErevTh, int c, int w, int g, int r)
+                                              const T* Kt, const T* Vt, const float* E32, int ldE,
+                                              const OwnFrags<T, D, MP>& erf, int c, int w, int g, int r)
 {
     using GG = Geo<T, D, MP>;
     using F = typename Frag<T>::type;
-    const float* Ec = E32h + (size_t)c * 2 * MP;
+    const float* Ec = E32 + (size_t)c * ldE;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o) {
         const int mt = w + GG::NW * o;
@@ -185,10 +287,7 @@ __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTil
             if (mt < GG::NMT) {
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
-                    F ef = (c == GG::C)
-                               ? ld_frag<T>(ErevTh + (size_t)(16 * (p * GG::NMT + mt) + r) * GG::C,
-                                            32 * kb, g)
-                               : erev_frag<T, MP>(E32h, c, p, mt, kb, g, r);
+                    const F ef = (c == GG::C) ? erf[o][p][kb] : erev_frag<T, MP>(E32, ldE, c, p, mt, kb, g, r);
 #pragma unroll
                     for (int dt = 0; dt < GG::NDT; ++dt) {
                         Zk[o][p][dt] = mma(kf[dt], ef, Zk[o][p][dt]);
@@ -211,12 +310,13 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
     T* Vt = lds + GG::KT_ELEMS;
     const int tid = threadIdx.x, w = tid >> 6, g = (tid & 63) >> 4, r = tid & 15;
     const int blk = blockIdx.x % a.nbs, bh = blockIdx.x / a.nbs, h = bh % a.H;
-    const T* kb = (const T*)a.k + (size_t)bh * a.L * D;
-    const T* vb = (const T*)a.v + (size_t)bh * a.L * D;
+    const T* kbase = (const T*)a.k + (size_t)bh * a.L * D;
+    const T* vbase = (const T*)a.v + (size_t)bh * a.L * D;
     const float* E32h = a.E32 + (size_t)h * (GG::C + 1) * 2 * MP;
-    const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C;
 
-    floatx4 Zk[GG::OWN][2][GG::NDT], Zv[GG::OWN][2][GG::NDT];
+    OwnFrags<T, D, MP> erf;
+    load_own_frags<T, D, MP>(erf, (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C, w, g, r);
+    StateTiles<T, D, MP> Zk, Zv;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o)
 #pragma unroll
@@ -224,12 +324,18 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
 #pragma unroll
             for (int dt = 0; dt < GG::NDT; ++dt) Zk[o][p][dt] = Zv[o][p][dt] = zero4();
 
+    Stage<T, D, MP> st;
+    const size_t first = (size_t)blk * a.cpb * GG::C;
+    stage_load<T, D, MP, false>(st, nullptr, kbase + first * D, vbase + first * D, GG::C, tid);
     for (int n = 0; n < a.cpb; ++n) {
-        const size_t tok0 = (size_t)(blk * a.cpb + n) * GG::C;
         __syncthreads();
-        stage_kv<T, D, MP>(Kt, Vt, kb + tok0 * D, vb + tok0 * D, GG::C, tid);
+        stage_store<T, D, MP, false>(st, nullptr, Kt, Vt, tid);
+        if (n + 1 < a.cpb) {
+            const size_t tok = first + (size_t)(n + 1) * GG::C;
+            stage_load<T, D, MP, false>(st, nullptr, kbase + tok * D, vbase + tok * D, GG::C, tid);
+        }
         __syncthreads();
-        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, ErevTh, GG::C, w, g, r);
+        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, 2 * MP, erf, GG::C, w, g, r);
     }
     float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
 #pragma unroll
@@ -257,12 +363,13 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     using GG = Geo<T, D, MP>;
     using F = typename Frag<T>::type;
     constexpr int C = GG::C, NT = GG::NT, NW = GG::NW, NMT = GG::NMT, NDT = GG::NDT, OWN = GG::OWN;
-    __shared__ __attribute__((aligned(16))) T lds[P::LDS_ELEMS];
-    T* Kt = lds;
+    __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
+    T* Kt = reinterpret_cast<T*>(lds_raw);
     T* Vt = Kt + GG::KT_ELEMS;
-    T* GT = Vt + GG::KT_ELEMS;
-    T* UT = GT + (size_t)C * P::LDG;
-    T* ZvT = UT + (size_t)C * P::LDU;
+    T* Qs = Vt + GG::KT_ELEMS;  // query rows of the chunk (phase A) ...
+    T* UT = Qs;                 // ... then U (phase B onwards)
+    T* GT = Qs + (size_t)C * P::LDQU;
+    T* ZvT = GT + (size_t)C * P::LDG;
 
     const int tid = threadIdx.x, w = tid >> 6, g = (tid & 63) >> 4, r = tid & 15;
     const int seg = blockIdx.x % a.nseg, bh = blockIdx.x / a.nseg, h = bh % a.H;
@@ -273,17 +380,57 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     const T* vb = (const T*)a.v + (size_t)bh * a.L * D;
     T* ob = (T*)a.o + (size_t)bh * a.L * D;
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
-    const T* EbarTh = (const T*)a.EbarT + (size_t)h * 2 * MP * C;
-    const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * C;
-    const T* Etabh = (const T*)a.Etab + (size_t)h * C * 2 * MP;
-    const T* ABs = (const T*)a.ABs;
-    const T* ABm = (const T*)a.ABm;
     const int* thh = a.theta + (size_t)h * SP;
 
+    // ---- tables: LDS copies when they fit, else straight from the workspace
+    const T* tABs;
+    const T* tABm;
+    const T* tEtab;
+    const float* tE32;
+    constexpr int sABs = P::TL ? P::LDAS : 2 * MP;
+    constexpr int sABm = P::TL ? P::LDAM : SP;
+    constexpr int sEtab = P::TL ? P::LDE : 2 * MP;
+    constexpr int sE32 = P::TL ? P::LDE32 : 2 * MP;
+    if constexpr (P::TL) {
+        T* lABs = ZvT + (size_t)D * GG::LDZ;
+        T* lABm = lABs + (size_t)SP * P::LDAS;
+        T* lEtab = lABm + (size_t)2 * MP * P::LDAM;
+        float* lE32 = reinterpret_cast<float*>(lEtab + (size_t)C * P::LDE);
+        copy_rows<T>(lABs, P::LDAS, (const T*)a.ABs, 2 * MP, SP, 2 * MP, tid);
+        copy_rows<T>(lABm, P::LDAM, (const T*)a.ABm, SP, 2 * MP, SP, tid);
+        copy_rows<T>(lEtab, P::LDE, (const T*)a.Etab + (size_t)h * C * 2 * MP, 2 * MP, C, 2 * MP, tid);
+        copy_rows<float>(lE32, P::LDE32, E32h, 2 * MP, C + 1, 2 * MP, tid);
+        tABs = lABs;
+        tABm = lABm;
+        tEtab = lEtab;
+        tE32 = lE32;
+    } else {
+        tABs = (const T*)a.ABs;
+        tABm = (const T*)a.ABm;
+        tEtab = (const T*)a.Etab + (size_t)h * C * 2 * MP;
+        tE32 = E32h;
+    }
+    OwnFrags<T, D, MP> ebf, erf;  // own rows of conj(E) and rho^{C-i}
+    load_own_frags<T, D, MP>(ebf, (const T*)a.EbarT + (size_t)h * 2 * MP * C, w, g, r);
+    load_own_frags<T, D, MP>(erf, (const T*)a.ErevT + (size_t)h * 2 * MP * C, w, g, r);
+
+    // first chunk's staging loads go out before the state set-up
+    Stage<T, D, MP> st;
+    F kpf[GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand)
+    {
+        const int tok0 = ch0 * C, c0 = min(C, a.L - tok0), i = 16 * w + r;
+        stage_load<T, D, MP, true>(st, qb + (size_t)tok0 * D, kb_ + (size_t)tok0 * D, vb + (size_t)tok0 * D, c0,
+                                   tid);
+#pragma unroll
+        for (int kb = 0; kb < GG::KBD; ++kb)
+            kpf[kb] = i < c0 ? ld_frag<T>(kb_ + (size_t)(tok0 + i) * D, 32 * kb, g) : zero_frag<T>();
+    }
+    if constexpr (P::TL) __syncthreads();  // LDS tables visible
+
     // ---- state entering the segment (pre-rotated: Z' = rho Z)
-    floatx4 Zk[OWN][2][NDT], Zv[OWN][2][NDT];
+    StateTiles<T, D, MP> Zk, Zv;
     if (seg == 0) {
-        const float* E1 = E32h + 2 * MP;
+        const float* E1 = tE32 + sE32;
 #pragma unroll
         for (int o = 0; o < OWN; ++o) {
             const int mt = w + NW * o;
@@ -341,9 +488,20 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     for (int n = 0; n < nch; ++n) {
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
-        __syncthreads();
-        stage_kv<T, D, MP>(Kt, Vt, kb_ + (size_t)tok0 * D, vb + (size_t)tok0 * D, c, tid);
-        __syncthreads();
+        __syncthreads();  // previous chunk done with Qs / Kt / Vt
+        stage_store<T, D, MP, true>(st, Qs, Kt, Vt, tid);
+        F kcur[GG::KBD];
+#pragma unroll
+        for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = kpf[kb];
+        if (n + 1 < nch) {
+            const int tn = tok0 + C, cn = min(C, a.L - tn), i = 16 * w + r;
+            stage_load<T, D, MP, true>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn,
+                                       tid);
+#pragma unroll
+            for (int kb = 0; kb < GG::KBD; ++kb)
+                kpf[kb] = i < cn ? ld_frag<T>(kb_ + (size_t)(tn + i) * D, 32 * kb, g) : zero_frag<T>();
+        }
+        __syncthreads();  // staging and ZvT visible
 
         // ---- phase A: Gram tile (key tile w) and Q Z'_k^T on owned mode tiles
         floatx4 U[OWN][2][NT];
@@ -358,16 +516,11 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             const int j = 16 * ct + r;
             F qf[GG::KBD];
 #pragma unroll
-            for (int kb = 0; kb < GG::KBD; ++kb)
-                qf[kb] = j < c ? ld_frag<T>(qb + (size_t)(tok0 + j) * D, 32 * kb, g) : zero_frag<T>();
+            for (int kb = 0; kb < GG::KBD; ++kb) qf[kb] = ld_frag<T>(Qs + (size_t)j * GG::LDQ, 32 * kb, g);
             if (ct >= w) {
-                const int i = 16 * w + r;
                 floatx4 acc = zero4();
 #pragma unroll
-                for (int kb = 0; kb < GG::KBD; ++kb) {
-                    F kf = i < c ? ld_frag<T>(kb_ + (size_t)(tok0 + i) * D, 32 * kb, g) : zero_frag<T>();
-                    acc = mma(kf, qf[kb], acc);
-                }
+                for (int kb = 0; kb < GG::KBD; ++kb) acc = mma(kcur[kb], qf[kb], acc);
                 if (ct == w) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
@@ -395,32 +548,23 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             const int mt = w + NW * o;
             if (mt < NMT) {
 #pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    F ef[GG::KBC];
+                for (int ct = 0; ct < NT; ++ct) {
 #pragma unroll
-                    for (int kb = 0; kb < GG::KBC; ++kb)
-                        ef[kb] = ld_frag<T>(EbarTh + (size_t)(16 * (p * NMT + mt) + r) * C, 32 * kb, g);
+                    for (int kb = 0; kb < GG::KBC; ++kb) {
+                        if (2 * kb <= ct) {
+                            const T* grow = GT + (size_t)(16 * ct + r) * P::LDG;
+                            const F gf = (2 * kb + 1 <= ct) ? ld_frag<T>(grow, 32 * kb, g)
+                                                            : ld_frag_lo<T>(grow, 32 * kb, g);
 #pragma unroll
-                    for (int ct = 0; ct < NT; ++ct) {
-#pragma unroll
-                        for (int kb = 0; kb < GG::KBC; ++kb) {
-                            if (2 * kb <= ct) {
-                                const T* grow = GT + (size_t)(16 * ct + r) * P::LDG;
-                                F gf = (2 * kb + 1 <= ct) ? ld_frag<T>(grow, 32 * kb, g)
-                                                          : ld_frag_lo<T>(grow, 32 * kb, g);
-                                U[o][p][ct] = mma(ef[kb], gf, U[o][p][ct]);
-                            }
+                            for (int p = 0; p < 2; ++p) U[o][p][ct] = mma(ebf[o][p][kb], gf, U[o][p][ct]);
                         }
                     }
-                }
-#pragma unroll
-                for (int ct = 0; ct < NT; ++ct) {
                     const int j = 16 * ct + r;
-                    const floatx4 cs = ld4f(E32h + (size_t)j * 2 * MP + 16 * mt + 4 * g);
-                    const floatx4 sn = ld4f(E32h + (size_t)j * 2 * MP + MP + 16 * mt + 4 * g);
+                    const floatx4 cs = ld4f(tE32 + (size_t)j * sE32 + 16 * mt + 4 * g);
+                    const floatx4 sn = ld4f(tE32 + (size_t)j * sE32 + MP + 16 * mt + 4 * g);
                     const floatx4 re = U[o][0][ct], im = U[o][1][ct];
-                    st4<T>(UT + (size_t)j * P::LDU + 16 * mt + 4 * g, cs * re - sn * im);
-                    st4<T>(UT + (size_t)j * P::LDU + MP + 16 * mt + 4 * g, sn * re + cs * im);
+                    st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, cs * re - sn * im);
+                    st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * mt + 4 * g, sn * re + cs * im);
                 }
             }
         }
@@ -432,34 +576,34 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             const long long pos = a.t0 + tok0 + j;
             F uf[GG::KBM];
 #pragma unroll
-            for (int kb = 0; kb < GG::KBM; ++kb) uf[kb] = ld_frag<T>(UT + (size_t)j * P::LDU, 32 * kb, g);
+            for (int kb = 0; kb < GG::KBM; ++kb) uf[kb] = ld_frag<T>(UT + (size_t)j * P::LDQU, 32 * kb, g);
             floatx4 sc[P::NST];
 #pragma unroll
-            for (int st = 0; st < P::NST; ++st) {
-                sc[st] = zero4();
+            for (int s4 = 0; s4 < P::NST; ++s4) {
+                sc[s4] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < GG::KBM; ++kb)
-                    sc[st] = mma(ld_frag<T>(ABs + (size_t)(16 * st + r) * 2 * MP, 32 * kb, g), uf[kb], sc[st]);
+                    sc[s4] = mma(ld_frag<T>(tABs + (size_t)(16 * s4 + r) * sABs, 32 * kb, g), uf[kb], sc[s4]);
             }
             float mx = -INFINITY;
 #pragma unroll
-            for (int st = 0; st < P::NST; ++st) {
-                const intx4 th = *reinterpret_cast<const intx4*>(thh + 16 * st + 4 * g);
+            for (int s4 = 0; s4 < P::NST; ++s4) {
+                const intx4 th = *reinterpret_cast<const intx4*>(thh + 16 * s4 + 4 * g);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    if (pos < (long long)th[e]) sc[st][e] = -INFINITY;
-                    mx = fmaxf(mx, sc[st][e]);
+                    if (pos < (long long)th[e]) sc[s4][e] = -INFINITY;
+                    mx = fmaxf(mx, sc[s4][e]);
                 }
             }
             mx = fmaxf(mx, __shfl_xor(mx, 16));
             mx = fmaxf(mx, __shfl_xor(mx, 32));
             float sum = 0.f;
 #pragma unroll
-            for (int st = 0; st < P::NST; ++st)
+            for (int s4 = 0; s4 < P::NST; ++s4)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float ex = __expf(sc[st][e] - mx);
-                    sc[st][e] = ex;
+                    const float ex = __expf(sc[s4][e] - mx);
+                    sc[s4][e] = ex;
                     sum += ex;
                 }
             sum += __shfl_xor(sum, 16);
@@ -475,12 +619,12 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                 wa[t] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < P::KBS; ++kb)
-                    wa[t] = mma(ld_frag<T>(ABm + (size_t)(16 * t + r) * SP, 32 * kb, g), pf[kb], wa[t]);
+                    wa[t] = mma(ld_frag<T>(tABm + (size_t)(16 * t + r) * sABm, 32 * kb, g), pf[kb], wa[t]);
             }
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = ld4f(E32h + (size_t)j * 2 * MP + 16 * mt + 4 * g);
-                const floatx4 sn = ld4f(E32h + (size_t)j * 2 * MP + MP + 16 * mt + 4 * g);
+                const floatx4 cs = ld4f(tE32 + (size_t)j * sE32 + 16 * mt + 4 * g);
+                const floatx4 sn = ld4f(tE32 + (size_t)j * sE32 + MP + 16 * mt + 4 * g);
                 const floatx4 am = wa[mt], bm = wa[NMT + mt];
                 wa[mt] = am * cs + bm * sn;
                 wa[NMT + mt] = am * sn - bm * cs;
@@ -504,8 +648,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                 if (kt <= w) {
 #pragma unroll
                     for (int kb = 0; kb < GG::KBM; ++kb)
-                        hh[kt] = mma(ld_frag<T>(Etabh + (size_t)(16 * kt + r) * 2 * MP, 32 * kb, g), wf[kb],
-                                     hh[kt]);
+                        hh[kt] = mma(ld_frag<T>(tEtab + (size_t)(16 * kt + r) * sEtab, 32 * kb, g), wf[kb], hh[kt]);
                     if (kt == w) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
@@ -527,15 +670,15 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                 for (int dt = 0; dt < NDT; ++dt) st4<T>(ob + (size_t)(tok0 + j) * D + 16 * dt + 4 * g, oa[dt]);
             }
         }
-        __syncthreads();
+        __syncthreads();  // everyone done reading ZvT
 
-        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, ErevTh, c, w, g, r);
+        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, tE32, sE32, erf, c, w, g, r);
         write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
     }
 
     // ---- final state (last segment): Z = conj(rho) Z'
     if (seg == a.nseg - 1) {
-        const float* E1 = E32h + 2 * MP;
+        const float* E1 = tE32 + sE32;
 #pragma unroll
         for (int o = 0; o < OWN; ++o) {
             const int mt = w + NW * o;
