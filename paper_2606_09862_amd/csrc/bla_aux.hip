@@ -141,18 +141,31 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(FwdArgs a, int MP, int D
     }
     const float cb = a.rotblk[(size_t)h * 2 * MP + m];
     const float sb = a.rotblk[(size_t)h * 2 * MP + MP + m];
-    const float* S = a.summ + (size_t)bh * a.nbs * U;
-    float* Cy = a.carry + (size_t)bh * (a.nseg - 1) * U;
-    for (int j = 0; j < a.nbs; ++j) {
-        float sr = S[(size_t)j * U + re], si = S[(size_t)j * U + im];
-        float nr = cb * zr - sb * zi + sr;
-        float ni = sb * zr + cb * zi + si;
-        zr = nr;
-        zi = ni;
-        if ((j + 1) % bps == 0) {
-            int g = (j + 1) / bps;  // segment that starts after this block
-            Cy[(size_t)(g - 1) * U + re] = zr;
-            Cy[(size_t)(g - 1) * U + im] = zi;
+    const float* __restrict__ S = a.summ + (size_t)bh * a.nbs * U;
+    float* __restrict__ Cy = a.carry + (size_t)bh * (a.nseg - 1) * U;
+    // blocks in groups of 4 so that their loads are in flight together
+    for (int j0 = 0; j0 < a.nbs; j0 += 4) {
+        float sr[4], si[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = j0 + u;
+            sr[u] = j < a.nbs ? S[(size_t)j * U + re] : 0.f;
+            si[u] = j < a.nbs ? S[(size_t)j * U + im] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = j0 + u;
+            if (j < a.nbs) {
+                const float nr = cb * zr - sb * zi + sr[u];
+                const float ni = sb * zr + cb * zi + si[u];
+                zr = nr;
+                zi = ni;
+                if ((j + 1) % bps == 0) {
+                    const int g = (j + 1) / bps;  // segment that starts after this block
+                    Cy[(size_t)(g - 1) * U + re] = zr;
+                    Cy[(size_t)(g - 1) * U + im] = zi;
+                }
+            }
         }
     }
 }

@@ -324,15 +324,21 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
 #pragma unroll
             for (int dt = 0; dt < GG::NDT; ++dt) Zk[o][p][dt] = Zv[o][p][dt] = zero4();
 
-    Stage<T, D, MP> st;
+    // Two chunks of K/V in flight ahead of the one being reduced: this kernel does
+    // little arithmetic per byte, so it is bound by how much load latency it hides.
+    Stage<T, D, MP> st0, st1;
     const size_t first = (size_t)blk * a.cpb * GG::C;
-    stage_load<T, D, MP, false>(st, nullptr, kbase + first * D, vbase + first * D, GG::C, tid);
+    stage_load<T, D, MP, false>(st0, nullptr, kbase + first * D, vbase + first * D, GG::C, tid);
+    if (a.cpb > 1)
+        stage_load<T, D, MP, false>(st1, nullptr, kbase + (first + GG::C) * D, vbase + (first + GG::C) * D,
+                                    GG::C, tid);
     for (int n = 0; n < a.cpb; ++n) {
         __syncthreads();
-        stage_store<T, D, MP, false>(st, nullptr, Kt, Vt, tid);
-        if (n + 1 < a.cpb) {
-            const size_t tok = first + (size_t)(n + 1) * GG::C;
-            stage_load<T, D, MP, false>(st, nullptr, kbase + tok * D, vbase + tok * D, GG::C, tid);
+        stage_store<T, D, MP, false>(st0, nullptr, Kt, Vt, tid);
+        st0 = st1;
+        if (n + 2 < a.cpb) {
+            const size_t tok = first + (size_t)(n + 2) * GG::C;
+            stage_load<T, D, MP, false>(st1, nullptr, kbase + tok * D, vbase + tok * D, GG::C, tid);
         }
         __syncthreads();
         advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, 2 * MP, erf, GG::C, w, g, r);
@@ -410,6 +416,10 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         tEtab = (const T*)a.Etab + (size_t)h * C * 2 * MP;
         tE32 = E32h;
     }
+    // start-mask thresholds of the slot rows this lane holds in the score tiles
+    intx4 thr[P::NST];
+#pragma unroll
+    for (int s4 = 0; s4 < P::NST; ++s4) thr[s4] = *reinterpret_cast<const intx4*>(thh + 16 * s4 + 4 * g);
     OwnFrags<T, D, MP> ebf, erf;  // own rows of conj(E) and rho^{C-i}
     load_own_frags<T, D, MP>(ebf, (const T*)a.EbarT + (size_t)h * 2 * MP * C, w, g, r);
     load_own_frags<T, D, MP>(erf, (const T*)a.ErevT + (size_t)h * 2 * MP * C, w, g, r);
@@ -588,10 +598,9 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             float mx = -INFINITY;
 #pragma unroll
             for (int s4 = 0; s4 < P::NST; ++s4) {
-                const intx4 th = *reinterpret_cast<const intx4*>(thh + 16 * s4 + 4 * g);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    if (pos < (long long)th[e]) sc[s4][e] = -INFINITY;
+                    if (pos < (long long)thr[s4][e]) sc[s4][e] = -INFINITY;
                     mx = fmaxf(mx, sc[s4][e]);
                 }
             }
