@@ -21,9 +21,12 @@ LIB = os.path.join(PKG, "libbla.so")
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-# Packed fp32 instructions are disabled for every HIP translation unit.
+# Packed fp32 instructions are disabled for every HIP translation unit.  Matrix-core
+# accumulators are allocated in ordinary VGPRs (the kernels post-process every
+# accumulator with vector ALU code, which cannot read AGPRs directly).
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}", f"-I{CSRC}",
-          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-result"]
+          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-result",
+          "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _compile(src: str) -> str:

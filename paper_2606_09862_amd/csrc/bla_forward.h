@@ -54,7 +54,11 @@ template <typename T, int D, int MP> struct Geo {
     static constexpr int KBM = 2 * MP / 32;     // reduction blocks over [Re | Im] modes
     static constexpr int KBC = C / 32;          // reduction blocks over chunk tokens
     static constexpr int OWN = (NMT + NW - 1) / NW;  // mode tiles owned per wave
-    static constexpr int PAD = 16 / (int)sizeof(T);  // 16-byte row padding in LDS
+    // Row padding in LDS: rows of a fragment read (16 lanes, one row each, 8 bytes per
+    // lane for bf16) land on distinct banks when the row stride is 8 bytes past a
+    // multiple of 128 (4 elements); for float32 rows the same 4 elements keep the
+    // 16-byte alignment of their 16-byte reads.
+    static constexpr int PAD = 4;
     static constexpr int LDK = C + PAD;         // Kt, Vt: [D][LDK]
     static constexpr int LDQ = D + PAD;         // Qs: [C][LDQ]
     static constexpr int LDZ = 2 * MP + PAD;    // ZvT: [D][LDZ]
@@ -77,16 +81,18 @@ template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
     static constexpr int LDU = 2 * MP + G::PAD;  // UT:   [C tokens][LDU]
     static constexpr int LDAS = 2 * MP + G::PAD; // ABs:  [SP][LDAS]
     static constexpr int LDAM = SP + G::PAD;     // ABm:  [2MP][LDAM]
-    static constexpr int LDE = 2 * MP + G::PAD;  // Etab: [C][LDE]
-    static constexpr int LDE32 = 2 * MP + 4;     // E32:  [C+1][LDE32] floats
+    static constexpr int LDE = 2 * MP + G::PAD;  // Etab: [C][LDE]  (also the phase twiddles)
+    static constexpr int LDR = G::C + G::PAD;    // EbarT, ErevT: [2MP][LDR]
     // Qs (read in phase A) and UT (written after the next barrier) share one buffer.
     static constexpr int LDQU = LDU > G::LDQ ? LDU : G::LDQ;
     static constexpr size_t BASE_ELEMS = 2 * G::KT_ELEMS + (size_t)G::C * LDQU + (size_t)G::C * LDG +
                                          (size_t)D * G::LDZ;
-    static constexpr size_t TAB_ELEMS = (size_t)SP * LDAS + (size_t)2 * MP * LDAM + (size_t)G::C * LDE;
-    static constexpr size_t E32_FLOATS = (size_t)(G::C + 1) * LDE32;
+    static constexpr size_t TAB_ELEMS = (size_t)SP * LDAS + (size_t)2 * MP * LDAM + (size_t)G::C * LDE +
+                                        (size_t)2 * 2 * MP * LDR;
+    // float32 rows rho and rho^C, then the int32 mask thresholds
+    static constexpr size_t SMALL_BYTES = (size_t)2 * 2 * MP * 4 + (size_t)SP * 4;
     static constexpr size_t BASE_BYTES = BASE_ELEMS * sizeof(T);
-    static constexpr size_t FULL_BYTES = BASE_BYTES + TAB_ELEMS * sizeof(T) + E32_FLOATS * 4;
+    static constexpr size_t FULL_BYTES = BASE_BYTES + TAB_ELEMS * sizeof(T) + SMALL_BYTES;
     static constexpr bool TL = FULL_BYTES <= kMaxLds;  // tables live in LDS
     static constexpr size_t LDS_BYTES = TL ? FULL_BYTES : BASE_BYTES;
     static_assert(SP % 32 == 0, "slot padding");
@@ -94,10 +100,6 @@ template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
 
 // The wave's fp32 state tiles: [owned mode tile][Re, Im][head-dim tile].
 template <typename T, int D, int MP> using StateTiles = floatx4[Geo<T, D, MP>::OWN][2][D / 16];
-// Per-wave register copies of table rows: [owned mode tile][Re, Im][reduction block].
-template <typename T, int D, int MP>
-using OwnFrags = typename Frag<T>::type[Geo<T, D, MP>::OWN][2][kChunk / 32];
-
 // ---------------------------------------------------------------------------------
 // Chunk staging: global -> registers (issued a chunk ahead) -> LDS.
 template <typename T, int D, int MP> struct Stage {
@@ -129,7 +131,7 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
 #pragma unroll
     for (int i = 0; i < GG::KVPT; ++i) {
         const int u = tid + i * kThreads;
-        const int which = u / UNITS, uu = u % UNITS, tq = uu / DO, dq = uu % DO;
+        const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
         const T* src = (which ? vc : kc) + (size_t)(4 * tq) * D + 8 * dq;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -163,7 +165,7 @@ __device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T*
     for (int i = 0; i < GG::KVPT; ++i) {
         const int u = tid + i * kThreads;
         if (u < GG::KVU) {
-            const int which = u / UNITS, uu = u % UNITS, tq = uu / DO, dq = uu % DO;
+            const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
             T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -176,17 +178,18 @@ __device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T*
     }
 }
 
-// Copy rows x cols elements (cols * sizeof(E) a multiple of 16 bytes) in 16-byte pieces.
+// Copy rows x cols elements (cols * sizeof(E) a multiple of 8 bytes) in 8-byte pieces.
 template <typename E>
 __device__ __forceinline__ void copy_rows(E* dst, int dstride, const E* src, int sstride, int rows,
                                           int cols, int tid)
 {
-    constexpr int PER = 16 / sizeof(E);
+    typedef int intx2 __attribute__((ext_vector_type(2)));
+    constexpr int PER = 8 / sizeof(E);
     const int pieces = cols / PER;
     for (int u = tid; u < rows * pieces; u += kThreads) {
         const int rr = u / pieces, cc = (u % pieces) * PER;
-        *reinterpret_cast<intx4*>(dst + (size_t)rr * dstride + cc) =
-            *reinterpret_cast<const intx4*>(src + (size_t)rr * sstride + cc);
+        *reinterpret_cast<intx2*>(dst + (size_t)rr * dstride + cc) =
+            *reinterpret_cast<const intx2*>(src + (size_t)rr * sstride + cc);
     }
 }
 
@@ -204,24 +207,6 @@ __device__ __forceinline__ typename Frag<T>::type erev_frag(const float* E32, in
         f[e] = (T)val;
     }
     return f;
-}
-
-// Register rows of a [2MP][C] table for the wave's own mode tiles.
-template <typename T, int D, int MP>
-__device__ __forceinline__ void load_own_frags(OwnFrags<T, D, MP>& f, const T* tab, int w, int g, int r)
-{
-    using GG = Geo<T, D, MP>;
-#pragma unroll
-    for (int o = 0; o < GG::OWN; ++o) {
-        const int mt = w + GG::NW * o;
-#pragma unroll
-        for (int p = 0; p < 2; ++p)
-#pragma unroll
-            for (int kb = 0; kb < GG::KBC; ++kb)
-                f[o][p][kb] = mt < GG::NMT ? ld_frag<T>(tab + (size_t)(16 * (p * GG::NMT + mt) + r) * GG::C,
-                                                        32 * kb, g)
-                                           : zero_frag<T>();
-    }
 }
 
 // Write the bf16/fp32 copy of Z'_v as ZvT[d][Re m | Im m] with the Im part negated
@@ -244,15 +229,17 @@ __device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP>& Zv
 }
 
 // Step 10: Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i] on the wave's own mode tiles.
-// E32 / ldE: phase table (rows 0..C); erf: rho^{C-i} fragments for full chunks.
+// rhoC: the row rho^C (full chunks); E32 (row stride 2MP): phase table for a ragged c;
+// Erev / ldR: the [2MP][C] table of rho^{C-i} (full chunks).
 template <typename T, int D, int MP>
 __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTiles<T, D, MP>& Zv,
-                                              const T* Kt, const T* Vt, const float* E32, int ldE,
-                                              const OwnFrags<T, D, MP>& erf, int c, int w, int g, int r)
+                                              const T* Kt, const T* Vt, const float* rhoC,
+                                              const float* E32, const T* Erev, int ldR, int c, int w,
+                                              int g, int r)
 {
     using GG = Geo<T, D, MP>;
     using F = typename Frag<T>::type;
-    const float* Ec = E32 + (size_t)c * ldE;
+    const float* Ec = (c == GG::C) ? rhoC : E32 + (size_t)c * 2 * MP;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o) {
         const int mt = w + GG::NW * o;
@@ -287,7 +274,9 @@ __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTil
             if (mt < GG::NMT) {
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
-                    const F ef = (c == GG::C) ? erf[o][p][kb] : erev_frag<T, MP>(E32, ldE, c, p, mt, kb, g, r);
+                    const F ef = (c == GG::C)
+                                     ? ld_frag<T>(Erev + (size_t)(16 * (p * GG::NMT + mt) + r) * ldR, 32 * kb, g)
+                                     : erev_frag<T, MP>(E32, 2 * MP, c, p, mt, kb, g, r);
 #pragma unroll
                     for (int dt = 0; dt < GG::NDT; ++dt) {
                         Zk[o][p][dt] = mma(kf[dt], ef, Zk[o][p][dt]);
@@ -308,14 +297,15 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
     __shared__ __attribute__((aligned(16))) T lds[2 * GG::KT_ELEMS];
     T* Kt = lds;
     T* Vt = lds + GG::KT_ELEMS;
-    const int tid = threadIdx.x, w = tid >> 6, g = (tid & 63) >> 4, r = tid & 15;
+    const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in a scalar register
     const int blk = blockIdx.x % a.nbs, bh = blockIdx.x / a.nbs, h = bh % a.H;
     const T* kbase = (const T*)a.k + (size_t)bh * a.L * D;
     const T* vbase = (const T*)a.v + (size_t)bh * a.L * D;
     const float* E32h = a.E32 + (size_t)h * (GG::C + 1) * 2 * MP;
 
-    OwnFrags<T, D, MP> erf;
-    load_own_frags<T, D, MP>(erf, (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C, w, g, r);
+    const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C;
+    const float* rhoC = E32h + (size_t)GG::C * 2 * MP;
     StateTiles<T, D, MP> Zk, Zv;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o)
@@ -341,7 +331,7 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
             stage_load<T, D, MP, false>(st1, nullptr, kbase + tok * D, vbase + tok * D, GG::C, tid);
         }
         __syncthreads();
-        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, E32h, 2 * MP, erf, GG::C, w, g, r);
+        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, rhoC, E32h, ErevTh, GG::C, GG::C, w, g, r);
     }
     float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
 #pragma unroll
@@ -377,7 +367,8 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     T* GT = Qs + (size_t)C * P::LDQU;
     T* ZvT = GT + (size_t)C * P::LDG;
 
-    const int tid = threadIdx.x, w = tid >> 6, g = (tid & 63) >> 4, r = tid & 15;
+    const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in a scalar register
     const int seg = blockIdx.x % a.nseg, bh = blockIdx.x / a.nseg, h = bh % a.H;
     const int ch0 = seg * a.cps;
     const int nch = min(a.cps, a.nch - ch0);
@@ -391,38 +382,52 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     // ---- tables: LDS copies when they fit, else straight from the workspace
     const T* tABs;
     const T* tABm;
-    const T* tEtab;
-    const float* tE32;
+    const T* tEtab;      // cos | sin of m w j, j < C: step 8 operand and the phase twiddles
+    const T* tEbar;      // [2MP][C] conj(rho^i) rows
+    const T* tErev;      // [2MP][C] rho^{C-i} rows
+    const float* rho1;   // rho   (float32, 2MP)
+    const float* rhoC;   // rho^C (float32, 2MP)
+    const int* tTheta;   // start-mask thresholds [SP]
     constexpr int sABs = P::TL ? P::LDAS : 2 * MP;
     constexpr int sABm = P::TL ? P::LDAM : SP;
     constexpr int sEtab = P::TL ? P::LDE : 2 * MP;
-    constexpr int sE32 = P::TL ? P::LDE32 : 2 * MP;
+    constexpr int sR = P::TL ? P::LDR : C;
+    const T* gEbar = (const T*)a.EbarT + (size_t)h * 2 * MP * C;
+    const T* gErev = (const T*)a.ErevT + (size_t)h * 2 * MP * C;
+    const T* gEtab = (const T*)a.Etab + (size_t)h * C * 2 * MP;
     if constexpr (P::TL) {
         T* lABs = ZvT + (size_t)D * GG::LDZ;
         T* lABm = lABs + (size_t)SP * P::LDAS;
         T* lEtab = lABm + (size_t)2 * MP * P::LDAM;
-        float* lE32 = reinterpret_cast<float*>(lEtab + (size_t)C * P::LDE);
+        T* lEbar = lEtab + (size_t)C * P::LDE;
+        T* lErev = lEbar + (size_t)2 * MP * P::LDR;
+        float* lRho = reinterpret_cast<float*>(lErev + (size_t)2 * MP * P::LDR);
+        int* lTheta = reinterpret_cast<int*>(lRho + 4 * MP);
         copy_rows<T>(lABs, P::LDAS, (const T*)a.ABs, 2 * MP, SP, 2 * MP, tid);
         copy_rows<T>(lABm, P::LDAM, (const T*)a.ABm, SP, 2 * MP, SP, tid);
-        copy_rows<T>(lEtab, P::LDE, (const T*)a.Etab + (size_t)h * C * 2 * MP, 2 * MP, C, 2 * MP, tid);
-        copy_rows<float>(lE32, P::LDE32, E32h, 2 * MP, C + 1, 2 * MP, tid);
+        copy_rows<T>(lEtab, P::LDE, gEtab, 2 * MP, C, 2 * MP, tid);
+        copy_rows<T>(lEbar, P::LDR, gEbar, C, 2 * MP, C, tid);
+        copy_rows<T>(lErev, P::LDR, gErev, C, 2 * MP, C, tid);
+        copy_rows<float>(lRho, 2 * MP, E32h + 2 * MP, (C - 1) * 2 * MP, 2, 2 * MP, tid);  // rows 1 and C
+        copy_rows<int>(lTheta, SP, thh, SP, 1, SP, tid);
         tABs = lABs;
         tABm = lABm;
         tEtab = lEtab;
-        tE32 = lE32;
+        tEbar = lEbar;
+        tErev = lErev;
+        rho1 = lRho;
+        rhoC = lRho + 2 * MP;
+        tTheta = lTheta;
     } else {
         tABs = (const T*)a.ABs;
         tABm = (const T*)a.ABm;
-        tEtab = (const T*)a.Etab + (size_t)h * C * 2 * MP;
-        tE32 = E32h;
+        tEtab = gEtab;
+        tEbar = gEbar;
+        tErev = gErev;
+        rho1 = E32h + 2 * MP;
+        rhoC = E32h + (size_t)C * 2 * MP;
+        tTheta = thh;
     }
-    // start-mask thresholds of the slot rows this lane holds in the score tiles
-    intx4 thr[P::NST];
-#pragma unroll
-    for (int s4 = 0; s4 < P::NST; ++s4) thr[s4] = *reinterpret_cast<const intx4*>(thh + 16 * s4 + 4 * g);
-    OwnFrags<T, D, MP> ebf, erf;  // own rows of conj(E) and rho^{C-i}
-    load_own_frags<T, D, MP>(ebf, (const T*)a.EbarT + (size_t)h * 2 * MP * C, w, g, r);
-    load_own_frags<T, D, MP>(erf, (const T*)a.ErevT + (size_t)h * 2 * MP * C, w, g, r);
 
     // first chunk's staging loads go out before the state set-up
     Stage<T, D, MP> st;
@@ -440,7 +445,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     // ---- state entering the segment (pre-rotated: Z' = rho Z)
     StateTiles<T, D, MP> Zk, Zv;
     if (seg == 0) {
-        const float* E1 = tE32 + sE32;
+        const float* E1 = rho1;
 #pragma unroll
         for (int o = 0; o < OWN; ++o) {
             const int mt = w + NW * o;
@@ -514,6 +519,14 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         __syncthreads();  // staging and ZvT visible
 
         // ---- phase A: Gram tile (key tile w) and Q Z'_k^T on owned mode tiles
+        F zkf[OWN][2][GG::KBD];  // Z'_k^T tiles as A fragments (rows m, reduction over d)
+#pragma unroll
+        for (int o = 0; o < OWN; ++o)
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int kb = 0; kb < GG::KBD; ++kb)
+                    zkf[o][p][kb] = frag_from_acc<T>(Zk[o][p][2 * kb], Zk[o][p][2 * kb + 1]);
         floatx4 U[OWN][2][NT];
 #pragma unroll
         for (int o = 0; o < OWN; ++o)
@@ -545,8 +558,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                     for (int p = 0; p < 2; ++p)
 #pragma unroll
                         for (int kb = 0; kb < GG::KBD; ++kb)
-                            U[o][p][ct] = mma(frag_from_acc<T>(Zk[o][p][2 * kb], Zk[o][p][2 * kb + 1]),
-                                              qf[kb], U[o][p][ct]);
+                            U[o][p][ct] = mma(zkf[o][p][kb], qf[kb], U[o][p][ct]);
                 }
             }
         }
@@ -566,12 +578,14 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                             const F gf = (2 * kb + 1 <= ct) ? ld_frag<T>(grow, 32 * kb, g)
                                                             : ld_frag_lo<T>(grow, 32 * kb, g);
 #pragma unroll
-                            for (int p = 0; p < 2; ++p) U[o][p][ct] = mma(ebf[o][p][kb], gf, U[o][p][ct]);
+                            for (int p = 0; p < 2; ++p)
+                                U[o][p][ct] = mma(ld_frag<T>(tEbar + (size_t)(16 * (p * NMT + mt) + r) * sR, 32 * kb, g),
+                                                  gf, U[o][p][ct]);
                         }
                     }
                     const int j = 16 * ct + r;
-                    const floatx4 cs = ld4f(tE32 + (size_t)j * sE32 + 16 * mt + 4 * g);
-                    const floatx4 sn = ld4f(tE32 + (size_t)j * sE32 + MP + 16 * mt + 4 * g);
+                    const floatx4 cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
+                    const floatx4 sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
                     const floatx4 re = U[o][0][ct], im = U[o][1][ct];
                     st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, cs * re - sn * im);
                     st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * mt + 4 * g, sn * re + cs * im);
@@ -598,9 +612,10 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             float mx = -INFINITY;
 #pragma unroll
             for (int s4 = 0; s4 < P::NST; ++s4) {
+                const intx4 th = *reinterpret_cast<const intx4*>(tTheta + 16 * s4 + 4 * g);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    if (pos < (long long)thr[s4][e]) sc[s4][e] = -INFINITY;
+                    if (pos < (long long)th[e]) sc[s4][e] = -INFINITY;
                     mx = fmaxf(mx, sc[s4][e]);
                 }
             }
@@ -632,8 +647,8 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             }
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = ld4f(tE32 + (size_t)j * sE32 + 16 * mt + 4 * g);
-                const floatx4 sn = ld4f(tE32 + (size_t)j * sE32 + MP + 16 * mt + 4 * g);
+                const floatx4 cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
+                const floatx4 sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
                 const floatx4 am = wa[mt], bm = wa[NMT + mt];
                 wa[mt] = am * cs + bm * sn;
                 wa[NMT + mt] = am * sn - bm * cs;
@@ -681,13 +696,13 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         }
         __syncthreads();  // everyone done reading ZvT
 
-        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, tE32, sE32, erf, c, w, g, r);
+        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, rhoC, E32h, tErev, sR, c, w, g, r);
         write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
     }
 
     // ---- final state (last segment): Z = conj(rho) Z'
     if (seg == a.nseg - 1) {
-        const float* E1 = tE32 + sE32;
+        const float* E1 = rho1;
 #pragma unroll
         for (int o = 0; o < OWN; ++o) {
             const int mt = w + NW * o;
