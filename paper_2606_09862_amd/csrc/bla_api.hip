@@ -9,28 +9,6 @@
 #include "bla.h"
 #include "bla_plan.h"
 
-namespace bla {
-hipError_t launch_forward_bf16(const Plan& p, const FwdArgs& a, hipStream_t s);
-hipError_t launch_forward_f32(const Plan& p, const FwdArgs& a, hipStream_t s);
-hipError_t launch_summary_bf16(const Plan& p, const FwdArgs& a, hipStream_t s);
-hipError_t launch_summary_f32(const Plan& p, const FwdArgs& a, hipStream_t s);
-bool forward_supported_bf16(int D, int MP, int SP);
-bool forward_supported_f32(int D, int MP, int SP);
-
-hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s)
-{
-    return p.bf16 ? launch_forward_bf16(p, a, s) : launch_forward_f32(p, a, s);
-}
-hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s)
-{
-    return p.bf16 ? launch_summary_bf16(p, a, s) : launch_summary_f32(p, a, s);
-}
-bool forward_supported(int bf16, int D, int MP, int SP)
-{
-    return bf16 ? forward_supported_bf16(D, MP, SP) : forward_supported_f32(D, MP, SP);
-}
-}  // namespace bla
-
 namespace {
 
 using namespace bla;

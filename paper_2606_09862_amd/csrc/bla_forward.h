@@ -109,7 +109,10 @@ template <typename T, int D, int MP> struct Stage {
     H kv[GG::KVPT][4][2];
 };
 
-// WQ: also stage the query rows.  c: valid tokens of the chunk (zero-filled past c).
+// WQ: also stage the query rows.  c: valid tokens of the chunk.  The loads never
+// depend on c (rows past c re-read row c-1, which exists); the zero fill past c is
+// applied when the registers are written to LDS, so no wait on the loads is forced
+// while they are in flight.
 template <typename T, int D, int MP, bool WQ>
 __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, const T* kc, const T* vc,
                                            int c, int tid)
@@ -119,12 +122,10 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
 #pragma unroll
     for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
         const int u = tid + i * kThreads;
-        const int t = u / DO, dq = u % DO;
-        if (u < GG::QU && t < c) {
+        const int t = min(u / DO, c - 1), dq = u % DO;
+        if (GG::QU % kThreads == 0 || u < GG::QU) {
             st.q[i][0] = ld4<T>(qc + (size_t)t * D + 8 * dq);
             st.q[i][1] = ld4<T>(qc + (size_t)t * D + 8 * dq + 4);
-        } else {
-            st.q[i][0] = st.q[i][1] = zero_half<T>();
         }
     }
     constexpr int UNITS = GG::KVU / 2;
@@ -132,64 +133,89 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
     for (int i = 0; i < GG::KVPT; ++i) {
         const int u = tid + i * kThreads;
         const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
-        const T* src = (which ? vc : kc) + (size_t)(4 * tq) * D + 8 * dq;
+        const T* src = (which ? vc : kc) + 8 * dq;
+        if (GG::KVU % kThreads == 0 || u < GG::KVU) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            if (u < GG::KVU && 4 * tq + t < c) {
-                st.kv[i][t][0] = ld4<T>(src + (size_t)t * D);
-                st.kv[i][t][1] = ld4<T>(src + (size_t)t * D + 4);
-            } else {
-                st.kv[i][t][0] = st.kv[i][t][1] = zero_half<T>();
+            for (int t = 0; t < 4; ++t) {
+                const int row = min(4 * tq + t, c - 1);
+                st.kv[i][t][0] = ld4<T>(src + (size_t)row * D);
+                st.kv[i][t][1] = ld4<T>(src + (size_t)row * D + 4);
             }
         }
     }
 }
 
 template <typename T, int D, int MP, bool WQ>
-__device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T* Kt, T* Vt, int tid)
+__device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T* Kt, T* Vt, int c, int tid)
 {
     using GG = Geo<T, D, MP>;
     using H = typename Frag<T>::half;
     constexpr int DO = D / 8;
+    const H z = zero_half<T>();
 #pragma unroll
     for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
         const int u = tid + i * kThreads;
-        if (u < GG::QU) {
+        if (GG::QU % kThreads == 0 || u < GG::QU) {
             const int t = u / DO, dq = u % DO;
-            *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq) = st.q[i][0];
-            *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq + 4) = st.q[i][1];
+            const bool ok = t < c;
+            *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq) = ok ? st.q[i][0] : z;
+            *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq + 4) = ok ? st.q[i][1] : z;
         }
     }
     constexpr int UNITS = GG::KVU / 2;
 #pragma unroll
     for (int i = 0; i < GG::KVPT; ++i) {
         const int u = tid + i * kThreads;
-        if (u < GG::KVU) {
+        if (GG::KVU % kThreads == 0 || u < GG::KVU) {
             const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
             T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
+            H x[4][2];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const bool ok = 4 * tq + t < c;
+                x[t][0] = ok ? st.kv[i][t][0] : z;
+                x[t][1] = ok ? st.kv[i][t][1] : z;
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                H a{st.kv[i][0][0][e], st.kv[i][1][0][e], st.kv[i][2][0][e], st.kv[i][3][0][e]};
-                H b{st.kv[i][0][1][e], st.kv[i][1][1][e], st.kv[i][2][1][e], st.kv[i][3][1][e]};
-                *reinterpret_cast<H*>(dst + e * GG::LDK) = a;
-                *reinterpret_cast<H*>(dst + (e + 4) * GG::LDK) = b;
+                H lo{x[0][0][e], x[1][0][e], x[2][0][e], x[3][0][e]};
+                H hi{x[0][1][e], x[1][1][e], x[2][1][e], x[3][1][e]};
+                *reinterpret_cast<H*>(dst + e * GG::LDK) = lo;
+                *reinterpret_cast<H*>(dst + (e + 4) * GG::LDK) = hi;
             }
         }
     }
 }
 
-// Copy rows x cols elements (cols * sizeof(E) a multiple of 8 bytes) in 8-byte pieces.
-template <typename E>
-__device__ __forceinline__ void copy_rows(E* dst, int dstride, const E* src, int sstride, int rows,
-                                          int cols, int tid)
+// A table copied from the workspace into LDS: ROWS x COLS elements of E, source
+// rows contiguous, destination row stride DSTRIDE (COLS * sizeof(E) a multiple of 8).
+template <typename E, int ROWS, int COLS, int DSTRIDE> struct TabCopy {
+    static constexpr int PER = 8 / (int)sizeof(E);        // elements per 8-byte piece
+    static constexpr int PIECES = ROWS * COLS / PER;
+    static constexpr int ITER = (PIECES + kThreads - 1) / kThreads;
+};
+
+// Copy up to two tables with every load of the thread in flight before the first
+// store (the copies run once per workgroup, so their latency is paid only once).
+template <typename E, int ROWS, int COLS, int DSTRIDE>
+__device__ __forceinline__ void copy_table(E* dst, const E* src, int tid)
 {
     typedef int intx2 __attribute__((ext_vector_type(2)));
-    constexpr int PER = 8 / sizeof(E);
-    const int pieces = cols / PER;
-    for (int u = tid; u < rows * pieces; u += kThreads) {
-        const int rr = u / pieces, cc = (u % pieces) * PER;
-        *reinterpret_cast<intx2*>(dst + (size_t)rr * dstride + cc) =
-            *reinterpret_cast<const intx2*>(src + (size_t)rr * sstride + cc);
+    using TC = TabCopy<E, ROWS, COLS, DSTRIDE>;
+    intx2 buf[TC::ITER];
+#pragma unroll
+    for (int i = 0; i < TC::ITER; ++i) {
+        const int u = tid + i * kThreads;
+        if (TC::PIECES % kThreads == 0 || u < TC::PIECES)
+            buf[i] = reinterpret_cast<const intx2*>(src)[u];
+    }
+#pragma unroll
+    for (int i = 0; i < TC::ITER; ++i) {
+        const int u = tid + i * kThreads;
+        if (TC::PIECES % kThreads == 0 || u < TC::PIECES) {
+            const int rr = u / (COLS / TC::PER), cc = (u % (COLS / TC::PER)) * TC::PER;
+            *reinterpret_cast<intx2*>(dst + (size_t)rr * DSTRIDE + cc) = buf[i];
+        }
     }
 }
 
@@ -324,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
                                     GG::C, tid);
     for (int n = 0; n < a.cpb; ++n) {
         __syncthreads();
-        stage_store<T, D, MP, false>(st0, nullptr, Kt, Vt, tid);
+        stage_store<T, D, MP, false>(st0, nullptr, Kt, Vt, GG::C, tid);
         st0 = st1;
         if (n + 2 < a.cpb) {
             const size_t tok = first + (size_t)(n + 2) * GG::C;
@@ -403,13 +429,14 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         T* lErev = lEbar + (size_t)2 * MP * P::LDR;
         float* lRho = reinterpret_cast<float*>(lErev + (size_t)2 * MP * P::LDR);
         int* lTheta = reinterpret_cast<int*>(lRho + 4 * MP);
-        copy_rows<T>(lABs, P::LDAS, (const T*)a.ABs, 2 * MP, SP, 2 * MP, tid);
-        copy_rows<T>(lABm, P::LDAM, (const T*)a.ABm, SP, 2 * MP, SP, tid);
-        copy_rows<T>(lEtab, P::LDE, gEtab, 2 * MP, C, 2 * MP, tid);
-        copy_rows<T>(lEbar, P::LDR, gEbar, C, 2 * MP, C, tid);
-        copy_rows<T>(lErev, P::LDR, gErev, C, 2 * MP, C, tid);
-        copy_rows<float>(lRho, 2 * MP, E32h + 2 * MP, (C - 1) * 2 * MP, 2, 2 * MP, tid);  // rows 1 and C
-        copy_rows<int>(lTheta, SP, thh, SP, 1, SP, tid);
+        copy_table<T, SP, 2 * MP, P::LDAS>(lABs, (const T*)a.ABs, tid);
+        copy_table<T, 2 * MP, SP, P::LDAM>(lABm, (const T*)a.ABm, tid);
+        copy_table<T, C, 2 * MP, P::LDE>(lEtab, gEtab, tid);
+        copy_table<T, 2 * MP, C, P::LDR>(lEbar, gEbar, tid);
+        copy_table<T, 2 * MP, C, P::LDR>(lErev, gErev, tid);
+        copy_table<float, 1, 2 * MP, 2 * MP>(lRho, E32h + 2 * MP, tid);                    // rho
+        copy_table<float, 1, 2 * MP, 2 * MP>(lRho + 2 * MP, E32h + (size_t)C * 2 * MP, tid);  // rho^C
+        copy_table<int, 1, SP, SP>(lTheta, thh, tid);
         tABs = lABs;
         tABm = lABm;
         tEtab = lEtab;
@@ -431,14 +458,13 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
 
     // first chunk's staging loads go out before the state set-up
     Stage<T, D, MP> st;
-    F kpf[GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand)
+    F kpf[GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand), unmasked
     {
-        const int tok0 = ch0 * C, c0 = min(C, a.L - tok0), i = 16 * w + r;
+        const int tok0 = ch0 * C, c0 = min(C, a.L - tok0), i = min(16 * w + r, c0 - 1);
         stage_load<T, D, MP, true>(st, qb + (size_t)tok0 * D, kb_ + (size_t)tok0 * D, vb + (size_t)tok0 * D, c0,
                                    tid);
 #pragma unroll
-        for (int kb = 0; kb < GG::KBD; ++kb)
-            kpf[kb] = i < c0 ? ld_frag<T>(kb_ + (size_t)(tok0 + i) * D, 32 * kb, g) : zero_frag<T>();
+        for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tok0 + i) * D, 32 * kb, g);
     }
     if constexpr (P::TL) __syncthreads();  // LDS tables visible
 
@@ -504,17 +530,16 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
         __syncthreads();  // previous chunk done with Qs / Kt / Vt
-        stage_store<T, D, MP, true>(st, Qs, Kt, Vt, tid);
+        stage_store<T, D, MP, true>(st, Qs, Kt, Vt, c, tid);
         F kcur[GG::KBD];
 #pragma unroll
-        for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = kpf[kb];
+        for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = (16 * w + r < c) ? kpf[kb] : zero_frag<T>();
         if (n + 1 < nch) {
-            const int tn = tok0 + C, cn = min(C, a.L - tn), i = 16 * w + r;
+            const int tn = tok0 + C, cn = min(C, a.L - tn), i = min(16 * w + r, cn - 1);
             stage_load<T, D, MP, true>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn,
                                        tid);
 #pragma unroll
-            for (int kb = 0; kb < GG::KBD; ++kb)
-                kpf[kb] = i < cn ? ld_frag<T>(kb_ + (size_t)(tn + i) * D, 32 * kb, g) : zero_frag<T>();
+            for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tn + i) * D, 32 * kb, g);
         }
         __syncthreads();  // staging and ZvT visible
 

@@ -1,8 +1,11 @@
-// Dispatch over the instantiated forward shapes for one operand type.
+// Launch wrappers of the forward kernels and the list of instantiated shapes.
 //
 // Shapes: head width D in {32, 64, 128}; padded modes MP in {16, 32, 64, 128};
 // padded slots SP in {32, 64, 128, 256} with SP <= max(32, 2 MP).  A shape whose
 // LDS tiles exceed the 160 KB of a gfx950 workgroup is reported unsupported.
+// Each group of shapes is instantiated in its own translation unit (bla_fwd_*.hip)
+// so that the units compile in parallel and can take their own compiler options;
+// bla_forward_dispatch.hip selects the instantiation at run time.
 #pragma once
 
 #include "bla_forward.h"
@@ -31,51 +34,30 @@ template <typename T, int D, int MP, int SP> constexpr bool fits()
     return Fwd<T, D, MP, SP>::LDS_BYTES <= kMaxLds;
 }
 
-template <typename T, int D, int MP, int SP>
-hipError_t launch_forward_t(const Plan& p, const FwdArgs& a, hipStream_t s)
-{
-    if constexpr (fits<T, D, MP, SP>()) {
-        hipLaunchKernelGGL((forward_kernel<T, D, MP, SP>), dim3((unsigned)(p.B * p.H * p.nseg)),
-                           dim3(kThreads), 0, s, a);
-        return hipGetLastError();
-    } else {
-        return hipErrorInvalidValue;
-    }
-}
-
-template <typename T, int D, int MP>
-hipError_t launch_summary_t(const Plan& p, const FwdArgs& a, hipStream_t s)
-{
-    hipLaunchKernelGGL((summary_kernel<T, D, MP>), dim3((unsigned)(p.B * p.H * p.nbs)), dim3(kThreads),
-                       0, s, a);
-    return hipGetLastError();
-}
+template <typename T, int D, int MP, int SP> struct Launch {
+    static hipError_t forward(const Plan& p, const FwdArgs& a, hipStream_t s);
+    static hipError_t summary(const Plan& p, const FwdArgs& a, hipStream_t s);
+};
 
 }  // namespace bla
 
-// Defines launch_forward_<NAME>, launch_summary_<NAME>, forward_supported_<NAME>.
-#define BLA_DEFINE_DISPATCH(T, NAME)                                                         \
-    namespace bla {                                                                          \
-    hipError_t launch_forward_##NAME(const Plan& p, const FwdArgs& a, hipStream_t s)         \
-    {                                                                                        \
-        BLA_FOR_EACH_SHAPE(BLA_FWD_CASE, T)                                                  \
-        return hipErrorInvalidValue;                                                         \
-    }                                                                                        \
-    hipError_t launch_summary_##NAME(const Plan& p, const FwdArgs& a, hipStream_t s)         \
-    {                                                                                        \
-        BLA_FOR_EACH_SHAPE(BLA_SUM_CASE, T)                                                  \
-        return hipErrorInvalidValue;                                                         \
-    }                                                                                        \
-    bool forward_supported_##NAME(int D, int MP, int SP)                                     \
-    {                                                                                        \
-        BLA_FOR_EACH_SHAPE(BLA_SUP_CASE, T)                                                  \
-        return false;                                                                        \
-    }                                                                                        \
+// Defines the launchers of one shape (used by the bla_fwd_*.hip units).
+#define BLA_INSTANTIATE(T, D, MP, SP)                                                                   \
+    namespace bla {                                                                                     \
+    template <> hipError_t Launch<T, D, MP, SP>::forward(const Plan& p, const FwdArgs& a, hipStream_t s) \
+    {                                                                                                   \
+        if constexpr (fits<T, D, MP, SP>()) {                                                           \
+            hipLaunchKernelGGL((forward_kernel<T, D, MP, SP>), dim3((unsigned)(p.B * p.H * p.nseg)),    \
+                               dim3(kThreads), 0, s, a);                                                \
+            return hipGetLastError();                                                                   \
+        } else {                                                                                        \
+            return hipErrorInvalidValue;                                                                \
+        }                                                                                               \
+    }                                                                                                   \
+    template <> hipError_t Launch<T, D, MP, SP>::summary(const Plan& p, const FwdArgs& a, hipStream_t s) \
+    {                                                                                                   \
+        hipLaunchKernelGGL((summary_kernel<T, D, MP>), dim3((unsigned)(p.B * p.H * p.nbs)),             \
+                           dim3(kThreads), 0, s, a);                                                    \
+        return hipGetLastError();                                                                       \
+    }                                                                                                   \
     }
-
-#define BLA_FWD_CASE(TT, DD, MMP, SSP) \
-    if (p.D == DD && p.MP == MMP && p.SP == SSP) return launch_forward_t<TT, DD, MMP, SSP>(p, a, s);
-#define BLA_SUM_CASE(TT, DD, MMP, SSP) \
-    if (p.D == DD && p.MP == MMP && p.SP == SSP) return launch_summary_t<TT, DD, MMP>(p, a, s);
-#define BLA_SUP_CASE(TT, DD, MMP, SSP) \
-    if (D == DD && MP == MMP && SP == SSP) return fits<TT, DD, MMP, SSP>();
