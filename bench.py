@@ -44,7 +44,7 @@ def forward_bytes(B, H, L, d, M, io_bytes):
 def kernel_sources_digest():
     csrc = os.path.join(ROOT, "paper_2606_09862_amd", "csrc")
     h = hashlib.sha256()
-    for name in ("bla_device.h", "bla_forward.h", "bla_plan.h"):
+    for name in ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -155,7 +155,7 @@ def bench_forward(args, hip):
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
     t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
     extra = {
-        "kernel": "forward_kernel<bf16,64,64,64>",
+        "kernel": "forward_pair_kernel<64,64,64>",
         "algorithmic_bytes_per_launch": nbytes,
         "algorithmic_flops_per_launch": flops,
         "forward_kernel_us": round(phase_ms["forward"] * 1e3, 2),

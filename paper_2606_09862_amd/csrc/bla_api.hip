@@ -86,10 +86,18 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->cps = pl->nch;
     pl->cpb = pl->nch;
     pl->nbs = 0;
+    pl->upw = 1;
+    pl->pair = 0;
+    if (!step) {
+        const int pu = forward_units_per_wg(pl->bf16, pl->D, pl->MP, pl->SP);
+        pl->upw = pu > 0 ? pu : 1;
+        pl->pair = pu > 0;
+    }
     if (!step && units > 0 && pl->nch > 1) {
         const int cus = device_cu_count();
-        if (units < cus) {
-            long long want = (cus + units - 1) / units;
+        const long long target = (long long)cus * pl->upw;  // units that fill every CU once
+        if (units < target) {
+            long long want = (target + units - 1) / units;
             int nseg = (int)(want < pl->nch ? want : pl->nch);
             int cps = (pl->nch + nseg - 1) / nseg;
             nseg = (pl->nch + cps - 1) / cps;
@@ -148,7 +156,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.h0 = h0;
         a.nh = pl.H - h0 < kMaxHeadsPerTableLaunch ? pl.H - h0 : kMaxHeadsPerTableLaunch;
         a.with_shared = h0 == 0;
-        a.scale = pl.scale;
+        a.scale = pl.pair ? 1.f : pl.scale;  // the pair kernel reads A | B unscaled
         for (int i = 0; i < a.nh; ++i) {
             const double tmin = 2.0 * pl.M - 1.0;
             a.T[i] = T[h0 + i] < tmin ? tmin : T[h0 + i];  // clamp, as Alg. 1 and Alg. 3 do
@@ -260,6 +268,7 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     a.cpb = pl.cpb;
     a.nbs = pl.nbs;
     a.t0 = pl.t0;
+    a.scale = pl.scale;
     if (pl.nseg > 1 && launch_summary(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
     if (!mark(2)) return BLA_ERR_HIP;
     if (pl.nseg > 1 && launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;

@@ -8,7 +8,7 @@ namespace bla {
 #define BLA_SUM_CASE(TT, DD, MMP, SSP) \
     if (p.D == DD && p.MP == MMP && p.SP == SSP) return Launch<TT, DD, MMP, SSP>::summary(p, a, s);
 #define BLA_SUP_CASE(TT, DD, MMP, SSP) \
-    if (D == DD && MP == MMP && SP == SSP) return fits<TT, DD, MMP, SSP>();
+    if (D == DD && MP == MMP && SP == SSP) return fits<TT, DD, MMP, SSP>() || pair_units<TT, DD, MMP, SSP>() > 0;
 
 hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s)
 {
@@ -28,6 +28,17 @@ hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s)
         BLA_FOR_EACH_SHAPE(BLA_SUM_CASE, float)
     }
     return hipErrorInvalidValue;
+}
+
+#define BLA_UNITS_CASE(TT, DD, MMP, SSP) \
+    if (D == DD && MP == MMP && SP == SSP) return pair_units<TT, DD, MMP, SSP>();
+
+int forward_units_per_wg(int is_bf16, int D, int MP, int SP)
+{
+    if (is_bf16) {
+        BLA_FOR_EACH_SHAPE(BLA_UNITS_CASE, bf16)
+    }
+    return 0;
 }
 
 bool forward_supported(int is_bf16, int D, int MP, int SP)

@@ -9,6 +9,7 @@
 #pragma once
 
 #include "bla_forward.h"
+#include "bla_forward_pair.h"
 
 #define BLA_FOR_EACH_MS(X, T, D) \
     X(T, D, 16, 32)              \
@@ -39,6 +40,16 @@ template <typename T, int D, int MP, int SP> struct Launch {
     static hipError_t summary(const Plan& p, const FwdArgs& a, hipStream_t s);
 };
 
+// Units per workgroup of the bf16 pair kernel for a shape (0: the shape uses forward_kernel).
+template <typename T, int D, int MP, int SP> constexpr int pair_units()
+{
+    if constexpr (sizeof(T) == 2) {
+        return Pair<D, MP, SP>::FITS ? Pair<D, MP, SP>::U : 0;
+    } else {
+        return 0;
+    }
+}
+
 }  // namespace bla
 
 // Defines the launchers of one shape (used by the bla_fwd_*.hip units).
@@ -46,7 +57,12 @@ template <typename T, int D, int MP, int SP> struct Launch {
     namespace bla {                                                                                     \
     template <> hipError_t Launch<T, D, MP, SP>::forward(const Plan& p, const FwdArgs& a, hipStream_t s) \
     {                                                                                                   \
-        if constexpr (fits<T, D, MP, SP>()) {                                                           \
+        if constexpr (pair_units<T, D, MP, SP>() > 0) {                                                 \
+            constexpr int UU = pair_units<T, D, MP, SP>();                                              \
+            dim3 grid((unsigned)((p.B * p.nseg + UU - 1) / UU), (unsigned)p.H);                         \
+            hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP>), grid, dim3(256 * UU), 0, s, a);        \
+            return hipGetLastError();                                                                   \
+        } else if constexpr (fits<T, D, MP, SP>()) {                                                    \
             hipLaunchKernelGGL((forward_kernel<T, D, MP, SP>), dim3((unsigned)(p.B * p.H * p.nseg)),    \
                                dim3(kThreads), 0, s, a);                                                \
             return hipGetLastError();                                                                   \

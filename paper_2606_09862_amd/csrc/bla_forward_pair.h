@@ -1,0 +1,545 @@
+// Chunked BLA forward for bf16 operands, two sequence units per workgroup.
+//
+// Same algebra as bla_forward.h (chunks of C = 64 tokens, pre-rotated state
+// Z' = rho Z, steps (1)-(10) of that file), reorganised for latency hiding on
+// gfx950:
+//
+//  * A workgroup of 8 waves runs U = 2 independent units (b, h, segment) of the
+//    same head, 4 waves each, so every SIMD holds two waves whose dependency
+//    chains interleave.  The head's tables are shared in LDS.
+//  * Each table is stored once.  The second layout a contraction needs (slot
+//    matrix [A|B] with the reduction over slots; the phase table with the
+//    reduction over tokens; K and V with the reduction over tokens) is read with
+//    the transposing LDS load ds_read_b64_tr_b16.
+//  * The state update uses rho^{c-i} = rho^c conj(rho^i):
+//        Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i]),
+//    so one phase table serves steps (3), (8), (10) and the twiddles, and a
+//    ragged last chunk needs no table of its own (rows past c are zero).
+#pragma once
+
+#include <math.h>
+
+#include "bla_forward.h"
+
+namespace bla {
+
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read: within each 16-lane group, lane 4a+b supplies the address
+// of 4 consecutive elements; lane 4b'+c receives element c of lane 4a+b' for a = 0..3.
+__device__ __forceinline__ bf16x4 ld_tr(const bf16* p)
+{
+    shortx4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) shortx4*)p);
+    return __builtin_bit_cast(bf16x4, v);
+}
+
+// Operand fragment for rows x0..x0+15 (lane r) and reduction block kb from an LDS
+// tile stored reduction-major, M[k][x] with row length ld: the fragment's element e
+// of lane (g, r) is M[k(e)][x0 + r], k(e) = 32kb + 16(e/4) + 4g + e%4.
+__device__ __forceinline__ bf16x8 ld_frag_tr(const bf16* M, int ld, int x0, int kb, int g, int r)
+{
+    const bf16* p = M + (size_t)(32 * kb + 4 * g + (r >> 2)) * ld + x0 + 4 * (r & 3);
+    return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
+}
+
+__device__ __forceinline__ bf16x8 neg8(bf16x8 x)
+{
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 u = __builtin_bit_cast(u32x4, x);
+    u ^= 0x80008000u;
+    return __builtin_bit_cast(bf16x8, u);
+}
+
+template <int D, int MP, int SP> struct Pair {
+    static constexpr int C = kChunk, NT = C / 16, WPU = 4;
+    static constexpr int NMT = MP / 16, NDT = D / 16, NST = SP / 16;
+    static constexpr int KBD = D / 32, KBM = 2 * MP / 32, KBC = C / 32, KBS = SP / 32;
+    static constexpr int OWN = (NMT + WPU - 1) / WPU;
+    // Row strides (elements).  Tiles read both row-wise and transposed use a
+    // 12-element pad (stride = 6 words mod 32 banks): row-wise fragment reads are
+    // conflict-free and transposed reads have at most 2-way conflicts.  Tiles read
+    // row-wise only use a 4-element pad (stride = 2 words mod 32).
+    static constexpr int LAB = 2 * MP + 12;  // [A|B]:     [SP][LAB]
+    static constexpr int LE = 2 * MP + 12;   // phase tab: [C][LE]
+    static constexpr int LK = D + 12;        // K, V:      [C][LK]
+    static constexpr int LQ = D + 4;         // Q:         [C][LQ]
+    static constexpr int LU = 2 * MP + 4;    // U:         [C][LU]
+    static constexpr int LQU = LQ > LU ? LQ : LU;
+    static constexpr int LG = C + 4;         // G^T:       [C][LG]
+    static constexpr int LZ = 2 * MP + 4;    // Z'_v:      [D][LZ]
+    static constexpr size_t AB_ELEMS = (size_t)SP * LAB;
+    static constexpr size_t E_ELEMS = (size_t)C * LE;
+    static constexpr size_t SHARED_BYTES = 2 * (AB_ELEMS + E_ELEMS) + 2 * 2 * MP * 4 + SP * 4;
+    static constexpr size_t UNIT_ELEMS = 2 * (size_t)C * LK + (size_t)C * LQU + (size_t)C * LG + (size_t)D * LZ;
+    static constexpr size_t UNIT_BYTES = 2 * UNIT_ELEMS;
+    static constexpr int U = (SHARED_BYTES + 2 * UNIT_BYTES <= kMaxLds) ? 2 : 1;
+    static constexpr bool FITS = SHARED_BYTES + U * UNIT_BYTES <= kMaxLds;
+    static constexpr size_t LDS_BYTES = SHARED_BYTES + U * UNIT_BYTES;
+    // staging: Q, K, V of one chunk in 16-byte pieces, spread over the unit's 256 threads
+    static constexpr int PIECES = 3 * C * D / 8;
+    static constexpr int PPT = (PIECES + 255) / 256;
+    static_assert(NT == WPU, "one token tile per wave of a unit");
+};
+
+template <int D, int MP, int SP> using PState = floatx4[Pair<D, MP, SP>::OWN][2][D / 16];
+template <int D, int MP, int SP> using PStage = bf16x8[Pair<D, MP, SP>::PPT];
+
+template <int D, int MP, int SP>
+__device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf16* q,
+                                                const bf16* k, const bf16* v, int c, int ut)
+{
+    using P = Pair<D, MP, SP>;
+    constexpr int PR = D / 8;  // pieces per row
+#pragma unroll
+    for (int i = 0; i < P::PPT; ++i) {
+        const int u = ut + 256 * i;
+        if (P::PIECES % 256 == 0 || u < P::PIECES) {
+            const int which = u / (P::C * PR), rem = u % (P::C * PR);
+            const int row = min(rem / PR, c - 1), pc = rem % PR;
+            const bf16* src = (which == 0 ? q : which == 1 ? k : v) + (size_t)row * D + 8 * pc;
+            st[i] = *reinterpret_cast<const bf16x8*>(src);
+        }
+    }
+}
+
+template <int D, int MP, int SP>
+__device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf16* Qs,
+                                                 bf16* Ks, bf16* Vs, int c, int ut)
+{
+    using P = Pair<D, MP, SP>;
+    constexpr int PR = D / 8;
+#pragma unroll
+    for (int i = 0; i < P::PPT; ++i) {
+        const int u = ut + 256 * i;
+        if (P::PIECES % 256 == 0 || u < P::PIECES) {
+            const int which = u / (P::C * PR), rem = u % (P::C * PR);
+            const int row = rem / PR, pc = rem % PR;
+            bf16* dst = which == 0 ? Qs + (size_t)row * P::LQ : (which == 1 ? Ks : Vs) + (size_t)row * P::LK;
+            const bf16x8 x = row < c ? st[i] : bf16x8{};
+            *reinterpret_cast<bf16x4*>(dst + 8 * pc) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
+            *reinterpret_cast<bf16x4*>(dst + 8 * pc + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
+        }
+    }
+}
+
+// Copy a table of ROWS x COLS bf16 (source rows contiguous) into LDS rows of stride DST,
+// all loads of a thread in flight before its stores.
+template <int ROWS, int COLS, int DST, int NTHR>
+__device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
+{
+    typedef int intx2 __attribute__((ext_vector_type(2)));
+    constexpr int PIECES = ROWS * COLS / 4, ITER = (PIECES + NTHR - 1) / NTHR;
+    intx2 buf[ITER];
+#pragma unroll
+    for (int i = 0; i < ITER; ++i) {
+        const int u = tid + i * NTHR;
+        if (PIECES % NTHR == 0 || u < PIECES) buf[i] = reinterpret_cast<const intx2*>(src)[u];
+    }
+#pragma unroll
+    for (int i = 0; i < ITER; ++i) {
+        const int u = tid + i * NTHR;
+        if (PIECES % NTHR == 0 || u < PIECES)
+            *reinterpret_cast<intx2*>(dst + (size_t)(u / (COLS / 4)) * DST + 4 * (u % (COLS / 4))) = buf[i];
+    }
+}
+
+template <int D, int MP, int SP>
+__device__ __forceinline__ void pair_write_zv(bf16* ZvT, const PState<D, MP, SP>& Zv, int wl, int g, int r)
+{
+    using P = Pair<D, MP, SP>;
+#pragma unroll
+    for (int o = 0; o < P::OWN; ++o) {
+        const int mt = wl + P::WPU * o;
+        if (mt < P::NMT) {
+#pragma unroll
+            for (int dt = 0; dt < P::NDT; ++dt) {
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + 16 * mt + 4 * g, Zv[o][0][dt]);
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + MP + 16 * mt + 4 * g, -Zv[o][1][dt]);
+            }
+        }
+    }
+}
+
+// grid: H x ceil(B*nseg/U) workgroups of 256*U threads; workgroup (h, x) runs the
+// units 2x and 2x+1 (U = 2) of head h, units numbered over (b, segment).
+template <int D, int MP, int SP>
+__global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kernel(FwdArgs a)
+{
+    using P = Pair<D, MP, SP>;
+    using F = bf16x8;
+    constexpr int C = P::C, NT = P::NT, NMT = P::NMT, NDT = P::NDT, OWN = P::OWN;
+    __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
+    bf16* sAB = reinterpret_cast<bf16*>(lds_raw);
+    bf16* sE = sAB + P::AB_ELEMS;
+    float* sRho = reinterpret_cast<float*>(sE + P::E_ELEMS);  // rho, then rho^C
+    int* sTheta = reinterpret_cast<int*>(sRho + 4 * MP);
+
+    const int tid = threadIdx.x;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int u = wv / P::WPU, wl = wv % P::WPU;  // unit and wave within the unit
+    const int ut = tid - 256 * u;                  // thread index within the unit
+    const int g = (tid & 63) >> 4, r = tid & 15;
+    const int h = blockIdx.y;
+    const int per_head = a.B * a.nseg;
+    const int v_unit = blockIdx.x * P::U + u;
+    const bool active = v_unit < per_head;
+    const int b = active ? v_unit / a.nseg : 0, seg = active ? v_unit % a.nseg : 0;
+    const int bh = b * a.H + h;
+
+    bf16* base = reinterpret_cast<bf16*>(lds_raw + P::SHARED_BYTES + (size_t)u * P::UNIT_BYTES);
+    bf16* Ks = base;
+    bf16* Vs = Ks + (size_t)C * P::LK;
+    bf16* Qs = Vs + (size_t)C * P::LK;   // Q in phase A, then U
+    bf16* UT = Qs;
+    bf16* GT = Qs + (size_t)C * P::LQU;
+    bf16* ZvT = GT + (size_t)C * P::LG;
+
+    const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
+    // ---- shared tables
+    pair_copy<SP, 2 * MP, P::LAB, 256 * P::U>(sAB, (const bf16*)a.ABs, tid);
+    pair_copy<C, 2 * MP, P::LE, 256 * P::U>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
+    for (int i = tid; i < 2 * MP; i += 256 * P::U) {
+        sRho[i] = E32h[2 * MP + i];
+        sRho[2 * MP + i] = E32h[(size_t)C * 2 * MP + i];
+    }
+    for (int i = tid; i < SP; i += 256 * P::U) sTheta[i] = a.theta[(size_t)h * SP + i];
+
+    const int ch0 = seg * a.cps;
+    const int nch = active ? min(a.cps, a.nch - ch0) : 0;
+    const bf16* qb = (const bf16*)a.q + (size_t)bh * a.L * D;
+    const bf16* kb_ = (const bf16*)a.k + (size_t)bh * a.L * D;
+    const bf16* vb = (const bf16*)a.v + (size_t)bh * a.L * D;
+    bf16* ob = (bf16*)a.o + (size_t)bh * a.L * D;
+
+    PStage<D, MP, SP> st;
+    if (nch > 0) {
+        const int t0c = ch0 * C, c0 = min(C, a.L - t0c);
+        pair_stage_load<D, MP, SP>(st, qb + (size_t)t0c * D, kb_ + (size_t)t0c * D, vb + (size_t)t0c * D, c0, ut);
+    }
+    __syncthreads();  // tables visible
+
+    // ---- state entering the unit's segment (pre-rotated: Z' = rho Z)
+    PState<D, MP, SP> Zk, Zv;
+    const float* E1 = sRho;
+#pragma unroll
+    for (int o = 0; o < OWN; ++o) {
+        const int mt = wl + P::WPU * o;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            Zk[o][0][dt] = Zk[o][1][dt] = Zv[o][0][dt] = Zv[o][1][dt] = zero4();
+            if (mt < NMT && active) {
+                if (seg == 0) {
+                    const int m = 16 * mt + r;
+                    floatx4 kr = zero4(), ki = zero4(), vr = zero4(), vi = zero4();
+                    if (a.sk_in && m < a.M) {
+                        kr = ld4f(a.sk_in + (((size_t)bh * 2 + 0) * a.M + m) * D + 16 * dt + 4 * g);
+                        ki = ld4f(a.sk_in + (((size_t)bh * 2 + 1) * a.M + m) * D + 16 * dt + 4 * g);
+                    }
+                    if (a.sv_in) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int mv = 16 * mt + 4 * g + e;
+                            if (mv < a.M) {
+                                vr[e] = a.sv_in[(((size_t)bh * 2 + 0) * a.M + mv) * D + 16 * dt + r];
+                                vi[e] = a.sv_in[(((size_t)bh * 2 + 1) * a.M + mv) * D + 16 * dt + r];
+                            }
+                        }
+                    }
+                    const float c1 = E1[m], s1 = E1[MP + m];
+                    Zk[o][0][dt] = c1 * kr - s1 * ki;
+                    Zk[o][1][dt] = s1 * kr + c1 * ki;
+                    const floatx4 cv = ld4f(E1 + 16 * mt + 4 * g), sv = ld4f(E1 + MP + 16 * mt + 4 * g);
+                    Zv[o][0][dt] = cv * vr - sv * vi;
+                    Zv[o][1][dt] = sv * vr + cv * vi;
+                } else {
+                    const float* cy = a.carry + ((size_t)bh * (a.nseg - 1) + (seg - 1)) * 4 * MP * D;
+#pragma unroll
+                    for (int p = 0; p < 2; ++p) {
+                        Zk[o][p][dt] = ld4f(cy + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
+                        Zv[o][p][dt] =
+                            ld4f(cy + (size_t)2 * MP * D + ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+                    }
+                }
+            }
+        }
+    }
+    pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
+
+    // both units run the same number of iterations (the barriers are workgroup-wide);
+    // an exhausted or idle unit computes on zero-filled tiles and stores nothing
+    const int nmax = a.cps;
+    for (int n = 0; n < nmax; ++n) {
+        const bool live = n < nch;
+        const int tok0 = (ch0 + n) * C;
+        const int c = live ? min(C, a.L - tok0) : 0;
+        __syncthreads();  // previous chunk done with Qs / Ks / Vs / UT
+        pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, c, ut);
+        if (n + 1 < nch) {
+            const int tn = tok0 + C, cn = min(C, a.L - tn);
+            pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn, ut);
+        }
+        __syncthreads();  // staging and Z'_v copy visible
+
+        // ---- phase A: Gram tile (key tile wl) and Q Z'_k^T on owned mode tiles
+        F zkf[OWN][2][P::KBD];
+#pragma unroll
+        for (int o = 0; o < OWN; ++o)
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int kb = 0; kb < P::KBD; ++kb)
+                    zkf[o][p][kb] = frag_from_acc<bf16>(Zk[o][p][2 * kb], Zk[o][p][2 * kb + 1]);
+        F kf[P::KBD];
+#pragma unroll
+        for (int kb = 0; kb < P::KBD; ++kb) kf[kb] = ld_frag<bf16>(Ks + (size_t)(16 * wl + r) * P::LK, 32 * kb, g);
+        floatx4 Uacc[OWN][2][NT];
+#pragma unroll
+        for (int ct = 0; ct < NT; ++ct) {
+            const int j = 16 * ct + r;
+            F qf[P::KBD];
+#pragma unroll
+            for (int kb = 0; kb < P::KBD; ++kb) qf[kb] = ld_frag<bf16>(Qs + (size_t)j * P::LQ, 32 * kb, g);
+            if (ct >= wl) {
+                floatx4 acc = zero4();
+#pragma unroll
+                for (int kb = 0; kb < P::KBD; ++kb) acc = mma(kf[kb], qf[kb], acc);
+                if (ct == wl) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (4 * g + e > r) acc[e] = 0.f;
+                }
+                st4<bf16>(GT + (size_t)j * P::LG + 16 * wl + 4 * g, acc);
+            }
+#pragma unroll
+            for (int o = 0; o < OWN; ++o)
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    Uacc[o][p][ct] = zero4();
+                    if (wl + P::WPU * o < NMT) {
+#pragma unroll
+                        for (int kb = 0; kb < P::KBD; ++kb) Uacc[o][p][ct] = mma(zkf[o][p][kb], qf[kb], Uacc[o][p][ct]);
+                    }
+                }
+        }
+        __syncthreads();
+
+        // ---- phase B: + G conj(E) (conj(E) read transposed from the phase table), twiddle, publish U
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = wl + P::WPU * o;
+            if (mt < NMT) {
+                F ecf[P::KBC], esf[P::KBC];  // cos rows and -sin rows of conj(E) for the owned modes
+#pragma unroll
+                for (int kb = 0; kb < P::KBC; ++kb) {
+                    ecf[kb] = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
+                    esf[kb] = neg8(ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r));
+                }
+#pragma unroll
+                for (int ct = 0; ct < NT; ++ct) {
+#pragma unroll
+                    for (int kb = 0; kb < P::KBC; ++kb) {
+                        if (2 * kb <= ct) {
+                            const bf16* grow = GT + (size_t)(16 * ct + r) * P::LG;
+                            const F gf = (2 * kb + 1 <= ct) ? ld_frag<bf16>(grow, 32 * kb, g)
+                                                            : ld_frag_lo<bf16>(grow, 32 * kb, g);
+                            Uacc[o][0][ct] = mma(ecf[kb], gf, Uacc[o][0][ct]);
+                            Uacc[o][1][ct] = mma(esf[kb], gf, Uacc[o][1][ct]);
+                        }
+                    }
+                    const int j = 16 * ct + r;
+                    const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
+                    const floatx4 sn = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                    const floatx4 re = Uacc[o][0][ct], im = Uacc[o][1][ct];
+                    st4<bf16>(UT + (size_t)j * P::LU + 16 * mt + 4 * g, cs * re - sn * im);
+                    st4<bf16>(UT + (size_t)j * P::LU + MP + 16 * mt + 4 * g, sn * re + cs * im);
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- per-token chain on token tile wl; the slot matrix in LDS is unscaled
+        {
+            const int j = 16 * wl + r;
+            const long long pos_ll = a.t0 + tok0 + j;
+            const int pos = pos_ll < (1ll << 30) ? (int)pos_ll : (1 << 30);  // every threshold is below 2^30
+            F uf[P::KBM];
+#pragma unroll
+            for (int kb = 0; kb < P::KBM; ++kb) uf[kb] = ld_frag<bf16>(UT + (size_t)j * P::LU, 32 * kb, g);
+            floatx4 sc[P::NST];
+#pragma unroll
+            for (int s4 = 0; s4 < P::NST; ++s4) {
+                sc[s4] = zero4();
+#pragma unroll
+                for (int kb = 0; kb < P::KBM; ++kb)
+                    sc[s4] = mma(ld_frag<bf16>(sAB + (size_t)(16 * s4 + r) * P::LAB, 32 * kb, g), uf[kb], sc[s4]);
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int s4 = 0; s4 < P::NST; ++s4) {
+                const intx4 th = *reinterpret_cast<const intx4*>(sTheta + 16 * s4 + 4 * g);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    sc[s4][e] = pos < th[e] ? -INFINITY : sc[s4][e] * a.scale;
+                    mx = fmaxf(mx, sc[s4][e]);
+                }
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            float sum = 0.f;
+#pragma unroll
+            for (int s4 = 0; s4 < P::NST; ++s4)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float ex = __expf(sc[s4][e] - mx);
+                    sc[s4][e] = ex;
+                    sum += ex;
+                }
+            sum += __shfl_xor(sum, 16);
+            sum += __shfl_xor(sum, 32);
+            const float inv = 1.f / sum;
+            F pf[P::KBS];
+#pragma unroll
+            for (int kb = 0; kb < P::KBS; ++kb) pf[kb] = frag_from_acc<bf16>(sc[2 * kb] * inv, sc[2 * kb + 1] * inv);
+
+            // (6) [a | b] = P [A | B], the slot matrix read transposed
+            floatx4 wa[2 * NMT];
+#pragma unroll
+            for (int t = 0; t < 2 * NMT; ++t) {
+                wa[t] = zero4();
+#pragma unroll
+                for (int kb = 0; kb < P::KBS; ++kb) wa[t] = mma(ld_frag_tr(sAB, P::LAB, 16 * t, kb, g, r), pf[kb], wa[t]);
+            }
+#pragma unroll
+            for (int mt = 0; mt < NMT; ++mt) {
+                const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
+                const floatx4 sn = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                const floatx4 am = wa[mt], bm = wa[NMT + mt];
+                wa[mt] = am * cs + bm * sn;
+                wa[NMT + mt] = am * sn - bm * cs;
+            }
+            F wf[P::KBM];
+#pragma unroll
+            for (int kb = 0; kb < P::KBM; ++kb) wf[kb] = frag_from_acc<bf16>(wa[2 * kb], wa[2 * kb + 1]);
+
+            floatx4 oa[NDT];
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                oa[dt] = zero4();
+#pragma unroll
+                for (int kb = 0; kb < P::KBM; ++kb)
+                    oa[dt] = mma(ld_frag<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ, 32 * kb, g), wf[kb], oa[dt]);
+            }
+            floatx4 hh[NT];
+#pragma unroll
+            for (int kt = 0; kt < NT; ++kt) {
+                hh[kt] = zero4();
+                if (kt <= wl) {
+#pragma unroll
+                    for (int kb = 0; kb < P::KBM; ++kb)
+                        hh[kt] = mma(ld_frag<bf16>(sE + (size_t)(16 * kt + r) * P::LE, 32 * kb, g), wf[kb], hh[kt]);
+                    if (kt == wl) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (4 * g + e > r) hh[kt][e] = 0.f;
+                    }
+                }
+            }
+            // (9) O += V^T H^T, V read transposed
+#pragma unroll
+            for (int kb = 0; kb < P::KBC; ++kb) {
+                if (2 * kb <= wl) {
+                    const F hf = frag_from_acc<bf16>(hh[2 * kb], hh[2 * kb + 1]);
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) oa[dt] = mma(ld_frag_tr(Vs, P::LK, 16 * dt, kb, g, r), hf, oa[dt]);
+                }
+            }
+            if (j < c) {
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) st4<bf16>(ob + (size_t)(tok0 + j) * D + 16 * dt + 4 * g, oa[dt]);
+            }
+        }
+        __syncthreads();  // everyone done reading ZvT
+
+        // ---- (10) Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i]) on the owned mode tiles
+        if (live) {
+#pragma unroll
+            for (int kb = 0; kb < P::KBC; ++kb) {
+                F ktf[NDT], vtf[NDT];
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    ktf[dt] = ld_frag_tr(Ks, P::LK, 16 * dt, kb, g, r);
+                    vtf[dt] = ld_frag_tr(Vs, P::LK, 16 * dt, kb, g, r);
+                }
+#pragma unroll
+                for (int o = 0; o < OWN; ++o) {
+                    const int mt = wl + P::WPU * o;
+                    if (mt < NMT) {
+                        const F ecf = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
+                        const F esf = neg8(ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r));
+#pragma unroll
+                        for (int dt = 0; dt < NDT; ++dt) {
+                            Zk[o][0][dt] = mma(ktf[dt], ecf, Zk[o][0][dt]);
+                            Zk[o][1][dt] = mma(ktf[dt], esf, Zk[o][1][dt]);
+                            Zv[o][0][dt] = mma(ecf, vtf[dt], Zv[o][0][dt]);
+                            Zv[o][1][dt] = mma(esf, vtf[dt], Zv[o][1][dt]);
+                        }
+                    }
+                }
+            }
+            const float* Ec = (c == C) ? sRho + 2 * MP : E32h + (size_t)c * 2 * MP;
+#pragma unroll
+            for (int o = 0; o < OWN; ++o) {
+                const int mt = wl + P::WPU * o;
+                if (mt < NMT) {
+                    const float cc = Ec[16 * mt + r], ss = Ec[MP + 16 * mt + r];
+                    const floatx4 cv = ld4f(Ec + 16 * mt + 4 * g), sv = ld4f(Ec + MP + 16 * mt + 4 * g);
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) {
+                        const floatx4 kr = Zk[o][0][dt], ki = Zk[o][1][dt];
+                        Zk[o][0][dt] = cc * kr - ss * ki;
+                        Zk[o][1][dt] = ss * kr + cc * ki;
+                        const floatx4 vr = Zv[o][0][dt], vi = Zv[o][1][dt];
+                        Zv[o][0][dt] = cv * vr - sv * vi;
+                        Zv[o][1][dt] = sv * vr + cv * vi;
+                    }
+                }
+            }
+            pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
+        }
+    }
+
+    // ---- final state (last segment): Z = conj(rho) Z'
+    if (active && seg == a.nseg - 1) {
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = wl + P::WPU * o;
+            if (mt < NMT) {
+                const int m = 16 * mt + r;
+                const float c1 = E1[m], s1 = E1[MP + m];
+                const floatx4 cv = ld4f(E1 + 16 * mt + 4 * g), sv = ld4f(E1 + MP + 16 * mt + 4 * g);
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    if (a.sk_out && m < a.M) {
+                        const floatx4 re = Zk[o][0][dt], im = Zk[o][1][dt];
+                        st4f(a.sk_out + (((size_t)bh * 2 + 0) * a.M + m) * D + 16 * dt + 4 * g, c1 * re + s1 * im);
+                        st4f(a.sk_out + (((size_t)bh * 2 + 1) * a.M + m) * D + 16 * dt + 4 * g, c1 * im - s1 * re);
+                    }
+                    if (a.sv_out) {
+                        const floatx4 re = Zv[o][0][dt], im = Zv[o][1][dt];
+                        const floatx4 nr = cv * re + sv * im, ni = cv * im - sv * re;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int mv = 16 * mt + 4 * g + e;
+                            if (mv < a.M) {
+                                a.sv_out[(((size_t)bh * 2 + 0) * a.M + mv) * D + 16 * dt + r] = nr[e];
+                                a.sv_out[(((size_t)bh * 2 + 1) * a.M + mv) * D + 16 * dt + r] = ni[e];
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+}  // namespace bla

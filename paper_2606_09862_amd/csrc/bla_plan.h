@@ -22,6 +22,8 @@ struct Plan {
     float scale;
     int nch;             // chunks per sequence
     int nseg, cps;       // segments per sequence, chunks per segment
+    int upw;             // sequence units per forward workgroup (1, or 2 for the pair kernel)
+    int pair;            // 1 if the bf16 pair kernel runs the forward pass
     int cpb, nbs;        // chunks per summarised block, summarised blocks per sequence
     size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
     // workspace byte offsets
@@ -40,7 +42,7 @@ struct TableArgs {
     int* theta;     // [H][SP]        start-mask thresholds (INT32_MAX for padded slots)
     float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
     int M, S, MP, SP, C, Lblk, h0, nh, with_shared;
-    float scale;
+    float scale;    // factor folded into ABs (1 when the kernel applies the score scale itself)
     double T[kMaxHeadsPerTableLaunch];  // clamped periods of heads h0..h0+nh-1
 };
 
@@ -66,6 +68,7 @@ struct FwdArgs {
     int B, H, L, M;
     int nch, nseg, cps, cpb, nbs;
     long long t0;
+    float scale;  // score scale (applied by the pair kernel; folded into ABs otherwise)
 };
 
 struct StepArgs {
@@ -92,7 +95,9 @@ hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_state_copy(const float* src, float* dst, size_t n, hipStream_t s);
 hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
 
-// Whether a forward kernel exists for (bf16, D, MP, SP); LDS bytes it needs.
+// Whether a forward kernel exists for (bf16, D, MP, SP).
 bool forward_supported(int bf16, int D, int MP, int SP);
+// Sequence units per workgroup of the bf16 pair kernel (0: the one-unit forward kernel runs).
+int forward_units_per_wg(int bf16, int D, int MP, int SP);
 
 }  // namespace bla
