@@ -128,4 +128,27 @@ __device__ __forceinline__ floatx4 to_f4(bf16x4 x)
 }
 __device__ __forceinline__ floatx4 to_f4(floatx4 x) { return x; }
 
+// Reductions over the four 16-lane rows of a wave: lane (g, r) receives the result for
+// column r over g = 0..3.  The two lane-swap instructions exchange rows 0,1 <-> 2,3 and
+// 0 <-> 1, 2 <-> 3 in registers; each pair (kept, received) is the pair (x[l], x[l^32]) or
+// (x[l], x[l^16]) in some order, so every lane of a column ends with identical bits.
+__device__ __forceinline__ float rows_max(float x)
+{
+    const unsigned u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const unsigned v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows_sum(float x)
+{
+    const unsigned u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const unsigned v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 }  // namespace bla

@@ -644,8 +644,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                     mx = fmaxf(mx, sc[s4][e]);
                 }
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = rows_max(mx);
             float sum = 0.f;
 #pragma unroll
             for (int s4 = 0; s4 < P::NST; ++s4)
@@ -655,9 +654,8 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                     sc[s4][e] = ex;
                     sum += ex;
                 }
-            sum += __shfl_xor(sum, 16);
-            sum += __shfl_xor(sum, 32);
-            const float inv = 1.f / sum;
+            sum = rows_sum(sum);
+            const float inv = __builtin_amdgcn_rcpf(sum);  // sum >= 1: the maximum slot contributes exp(0)
             F pf[P::KBS];
 #pragma unroll
             for (int kb = 0; kb < P::KBS; ++kb) pf[kb] = frag_from_acc<T>(sc[2 * kb] * inv, sc[2 * kb + 1] * inv);

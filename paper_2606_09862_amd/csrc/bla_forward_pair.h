@@ -69,7 +69,7 @@ template <int D, int MP, int SP> struct Pair {
     static constexpr int LZ = 2 * MP + 4;    // Z'_v:      [D][LZ]
     static constexpr size_t AB_ELEMS = (size_t)SP * LAB;
     static constexpr size_t E_ELEMS = (size_t)C * LE;
-    static constexpr size_t SHARED_BYTES = 2 * (AB_ELEMS + E_ELEMS) + 2 * 2 * MP * 4 + SP * 4;
+    static constexpr size_t SHARED_BYTES = 2 * (AB_ELEMS + E_ELEMS) + 3 * 2 * MP * 4 + SP * 4;
     static constexpr size_t UNIT_ELEMS = 2 * (size_t)C * LK + (size_t)C * LQU + (size_t)C * LG + (size_t)D * LZ;
     static constexpr size_t UNIT_BYTES = 2 * UNIT_ELEMS;
     static constexpr int U = (SHARED_BYTES + 2 * UNIT_BYTES <= kMaxLds) ? 2 : 1;
@@ -171,8 +171,10 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
     bf16* sAB = reinterpret_cast<bf16*>(lds_raw);
     bf16* sE = sAB + P::AB_ELEMS;
-    float* sRho = reinterpret_cast<float*>(sE + P::E_ELEMS);  // rho, then rho^C
-    int* sTheta = reinterpret_cast<int*>(sRho + 4 * MP);
+    // rho, rho^C and rho^c_last (c_last: length of the last chunk, the same for every
+    // unit of the workgroup)
+    float* sRho = reinterpret_cast<float*>(sE + P::E_ELEMS);
+    int* sTheta = reinterpret_cast<int*>(sRho + 6 * MP);
 
     const int tid = threadIdx.x;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -198,9 +200,11 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     // ---- shared tables
     pair_copy<SP, 2 * MP, P::LAB, 256 * P::U>(sAB, (const bf16*)a.ABs, tid);
     pair_copy<C, 2 * MP, P::LE, 256 * P::U>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
+    const int c_last = a.L - (a.nch - 1) * C;
     for (int i = tid; i < 2 * MP; i += 256 * P::U) {
         sRho[i] = E32h[2 * MP + i];
         sRho[2 * MP + i] = E32h[(size_t)C * 2 * MP + i];
+        sRho[4 * MP + i] = E32h[(size_t)c_last * 2 * MP + i];
     }
     for (int i = tid; i < SP; i += 256 * P::U) sTheta[i] = a.theta[(size_t)h * SP + i];
 
@@ -383,8 +387,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     mx = fmaxf(mx, sc[s4][e]);
                 }
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = rows_max(mx);
             float sum = 0.f;
 #pragma unroll
             for (int s4 = 0; s4 < P::NST; ++s4)
@@ -394,9 +397,8 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     sc[s4][e] = ex;
                     sum += ex;
                 }
-            sum += __shfl_xor(sum, 16);
-            sum += __shfl_xor(sum, 32);
-            const float inv = 1.f / sum;
+            sum = rows_sum(sum);
+            const float inv = __builtin_amdgcn_rcpf(sum);  // sum >= 1: the maximum slot contributes exp(0)
             F pf[P::KBS];
 #pragma unroll
             for (int kb = 0; kb < P::KBS; ++kb) pf[kb] = frag_from_acc<bf16>(sc[2 * kb] * inv, sc[2 * kb + 1] * inv);
@@ -486,7 +488,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     }
                 }
             }
-            const float* Ec = (c == C) ? sRho + 2 * MP : E32h + (size_t)c * 2 * MP;
+            const float* Ec = sRho + (c == C ? 2 * MP : 4 * MP);  // a chunk shorter than C is the last one
 #pragma unroll
             for (int o = 0; o < OWN; ++o) {
                 const int mt = wl + P::WPU * o;
