@@ -130,20 +130,25 @@ def bench_forward(args, hip):
 
     for _ in range(args.warmup):
         call(None)
-    torch.cuda.synchronize(dev)
-    evs = [[hip.event() for _ in range(5)] for _ in range(args.steps)]
+    # whole steps, nothing recorded between the launches of a step
     t_start, t_stop = hip.event(), hip.event()
     torch.cuda.synchronize(dev)
     hip.record(t_start, sptr)
     for i in range(args.steps):
-        call(evs[i])
+        call(None)
     hip.record(t_stop, sptr)
     torch.cuda.synchronize(dev)
-    total_ms = hip.elapsed_ms(t_start, t_stop)
+    ms = hip.elapsed_ms(t_start, t_stop) / args.steps
+    # the same steps again with events between the phases (the forward kernel's duration
+    # for the roofline; the intervals of the other phases include the event overhead)
+    evs = [[hip.event() for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    for i in range(args.steps):
+        call(evs[i])
+    torch.cuda.synchronize(dev)
     phases = ["tables", "summary", "scan", "forward"]
     phase_ms = {ph: float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs]))
                 for j, ph in enumerate(phases)}
-    ms = total_ms / args.steps
     tokens = w.B * w.L
     flops = forward_flops_per_token_head(w.chunk, w.d, w.M, w.S) * w.B * w.H * w.L
     nbytes = forward_bytes(w.B, w.H, w.L, w.d, w.M, 2)

@@ -106,9 +106,10 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
             if (nseg > 1) {
                 // Blocks per segment: enough summary workgroups to fill the device, within
                 // the scratch cap; always a divisor of cps.
+                // The pair kernel combines the summaries itself: one block per segment.
                 int bps = 1;
                 const size_t unit_bytes = pl->unit_floats * sizeof(float);
-                while (units * (nseg - 1) * bps < 2 * cus && cps % (2 * bps) == 0 &&
+                while (!pl->pair && units * (nseg - 1) * bps < 2 * cus && cps % (2 * bps) == 0 &&
                        (size_t)units * (nseg - 1) * (2 * bps) * unit_bytes <= kMaxSummaryBytes)
                     bps *= 2;
                 pl->cpb = cps / bps;
@@ -129,7 +130,8 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->off_theta = off;  off = align_up(off + H * SP * 4);
     pl->off_rotblk = off; off = align_up(off + H * MP2 * 4);
     pl->off_summ = off;   off = align_up(off + (size_t)units * pl->nbs * pl->unit_floats * 4);
-    pl->off_carry = off;  off = align_up(off + (size_t)units * (pl->nseg - 1) * pl->unit_floats * 4);
+    const size_t ncarry = pl->pair ? 0 : (size_t)(pl->nseg - 1);  // the pair kernel needs no carries
+    pl->off_carry = off;  off = align_up(off + (size_t)units * ncarry * pl->unit_floats * 4);
     pl->total = off;
 }
 
@@ -271,7 +273,7 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     a.scale = pl.scale;
     if (pl.nseg > 1 && launch_summary(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
     if (!mark(2)) return BLA_ERR_HIP;
-    if (pl.nseg > 1 && launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    if (pl.nseg > 1 && !pl.pair && launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
     if (!mark(3)) return BLA_ERR_HIP;
     if (launch_forward(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
     if (!mark(4)) return BLA_ERR_HIP;

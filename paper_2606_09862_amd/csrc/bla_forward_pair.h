@@ -15,6 +15,11 @@
 //        Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i]),
 //    so one phase table serves steps (3), (8), (10) and the twiddles, and a
 //    ragged last chunk needs no table of its own (rows past c are zero).
+//  * Sequences are split into segments.  summary_pair_kernel reduces every segment
+//    but the last to its summary (step (10) alone from a zero state); a unit then
+//    starts from the preceding summaries combined in its prologue,
+//        Z'_g = rho^{L_s} o (... (rho^{L_s} o (rho Z_in) + S_0) ...) + S_{g-1},
+//    which is the state recurrence taken a whole segment (L_s tokens) at a time.
 #pragma once
 
 #include <math.h>
@@ -81,7 +86,8 @@ template <int D, int MP, int SP> struct Pair {
     static_assert(NT == WPU, "one token tile per wave of a unit");
 };
 
-template <int D, int MP, int SP> using PState = floatx4[Pair<D, MP, SP>::OWN][2][D / 16];
+template <int D, int MP> using PStateDM = floatx4[(MP / 16 + 3) / 4][2][D / 16];
+template <int D, int MP, int SP> using PState = PStateDM<D, MP>;
 template <int D, int MP, int SP> using PStage = bf16x8[Pair<D, MP, SP>::PPT];
 
 template <int D, int MP, int SP>
@@ -160,8 +166,177 @@ __device__ __forceinline__ void pair_write_zv(bf16* ZvT, const PState<D, MP, SP>
     }
 }
 
-// grid: H x ceil(B*nseg/U) workgroups of 256*U threads; workgroup (h, x) runs the
-// units 2x and 2x+1 (U = 2) of head h, units numbered over (b, segment).
+// Step (10) on the wave's owned mode tiles: Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i])
+// with K, V ([C][LK], rows past c zero) and the phase table ([C][LE]) read transposed
+// from LDS, and rho^c (cos | sin, float32) from Ec.
+template <int D, int MP, int LK, int LE>
+__device__ __forceinline__ void pair_advance(PStateDM<D, MP>& Zk, PStateDM<D, MP>& Zv, const bf16* Ks,
+                                             const bf16* Vs, const bf16* sE, const float* Ec, int wl,
+                                             int g, int r)
+{
+    using F = bf16x8;
+    constexpr int NMT = MP / 16, NDT = D / 16, OWN = (NMT + 3) / 4, KBC = kChunk / 32;
+#pragma unroll
+    for (int kb = 0; kb < KBC; ++kb) {
+        F ktf[NDT], vtf[NDT];
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            ktf[dt] = ld_frag_tr(Ks, LK, 16 * dt, kb, g, r);
+            vtf[dt] = ld_frag_tr(Vs, LK, 16 * dt, kb, g, r);
+        }
+#pragma unroll
+        for (int o = 0; o < OWN; ++o) {
+            const int mt = wl + 4 * o;
+            if (mt < NMT) {
+                const F ecf = ld_frag_tr(sE, LE, 16 * mt, kb, g, r);
+                const F esf = neg8(ld_frag_tr(sE, LE, MP + 16 * mt, kb, g, r));
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    Zk[o][0][dt] = mma(ktf[dt], ecf, Zk[o][0][dt]);
+                    Zk[o][1][dt] = mma(ktf[dt], esf, Zk[o][1][dt]);
+                    Zv[o][0][dt] = mma(ecf, vtf[dt], Zv[o][0][dt]);
+                    Zv[o][1][dt] = mma(esf, vtf[dt], Zv[o][1][dt]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 0; o < OWN; ++o) {
+        const int mt = wl + 4 * o;
+        if (mt < NMT) {
+            const float cc = Ec[16 * mt + r], ss = Ec[MP + 16 * mt + r];
+            const floatx4 cv = ld4f(Ec + 16 * mt + 4 * g), sv = ld4f(Ec + MP + 16 * mt + 4 * g);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const floatx4 kr = Zk[o][0][dt], ki = Zk[o][1][dt];
+                Zk[o][0][dt] = cc * kr - ss * ki;
+                Zk[o][1][dt] = ss * kr + cc * ki;
+                const floatx4 vr = Zv[o][0][dt], vi = Zv[o][1][dt];
+                Zv[o][0][dt] = cv * vr - sv * vi;
+                Zv[o][1][dt] = sv * vr + cv * vi;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// Segment summaries: one workgroup of 4 waves per (b, h, summarised block).  Every
+// summarised chunk is full (only the last chunk of a sequence can be shorter, and the
+// last segment is never summarised).  K and V are staged two chunks ahead.
+template <int D, int MP> struct SumPair {
+    static constexpr int C = kChunk;
+    static constexpr int LK = D + 12, LE = 2 * MP + 12;
+    static constexpr size_t E_ELEMS = (size_t)C * LE, KV_ELEMS = (size_t)C * LK;
+    static constexpr size_t LDS_BYTES = 2 * (E_ELEMS + 2 * KV_ELEMS) + 2 * MP * 4;
+    static constexpr int PIECES = 2 * C * D / 8;  // 16-byte pieces of K and V
+    static constexpr int PPT = (PIECES + 255) / 256;
+};
+template <int D, int MP> using SStage = bf16x8[SumPair<D, MP>::PPT];
+
+template <int D, int MP>
+__device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k, const bf16* v, int tid)
+{
+    using P = SumPair<D, MP>;
+    constexpr int PR = D / 8;
+#pragma unroll
+    for (int i = 0; i < P::PPT; ++i) {
+        const int u = tid + 256 * i;
+        if (P::PIECES % 256 == 0 || u < P::PIECES) {
+            const int which = u / (P::C * PR), rem = u % (P::C * PR);
+            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + (size_t)rem * 8);
+        }
+    }
+}
+
+template <int D, int MP>
+__device__ __forceinline__ void sum_stage_store(const SStage<D, MP>& st, bf16* Ks, bf16* Vs, int tid)
+{
+    using P = SumPair<D, MP>;
+    constexpr int PR = D / 8;
+#pragma unroll
+    for (int i = 0; i < P::PPT; ++i) {
+        const int u = tid + 256 * i;
+        if (P::PIECES % 256 == 0 || u < P::PIECES) {
+            const int which = u / (P::C * PR), rem = u % (P::C * PR);
+            bf16* dst = (which == 0 ? Ks : Vs) + (size_t)(rem / PR) * P::LK + 8 * (rem % PR);
+            const bf16x8 x = st[i];
+            *reinterpret_cast<bf16x4*>(dst) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
+            *reinterpret_cast<bf16x4*>(dst + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
+        }
+    }
+}
+
+// grid: (B * nbs) x H workgroups of 256 threads; block blk of sequence (b, h) covers
+// chunks [blk * cpb, (blk + 1) * cpb).
+template <int D, int MP>
+__global__ __launch_bounds__(256) void summary_pair_kernel(FwdArgs a)
+{
+    using P = SumPair<D, MP>;
+    constexpr int C = P::C, NMT = MP / 16, NDT = D / 16, OWN = (NMT + 3) / 4;
+    __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
+    bf16* sE = reinterpret_cast<bf16*>(lds_raw);
+    bf16* Ks = sE + P::E_ELEMS;
+    bf16* Vs = Ks + P::KV_ELEMS;
+    float* sRhoC = reinterpret_cast<float*>(Vs + P::KV_ELEMS);
+
+    const int tid = threadIdx.x;
+    const int wl = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = (tid & 63) >> 4, r = tid & 15;
+    const int h = blockIdx.y, b = blockIdx.x / a.nbs, blk = blockIdx.x % a.nbs;
+    const int bh = b * a.H + h;
+    const size_t first = (size_t)blk * a.cpb * C;
+    const bf16* kb_ = (const bf16*)a.k + ((size_t)bh * a.L + first) * D;
+    const bf16* vb = (const bf16*)a.v + ((size_t)bh * a.L + first) * D;
+
+    SStage<D, MP> st0, st1;
+    sum_stage_load<D, MP>(st0, kb_, vb, tid);
+    if (a.cpb > 1) sum_stage_load<D, MP>(st1, kb_ + (size_t)C * D, vb + (size_t)C * D, tid);
+    pair_copy<C, 2 * MP, P::LE, 256>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
+    const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
+    for (int i = tid; i < 2 * MP; i += 256) sRhoC[i] = E32h[(size_t)C * 2 * MP + i];
+
+    PStateDM<D, MP> Zk, Zv;
+#pragma unroll
+    for (int o = 0; o < OWN; ++o)
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) Zk[o][p][dt] = Zv[o][p][dt] = zero4();
+
+    for (int n = 0; n < a.cpb; ++n) {
+        __syncthreads();  // previous chunk done with Ks / Vs (and the tables visible)
+        sum_stage_store<D, MP>(st0, Ks, Vs, tid);
+#pragma unroll
+        for (int i = 0; i < P::PPT; ++i) st0[i] = st1[i];
+        if (n + 2 < a.cpb) {
+            const size_t off = (size_t)(n + 2) * C * D;
+            sum_stage_load<D, MP>(st1, kb_ + off, vb + off, tid);
+        }
+        __syncthreads();
+        pair_advance<D, MP, P::LK, P::LE>(Zk, Zv, Ks, Vs, sE, sRhoC, wl, g, r);
+    }
+
+    float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
+#pragma unroll
+    for (int o = 0; o < OWN; ++o) {
+        const int mt = wl + 4 * o;
+        if (mt < NMT) {
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    st4f(S + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[o][p][dt]);
+                    st4f(S + (size_t)2 * MP * D + ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
+                         Zv[o][p][dt]);
+                }
+        }
+    }
+}
+
+// grid: ceil(B*nseg/U) x H workgroups of 256*U threads; workgroup (x, h) runs the
+// units 2x and 2x+1 (U = 2) of head h.  Units are numbered over (b, i) with
+// i = 0, 1, 2, 3, ... taking segments 0, nseg-1, 1, nseg-2, ..., so that the two units
+// of a workgroup combine about nseg-1 segment summaries between them.
 template <int D, int MP, int SP>
 __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kernel(FwdArgs a)
 {
@@ -185,7 +360,8 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     const int per_head = a.B * a.nseg;
     const int v_unit = blockIdx.x * P::U + u;
     const bool active = v_unit < per_head;
-    const int b = active ? v_unit / a.nseg : 0, seg = active ? v_unit % a.nseg : 0;
+    const int b = active ? v_unit / a.nseg : 0, si = active ? v_unit % a.nseg : 0;
+    const int seg = (si & 1) ? a.nseg - 1 - (si >> 1) : (si >> 1);
     const int bh = b * a.H + h;
 
     bf16* base = reinterpret_cast<bf16*>(lds_raw + P::SHARED_BYTES + (size_t)u * P::UNIT_BYTES);
@@ -232,36 +408,58 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         for (int dt = 0; dt < NDT; ++dt) {
             Zk[o][0][dt] = Zk[o][1][dt] = Zv[o][0][dt] = Zv[o][1][dt] = zero4();
             if (mt < NMT && active) {
-                if (seg == 0) {
-                    const int m = 16 * mt + r;
-                    floatx4 kr = zero4(), ki = zero4(), vr = zero4(), vi = zero4();
-                    if (a.sk_in && m < a.M) {
-                        kr = ld4f(a.sk_in + (((size_t)bh * 2 + 0) * a.M + m) * D + 16 * dt + 4 * g);
-                        ki = ld4f(a.sk_in + (((size_t)bh * 2 + 1) * a.M + m) * D + 16 * dt + 4 * g);
-                    }
-                    if (a.sv_in) {
+                const int m = 16 * mt + r;
+                floatx4 kr = zero4(), ki = zero4(), vr = zero4(), vi = zero4();
+                if (a.sk_in && m < a.M) {
+                    kr = ld4f(a.sk_in + (((size_t)bh * 2 + 0) * a.M + m) * D + 16 * dt + 4 * g);
+                    ki = ld4f(a.sk_in + (((size_t)bh * 2 + 1) * a.M + m) * D + 16 * dt + 4 * g);
+                }
+                if (a.sv_in) {
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const int mv = 16 * mt + 4 * g + e;
-                            if (mv < a.M) {
-                                vr[e] = a.sv_in[(((size_t)bh * 2 + 0) * a.M + mv) * D + 16 * dt + r];
-                                vi[e] = a.sv_in[(((size_t)bh * 2 + 1) * a.M + mv) * D + 16 * dt + r];
-                            }
+                    for (int e = 0; e < 4; ++e) {
+                        const int mv = 16 * mt + 4 * g + e;
+                        if (mv < a.M) {
+                            vr[e] = a.sv_in[(((size_t)bh * 2 + 0) * a.M + mv) * D + 16 * dt + r];
+                            vi[e] = a.sv_in[(((size_t)bh * 2 + 1) * a.M + mv) * D + 16 * dt + r];
                         }
                     }
-                    const float c1 = E1[m], s1 = E1[MP + m];
-                    Zk[o][0][dt] = c1 * kr - s1 * ki;
-                    Zk[o][1][dt] = s1 * kr + c1 * ki;
-                    const floatx4 cv = ld4f(E1 + 16 * mt + 4 * g), sv = ld4f(E1 + MP + 16 * mt + 4 * g);
-                    Zv[o][0][dt] = cv * vr - sv * vi;
-                    Zv[o][1][dt] = sv * vr + cv * vi;
-                } else {
-                    const float* cy = a.carry + ((size_t)bh * (a.nseg - 1) + (seg - 1)) * 4 * MP * D;
+                }
+                const float c1 = E1[m], s1 = E1[MP + m];
+                Zk[o][0][dt] = c1 * kr - s1 * ki;
+                Zk[o][1][dt] = s1 * kr + c1 * ki;
+                const floatx4 cv = ld4f(E1 + 16 * mt + 4 * g), sv = ld4f(E1 + MP + 16 * mt + 4 * g);
+                Zv[o][0][dt] = cv * vr - sv * vi;
+                Zv[o][1][dt] = sv * vr + cv * vi;
+            }
+        }
+    }
+    // combine the summaries of the blocks before this segment (Horner, block by block)
+    if (active && seg > 0) {
+        const int nblk = seg * (a.cps / a.cpb);
+        const float* rb = a.rotblk + (size_t)h * 2 * MP;
+        const float* Sb = a.summ + (size_t)bh * a.nbs * 4 * MP * D;
+        for (int j = 0; j < nblk; ++j) {
+            const float* Sj = Sb + (size_t)j * 4 * MP * D;
 #pragma unroll
-                    for (int p = 0; p < 2; ++p) {
-                        Zk[o][p][dt] = ld4f(cy + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
-                        Zv[o][p][dt] =
-                            ld4f(cy + (size_t)2 * MP * D + ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+            for (int o = 0; o < OWN; ++o) {
+                const int mt = wl + P::WPU * o;
+                if (mt < NMT) {
+                    const float cc = rb[16 * mt + r], ss = rb[MP + 16 * mt + r];
+                    const floatx4 cv = ld4f(rb + 16 * mt + 4 * g), sv = ld4f(rb + MP + 16 * mt + 4 * g);
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) {
+                        const floatx4 skr = ld4f(Sj + ((size_t)0 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
+                        const floatx4 ski = ld4f(Sj + ((size_t)1 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
+                        const floatx4 svr =
+                            ld4f(Sj + (size_t)2 * MP * D + ((size_t)0 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+                        const floatx4 svi =
+                            ld4f(Sj + (size_t)2 * MP * D + ((size_t)1 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+                        const floatx4 kr = Zk[o][0][dt], ki = Zk[o][1][dt];
+                        Zk[o][0][dt] = cc * kr - ss * ki + skr;
+                        Zk[o][1][dt] = ss * kr + cc * ki + ski;
+                        const floatx4 vr = Zv[o][0][dt], vi = Zv[o][1][dt];
+                        Zv[o][0][dt] = cv * vr - sv * vi + svr;
+                        Zv[o][1][dt] = sv * vr + cv * vi + svi;
                     }
                 }
             }
@@ -462,50 +660,10 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         }
         __syncthreads();  // everyone done reading ZvT
 
-        // ---- (10) Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i]) on the owned mode tiles
+        // ---- (10) state update on the owned mode tiles
         if (live) {
-#pragma unroll
-            for (int kb = 0; kb < P::KBC; ++kb) {
-                F ktf[NDT], vtf[NDT];
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    ktf[dt] = ld_frag_tr(Ks, P::LK, 16 * dt, kb, g, r);
-                    vtf[dt] = ld_frag_tr(Vs, P::LK, 16 * dt, kb, g, r);
-                }
-#pragma unroll
-                for (int o = 0; o < OWN; ++o) {
-                    const int mt = wl + P::WPU * o;
-                    if (mt < NMT) {
-                        const F ecf = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
-                        const F esf = neg8(ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r));
-#pragma unroll
-                        for (int dt = 0; dt < NDT; ++dt) {
-                            Zk[o][0][dt] = mma(ktf[dt], ecf, Zk[o][0][dt]);
-                            Zk[o][1][dt] = mma(ktf[dt], esf, Zk[o][1][dt]);
-                            Zv[o][0][dt] = mma(ecf, vtf[dt], Zv[o][0][dt]);
-                            Zv[o][1][dt] = mma(esf, vtf[dt], Zv[o][1][dt]);
-                        }
-                    }
-                }
-            }
             const float* Ec = sRho + (c == C ? 2 * MP : 4 * MP);  // a chunk shorter than C is the last one
-#pragma unroll
-            for (int o = 0; o < OWN; ++o) {
-                const int mt = wl + P::WPU * o;
-                if (mt < NMT) {
-                    const float cc = Ec[16 * mt + r], ss = Ec[MP + 16 * mt + r];
-                    const floatx4 cv = ld4f(Ec + 16 * mt + 4 * g), sv = ld4f(Ec + MP + 16 * mt + 4 * g);
-#pragma unroll
-                    for (int dt = 0; dt < NDT; ++dt) {
-                        const floatx4 kr = Zk[o][0][dt], ki = Zk[o][1][dt];
-                        Zk[o][0][dt] = cc * kr - ss * ki;
-                        Zk[o][1][dt] = ss * kr + cc * ki;
-                        const floatx4 vr = Zv[o][0][dt], vi = Zv[o][1][dt];
-                        Zv[o][0][dt] = cv * vr - sv * vi;
-                        Zv[o][1][dt] = sv * vr + cv * vi;
-                    }
-                }
-            }
+            pair_advance<D, MP, P::LK, P::LE>(Zk, Zv, Ks, Vs, sE, Ec, wl, g, r);
             pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
         }
     }
