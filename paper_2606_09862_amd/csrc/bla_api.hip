@@ -158,6 +158,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.h0 = h0;
         a.nh = pl.H - h0 < kMaxHeadsPerTableLaunch ? pl.H - h0 : kMaxHeadsPerTableLaunch;
         a.with_shared = h0 == 0;
+        a.conj_tab = pl.pair;
         a.scale = pl.pair ? 1.f : pl.scale;  // the pair kernel reads A | B unscaled
         for (int i = 0; i < a.nh; ++i) {
             const double tmin = 2.0 * pl.M - 1.0;

@@ -43,7 +43,7 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
             EbarT[(size_t)m * C + j] = (T)(float)cs;           // conj(rho^j)
             EbarT[(size_t)(MP + m) * C + j] = (T)(float)(-sn);
             Etab[(size_t)j * MP2 + m] = (T)(float)cs;
-            Etab[(size_t)j * MP2 + MP + m] = (T)(float)sn;
+            Etab[(size_t)j * MP2 + MP + m] = (T)(float)(a.conj_tab ? -sn : sn);
         }
         if (j >= 1) {                                          // rho^{C-i} at i = C - j
             ErevT[(size_t)m * C + (C - j)] = (T)(float)cs;

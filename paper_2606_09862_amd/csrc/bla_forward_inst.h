@@ -73,8 +73,9 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
     template <> hipError_t Launch<T, D, MP, SP>::summary(const Plan& p, const FwdArgs& a, hipStream_t s) \
     {                                                                                                   \
         if constexpr (pair_units<T, D, MP, SP>() > 0) {                                                 \
-            hipLaunchKernelGGL((summary_pair_kernel<D, MP>), dim3((unsigned)(p.B * p.nbs), (unsigned)p.H), \
-                               dim3(256), 0, s, a);                                                     \
+            hipLaunchKernelGGL((summary_pair_kernel<D, MP>),                                            \
+                               dim3((unsigned)(p.B * p.nbs * summary_splits<D, MP>()), (unsigned)p.H),   \
+                               dim3(summary_threads<D, MP>()), 0, s, a);                                \
         } else {                                                                                        \
             hipLaunchKernelGGL((summary_kernel<T, D, MP>), dim3((unsigned)(p.B * p.H * p.nbs)),         \
                                dim3(kThreads), 0, s, a);                                                \

@@ -11,6 +11,10 @@
 //    matrix [A|B] with the reduction over slots; the phase table with the
 //    reduction over tokens; K and V with the reduction over tokens) is read with
 //    the transposing LDS load ds_read_b64_tr_b16.
+//  * The phase table holds conj(rho^i) = [cos | -sin] (row i, modes along the row).
+//    It serves the twiddles, the transposed operands of steps (3) and (10) and the
+//    rows of step (8) without sign changes: the readout weights are kept as
+//    [Re W'' | -Im W''] and Z'_v is published as [Re | Im].
 //  * The state update uses rho^{c-i} = rho^c conj(rho^i):
 //        Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i]),
 //    so one phase table serves steps (3), (8), (10) and the twiddles, and a
@@ -45,14 +49,6 @@ __device__ __forceinline__ bf16x8 ld_frag_tr(const bf16* M, int ld, int x0, int 
 {
     const bf16* p = M + (size_t)(32 * kb + 4 * g + (r >> 2)) * ld + x0 + 4 * (r & 3);
     return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
-}
-
-__device__ __forceinline__ bf16x8 neg8(bf16x8 x)
-{
-    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-    u32x4 u = __builtin_bit_cast(u32x4, x);
-    u ^= 0x80008000u;
-    return __builtin_bit_cast(bf16x8, u);
 }
 
 template <int D, int MP, int SP> struct Pair {
@@ -90,6 +86,7 @@ template <int D, int MP> using PStateDM = floatx4[(MP / 16 + 3) / 4][2][D / 16];
 template <int D, int MP, int SP> using PState = PStateDM<D, MP>;
 template <int D, int MP, int SP> using PStage = bf16x8[Pair<D, MP, SP>::PPT];
 
+// ut: thread index within the unit (0..255); q, k, v: the chunk's first rows.
 template <int D, int MP, int SP>
 __device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf16* q,
                                                 const bf16* k, const bf16* v, int c, int ut)
@@ -102,7 +99,8 @@ __device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf1
         if (P::PIECES % 256 == 0 || u < P::PIECES) {
             const int which = u / (P::C * PR), rem = u % (P::C * PR);
             const int row = min(rem / PR, c - 1), pc = rem % PR;
-            const bf16* src = (which == 0 ? q : which == 1 ? k : v) + (size_t)row * D + 8 * pc;
+            const unsigned off = (unsigned)(row * D + 8 * pc);  // within one chunk
+            const bf16* src = (which == 0 ? q : which == 1 ? k : v) + off;
             st[i] = *reinterpret_cast<const bf16x8*>(src);
         }
     }
@@ -121,7 +119,7 @@ __device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf
             const int which = u / (P::C * PR), rem = u % (P::C * PR);
             const int row = rem / PR, pc = rem % PR;
             bf16* dst = which == 0 ? Qs + (size_t)row * P::LQ : (which == 1 ? Ks : Vs) + (size_t)row * P::LK;
-            const bf16x8 x = row < c ? st[i] : bf16x8{};
+            const bf16x8 x = (c == P::C || row < c) ? st[i] : bf16x8{};
             *reinterpret_cast<bf16x4*>(dst + 8 * pc) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
             *reinterpret_cast<bf16x4*>(dst + 8 * pc + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
         }
@@ -160,7 +158,7 @@ __device__ __forceinline__ void pair_write_zv(bf16* ZvT, const PState<D, MP, SP>
 #pragma unroll
             for (int dt = 0; dt < P::NDT; ++dt) {
                 st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + 16 * mt + 4 * g, Zv[o][0][dt]);
-                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + MP + 16 * mt + 4 * g, -Zv[o][1][dt]);
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + MP + 16 * mt + 4 * g, Zv[o][1][dt]);
             }
         }
     }
@@ -189,7 +187,7 @@ __device__ __forceinline__ void pair_advance(PStateDM<D, MP>& Zk, PStateDM<D, MP
             const int mt = wl + 4 * o;
             if (mt < NMT) {
                 const F ecf = ld_frag_tr(sE, LE, 16 * mt, kb, g, r);
-                const F esf = neg8(ld_frag_tr(sE, LE, MP + 16 * mt, kb, g, r));
+                const F esf = ld_frag_tr(sE, LE, MP + 16 * mt, kb, g, r);
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) {
                     Zk[o][0][dt] = mma(ktf[dt], ecf, Zk[o][0][dt]);
@@ -220,30 +218,52 @@ __device__ __forceinline__ void pair_advance(PStateDM<D, MP>& Zk, PStateDM<D, MP
 }
 
 // ---------------------------------------------------------------------------------
-// Segment summaries: one workgroup of 4 waves per (b, h, summarised block).  Every
-// summarised chunk is full (only the last chunk of a sequence can be shorter, and the
-// last segment is never summarised).  K and V are staged two chunks ahead.
+// Segment summaries: DS workgroups per (b, h, summarised block), each reducing DW = D/DS
+// columns of K and V.  Every summarised chunk is full (only the last chunk of a sequence
+// can be shorter, and the last segment is never summarised).
+//
+// Wave w owns column tiles wd + WD*i of its workgroup and mode tiles wm + WM*j
+// (w = wd + WD*wm): it reads from LDS only the K/V columns of its tiles, and keeps the
+// phase-table fragments of its mode tiles in registers for the whole block when they
+// fit.  K and V are staged several chunks ahead in registers and double-buffered in LDS
+// (one barrier per chunk).
 template <int D, int MP> struct SumPair {
-    static constexpr int C = kChunk;
-    static constexpr int LK = D + 12, LE = 2 * MP + 12;
+    static constexpr int C = kChunk, KBC = C / 32;
+    static constexpr int DS = D >= 128 ? 2 : 1, DW = D / DS;
+    static constexpr int NDT = DW / 16, NMT = MP / 16;
+    static constexpr int WD = NDT < 4 ? NDT : 4, WM = WD == 2 ? 2 : 1, NW = WD * WM;
+    static constexpr int NTHR = 64 * NW;
+    static constexpr int ODT = NDT / WD, OMT = (NMT + WM - 1) / WM;
+    static constexpr bool EREG = 16 * OMT <= 64;  // phase-table fragments held in VGPRs
+    // K/V row stride: 16 elements of pad puts the four rows of a transposed read's
+    // 16-lane group 8 banks apart (conflict-free)
+    static constexpr int LK = DW + 16;
+    static constexpr int LE = 2 * MP + 12;
     static constexpr size_t E_ELEMS = (size_t)C * LE, KV_ELEMS = (size_t)C * LK;
-    static constexpr size_t LDS_BYTES = 2 * (E_ELEMS + 2 * KV_ELEMS) + 2 * MP * 4;
-    static constexpr int PIECES = 2 * C * D / 8;  // 16-byte pieces of K and V
-    static constexpr int PPT = (PIECES + 255) / 256;
+    static constexpr size_t LDS_BYTES = 2 * (E_ELEMS + 4 * KV_ELEMS) + 2 * MP * 4;
+    static constexpr int PR = DW / 8;                 // 16-byte pieces per row of a tile
+    static constexpr int PIECES = 2 * C * PR;         // pieces of K and V per chunk
+    static constexpr int PPT = (PIECES + NTHR - 1) / NTHR;
+    static constexpr int NPF = 2;  // chunks in flight in registers (plus one in LDS)
+    static_assert(NDT % WD == 0, "column tiles split evenly over the waves");
+    static_assert(NPF % 2 == 0, "the LDS buffer parity follows the unrolled stage index");
 };
 template <int D, int MP> using SStage = bf16x8[SumPair<D, MP>::PPT];
+template <int D, int MP> using SState = floatx4[SumPair<D, MP>::OMT][SumPair<D, MP>::ODT][2];
+template <int D, int MP> using SEFrag = bf16x8[SumPair<D, MP>::EREG ? SumPair<D, MP>::OMT : 1][SumPair<D, MP>::KBC][2];
 
+// k, v: first row of the chunk, column offset of the workgroup's slice applied
 template <int D, int MP>
 __device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k, const bf16* v, int tid)
 {
     using P = SumPair<D, MP>;
-    constexpr int PR = D / 8;
 #pragma unroll
     for (int i = 0; i < P::PPT; ++i) {
-        const int u = tid + 256 * i;
-        if (P::PIECES % 256 == 0 || u < P::PIECES) {
-            const int which = u / (P::C * PR), rem = u % (P::C * PR);
-            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + (size_t)rem * 8);
+        const int u = tid + P::NTHR * i;
+        if (P::PIECES % P::NTHR == 0 || u < P::PIECES) {
+            const int which = u / (P::C * P::PR), rem = u % (P::C * P::PR);
+            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + (size_t)(rem / P::PR) * D +
+                                                     8 * (rem % P::PR));
         }
     }
 }
@@ -252,13 +272,12 @@ template <int D, int MP>
 __device__ __forceinline__ void sum_stage_store(const SStage<D, MP>& st, bf16* Ks, bf16* Vs, int tid)
 {
     using P = SumPair<D, MP>;
-    constexpr int PR = D / 8;
 #pragma unroll
     for (int i = 0; i < P::PPT; ++i) {
-        const int u = tid + 256 * i;
-        if (P::PIECES % 256 == 0 || u < P::PIECES) {
-            const int which = u / (P::C * PR), rem = u % (P::C * PR);
-            bf16* dst = (which == 0 ? Ks : Vs) + (size_t)(rem / PR) * P::LK + 8 * (rem % PR);
+        const int u = tid + P::NTHR * i;
+        if (P::PIECES % P::NTHR == 0 || u < P::PIECES) {
+            const int which = u / (P::C * P::PR), rem = u % (P::C * P::PR);
+            bf16* dst = (which == 0 ? Ks : Vs) + (size_t)(rem / P::PR) * P::LK + 8 * (rem % P::PR);
             const bf16x8 x = st[i];
             *reinterpret_cast<bf16x4*>(dst) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
             *reinterpret_cast<bf16x4*>(dst + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
@@ -266,69 +285,223 @@ __device__ __forceinline__ void sum_stage_store(const SStage<D, MP>& st, bf16* K
     }
 }
 
-// grid: (B * nbs) x H workgroups of 256 threads; block blk of sequence (b, h) covers
-// chunks [blk * cpb, (blk + 1) * cpb).
+template <int D, int MP> constexpr int summary_threads() { return SumPair<D, MP>::NTHR; }
+template <int D, int MP> constexpr int summary_splits() { return SumPair<D, MP>::DS; }
+
+// grid: (B * nbs * DS) x H workgroups of NTHR threads; workgroup x covers column slice
+// x % DS of block (x / DS) % nbs of sequence (b = x / (DS * nbs), h), i.e. chunks
+// [blk * cpb, (blk + 1) * cpb).
 template <int D, int MP>
-__global__ __launch_bounds__(256) void summary_pair_kernel(FwdArgs a)
+__global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(FwdArgs a)
 {
     using P = SumPair<D, MP>;
-    constexpr int C = P::C, NMT = MP / 16, NDT = D / 16, OWN = (NMT + 3) / 4;
+    using F = bf16x8;
+    constexpr int C = P::C, NMT = P::NMT, ODT = P::ODT, OMT = P::OMT, WD = P::WD, WM = P::WM, DS = P::DS;
     __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
     bf16* sE = reinterpret_cast<bf16*>(lds_raw);
-    bf16* Ks = sE + P::E_ELEMS;
-    bf16* Vs = Ks + P::KV_ELEMS;
-    float* sRhoC = reinterpret_cast<float*>(Vs + P::KV_ELEMS);
+    bf16* KV = sE + P::E_ELEMS;  // [buffer][K | V][C][LK]
+    float* sRhoC = reinterpret_cast<float*>(KV + 4 * P::KV_ELEMS);
 
     const int tid = threadIdx.x;
-    const int wl = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    __builtin_assume(w >= 0 && w < P::NW);
+    // with one wave row along the modes every wave owns every mode tile (known statically)
+    const int wd = WM == 1 ? w : w % WD, wm = WM == 1 ? 0 : w / WD;
     const int g = (tid & 63) >> 4, r = tid & 15;
-    const int h = blockIdx.y, b = blockIdx.x / a.nbs, blk = blockIdx.x % a.nbs;
+    const int h = blockIdx.y, ds = blockIdx.x % DS, blk = (blockIdx.x / DS) % a.nbs, b = blockIdx.x / (DS * a.nbs);
     const int bh = b * a.H + h;
     const size_t first = (size_t)blk * a.cpb * C;
-    const bf16* kb_ = (const bf16*)a.k + ((size_t)bh * a.L + first) * D;
-    const bf16* vb = (const bf16*)a.v + ((size_t)bh * a.L + first) * D;
+    const bf16* kb_ = (const bf16*)a.k + ((size_t)bh * a.L + first) * D + ds * P::DW;
+    const bf16* vb = (const bf16*)a.v + ((size_t)bh * a.L + first) * D + ds * P::DW;
 
-    SStage<D, MP> st0, st1;
-    sum_stage_load<D, MP>(st0, kb_, vb, tid);
-    if (a.cpb > 1) sum_stage_load<D, MP>(st1, kb_ + (size_t)C * D, vb + (size_t)C * D, tid);
-    pair_copy<C, 2 * MP, P::LE, 256>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
+    // tables first: their loads are then the oldest in flight when they are stored
+    pair_copy<C, 2 * MP, P::LE, P::NTHR>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
-    for (int i = tid; i < 2 * MP; i += 256) sRhoC[i] = E32h[(size_t)C * 2 * MP + i];
+    for (int i = tid; i < 2 * MP; i += P::NTHR) sRhoC[i] = E32h[(size_t)C * 2 * MP + i];
 
-    PStateDM<D, MP> Zk, Zv;
+    // NPF chunks of K/V in flight ahead of the one being reduced.  The loop is unrolled
+    // NPF times so that the staging registers keep fixed roles, and every load is
+    // unconditional (chunk indices past the block re-read its last chunk), so the wait
+    // before each store covers exactly the loads of that stage.
+    constexpr int NPF = P::NPF;
+    const int last = a.cpb - 1;
+    SStage<D, MP> st[NPF];
 #pragma unroll
-    for (int o = 0; o < OWN; ++o)
-#pragma unroll
-        for (int p = 0; p < 2; ++p)
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) Zk[o][p][dt] = Zv[o][p][dt] = zero4();
+    for (int i = 0; i < NPF; ++i) {
+        const size_t off = (size_t)min(i, last) * C * D;
+        sum_stage_load<D, MP>(st[i], kb_ + off, vb + off, tid);
+    }
+    sum_stage_store<D, MP>(st[0], KV, KV + P::KV_ELEMS, tid);
+    {
+        const size_t off = (size_t)min(NPF, last) * C * D;
+        sum_stage_load<D, MP>(st[0], kb_ + off, vb + off, tid);
+    }
+    __syncthreads();  // tables and chunk 0 visible
 
-    for (int n = 0; n < a.cpb; ++n) {
-        __syncthreads();  // previous chunk done with Ks / Vs (and the tables visible)
-        sum_stage_store<D, MP>(st0, Ks, Vs, tid);
+    // conj(rho^i) fragments of the owned mode tiles: [cos | -sin] with the reduction over i
+    SEFrag<D, MP> ef;
+    if constexpr (P::EREG) {
 #pragma unroll
-        for (int i = 0; i < P::PPT; ++i) st0[i] = st1[i];
-        if (n + 2 < a.cpb) {
-            const size_t off = (size_t)(n + 2) * C * D;
-            sum_stage_load<D, MP>(st1, kb_ + off, vb + off, tid);
+        for (int j = 0; j < OMT; ++j) {
+            const int mt = min(wm + WM * j, NMT - 1);
+#pragma unroll
+            for (int kb = 0; kb < P::KBC; ++kb) {
+                ef[j][kb][0] = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
+                ef[j][kb][1] = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
+            }
         }
-        __syncthreads();
-        pair_advance<D, MP, P::LK, P::LE>(Zk, Zv, Ks, Vs, sE, sRhoC, wl, g, r);
     }
 
+    SState<D, MP> Zk, Zv;  // [mode tile][column tile][Re, Im]
+#pragma unroll
+    for (int j = 0; j < OMT; ++j)
+#pragma unroll
+        for (int i = 0; i < ODT; ++i) Zk[j][i][0] = Zk[j][i][1] = Zv[j][i][0] = Zv[j][i][1] = zero4();
+
+    // Per chunk: Zk <- rho^C o (Zk + Yk) and Zv <- rho^C o (Zv + Yv).  The rotation of Zv
+    // is deferred to the start of the next chunk, so that each block below pairs 16
+    // matrix-core products with 64 independent vector operations:
+    //   block 1: Zk += Yk (MFMA)  with  Zv <- rho^C o Zv (previous chunk's rotation)
+    //   block 2: Zv += Yv (MFMA)  with  Zk <- rho^C o Zk
+    for (int n0 = 0; n0 < a.cpb; n0 += NPF) {
+#pragma unroll
+        for (int s = 0; s < NPF; ++s) {
+            const int n = n0 + s;
+            const bf16* Ks = KV + (size_t)(s & 1) * 2 * P::KV_ELEMS;  // chunk n (n and s share parity)
+            const bf16* Vs = Ks + P::KV_ELEMS;
+            // chunk n + 1 into the other buffer (last read by chunk n - 1, before the
+            // previous barrier), then chunk n + 1 + NPF into the freed registers
+            {
+                const int s1 = (s + 1) % NPF;  // a constant once the loop is unrolled
+                bf16* Kn = KV + (size_t)(s1 & 1) * 2 * P::KV_ELEMS;
+                sum_stage_store<D, MP>(st[s1], Kn, Kn + P::KV_ELEMS, tid);
+                const size_t off = (size_t)min(n + 1 + NPF, last) * C * D;
+                sum_stage_load<D, MP>(st[s1], kb_ + off, vb + off, tid);
+            }
+            if (n < a.cpb) {
+                F ktf[P::KBC][ODT], vtf[P::KBC][ODT];
+#pragma unroll
+                for (int kb = 0; kb < P::KBC; ++kb)
+#pragma unroll
+                    for (int i = 0; i < ODT; ++i) {
+                        ktf[kb][i] = ld_frag_tr(Ks, P::LK, 16 * (wd + WD * i), kb, g, r);
+                        vtf[kb][i] = ld_frag_tr(Vs, P::LK, 16 * (wd + WD * i), kb, g, r);
+                    }
+                // block 1
+#pragma unroll
+                for (int kb = 0; kb < P::KBC; ++kb)
+#pragma unroll
+                    for (int j = 0; j < OMT; ++j) {
+                        const int mt = wm + WM * j;
+                        if (mt < NMT) {
+                            F ecf, esf;
+                            if constexpr (P::EREG) {
+                                ecf = ef[j][kb][0];
+                                esf = ef[j][kb][1];
+                            } else {
+                                ecf = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
+                                esf = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
+                            }
+#pragma unroll
+                            for (int i = 0; i < ODT; ++i) {
+                                Zk[j][i][0] = mma(ktf[kb][i], ecf, Zk[j][i][0]);
+                                Zk[j][i][1] = mma(ktf[kb][i], esf, Zk[j][i][1]);
+                            }
+                        }
+                    }
+#pragma unroll
+                for (int j = 0; j < OMT; ++j) {
+                    const int mt = wm + WM * j;
+                    if (mt < NMT) {
+                        const floatx4 cv = ld4f(sRhoC + 16 * mt + 4 * g), sv = ld4f(sRhoC + MP + 16 * mt + 4 * g);
+#pragma unroll
+                        for (int i = 0; i < ODT; ++i) {
+                            const floatx4 vr = Zv[j][i][0], vi = Zv[j][i][1];
+                            Zv[j][i][0] = cv * vr - sv * vi;
+                            Zv[j][i][1] = sv * vr + cv * vi;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 4 * ODT * OMT; ++q) {
+                    __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);  // one MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x2, 4, 0);  // four VALU
+                }
+                // block 2
+#pragma unroll
+                for (int kb = 0; kb < P::KBC; ++kb)
+#pragma unroll
+                    for (int j = 0; j < OMT; ++j) {
+                        const int mt = wm + WM * j;
+                        if (mt < NMT) {
+                            F ecf, esf;
+                            if constexpr (P::EREG) {
+                                ecf = ef[j][kb][0];
+                                esf = ef[j][kb][1];
+                            } else {
+                                ecf = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
+                                esf = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
+                            }
+#pragma unroll
+                            for (int i = 0; i < ODT; ++i) {
+                                Zv[j][i][0] = mma(ecf, vtf[kb][i], Zv[j][i][0]);
+                                Zv[j][i][1] = mma(esf, vtf[kb][i], Zv[j][i][1]);
+                            }
+                        }
+                    }
+#pragma unroll
+                for (int j = 0; j < OMT; ++j) {
+                    const int mt = wm + WM * j;
+                    if (mt < NMT) {
+                        const float cc = sRhoC[16 * mt + r], ss = sRhoC[MP + 16 * mt + r];
+#pragma unroll
+                        for (int i = 0; i < ODT; ++i) {
+                            const floatx4 kr = Zk[j][i][0], ki = Zk[j][i][1];
+                            Zk[j][i][0] = cc * kr - ss * ki;
+                            Zk[j][i][1] = ss * kr + cc * ki;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 4 * ODT * OMT; ++q) {
+                    __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x2, 4, 0);
+                }
+            }
+            __syncthreads();  // chunk n + 1 visible; chunk n's buffer free
+        }
+    }
+    // the deferred rotation of the last chunk
+#pragma unroll
+    for (int j = 0; j < OMT; ++j) {
+        const int mt = wm + WM * j;
+        if (mt < NMT) {
+            const floatx4 cv = ld4f(sRhoC + 16 * mt + 4 * g), sv = ld4f(sRhoC + MP + 16 * mt + 4 * g);
+#pragma unroll
+            for (int i = 0; i < ODT; ++i) {
+                const floatx4 vr = Zv[j][i][0], vi = Zv[j][i][1];
+                Zv[j][i][0] = cv * vr - sv * vi;
+                Zv[j][i][1] = sv * vr + cv * vi;
+            }
+        }
+    }
+
+    // Zk tiles hold (d rows, m columns), Zv tiles (m rows, d columns)
     float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
 #pragma unroll
-    for (int o = 0; o < OWN; ++o) {
-        const int mt = wl + 4 * o;
+    for (int j = 0; j < OMT; ++j) {
+        const int mt = wm + WM * j;
         if (mt < NMT) {
 #pragma unroll
-            for (int p = 0; p < 2; ++p)
+            for (int i = 0; i < ODT; ++i) {
+                const int dt = ds * P::NDT + wd + WD * i;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    st4f(S + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[o][p][dt]);
+                for (int p = 0; p < 2; ++p) {
+                    st4f(S + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[j][i][p]);
                     st4f(S + (size_t)2 * MP * D + ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
-                         Zv[o][p][dt]);
+                         Zv[j][i][p]);
                 }
+            }
         }
     }
 }
@@ -354,7 +527,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     const int tid = threadIdx.x;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int u = wv / P::WPU, wl = wv % P::WPU;  // unit and wave within the unit
-    const int ut = tid - 256 * u;                  // thread index within the unit
+    const int ut = tid & 255;                      // thread index within the unit
     const int g = (tid & 63) >> 4, r = tid & 15;
     const int h = blockIdx.y;
     const int per_head = a.B * a.nseg;
@@ -534,7 +707,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 #pragma unroll
                 for (int kb = 0; kb < P::KBC; ++kb) {
                     ecf[kb] = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
-                    esf[kb] = neg8(ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r));
+                    esf[kb] = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
                 }
 #pragma unroll
                 for (int ct = 0; ct < NT; ++ct) {
@@ -550,10 +723,10 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     }
                     const int j = 16 * ct + r;
                     const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
-                    const floatx4 sn = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                    const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
                     const floatx4 re = Uacc[o][0][ct], im = Uacc[o][1][ct];
-                    st4<bf16>(UT + (size_t)j * P::LU + 16 * mt + 4 * g, cs * re - sn * im);
-                    st4<bf16>(UT + (size_t)j * P::LU + MP + 16 * mt + 4 * g, sn * re + cs * im);
+                    st4<bf16>(UT + (size_t)j * P::LU + 16 * mt + 4 * g, cs * re + ns * im);
+                    st4<bf16>(UT + (size_t)j * P::LU + MP + 16 * mt + 4 * g, cs * im - ns * re);
                 }
             }
         }
@@ -575,15 +748,29 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 for (int kb = 0; kb < P::KBM; ++kb)
                     sc[s4] = mma(ld_frag<bf16>(sAB + (size_t)(16 * s4 + r) * P::LAB, 32 * kb, g), uf[kb], sc[s4]);
             }
+            // scores in base-2 units (z * scale * log2 e).  Thresholds grow with the slot
+            // and padded slots carry INT32_MAX, so a chunk whose first position reaches the
+            // last threshold needs no mask.
+            const float k2 = a.scale * 1.44269504088896341f;
             float mx = -INFINITY;
+            if (a.t0 + tok0 < (long long)sTheta[SP - 1]) {
 #pragma unroll
-            for (int s4 = 0; s4 < P::NST; ++s4) {
-                const intx4 th = *reinterpret_cast<const intx4*>(sTheta + 16 * s4 + 4 * g);
+                for (int s4 = 0; s4 < P::NST; ++s4) {
+                    const intx4 th = *reinterpret_cast<const intx4*>(sTheta + 16 * s4 + 4 * g);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    sc[s4][e] = pos < th[e] ? -INFINITY : sc[s4][e] * a.scale;
-                    mx = fmaxf(mx, sc[s4][e]);
+                    for (int e = 0; e < 4; ++e) {
+                        sc[s4][e] = pos < th[e] ? -INFINITY : sc[s4][e] * k2;
+                        mx = fmaxf(mx, sc[s4][e]);
+                    }
                 }
+            } else {
+#pragma unroll
+                for (int s4 = 0; s4 < P::NST; ++s4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        sc[s4][e] *= k2;
+                        mx = fmaxf(mx, sc[s4][e]);
+                    }
             }
             mx = rows_max(mx);
             float sum = 0.f;
@@ -591,7 +778,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             for (int s4 = 0; s4 < P::NST; ++s4)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float ex = __expf(sc[s4][e] - mx);
+                    const float ex = __builtin_amdgcn_exp2f(sc[s4][e] - mx);
                     sc[s4][e] = ex;
                     sum += ex;
                 }
@@ -611,11 +798,12 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             }
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
+                // [Re W'' | -Im W''] with W'' = (a - i b) o E
                 const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
-                const floatx4 sn = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
                 const floatx4 am = wa[mt], bm = wa[NMT + mt];
-                wa[mt] = am * cs + bm * sn;
-                wa[NMT + mt] = am * sn - bm * cs;
+                wa[mt] = am * cs - bm * ns;
+                wa[NMT + mt] = am * ns + bm * cs;
             }
             F wf[P::KBM];
 #pragma unroll
@@ -654,8 +842,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 }
             }
             if (j < c) {
+                bf16* oc = ob + (size_t)tok0 * D;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) st4<bf16>(ob + (size_t)(tok0 + j) * D + 16 * dt + 4 * g, oa[dt]);
+                for (int dt = 0; dt < NDT; ++dt) st4<bf16>(oc + (unsigned)(j * D + 16 * dt + 4 * g), oa[dt]);
             }
         }
         __syncthreads();  // everyone done reading ZvT

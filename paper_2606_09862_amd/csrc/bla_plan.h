@@ -35,13 +35,14 @@ struct TableArgs {
     float* E32;     // [H][C+1][2MP]  cos | sin of m w j, j = 0..C
     void* EbarT;    // [H][2MP][C]    cos(m w i) | -sin(m w i)       (operand type)
     void* ErevT;    // [H][2MP][C]    cos(m w (C-i)) | sin(m w (C-i)) (operand type)
-    void* Etab;     // [H][C][2MP]    cos(m w i) | sin(m w i)        (operand type)
+    void* Etab;     // [H][C][2MP]    cos(m w i) | sin(m w i), or | -sin(m w i) if conj_tab (operand type)
     void* ABs;      // [SP][2MP]      scale * (A | B)                (operand type)
     void* ABm;      // [2MP][SP]      (A | B) transposed             (operand type)
     float* AB32;    // [SP][2MP]      A | B in float32
     int* theta;     // [H][SP]        start-mask thresholds (INT32_MAX for padded slots)
     float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
     int M, S, MP, SP, C, Lblk, h0, nh, with_shared;
+    int conj_tab;   // Etab holds conj(rho^i) (the bf16 pair kernels' convention)
     float scale;    // factor folded into ABs (1 when the kernel applies the score scale itself)
     double T[kMaxHeadsPerTableLaunch];  // clamped periods of heads h0..h0+nh-1
 };
