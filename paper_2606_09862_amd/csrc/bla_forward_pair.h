@@ -64,16 +64,17 @@ template <int D, int MP, int SP> struct Pair {
     static constexpr int LE = 2 * MP + 12;   // phase tab: [C][LE]
     static constexpr int LK = D + 12;        // K, V:      [C][LK]
     static constexpr int LQ = D + 4;         // Q:         [C][LQ]
-    static constexpr int LU = 2 * MP + 4;    // U:         [C][LU]
-    static constexpr int LQU = LQ > LU ? LQ : LU;
-    static constexpr int LG = C + 4;         // G^T:       [C][LG]
-    static constexpr int LZ = 2 * MP + 4;    // Z'_v:      [D][LZ]
+    static constexpr int LZK = D + 4;        // Z'_k:      [2MP][LZK]  (Re rows, then Im rows)
+    static constexpr int LZ = 2 * MP + 4;    // Z'_v:      [D][LZ]     (Re | Im along the row)
     static constexpr size_t AB_ELEMS = (size_t)SP * LAB;
     static constexpr size_t E_ELEMS = (size_t)C * LE;
     static constexpr size_t SHARED_BYTES = 2 * (AB_ELEMS + E_ELEMS) + 3 * 2 * MP * 4 + SP * 4;
-    static constexpr size_t UNIT_ELEMS = 2 * (size_t)C * LK + (size_t)C * LQU + (size_t)C * LG + (size_t)D * LZ;
+    static constexpr size_t UNIT_ELEMS =
+        2 * (size_t)C * LK + (size_t)C * LQ + (size_t)2 * MP * LZK + (size_t)D * LZ;
     static constexpr size_t UNIT_BYTES = 2 * UNIT_ELEMS;
-    static constexpr int U = (SHARED_BYTES + 2 * UNIT_BYTES <= kMaxLds) ? 2 : 1;
+    // two units per workgroup (two waves per SIMD) when their tiles fit in LDS and their
+    // registers in half of the file (at most four owned state tiles per wave)
+    static constexpr int U = (SHARED_BYTES + 2 * UNIT_BYTES <= kMaxLds && D <= 64 && MP <= 64) ? 2 : 1;
     static constexpr bool FITS = SHARED_BYTES + U * UNIT_BYTES <= kMaxLds;
     static constexpr size_t LDS_BYTES = SHARED_BYTES + U * UNIT_BYTES;
     // staging: Q, K, V of one chunk in 16-byte pieces, spread over the unit's 256 threads
@@ -144,6 +145,25 @@ __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
         const int u = tid + i * NTHR;
         if (PIECES % NTHR == 0 || u < PIECES)
             *reinterpret_cast<intx2*>(dst + (size_t)(u / (COLS / 4)) * DST + 4 * (u % (COLS / 4))) = buf[i];
+    }
+}
+
+// Publish the owned mode tiles of the state as bf16 operands: Z'_k as [2MP][LZK] rows
+// (mode m, head-dim along the row) and Z'_v as [D][LZ] rows (head-dim d, modes along the row).
+template <int D, int MP, int SP>
+__device__ __forceinline__ void pair_write_zk(bf16* ZkT, const PState<D, MP, SP>& Zk, int wl, int g, int r)
+{
+    using P = Pair<D, MP, SP>;
+#pragma unroll
+    for (int o = 0; o < P::OWN; ++o) {
+        const int mt = wl + P::WPU * o;
+        if (mt < P::NMT) {
+#pragma unroll
+            for (int dt = 0; dt < P::NDT; ++dt) {
+                st4<bf16>(ZkT + (size_t)(16 * mt + r) * P::LZK + 16 * dt + 4 * g, Zk[o][0][dt]);
+                st4<bf16>(ZkT + (size_t)(MP + 16 * mt + r) * P::LZK + 16 * dt + 4 * g, Zk[o][1][dt]);
+            }
+        }
     }
 }
 
@@ -510,6 +530,14 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
 // units 2x and 2x+1 (U = 2) of head h.  Units are numbered over (b, i) with
 // i = 0, 1, 2, 3, ... taking segments 0, nseg-1, 1, nseg-2, ..., so that the two units
 // of a workgroup combine about nseg-1 segment summaries between them.
+//
+// Per chunk, two phases separated by barriers:
+//   1. each wave runs the whole per-token chain of one token tile in registers (steps
+//      (1)-(9), reading the published state of the chunk start), and independently
+//      advances its owned mode tiles of the float32 state (step (10));
+//   2. each wave publishes its state tiles for the next chunk and stages the next chunk.
+// The second unit takes the token tiles in reverse order, so that every SIMD runs one
+// short and one long causal tile.
 template <int D, int MP, int SP>
 __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kernel(FwdArgs a)
 {
@@ -529,6 +557,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     const int u = wv / P::WPU, wl = wv % P::WPU;  // unit and wave within the unit
     const int ut = tid & 255;                      // thread index within the unit
     const int g = (tid & 63) >> 4, r = tid & 15;
+    const int tt = u == 0 ? wl : NT - 1 - wl;      // token tile of this wave's chain
     const int h = blockIdx.y;
     const int per_head = a.B * a.nseg;
     const int v_unit = blockIdx.x * P::U + u;
@@ -540,10 +569,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     bf16* base = reinterpret_cast<bf16*>(lds_raw + P::SHARED_BYTES + (size_t)u * P::UNIT_BYTES);
     bf16* Ks = base;
     bf16* Vs = Ks + (size_t)C * P::LK;
-    bf16* Qs = Vs + (size_t)C * P::LK;   // Q in phase A, then U
-    bf16* UT = Qs;
-    bf16* GT = Qs + (size_t)C * P::LQU;
-    bf16* ZvT = GT + (size_t)C * P::LG;
+    bf16* Qs = Vs + (size_t)C * P::LK;
+    bf16* ZkT = Qs + (size_t)C * P::LQ;
+    bf16* ZvT = ZkT + (size_t)2 * MP * P::LZK;
 
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     // ---- shared tables
@@ -563,12 +591,17 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     const bf16* kb_ = (const bf16*)a.k + (size_t)bh * a.L * D;
     const bf16* vb = (const bf16*)a.v + (size_t)bh * a.L * D;
     bf16* ob = (bf16*)a.o + (size_t)bh * a.L * D;
+    // Chunk n + 1 is loaded into registers during chunk n; every load is unconditional
+    // (an exhausted or idle unit re-reads a chunk that exists), so the wait before each
+    // store to LDS covers only that stage's loads.
+    const int last = max(nch - 1, 0);
+    auto stage_chunk = [&](PStage<D, MP, SP>& st, int n) {
+        const int tn = (ch0 + min(n, last)) * C, cn = min(C, a.L - tn);
+        pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn, ut);
+    };
 
     PStage<D, MP, SP> st;
-    if (nch > 0) {
-        const int t0c = ch0 * C, c0 = min(C, a.L - t0c);
-        pair_stage_load<D, MP, SP>(st, qb + (size_t)t0c * D, kb_ + (size_t)t0c * D, vb + (size_t)t0c * D, c0, ut);
-    }
+    stage_chunk(st, 0);
     __syncthreads();  // tables visible
 
     // ---- state entering the unit's segment (pre-rotated: Z' = rho Z)
@@ -638,7 +671,11 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             }
         }
     }
+    pair_write_zk<D, MP, SP>(ZkT, Zk, wl, g, r);
     pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
+    pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, nch > 0 ? min(C, a.L - ch0 * C) : 0, ut);
+    stage_chunk(st, 1);
+    __syncthreads();  // chunk 0 and the initial state visible
 
     // both units run the same number of iterations (the barriers are workgroup-wide);
     // an exhausted or idle unit computes on zero-filled tiles and stores nothing
@@ -647,99 +684,64 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         const bool live = n < nch;
         const int tok0 = (ch0 + n) * C;
         const int c = live ? min(C, a.L - tok0) : 0;
-        __syncthreads();  // previous chunk done with Qs / Ks / Vs / UT
-        pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, c, ut);
-        if (n + 1 < nch) {
-            const int tn = tok0 + C, cn = min(C, a.L - tn);
-            pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn, ut);
-        }
-        __syncthreads();  // staging and Z'_v copy visible
 
-        // ---- phase A: Gram tile (key tile wl) and Q Z'_k^T on owned mode tiles
-        F zkf[OWN][2][P::KBD];
-#pragma unroll
-        for (int o = 0; o < OWN; ++o)
-#pragma unroll
-            for (int p = 0; p < 2; ++p)
-#pragma unroll
-                for (int kb = 0; kb < P::KBD; ++kb)
-                    zkf[o][p][kb] = frag_from_acc<bf16>(Zk[o][p][2 * kb], Zk[o][p][2 * kb + 1]);
-        F kf[P::KBD];
-#pragma unroll
-        for (int kb = 0; kb < P::KBD; ++kb) kf[kb] = ld_frag<bf16>(Ks + (size_t)(16 * wl + r) * P::LK, 32 * kb, g);
-        floatx4 Uacc[OWN][2][NT];
-#pragma unroll
-        for (int ct = 0; ct < NT; ++ct) {
-            const int j = 16 * ct + r;
+        // ================= phase 1: the token chain of tile tt (steps 1-9)
+        {
+            const int j = 16 * tt + r;
             F qf[P::KBD];
 #pragma unroll
             for (int kb = 0; kb < P::KBD; ++kb) qf[kb] = ld_frag<bf16>(Qs + (size_t)j * P::LQ, 32 * kb, g);
-            if (ct >= wl) {
-                floatx4 acc = zero4();
+            // (1)-(2) X = Q Z'_k^T + G conj(E): tiles over [Re | Im] modes (rows) x tokens (columns)
+            floatx4 ua[2 * NMT];
 #pragma unroll
-                for (int kb = 0; kb < P::KBD; ++kb) acc = mma(kf[kb], qf[kb], acc);
-                if (ct == wl) {
+            for (int t = 0; t < 2 * NMT; ++t) {
+                ua[t] = zero4();
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (4 * g + e > r) acc[e] = 0.f;
-                }
-                st4<bf16>(GT + (size_t)j * P::LG + 16 * wl + 4 * g, acc);
+                for (int kb = 0; kb < P::KBD; ++kb)
+                    ua[t] = mma(ld_frag<bf16>(ZkT + (size_t)(16 * t + r) * P::LZK, 32 * kb, g), qf[kb], ua[t]);
             }
+            floatx4 ga[NT];  // Gram tiles: keys (rows) x this tile's queries (columns), keys <= query
 #pragma unroll
-            for (int o = 0; o < OWN; ++o)
+            for (int kt = 0; kt < NT; ++kt) {
+                ga[kt] = zero4();
+                if (kt <= tt) {
 #pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    Uacc[o][p][ct] = zero4();
-                    if (wl + P::WPU * o < NMT) {
+                    for (int kb = 0; kb < P::KBD; ++kb)
+                        ga[kt] = mma(ld_frag<bf16>(Ks + (size_t)(16 * kt + r) * P::LK, 32 * kb, g), qf[kb], ga[kt]);
+                    if (kt == tt) {
 #pragma unroll
-                        for (int kb = 0; kb < P::KBD; ++kb) Uacc[o][p][ct] = mma(zkf[o][p][kb], qf[kb], Uacc[o][p][ct]);
+                        for (int e = 0; e < 4; ++e)
+                            if (4 * g + e > r) ga[kt][e] = 0.f;
                     }
                 }
-        }
-        __syncthreads();
-
-        // ---- phase B: + G conj(E) (conj(E) read transposed from the phase table), twiddle, publish U
+            }
 #pragma unroll
-        for (int o = 0; o < OWN; ++o) {
-            const int mt = wl + P::WPU * o;
-            if (mt < NMT) {
-                F ecf[P::KBC], esf[P::KBC];  // cos rows and -sin rows of conj(E) for the owned modes
+            for (int kb = 0; kb < P::KBC; ++kb) {
+                if (2 * kb <= tt) {
+                    const F gf = frag_from_acc<bf16>(ga[2 * kb], ga[2 * kb + 1]);
 #pragma unroll
-                for (int kb = 0; kb < P::KBC; ++kb) {
-                    ecf[kb] = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
-                    esf[kb] = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
-                }
-#pragma unroll
-                for (int ct = 0; ct < NT; ++ct) {
-#pragma unroll
-                    for (int kb = 0; kb < P::KBC; ++kb) {
-                        if (2 * kb <= ct) {
-                            const bf16* grow = GT + (size_t)(16 * ct + r) * P::LG;
-                            const F gf = (2 * kb + 1 <= ct) ? ld_frag<bf16>(grow, 32 * kb, g)
-                                                            : ld_frag_lo<bf16>(grow, 32 * kb, g);
-                            Uacc[o][0][ct] = mma(ecf[kb], gf, Uacc[o][0][ct]);
-                            Uacc[o][1][ct] = mma(esf[kb], gf, Uacc[o][1][ct]);
-                        }
+                    for (int mt = 0; mt < NMT; ++mt) {
+                        ua[mt] = mma(ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r), gf, ua[mt]);
+                        ua[NMT + mt] = mma(ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r), gf, ua[NMT + mt]);
                     }
-                    const int j = 16 * ct + r;
-                    const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
-                    const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
-                    const floatx4 re = Uacc[o][0][ct], im = Uacc[o][1][ct];
-                    st4<bf16>(UT + (size_t)j * P::LU + 16 * mt + 4 * g, cs * re + ns * im);
-                    st4<bf16>(UT + (size_t)j * P::LU + MP + 16 * mt + 4 * g, cs * im - ns * re);
                 }
             }
-        }
-        __syncthreads();
-
-        // ---- per-token chain on token tile wl; the slot matrix in LDS is unscaled
-        {
-            const int j = 16 * wl + r;
-            const long long pos_ll = a.t0 + tok0 + j;
-            const int pos = pos_ll < (1ll << 30) ? (int)pos_ll : (1 << 30);  // every threshold is below 2^30
+            // (3) U = E o X
+#pragma unroll
+            for (int mt = 0; mt < NMT; ++mt) {
+                const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
+                const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                const floatx4 re = ua[mt], im = ua[NMT + mt];
+                ua[mt] = cs * re + ns * im;
+                ua[NMT + mt] = cs * im - ns * re;
+            }
             F uf[P::KBM];
 #pragma unroll
-            for (int kb = 0; kb < P::KBM; ++kb) uf[kb] = ld_frag<bf16>(UT + (size_t)j * P::LU, 32 * kb, g);
+            for (int kb = 0; kb < P::KBM; ++kb) uf[kb] = frag_from_acc<bf16>(ua[2 * kb], ua[2 * kb + 1]);
+
+            // (4) scores against the slot matrix (unscaled in LDS)
+            const long long pos_ll = a.t0 + tok0 + j;
+            const int pos = pos_ll < (1ll << 30) ? (int)pos_ll : (1 << 30);  // every threshold is below 2^30
             floatx4 sc[P::NST];
 #pragma unroll
             for (int s4 = 0; s4 < P::NST; ++s4) {
@@ -748,9 +750,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 for (int kb = 0; kb < P::KBM; ++kb)
                     sc[s4] = mma(ld_frag<bf16>(sAB + (size_t)(16 * s4 + r) * P::LAB, 32 * kb, g), uf[kb], sc[s4]);
             }
-            // scores in base-2 units (z * scale * log2 e).  Thresholds grow with the slot
-            // and padded slots carry INT32_MAX, so a chunk whose first position reaches the
-            // last threshold needs no mask.
+            // (5) masked softmax in base-2 units (z * scale * log2 e).  Thresholds grow with
+            // the slot and padded slots carry INT32_MAX, so a chunk whose first position
+            // reaches the last threshold needs no mask.
             const float k2 = a.scale * 1.44269504088896341f;
             float mx = -INFINITY;
             if (a.t0 + tok0 < (long long)sTheta[SP - 1]) {
@@ -796,9 +798,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 #pragma unroll
                 for (int kb = 0; kb < P::KBS; ++kb) wa[t] = mma(ld_frag_tr(sAB, P::LAB, 16 * t, kb, g, r), pf[kb], wa[t]);
             }
+            // (7) [Re W'' | -Im W''] with W'' = (a - i b) o E
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                // [Re W'' | -Im W''] with W'' = (a - i b) o E
                 const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
                 const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
                 const floatx4 am = wa[mt], bm = wa[NMT + mt];
@@ -809,6 +811,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 #pragma unroll
             for (int kb = 0; kb < P::KBM; ++kb) wf[kb] = frag_from_acc<bf16>(wa[2 * kb], wa[2 * kb + 1]);
 
+            // (8) O = Re(W'' Z'_v) + V^T H^T with H = tril(Re(W'' conj(E)^T))
             floatx4 oa[NDT];
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
@@ -821,11 +824,11 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 #pragma unroll
             for (int kt = 0; kt < NT; ++kt) {
                 hh[kt] = zero4();
-                if (kt <= wl) {
+                if (kt <= tt) {
 #pragma unroll
                     for (int kb = 0; kb < P::KBM; ++kb)
                         hh[kt] = mma(ld_frag<bf16>(sE + (size_t)(16 * kt + r) * P::LE, 32 * kb, g), wf[kb], hh[kt]);
-                    if (kt == wl) {
+                    if (kt == tt) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
                             if (4 * g + e > r) hh[kt][e] = 0.f;
@@ -835,7 +838,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             // (9) O += V^T H^T, V read transposed
 #pragma unroll
             for (int kb = 0; kb < P::KBC; ++kb) {
-                if (2 * kb <= wl) {
+                if (2 * kb <= tt) {
                     const F hf = frag_from_acc<bf16>(hh[2 * kb], hh[2 * kb + 1]);
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) oa[dt] = mma(ld_frag_tr(Vs, P::LK, 16 * dt, kb, g, r), hf, oa[dt]);
@@ -847,14 +850,22 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 for (int dt = 0; dt < NDT; ++dt) st4<bf16>(oc + (unsigned)(j * D + 16 * dt + 4 * g), oa[dt]);
             }
         }
-        __syncthreads();  // everyone done reading ZvT
-
-        // ---- (10) state update on the owned mode tiles
+        // ================= phase 1 (independent of the chain): step (10) on the owned mode tiles
         if (live) {
             const float* Ec = sRho + (c == C ? 2 * MP : 4 * MP);  // a chunk shorter than C is the last one
             pair_advance<D, MP, P::LK, P::LE>(Zk, Zv, Ks, Vs, sE, Ec, wl, g, r);
+        }
+        __syncthreads();  // chunk n and its published state no longer read
+
+        // ================= phase 2: publish the state of chunk n + 1, stage chunk n + 1
+        if (live) {
+            pair_write_zk<D, MP, SP>(ZkT, Zk, wl, g, r);
             pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
         }
+        const int cn = n + 1 < nch ? min(C, a.L - (tok0 + C)) : 0;
+        pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, cn, ut);
+        stage_chunk(st, n + 2);
+        __syncthreads();  // chunk n + 1 and its state visible
     }
 
     // ---- final state (last segment): Z = conj(rho) Z'
