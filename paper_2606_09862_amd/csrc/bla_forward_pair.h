@@ -600,8 +600,6 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn, ut);
     };
 
-    PStage<D, MP, SP> st;
-    stage_chunk(st, 0);
     __syncthreads();  // tables visible
 
     // ---- state entering the unit's segment (pre-rotated: Z' = rho Z)
@@ -639,13 +637,29 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             }
         }
     }
-    // combine the summaries of the blocks before this segment (Horner, block by block)
+    // combine the summaries of the blocks before this segment (Horner, block by block);
+    // the next block's summary is loaded while the current one is combined (every load
+    // unconditional, indices clamped, so each wait covers exactly one block's loads)
     if (active && seg > 0) {
         const int nblk = seg * (a.cps / a.cpb);
         const float* rb = a.rotblk + (size_t)h * 2 * MP;
         const float* Sb = a.summ + (size_t)bh * a.nbs * 4 * MP * D;
-        for (int j = 0; j < nblk; ++j) {
-            const float* Sj = Sb + (size_t)j * 4 * MP * D;
+        floatx4 sj[2][OWN][NDT][4];  // [buffer][owned tile][head-dim tile][Re k, Im k, Re v, Im v]
+        auto load_block = [&](floatx4 (&dst)[OWN][NDT][4], int j) {
+            const float* Sj = Sb + (size_t)min(j, nblk - 1) * 4 * MP * D;
+#pragma unroll
+            for (int o = 0; o < OWN; ++o) {
+                const int mt = min(wl + P::WPU * o, NMT - 1);
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    dst[o][dt][0] = ld4f(Sj + ((size_t)0 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
+                    dst[o][dt][1] = ld4f(Sj + ((size_t)1 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
+                    dst[o][dt][2] = ld4f(Sj + (size_t)2 * MP * D + ((size_t)0 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+                    dst[o][dt][3] = ld4f(Sj + (size_t)2 * MP * D + ((size_t)1 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
+                }
+            }
+        };
+        auto combine = [&](const floatx4 (&src)[OWN][NDT][4]) {
 #pragma unroll
             for (int o = 0; o < OWN; ++o) {
                 const int mt = wl + P::WPU * o;
@@ -654,23 +668,28 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     const floatx4 cv = ld4f(rb + 16 * mt + 4 * g), sv = ld4f(rb + MP + 16 * mt + 4 * g);
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) {
-                        const floatx4 skr = ld4f(Sj + ((size_t)0 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
-                        const floatx4 ski = ld4f(Sj + ((size_t)1 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
-                        const floatx4 svr =
-                            ld4f(Sj + (size_t)2 * MP * D + ((size_t)0 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
-                        const floatx4 svi =
-                            ld4f(Sj + (size_t)2 * MP * D + ((size_t)1 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
                         const floatx4 kr = Zk[o][0][dt], ki = Zk[o][1][dt];
-                        Zk[o][0][dt] = cc * kr - ss * ki + skr;
-                        Zk[o][1][dt] = ss * kr + cc * ki + ski;
+                        Zk[o][0][dt] = cc * kr - ss * ki + src[o][dt][0];
+                        Zk[o][1][dt] = ss * kr + cc * ki + src[o][dt][1];
                         const floatx4 vr = Zv[o][0][dt], vi = Zv[o][1][dt];
-                        Zv[o][0][dt] = cv * vr - sv * vi + svr;
-                        Zv[o][1][dt] = sv * vr + cv * vi + svi;
+                        Zv[o][0][dt] = cv * vr - sv * vi + src[o][dt][2];
+                        Zv[o][1][dt] = sv * vr + cv * vi + src[o][dt][3];
                     }
                 }
             }
+        };
+        load_block(sj[0], 0);
+        for (int j = 0; j < nblk; j += 2) {
+            load_block(sj[1], j + 1);
+            combine(sj[0]);
+            if (j + 1 < nblk) {
+                load_block(sj[0], j + 2);
+                combine(sj[1]);
+            }
         }
     }
+    PStage<D, MP, SP> st;
+    stage_chunk(st, 0);
     pair_write_zk<D, MP, SP>(ZkT, Zk, wl, g, r);
     pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
     pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, nch > 0 ? min(C, a.L - ch0 * C) : 0, ut);
