@@ -129,13 +129,15 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->off_AB32 = off;   off = align_up(off + SP * MP2 * 4);
     pl->off_theta = off;  off = align_up(off + H * SP * 4);
     pl->off_rotblk = off; off = align_up(off + H * MP2 * 4);
+    pl->off_trig = off;   off = align_up(off + 2 * SP * 4);
     pl->off_summ = off;   off = align_up(off + (size_t)units * pl->nbs * pl->unit_floats * 4);
     const size_t ncarry = pl->pair ? 0 : (size_t)(pl->nseg - 1);  // the pair kernel needs no carries
     pl->off_carry = off;  off = align_up(off + (size_t)units * ncarry * pl->unit_floats * 4);
     pl->total = off;
 }
 
-bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s)
+// step: a decode step needs the phase rows j = 0, 1 only
+bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s, bool step)
 {
     for (int h0 = 0; h0 < pl.H; h0 += kMaxHeadsPerTableLaunch) {
         TableArgs a;
@@ -159,6 +161,8 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.nh = pl.H - h0 < kMaxHeadsPerTableLaunch ? pl.H - h0 : kMaxHeadsPerTableLaunch;
         a.with_shared = h0 == 0;
         a.conj_tab = pl.pair;
+        a.jrows = step ? 2 : kChunk + 1;
+        a.trig = (float*)(ws + pl.off_trig);
         a.scale = pl.pair ? 1.f : pl.scale;  // the pair kernel reads A | B unscaled
         for (int i = 0; i < a.nh; ++i) {
             const double tmin = 2.0 * pl.M - 1.0;
@@ -238,7 +242,7 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
         return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
     };
     if (!mark(0)) return BLA_ERR_HIP;
-    if ((st = build_tables(pl, T, ws, s)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, false)) != BLA_OK) return st;
     if (!mark(1)) return BLA_ERR_HIP;
 
     FwdArgs a;
@@ -318,7 +322,7 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
     if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if ((st = build_tables(pl, T, ws, s)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
     StepArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
@@ -329,11 +333,13 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
     a.sk = state_k;
     a.sv = state_v;
     a.E32 = (const float*)(ws + pl.off_E32);
-    a.AB32 = (const float*)(ws + pl.off_AB32);
+    a.trig = (const float*)(ws + pl.off_trig);
     a.theta = (const int*)(ws + pl.off_theta);
     a.B = pl.B;
     a.H = pl.H;
     a.M = pl.M;
+    a.S = pl.S;
+    a.SP = pl.SP;
     a.t0 = pl.t0;
     a.scale = pl.scale;
     if (launch_step(pl, a, s) != hipSuccess) return BLA_ERR_HIP;

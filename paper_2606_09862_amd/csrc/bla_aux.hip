@@ -23,13 +23,15 @@ template <typename T>
 __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
 {
     const int MP = a.MP, MP2 = 2 * MP, C = a.C;
-    const long long n_head = (long long)a.nh * (C + 1) * MP;   // (h, j, m)
+    const int J = a.jrows;                                      // rows j = 0..J-1 (stride C + 1)
+    const long long n_head = (long long)a.nh * J * MP;          // (h, j, m)
     const long long n_misc = (long long)a.nh * (a.SP + MP);     // theta, rotblk
     const long long n_ab = a.with_shared ? (long long)a.SP * MP : 0;
+    const long long n_trig = a.with_shared ? (long long)a.SP : 0;
     const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < n_head) {
-        const int hl = (int)(gid / ((C + 1) * MP));
-        const int rem = (int)(gid % ((C + 1) * MP));
+        const int hl = (int)(gid / (J * MP));
+        const int rem = (int)(gid % (J * MP));
         const int j = rem / MP, m = rem % MP, h = a.h0 + hl;
         double sn = 0.0, cs = 0.0;
         if (m < a.M) sincos(mode_phase((long long)m * j, a.T[hl]), &sn, &cs);
@@ -86,13 +88,22 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
         ((T*)a.ABs)[(size_t)s * MP2 + MP + m] = (T)(sa * a.scale);
         ((T*)a.ABm)[(size_t)m * a.SP + s] = (T)ca;
         ((T*)a.ABm)[(size_t)(MP + m) * a.SP + s] = (T)sa;
+        return;
+    }
+    if (gid < n_head + n_misc + n_ab + n_trig) {
+        // cos | sin of 2 pi k / S: the slot matrices are c_m times these at k = m s mod S
+        const int k = (int)(gid - n_head - n_misc - n_ab);
+        double sn = 0.0, cs = 0.0;
+        if (k < a.S) sincos(2.0 * M_PI * (double)k / (double)a.S, &sn, &cs);
+        a.trig[k] = (float)cs;
+        a.trig[a.SP + k] = (float)sn;
     }
 }
 
 hipError_t launch_tables(const TableArgs& a, int is_bf16, hipStream_t s)
 {
-    const long long n = (long long)a.nh * (a.C + 1) * a.MP + (long long)a.nh * (a.SP + a.MP) +
-                        (a.with_shared ? (long long)a.SP * a.MP : 0);
+    const long long n = (long long)a.nh * a.jrows * a.MP + (long long)a.nh * (a.SP + a.MP) +
+                        (a.with_shared ? (long long)a.SP * a.MP + a.SP : 0);
     dim3 grid((unsigned)((n + kThreads - 1) / kThreads));
     if (is_bf16)
         hipLaunchKernelGGL(tables_kernel<bf16>, grid, dim3(kThreads), 0, s, a);

@@ -28,7 +28,7 @@ struct Plan {
     size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
     // workspace byte offsets
     size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_AB32, off_theta,
-        off_rotblk, off_summ, off_carry, total;
+        off_rotblk, off_trig, off_summ, off_carry, total;
 };
 
 struct TableArgs {
@@ -41,8 +41,10 @@ struct TableArgs {
     float* AB32;    // [SP][2MP]      A | B in float32
     int* theta;     // [H][SP]        start-mask thresholds (INT32_MAX for padded slots)
     float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
+    float* trig;    // [2][SP]        cos | sin of 2 pi k / S, k < S (zero past S)
     int M, S, MP, SP, C, Lblk, h0, nh, with_shared;
     int conj_tab;   // Etab holds conj(rho^i) (the bf16 pair kernels' convention)
+    int jrows;      // phase rows j = 0..jrows-1 computed (C + 1; 2 for a decode step)
     float scale;    // factor folded into ABs (1 when the kernel applies the score scale itself)
     double T[kMaxHeadsPerTableLaunch];  // clamped periods of heads h0..h0+nh-1
 };
@@ -81,9 +83,9 @@ struct StepArgs {
     float* sk;
     float* sv;
     const float* E32;
-    const float* AB32;
+    const float* trig;
     const int* theta;
-    int B, H, M;
+    int B, H, M, S, SP;
     long long t0;
     float scale;
 };
