@@ -155,7 +155,7 @@ def bench_forward(args, hip):
     t_fwd = phase_ms["forward"] * 1e-3
     achieved_gbs = nbytes / t_fwd / 1e9
     digest = kernel_sources_digest()
-    traffic = read_traffic(os.path.join(ROOT, "profiles", "forward_kernel_lm_layer_traffic.txt"), digest)
+    traffic = read_traffic(os.path.join(ROOT, "profiles", "forward_pair_kernel_lm_layer_traffic.txt"), digest)
     roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
     t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
