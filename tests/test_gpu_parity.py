@@ -106,6 +106,19 @@ def test_small_shapes(dtype, B, H, L, d, M, S, T):
     run_case(q, k, v, T, M, S, dtype, label=f"small {B}x{H}x{L}x{d}")
 
 
+@pytest.mark.parametrize("B,H,L,d,M,S,T", [
+    (1, 2, 300, 128, 20, 30, (41.0, 82.5)),           # d = 128: one sequence unit per workgroup
+    (1, 1, 200, 32, 100, 120, (199.0,)),              # M = 128 padded: two owned mode tiles per wave
+    (1, 1, 64 * 8 + 20, 64, 64, 64, (127.0,)),        # 9 segments: an idle partner unit in the last workgroup
+    (2, 1, 64 * 30 + 33, 64, 64, 64, (127.0, 254.0)), # several chunks per segment, ragged last segment
+])
+def test_bf16_unit_layouts(B, H, L, d, M, S, T):
+    """Layouts of the bf16 kernels: one or two units per workgroup, one or two owned mode
+    tiles per wave, idle units, segments of several chunks."""
+    q, k, v = gauss(L * 3 + d + M, B, H, L, d, torch.bfloat16)
+    run_case(q, k, v, T[:H], M, S, torch.bfloat16, label=f"layout {B}x{H}x{L}x{d} M={M}")
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_state_in_and_offset(dtype):
     """Continue a sequence: state_in from the oracle, t0 > 0 (start mask at absolute positions)."""

@@ -18,6 +18,8 @@ pytestmark = pytest.mark.gpu
     (2, 3, 64, 24, 40, (47.0, 94.0, 60.5), 100),
     (4, 1, 128, 16, 31, (31.0,), 10),
     (2, 2, 64, 64, 64, (127.0, 254.0), 300),
+    (2, 2, 128, 128, 256, (255.0, 510.0), 20),        # largest modes and slots (512-thread workgroup)
+    (2, 1, 32, 100, 120, (199.0,), 50),               # padded modes and slots, d = 32
 ])
 def test_step_small(dtype, B, H, d, M, S, T, L):
     bla = _bla()
