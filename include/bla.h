@@ -77,6 +77,20 @@ const char* bla_status_string(bla_status s);
 bla_status bla_supported(const bla_params* p);
 
 /*
+ * Host-side float64 slot tables of one head (Sec. 3.1: the interpolation coefficients of
+ * Eq. translated evaluated at the slot lags tau_s = s T / S, Alg. 2's dilated time grid):
+ *   A[s*M + m] = c_m cos(2 pi m s / S),  B[s*M + m] = c_m sin(2 pi m s / S),
+ *   c_0 = 1/(2M-1), c_m = 2/(2M-1) for m >= 1,
+ *   theta[s] = rint(s T / S)  (round half to even), the first position at which slot s
+ *   is visible (the start mask of Eq. output),
+ * with T clamped to at least 2M-1 as the kernels do.  A and B are [S][M] row-major,
+ * caller-owned host arrays; theta has S entries.  BLA_ERR_INVALID_ARG for M < 1, S < 1,
+ * a null pointer, or T not finite and positive.  The device tables of bla_forward and
+ * bla_step follow the same formulas (rounded to float32 / the operand type).
+ */
+bla_status bla_interp_tables(int32_t M, int32_t S, double T, double* A, double* B, int32_t* theta);
+
+/*
  * Bytes of device workspace bla_forward needs for *p on the current device
  * (0 if *p is invalid or unsupported).  The value depends on B, H, L, d, M, S
  * and the device's compute-unit count, not on the data.

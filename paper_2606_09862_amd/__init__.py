@@ -60,6 +60,9 @@ def lib():
         L.bla_forward.argtypes = [P, _dp] + [_vp] * 9 + [ctypes.c_size_t, _vp]
         L.bla_forward.restype = ctypes.c_int
         L.bla_step.argtypes = [P, _dp] + [_vp] * 8 + [ctypes.c_size_t, _vp]
+        L.bla_interp_tables.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dp, _dp,
+                                        ctypes.POINTER(ctypes.c_int32)]
+        L.bla_interp_tables.restype = ctypes.c_int
         L.bla_step.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -86,6 +89,19 @@ def _ptr(t):
 
 def _stream(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def interp_tables(M: int, S: int, T: float):
+    """Float64 slot tables of one head from the library: A, B [S, M] and thresholds [S]."""
+    import numpy as np
+    A = np.zeros((S, M), np.float64)
+    B = np.zeros((S, M), np.float64)
+    th = np.zeros((S,), np.int32)
+    st = lib().bla_interp_tables(M, S, float(T), A.ctypes.data_as(_dp), B.ctypes.data_as(_dp),
+                                 th.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+    if st != 0:
+        raise BlaError(st, "bla_interp_tables")
+    return A, B, th
 
 
 def supported(p: Params) -> int:

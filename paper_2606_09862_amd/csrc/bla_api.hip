@@ -126,7 +126,6 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->off_Etab = off;   off = align_up(off + H * C * MP2 * esz);
     pl->off_ABs = off;    off = align_up(off + SP * MP2 * esz);
     pl->off_ABm = off;    off = align_up(off + MP2 * SP * esz);
-    pl->off_AB32 = off;   off = align_up(off + SP * MP2 * 4);
     pl->off_theta = off;  off = align_up(off + H * SP * 4);
     pl->off_rotblk = off; off = align_up(off + H * MP2 * 4);
     pl->off_trig = off;   off = align_up(off + 2 * SP * 4);
@@ -148,7 +147,6 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.Etab = ws + pl.off_Etab;
         a.ABs = ws + pl.off_ABs;
         a.ABm = ws + pl.off_ABm;
-        a.AB32 = (float*)(ws + pl.off_AB32);
         a.theta = (int*)(ws + pl.off_theta);
         a.rotblk = (float*)(ws + pl.off_rotblk);
         a.M = pl.M;
@@ -190,6 +188,22 @@ const char* bla_status_string(bla_status s)
 }
 
 bla_status bla_supported(const bla_params* p) { return check_shape(p, false); }
+
+bla_status bla_interp_tables(int32_t M, int32_t S, double T, double* A, double* B, int32_t* theta)
+{
+    if (M < 1 || S < 1 || !A || !B || !theta || !isfinite(T) || T <= 0.0) return BLA_ERR_INVALID_ARG;
+    const double Tc = T < 2.0 * M - 1.0 ? 2.0 * M - 1.0 : T;
+    for (int s = 0; s < S; ++s) {
+        for (int m = 0; m < M; ++m) {
+            const double cm = (m == 0 ? 1.0 : 2.0) / (2.0 * M - 1.0);
+            const double ph = 2.0 * M_PI * (double)(((long long)m * s) % S) / (double)S;  // exact m s mod S
+            A[(size_t)s * M + m] = cm * cos(ph);
+            B[(size_t)s * M + m] = cm * sin(ph);
+        }
+        theta[s] = (int32_t)rint((double)s * Tc / (double)S);
+    }
+    return BLA_OK;
+}
 
 size_t bla_workspace_size(const bla_params* p)
 {

@@ -38,18 +38,23 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
         float* E32 = a.E32 + (size_t)h * (C + 1) * MP2;
         E32[(size_t)j * MP2 + m] = (float)cs;
         E32[(size_t)j * MP2 + MP + m] = (float)sn;
-        T* EbarT = (T*)a.EbarT + (size_t)h * MP2 * C;
-        T* ErevT = (T*)a.ErevT + (size_t)h * MP2 * C;
         T* Etab = (T*)a.Etab + (size_t)h * C * MP2;
         if (j < C) {
-            EbarT[(size_t)m * C + j] = (T)(float)cs;           // conj(rho^j)
-            EbarT[(size_t)(MP + m) * C + j] = (T)(float)(-sn);
             Etab[(size_t)j * MP2 + m] = (T)(float)cs;
             Etab[(size_t)j * MP2 + MP + m] = (T)(float)(a.conj_tab ? -sn : sn);
         }
-        if (j >= 1) {                                          // rho^{C-i} at i = C - j
-            ErevT[(size_t)m * C + (C - j)] = (T)(float)cs;
-            ErevT[(size_t)(MP + m) * C + (C - j)] = (T)(float)sn;
+        if (!a.conj_tab) {
+            // the transposed tables of the one-unit kernels (the pair kernels read Etab transposed)
+            T* EbarT = (T*)a.EbarT + (size_t)h * MP2 * C;
+            T* ErevT = (T*)a.ErevT + (size_t)h * MP2 * C;
+            if (j < C) {
+                EbarT[(size_t)m * C + j] = (T)(float)cs;           // conj(rho^j)
+                EbarT[(size_t)(MP + m) * C + j] = (T)(float)(-sn);
+            }
+            if (j >= 1) {                                          // rho^{C-i} at i = C - j
+                ErevT[(size_t)m * C + (C - j)] = (T)(float)cs;
+                ErevT[(size_t)(MP + m) * C + (C - j)] = (T)(float)sn;
+            }
         }
         return;
     }
@@ -82,12 +87,12 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
             ca = (float)(cm * cs);
             sa = (float)(cm * sn);
         }
-        a.AB32[(size_t)s * MP2 + m] = ca;
-        a.AB32[(size_t)s * MP2 + MP + m] = sa;
         ((T*)a.ABs)[(size_t)s * MP2 + m] = (T)(ca * a.scale);
         ((T*)a.ABs)[(size_t)s * MP2 + MP + m] = (T)(sa * a.scale);
-        ((T*)a.ABm)[(size_t)m * a.SP + s] = (T)ca;
-        ((T*)a.ABm)[(size_t)(MP + m) * a.SP + s] = (T)sa;
+        if (!a.conj_tab) {
+            ((T*)a.ABm)[(size_t)m * a.SP + s] = (T)ca;
+            ((T*)a.ABm)[(size_t)(MP + m) * a.SP + s] = (T)sa;
+        }
         return;
     }
     if (gid < n_head + n_misc + n_ab + n_trig) {

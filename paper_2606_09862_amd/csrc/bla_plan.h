@@ -27,7 +27,7 @@ struct Plan {
     int cpb, nbs;        // chunks per summarised block, summarised blocks per sequence
     size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
     // workspace byte offsets
-    size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_AB32, off_theta,
+    size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_theta,
         off_rotblk, off_trig, off_summ, off_carry, total;
 };
 
@@ -38,7 +38,6 @@ struct TableArgs {
     void* Etab;     // [H][C][2MP]    cos(m w i) | sin(m w i), or | -sin(m w i) if conj_tab (operand type)
     void* ABs;      // [SP][2MP]      scale * (A | B)                (operand type)
     void* ABm;      // [2MP][SP]      (A | B) transposed             (operand type)
-    float* AB32;    // [SP][2MP]      A | B in float32
     int* theta;     // [H][SP]        start-mask thresholds (INT32_MAX for padded slots)
     float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
     float* trig;    // [2][SP]        cos | sin of 2 pi k / S, k < S (zero past S)

@@ -5,6 +5,7 @@ import math
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2606_09862_amd as bla
@@ -159,3 +160,28 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(bla, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         bla.lib()
+
+
+@pytest.mark.parametrize("M,S,T", [(16, 16, 31.0), (8, 15, 15.0), (64, 64, 254.0), (5, 9, 3.0), (24, 40, 47.5),
+                                   (16, 16, 62.0)])
+def test_interp_tables_match_oracle(lib, M, S, T):
+    """The library's host slot tables against the oracle's (independent code, same formulas);
+    T = 3 is clamped to 2M-1 = 9, and S = 16, T = 62 hits a rounding tie (s = 12: 46.5 -> 46)."""
+    import oracle
+    A, B, th = bla.interp_tables(M, S, T)
+    A2, B2, th2 = oracle.interp(M, S, T)
+    assert np.max(np.abs(A - A2)) < 1e-13 and np.max(np.abs(B - B2)) < 1e-13
+    assert np.array_equal(th.astype(np.int64), th2)
+
+
+def test_interp_tables_errors(lib):
+    A = np.zeros(16, np.float64)
+    th = np.zeros(4, np.int32)
+    dp = ctypes.POINTER(ctypes.c_double)
+    ip = ctypes.POINTER(ctypes.c_int32)
+    f = lib.bla_interp_tables
+    ok = f(4, 4, 7.0, A.ctypes.data_as(dp), A.ctypes.data_as(dp), th.ctypes.data_as(ip))
+    assert ok == 0
+    for args in [(0, 4, 7.0), (4, 0, 7.0), (4, 4, 0.0), (4, 4, float("nan")), (4, 4, float("inf"))]:
+        assert f(*args, A.ctypes.data_as(dp), A.ctypes.data_as(dp), th.ctypes.data_as(ip)) == INVALID
+    assert f(4, 4, 7.0, None, A.ctypes.data_as(dp), th.ctypes.data_as(ip)) == INVALID
