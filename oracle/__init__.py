@@ -9,6 +9,8 @@ the mode-state recurrence of Sec. 3.1 Eq. recurrence, the blurry slots of
 Eq. compressed and the masked slot softmax of Eq. output) token by token in
 double precision.  ``interp`` exposes its interpolation matrices (Eq. translated
 evaluated on the dilated slot grid) so the tests can pin them.
+``forward_anchored`` runs the absolute-phase form of Sec. 3.3 (Alg. 1: slots
+anchored at phase 0, slot states accumulated as a cumulative sum) token by token.
 
 Parity status of each function (what pins it) is listed in the tests
 (``tests/test_oracle_pins.py``); every function here is pinned.
@@ -57,6 +59,10 @@ def _load():
         lib.bla_oracle_step.argtypes = [ctypes.c_int] * 6 + [
             _dp, _ip, ctypes.c_double, _dp, _dp, _dp, _dp, _dp, _dp, ctypes.c_int]
         lib.bla_oracle_step.restype = ctypes.c_int
+        lib.bla_oracle_forward_anchored.argtypes = [ctypes.c_int] * 7 + [
+            _dp, ctypes.c_int64, ctypes.c_double, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp,
+            ctypes.c_int]
+        lib.bla_oracle_forward_anchored.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -126,3 +132,30 @@ def step(q, k, v, T, M: int, S: int, state_k, state_v, pos, scale=None, nthreads
     if rc != 0:
         raise ValueError("bla_oracle_step rejected its arguments")
     return o, sk, sv
+
+
+def forward_anchored(q, k, v, T, M: int, S: int, t0: int = 0, scale=None, slot_k=None,
+                     slot_v=None, nthreads: int = 0):
+    """Alg. 1 (absolute-phase slots, Sec. 3.3) over q,k [B,H,L,dk], v [B,H,L,dv].
+
+    slot_k / slot_v [B,H,S,d] are the slot states before token 0 (None = zero).
+    Returns (o [B,H,L,dv], slot_k [B,H,S,dk], slot_v [B,H,S,dv]) in float64.
+    """
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    Bn, H, L, dk = q.shape
+    dv = v.shape[-1]
+    assert k.shape == q.shape and v.shape[:3] == (Bn, H, L)
+    T = np.ascontiguousarray(np.broadcast_to(np.asarray(T, np.float64), (H,)))
+    if scale is None:
+        scale = 1.0 / np.sqrt(dk)
+    kt_in, vt_in = _f64(slot_k), _f64(slot_v)
+    o = np.zeros((Bn, H, L, dv), np.float64)
+    kt = np.zeros((Bn, H, S, dk), np.float64)
+    vt = np.zeros((Bn, H, S, dv), np.float64)
+    rc = _load().bla_oracle_forward_anchored(Bn, H, L, dk, dv, M, S, _ptr(T), int(t0),
+                                             float(scale), _ptr(q), _ptr(k), _ptr(v),
+                                             _ptr(kt_in), _ptr(vt_in), _ptr(o), _ptr(kt),
+                                             _ptr(vt), int(nthreads))
+    if rc != 0:
+        raise ValueError("bla_oracle_forward_anchored rejected its arguments")
+    return o, kt, vt

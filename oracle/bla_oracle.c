@@ -266,3 +266,123 @@ int bla_oracle_step(int Bn, int H, int dk, int dv, int M, int S, const double* T
     }
     return 0;
 }
+
+/*
+ * Absolute-phase ("efficient") form of Sec. 3.3 (Eqs. permuted and
+ * compressed_simplified; Alg. 1 recurrent, Alg. 3 chunked).  The slots are anchored
+ * at phase 0 instead of at the current token, so the state is a plain cumulative sum
+ * over slot vectors and needs no rotation.  Per token at absolute position p:
+ *
+ *   interpolation weights (Eq. compressed_simplified, the translated Dirichlet kernel
+ *   evaluated at p):   g[s] = sum_m cos(m w p) A[s][m] + sin(m w p) B[s][m]
+ *   slot states (Eq. permuted, accumulated):   Kt[s] += g[s] k_t,  Vt[s] += g[s] v_t
+ *   output:   z_s = scale <q_t, Kt[s]> if p >= theta_s else -inf,
+ *             o_t = sum_s softmax(z)_s Vt[s]
+ *
+ * m w p is reduced as w * fmod(m p, T): m p is an exact integer in double and fmod is
+ * exact, so long positions lose no phase accuracy.  States are the slot states
+ * [Bn][H][S][d] of Alg. 1 (K_prev, V_prev), not mode states.  Same argument rules
+ * and return codes as bla_oracle_forward.
+ */
+static void run_sequence_anchored(int L, int dk, int dv, int M, int S, double T_in,
+                                  int64_t t0, double scale, const double* q, const double* k,
+                                  const double* v, double* Kt, double* Vt, double* o,
+                                  double* work)
+{
+    double T = clamp_period(T_in, M);
+    double w = 2.0 * ORACLE_PI / T;
+    double* A = work;                              /* S*M */
+    double* Bm = A + (size_t)S * M;                /* S*M */
+    int64_t* theta = (int64_t*)(Bm + (size_t)S * M); /* S */
+    double* cm = (double*)(theta + S);             /* M */
+    double* sm = cm + M;                           /* M */
+    double* g = sm + M;                            /* S */
+    double* z = g + S;                             /* S */
+
+    bla_oracle_interp(M, S, T, A, Bm, theta);
+    for (int t = 0; t < L; ++t) {
+        const double* qt = q + (size_t)t * dk;
+        const double* kt = k + (size_t)t * dk;
+        const double* vt = v + (size_t)t * dv;
+        double* ot = o + (size_t)t * dv;
+        int64_t pos = t0 + t;
+
+        for (int m = 0; m < M; ++m) {
+            double ph = w * fmod((double)m * (double)pos, T);
+            cm[m] = cos(ph);
+            sm[m] = sin(ph);
+        }
+        for (int s = 0; s < S; ++s) {
+            double acc = 0.0;
+            for (int m = 0; m < M; ++m)
+                acc += cm[m] * A[(size_t)s * M + m] + sm[m] * Bm[(size_t)s * M + m];
+            g[s] = acc;
+        }
+        for (int s = 0; s < S; ++s) {
+            for (int d = 0; d < dk; ++d) Kt[(size_t)s * dk + d] += g[s] * kt[d];
+            for (int d = 0; d < dv; ++d) Vt[(size_t)s * dv + d] += g[s] * vt[d];
+        }
+
+        double zmax = -INFINITY;
+        for (int s = 0; s < S; ++s) {
+            double dot = 0.0;
+            for (int d = 0; d < dk; ++d) dot += qt[d] * Kt[(size_t)s * dk + d];
+            z[s] = pos < theta[s] ? -INFINITY : scale * dot;
+            if (z[s] > zmax) zmax = z[s];
+        }
+        double den = 0.0;
+        for (int s = 0; s < S; ++s) {
+            z[s] = (z[s] == -INFINITY) ? 0.0 : exp(z[s] - zmax);
+            den += z[s];
+        }
+        for (int d = 0; d < dv; ++d) {
+            double acc = 0.0;
+            for (int s = 0; s < S; ++s) acc += z[s] * Vt[(size_t)s * dv + d];
+            ot[d] = acc / den;
+        }
+    }
+}
+
+int bla_oracle_forward_anchored(int Bn, int H, int L, int dk, int dv, int M, int S,
+                                const double* T, int64_t t0, double scale, const double* q,
+                                const double* k, const double* v, const double* kt_in,
+                                const double* vt_in, double* o, double* kt_out,
+                                double* vt_out, int nthreads)
+{
+    if (Bn < 0 || H < 0 || L < 0 || dk <= 0 || dv <= 0 || M <= 0 || S <= 0 || t0 < 0) return -1;
+    size_t nseq = (size_t)Bn * H;
+    size_t wlen = 2 * (size_t)S * M + (size_t)S + 2 * (size_t)M + 2 * (size_t)S;
+    size_t skl = (size_t)S * dk, svl = (size_t)S * dv;
+    int err = 0;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+#pragma omp parallel
+    {
+        double* work = (double*)malloc(wlen * sizeof(double));
+        double* st = (double*)malloc((skl + svl) * sizeof(double));
+        if (!work || !st) {
+#pragma omp atomic write
+            err = 1;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (long long i = 0; i < (long long)nseq; ++i) {
+            if (!work || !st) continue;
+            int h = (int)(i % H);
+            if (kt_in) memcpy(st, kt_in + i * skl, skl * sizeof(double));
+            else memset(st, 0, skl * sizeof(double));
+            if (vt_in) memcpy(st + skl, vt_in + i * svl, svl * sizeof(double));
+            else memset(st + skl, 0, svl * sizeof(double));
+            run_sequence_anchored(L, dk, dv, M, S, T[h], t0, scale, q + i * (size_t)L * dk,
+                                  k + i * (size_t)L * dk, v + i * (size_t)L * dv, st, st + skl,
+                                  o + i * (size_t)L * dv, work);
+            if (kt_out) memcpy(kt_out + i * skl, st, skl * sizeof(double));
+            if (vt_out) memcpy(vt_out + i * svl, st + skl, svl * sizeof(double));
+        }
+        free(work);
+        free(st);
+    }
+    return err ? -1 : 0;
+}

@@ -343,3 +343,142 @@ def test_empty_sequence():
                                  state_v=sv)
     assert o.shape == (1, 2, 0, 2)
     assert np.array_equal(sk2, sk) and np.array_equal(sv2, sv)
+
+
+# ---------------------------------------------------------------- P6: absolute-phase form
+def brute_force_anchored(q, k, v, M, S, T, t0=0, scale=None):
+    """Sec. 3.3 Eq. permuted written as a direct sum: at absolute position p = t0 + t,
+    slot s holds sum_{t'<=t} D_M(t0 + t' - tau_s) k_t' (the Dirichlet kernel translated to
+    the slot's lag and evaluated at the key's own absolute position); masked where
+    p < rint(tau_s).  Uses the closed-form Dirichlet kernel, never mode or slot states.
+    """
+    L, d = q.shape
+    Tc = max(T, 2 * M - 1)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    tau = np.arange(S) * Tc / S
+    theta = np.rint(tau)
+    W = dirichlet_closed((t0 + np.arange(L))[None, :] - tau[:, None], M, Tc)   # [S, L]
+    o = np.zeros((L, v.shape[1]))
+    for t in range(L):
+        ks = W[:, : t + 1] @ k[: t + 1]
+        vs = W[:, : t + 1] @ v[: t + 1]
+        z = scale * (ks @ q[t])
+        z = np.where(t0 + t >= theta, z, -np.inf)
+        p = np.exp(z - z.max())
+        p /= p.sum()
+        o[t] = p @ vs
+    return o
+
+
+@pytest.mark.parametrize("M,S,T,L,t0", [(4, 7, 7.0, 23, 0), (4, 4, 9.0, 30, 0), (5, 9, 18.5, 40, 3),
+                                        (3, 8, 5.0, 19, 0), (8, 15, 30.0, 50, 2), (6, 6, 22.0, 37, 5)])
+def test_p6_anchored_brute_force(M, S, T, L, t0):
+    """Alg. 1 against the O(L^2) direct sum of Eq. permuted with the closed-form kernel.
+
+    Catches a wrong sign of the sine table (D is even in the lag, so a flipped B evaluates
+    the kernel at p + tau_s), a phase origin off by one token or by t0, and mask errors.
+    """
+    rng = np.random.default_rng(20)
+    q, k, v = _inputs(rng, 1, 2, L, 6, 4)
+    Ts = [T, T + 3.25]
+    o, _, _ = oracle.forward_anchored(q, k, v, Ts, M, S, t0=t0)
+    for h in range(2):
+        ref = brute_force_anchored(q[0, h], k[0, h], v[0, h], M, S, Ts[h], t0=t0)
+        assert _relerr(o[0, h], ref) < 1e-12
+
+
+@pytest.mark.parametrize("M,T,t0", [(2, 3, 0), (4, 7, 0), (5, 9, 4), (8, 15, 0), (4, 12, 0),
+                                    (5, 20, 7)])
+def test_p6_anchored_equals_rotating_at_integer_period(M, T, t0):
+    """Sec. 3.3: with one slot per integer lag (S = T, the paper's case being T = S = 2M-1)
+    the anchored slots are a permutation of the rotating ones at every step (slot s holds
+    lag (p - s) mod T), the start mask maps onto itself, and softmax ignores the order, so
+    Alg. 1 gives exactly the output of Alg. 2.  At S = T > 2M-1 this is the same
+    permutation on a finer grid.
+    """
+    rng = np.random.default_rng(21)
+    L = 3 * T + 5
+    q, k, v = _inputs(rng, 2, 2, L, 5, 3)
+    o_a, _, _ = oracle.forward_anchored(q, k, v, [float(T)] * 2, M, T, t0=t0)
+    o_r, _, _ = oracle.forward(q, k, v, [float(T)] * 2, M, T, t0=t0)
+    assert _relerr(o_a, o_r) < 1e-12
+
+
+def test_p6_anchored_differs_off_the_integer_grid():
+    """The permutation argument needs integer slot lags: at T = 2(2M-1) with S = 2M-1 the
+    two forms give different outputs (the rotating form is the operator of Sec. 3.1)."""
+    rng = np.random.default_rng(22)
+    M, L = 4, 40
+    q, k, v = _inputs(rng, 1, 1, L, 5, 3)
+    o_a, _, _ = oracle.forward_anchored(q, k, v, [14.0], M, 7)
+    o_r, _, _ = oracle.forward(q, k, v, [14.0], M, 7)
+    assert _relerr(o_a, o_r) > 1e-2
+
+
+@pytest.mark.parametrize("M,S,T,L,t0", [(4, 7, 14.0, 33, 0), (5, 9, 18.5, 41, 6), (3, 5, 7.25, 20, 0)])
+def test_p6_anchored_slots_are_rotating_slots_at_moving_lags(M, S, T, L, t0):
+    """Sec. 3.3's derivation: after the token at absolute position p, anchored slot s holds
+    the rotating operator's blurry slot at lag p - tau_s, i.e. the Dirichlet-weighted
+    history read from the Alg. 2 mode state with coefficients c_m (Eq. dirichlet) at that
+    lag.  This is the identity that lets one mode state serve both forms.
+    """
+    rng = np.random.default_rng(23)
+    q, k, v = _inputs(rng, 1, 2, L, 5, 3)
+    Ts = [T, T + 1.5]
+    _, kt, vt = oracle.forward_anchored(q, k, v, Ts, M, S, t0=t0)
+    _, sk, sv = oracle.forward(q, k, v, Ts, M, S, t0=t0)
+    p = t0 + L - 1
+    c = np.array([1.0] + [2.0] * (M - 1)) / (2 * M - 1)
+    for h in range(2):
+        Tc = max(Ts[h], 2 * M - 1)
+        w = 2 * np.pi / Tc
+        lag = p - np.arange(S) * Tc / S
+        cosm = c[None, :] * np.cos(np.outer(lag, np.arange(M)) * w)   # [S, M]
+        sinm = c[None, :] * np.sin(np.outer(lag, np.arange(M)) * w)
+        assert _relerr(kt[0, h], cosm @ sk[0, h, 0] + sinm @ sk[0, h, 1]) < 1e-12
+        assert _relerr(vt[0, h], cosm @ sv[0, h, 0] + sinm @ sv[0, h, 1]) < 1e-12
+
+
+@pytest.mark.parametrize("L1", [1, 17, 40])
+def test_p6_anchored_split_call(L1):
+    """Alg. 1 carries K_prev / V_prev across tokens: a run over L tokens equals L1 tokens,
+    then L - L1 more from the returned slot states with t0 = L1."""
+    rng = np.random.default_rng(24)
+    M, S, L = 5, 7, 57
+    q, k, v = _inputs(rng, 2, 2, L, 4, 3)
+    Ts = [9.0, 13.5]
+    o, kt, vt = oracle.forward_anchored(q, k, v, Ts, M, S)
+    o1, kt1, vt1 = oracle.forward_anchored(q[:, :, :L1], k[:, :, :L1], v[:, :, :L1], Ts, M, S)
+    o2, kt2, vt2 = oracle.forward_anchored(q[:, :, L1:], k[:, :, L1:], v[:, :, L1:], Ts, M, S,
+                                           t0=L1, slot_k=kt1, slot_v=vt1)
+    assert _relerr(np.concatenate([o1, o2], axis=2), o) < 1e-13
+    assert _relerr(kt2, kt) < 1e-13 and _relerr(vt2, vt) < 1e-13
+
+
+def test_p6_anchored_single_mode_and_attention_limit():
+    """M = 1: every weight g_s is D_1 = 1, so o_t = sum_{t'<=t} v_t'.  T = S = 2M-1 with
+    L <= 2M-1: causal softmax attention (torch's float64 CPU attention as reference)."""
+    rng = np.random.default_rng(25)
+    q, k, v = _inputs(rng, 2, 2, 33, 4, 3)
+    o, _, _ = oracle.forward_anchored(q, k, v, [1.0, 6.5], 1, 5)
+    assert _relerr(o, np.cumsum(v, axis=2)) < 1e-12
+    M = 5
+    W = 2 * M - 1
+    q, k, v = _inputs(rng, 2, 3, W, 8, 5)
+    o, _, _ = oracle.forward_anchored(q, k, v, [float(W)] * 3, M, W)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v), is_causal=True,
+        scale=1.0 / math.sqrt(8)).numpy()
+    assert _relerr(o, ref) < 1e-12
+
+
+def test_p6_anchored_long_positions():
+    """Phases at large absolute positions: the period of the anchored weights is T, so
+    shifting t0 by a multiple of an integer T leaves the output unchanged (the oracle
+    reduces m p modulo T exactly)."""
+    rng = np.random.default_rng(26)
+    M, S, T, L = 6, 11, 23.0, 30
+    q, k, v = _inputs(rng, 1, 1, L, 4, 3)
+    a, _, _ = oracle.forward_anchored(q, k, v, [T], M, S, t0=40)
+    b, _, _ = oracle.forward_anchored(q, k, v, [T], M, S, t0=40 + 23 * 100003)
+    assert _relerr(a, b) < 1e-13
