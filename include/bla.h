@@ -18,6 +18,17 @@
  * The paper's own slot count is S = 2M-1; any S >= 1 is accepted and places the
  * slots on the grid tau_s = s T / S (at S = 2M-1 this is the paper's dilated grid).
  *
+ * Anchored slots (phase_anchor = 1; Sec. 3.3, Eqs. permuted and compressed_simplified,
+ * Alg. 1 and Alg. 3).  The paper's "efficient" form places the slots at fixed phases
+ * instead of at lags behind the current token: slot s holds
+ *        K~[s] = sum_{t' <= t} D_M(p' - tau_s) k_t'     (p' the absolute position of t')
+ * with D_M the Dirichlet kernel of step 2's coefficients, and step 3 is unchanged.  The
+ * state buffers hold the SAME mode state Z in both forms (the anchored slots are read
+ * from it at the token's absolute phase, K~[s] = sum_m c_m Re(exp(-i m w (p - tau_s)) Z[m])),
+ * so state_k / state_v mean the same thing and may be handed between the two forms.  The
+ * two forms give the same outputs exactly when S = T_h is an integer (the paper's case
+ * T = S = 2M-1), where the anchored slots are a permutation of the rotating ones.
+ *
  * Conventions shared by every entry point:
  *   - All tensors are row-major and contiguous, in device memory, 16-byte aligned:
  *       q, k: [B, H, L, d_k]   v, o: [B, H, L, d_v]   (bla_step: L is absent)
@@ -68,6 +79,9 @@ typedef struct {
     int64_t t0;          /* absolute position of token 0 (start mask only), >= 0         */
     float scale;         /* softmax scale; 0 selects 1/sqrt(d_k) (Eq. output)            */
     int32_t io_dtype;    /* bla_dtype of q, k, v, o                                      */
+    int32_t phase_anchor; /* 0: slots at lags behind the current token (the operator above,
+                            Sec. 3.1, Alg. 2); 1: slots anchored at absolute phase 0 (Sec. 3.3,
+                            Alg. 1 / Alg. 3); any other value is BLA_ERR_INVALID_ARG        */
 } bla_params;
 
 /* Human-readable name of a status code (static string, never NULL). */

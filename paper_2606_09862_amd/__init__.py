@@ -32,7 +32,8 @@ class Params(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("L", ctypes.c_int32),
                 ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("M", ctypes.c_int32),
                 ("S", ctypes.c_int32), ("chunk", ctypes.c_int32), ("t0", ctypes.c_int64),
-                ("scale", ctypes.c_float), ("io_dtype", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("io_dtype", ctypes.c_int32),
+                ("phase_anchor", ctypes.c_int32)]
 
 
 _lib = None
@@ -68,9 +69,9 @@ def lib():
     return _lib
 
 
-def make_params(B, H, L, d, M, S, dtype, t0=0, scale=0.0, chunk=0) -> Params:
+def make_params(B, H, L, d, M, S, dtype, t0=0, scale=0.0, chunk=0, phase_anchor=False) -> Params:
     io = BLA_BF16 if dtype == torch.bfloat16 else BLA_F32
-    return Params(B, H, L, d, d, M, S, chunk, int(t0), float(scale), io)
+    return Params(B, H, L, d, d, M, S, chunk, int(t0), float(scale), io, int(phase_anchor))
 
 
 def _periods(T, H):
@@ -123,18 +124,21 @@ def _check(t, shape, dtype, name):
 
 
 def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
-            state_k=None, state_v=None, want_state: bool = True, workspace=None, out=None):
+            state_k=None, state_v=None, want_state: bool = True, workspace=None, out=None,
+            phase_anchor: bool = False):
     """bla_forward on q, k, v [B,H,L,d] (float32 or bfloat16 cuda tensors).
 
     Returns (o, state_k_out, state_v_out); the states are float32 [B,H,2,M,d]
-    (None when want_state is False).
+    (None when want_state is False).  phase_anchor selects the anchored slots of
+    Sec. 3.3 (Alg. 1 / Alg. 3); the state is the same mode state in both forms.
     """
     B, H, L, d = q.shape
     dt = q.dtype
     for name, t in (("k", k), ("v", v)):
         _check(t, (B, H, L, d), dt, name)
     _check(q, (B, H, L, d), dt, "q")
-    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale,
+                    phase_anchor=phase_anchor)
     for name, t in (("state_k", state_k), ("state_v", state_v)):
         if t is not None:
             _check(t, (B, H, 2, M, d), torch.float32, name)
@@ -156,7 +160,7 @@ def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
 
 
 def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
-         scale: float | None = None, workspace=None, out=None):
+         scale: float | None = None, workspace=None, out=None, phase_anchor: bool = False):
     """bla_step: one decode token per row; q,k,v [B,H,d]; updates state_k/state_v in place."""
     B, H, d = q.shape
     dt = q.dtype
@@ -167,7 +171,8 @@ def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
     _check(state_v, (B, H, 2, M, d), torch.float32, "state_v")
     if pos is not None:
         _check(pos, (B,), torch.int64, "pos")
-    p = make_params(B, H, 1, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    p = make_params(B, H, 1, d, M, S, dt, t0, 0.0 if scale is None else scale,
+                    phase_anchor=phase_anchor)
     dev = q.device
     o = torch.empty_like(q) if out is None else out
     need = step_workspace_size(p)

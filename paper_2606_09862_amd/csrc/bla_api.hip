@@ -45,6 +45,7 @@ bla_status check_shape(const bla_params* p, bool step)
     if (p->d_k <= 0 || p->d_v <= 0 || p->M <= 0 || p->S <= 0 || p->t0 < 0) return BLA_ERR_INVALID_ARG;
     if (p->io_dtype != BLA_F32 && p->io_dtype != BLA_BF16) return BLA_ERR_INVALID_ARG;
     if (!isfinite(p->scale)) return BLA_ERR_INVALID_ARG;
+    if (p->phase_anchor != 0 && p->phase_anchor != 1) return BLA_ERR_INVALID_ARG;
     if (p->chunk != 0 && p->chunk != kChunk) return BLA_ERR_UNSUPPORTED;
     if (p->d_k != p->d_v) return BLA_ERR_UNSUPPORTED;
     if (p->d_k != 32 && p->d_k != 64 && p->d_k != 128) return BLA_ERR_UNSUPPORTED;
@@ -78,6 +79,7 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->C = kChunk;
     pl->bf16 = p->io_dtype == BLA_BF16;
     pl->t0 = p->t0;
+    pl->anchor = p->phase_anchor;
     pl->scale = p->scale != 0.f ? p->scale : 1.f / sqrtf((float)p->d_k);
     pl->unit_floats = (size_t)4 * pl->MP * pl->D;
     const long long units = (long long)p->B * p->H;
@@ -129,6 +131,7 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->off_theta = off;  off = align_up(off + H * SP * 4);
     pl->off_rotblk = off; off = align_up(off + H * MP2 * 4);
     pl->off_trig = off;   off = align_up(off + 2 * SP * 4);
+    pl->off_rperiod = off; off = align_up(off + H * 8);
     pl->off_summ = off;   off = align_up(off + (size_t)units * pl->nbs * pl->unit_floats * 4);
     const size_t ncarry = pl->pair ? 0 : (size_t)(pl->nseg - 1);  // the pair kernel needs no carries
     pl->off_carry = off;  off = align_up(off + (size_t)units * ncarry * pl->unit_floats * 4);
@@ -161,6 +164,8 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.conj_tab = pl.pair;
         a.jrows = step ? 2 : kChunk + 1;
         a.trig = (float*)(ws + pl.off_trig);
+        a.rperiod = (double*)(ws + pl.off_rperiod);
+        a.negB = pl.anchor;
         a.scale = pl.pair ? 1.f : pl.scale;  // the pair kernel reads A | B unscaled
         for (int i = 0; i < a.nh; ++i) {
             const double tmin = 2.0 * pl.M - 1.0;
@@ -279,6 +284,8 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     a.summ = (float*)(ws + pl.off_summ);
     a.carry = (float*)(ws + pl.off_carry);
     a.rotblk = (const float*)(ws + pl.off_rotblk);
+    a.rperiod = (const double*)(ws + pl.off_rperiod);
+    a.anchor = pl.anchor;
     a.B = pl.B;
     a.H = pl.H;
     a.L = pl.L;
@@ -349,6 +356,8 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
     a.E32 = (const float*)(ws + pl.off_E32);
     a.trig = (const float*)(ws + pl.off_trig);
     a.theta = (const int*)(ws + pl.off_theta);
+    a.rperiod = (const double*)(ws + pl.off_rperiod);
+    a.anchor = pl.anchor;
     a.B = pl.B;
     a.H = pl.H;
     a.M = pl.M;

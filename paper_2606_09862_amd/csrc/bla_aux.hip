@@ -64,6 +64,7 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
         const double Tp = a.T[hl];
         if (k < a.SP) {
             a.theta[(size_t)h * a.SP + k] = k < a.S ? (int)rint((double)k * Tp / (double)a.S) : INT32_MAX;
+            if (k == 0) a.rperiod[h] = 1.0 / Tp;
         } else {
             const int m = k - a.SP;
             double sn = 0.0, cs = 0.0;
@@ -85,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
             double sn, cs;
             sincos(ph, &sn, &cs);
             ca = (float)(cm * cs);
-            sa = (float)(cm * sn);
+            sa = (float)(a.negB ? -cm * sn : cm * sn);
         }
         ((T*)a.ABs)[(size_t)s * MP2 + m] = (T)(ca * a.scale);
         ((T*)a.ABs)[(size_t)s * MP2 + MP + m] = (T)(sa * a.scale);

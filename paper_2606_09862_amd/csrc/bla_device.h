@@ -115,6 +115,14 @@ template <typename T> __device__ __forceinline__ void st4(T* p, floatx4 x)
     *reinterpret_cast<typename Frag<T>::half*>(p) = cvt4(x, T());
 }
 
+// Same, from LDS through an LDS-typed pointer: a load that cannot be merged with a global
+// load of another branch into one generic (flat) load.
+template <typename T> __device__ __forceinline__ typename Frag<T>::half ld4_lds(const T* p)
+{
+    typedef typename Frag<T>::half H;
+    return *(const __attribute__((address_space(3))) H*)p;
+}
+
 __device__ __forceinline__ floatx4 ld4f(const float* p) { return *reinterpret_cast<const floatx4*>(p); }
 __device__ __forceinline__ void st4f(float* p, floatx4 x) { *reinterpret_cast<floatx4*>(p) = x; }
 
@@ -149,6 +157,17 @@ __device__ __forceinline__ float rows_sum(float x)
     const unsigned v = __float_as_uint(y);
     const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// cos and sin of the absolute phase m w P (w = 2 pi / T) for the anchored slots of
+// Sec. 3.3, from the reciprocal period rT = 1 / T.  m P is an exact integer in double;
+// the revolutions m P / T are reduced to [0, 1) in double before the single-precision
+// sincos, so a position far past the period keeps the phase accuracy of a small one.
+__device__ __forceinline__ void anchor_phase(int m, long long P, double rT, float& c, float& s)
+{
+    const double x = (double)m * (double)P * rT;
+    const float f = (float)(x - floor(x));
+    sincospif(2.f * f, &s, &c);
 }
 
 }  // namespace bla

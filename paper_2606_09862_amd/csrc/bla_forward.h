@@ -29,6 +29,12 @@
 // per-chunk tiles; the wave's own rows of conj(E) and rho^{C-i} stay in
 // registers for the whole segment.
 //
+// Anchored slots (Sec. 3.3, Alg. 1/3) share the mode state and steps (1), (2), (8)-(10);
+// with P the chunk's absolute start and X = Q Z'_k^T + G conj(E), they read out
+// U = rho^P o conj(X) and W'' = (P A + i P B) o conj(rho^P).  With -B in both slot
+// matrices these are the twiddles of (3) and (6) applied with the single row
+// conj(rho^P) = [cos | -sin](m w P) for every token of the chunk.
+//
 // A sequence is split into nseg segments processed by separate workgroups.  The
 // state entering segment g >= 1 comes from a scan over per-block summaries
 // (summary_kernel: step 10 alone, from a zero state) -- the recurrence is
@@ -85,8 +91,9 @@ template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
     static constexpr int LDR = G::C + G::PAD;    // EbarT, ErevT: [2MP][LDR]
     // Qs (read in phase A) and UT (written after the next barrier) share one buffer.
     static constexpr int LDQU = LDU > G::LDQ ? LDU : G::LDQ;
+    // ... + the anchored twiddle row [2MP] of the chunk
     static constexpr size_t BASE_ELEMS = 2 * G::KT_ELEMS + (size_t)G::C * LDQU + (size_t)G::C * LDG +
-                                         (size_t)D * G::LDZ;
+                                         (size_t)D * G::LDZ + (size_t)2 * MP;
     static constexpr size_t TAB_ELEMS = (size_t)SP * LDAS + (size_t)2 * MP * LDAM + (size_t)G::C * LDE +
                                         (size_t)2 * 2 * MP * LDR;
     // float32 rows rho and rho^C, then the int32 mask thresholds
@@ -377,8 +384,9 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
 }
 
 // ---------------------------------------------------------------------------------
-// One workgroup per (b, h, segment): the chunk loop over the segment.
-template <typename T, int D, int MP, int SP>
+// One workgroup per (b, h, segment): the chunk loop over the segment.  AN: anchored slots
+// (a separate instantiation, so that the rotating form keeps its own register allocation).
+template <typename T, int D, int MP, int SP, bool AN>
 __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
 {
     using P = Fwd<T, D, MP, SP>;
@@ -392,6 +400,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     T* UT = Qs;                 // ... then U (phase B onwards)
     T* GT = Qs + (size_t)C * P::LDQU;
     T* ZvT = GT + (size_t)C * P::LDG;
+    T* lPh = ZvT + (size_t)D * GG::LDZ;  // anchored twiddle row conj(rho^P) of the chunk
 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in a scalar register
@@ -422,7 +431,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     const T* gErev = (const T*)a.ErevT + (size_t)h * 2 * MP * C;
     const T* gEtab = (const T*)a.Etab + (size_t)h * C * 2 * MP;
     if constexpr (P::TL) {
-        T* lABs = ZvT + (size_t)D * GG::LDZ;
+        T* lABs = lPh + (size_t)2 * MP;
         T* lABm = lABs + (size_t)SP * P::LDAS;
         T* lEtab = lABm + (size_t)2 * MP * P::LDAM;
         T* lEbar = lEtab + (size_t)C * P::LDE;
@@ -525,12 +534,21 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         }
     }
     write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
+    const double rT = AN ? a.rperiod[h] : 0.0;
 
     for (int n = 0; n < nch; ++n) {
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
-        __syncthreads();  // previous chunk done with Qs / Kt / Vt
+        __syncthreads();  // previous chunk done with Qs / Kt / Vt and the twiddle row
         stage_store<T, D, MP, true>(st, Qs, Kt, Vt, c, tid);
+        if constexpr (AN) {
+            for (int m = tid; m < MP; m += kThreads) {
+                float cs = 0.f, sn = 0.f;
+                if (m < a.M) anchor_phase(m, a.t0 + tok0, rT, cs, sn);
+                lPh[m] = (T)cs;
+                lPh[MP + m] = (T)(-sn);
+            }
+        }
         F kcur[GG::KBD];
 #pragma unroll
         for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = (16 * w + r < c) ? kpf[kb] : zero_frag<T>();
@@ -609,8 +627,14 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
                         }
                     }
                     const int j = 16 * ct + r;
-                    const floatx4 cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
-                    const floatx4 sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                    floatx4 cs, sn;
+                    if constexpr (AN) {
+                        cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
+                        sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
+                    } else {
+                        cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
+                        sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                    }
                     const floatx4 re = U[o][0][ct], im = U[o][1][ct];
                     st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, cs * re - sn * im);
                     st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * mt + 4 * g, sn * re + cs * im);
@@ -670,8 +694,14 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
             }
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
-                const floatx4 sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                floatx4 cs, sn;
+                if constexpr (AN) {
+                    cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
+                    sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
+                } else {
+                    cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
+                    sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                }
                 const floatx4 am = wa[mt], bm = wa[NMT + mt];
                 wa[mt] = am * cs + bm * sn;
                 wa[NMT + mt] = am * sn - bm * cs;

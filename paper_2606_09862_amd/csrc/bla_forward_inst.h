@@ -63,8 +63,11 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
             hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP>), grid, dim3(256 * UU), 0, s, a);        \
             return hipGetLastError();                                                                   \
         } else if constexpr (fits<T, D, MP, SP>()) {                                                    \
-            hipLaunchKernelGGL((forward_kernel<T, D, MP, SP>), dim3((unsigned)(p.B * p.H * p.nseg)),    \
-                               dim3(kThreads), 0, s, a);                                                \
+            const dim3 grid((unsigned)(p.B * p.H * p.nseg));                                            \
+            if (a.anchor)                                                                               \
+                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, true>), grid, dim3(kThreads), 0, s, a); \
+            else                                                                                        \
+                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, false>), grid, dim3(kThreads), 0, s, a); \
             return hipGetLastError();                                                                   \
         } else {                                                                                        \
             return hipErrorInvalidValue;                                                                \

@@ -19,6 +19,12 @@
 //        Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i]),
 //    so one phase table serves steps (3), (8), (10) and the twiddles, and a
 //    ragged last chunk needs no table of its own (rows past c are zero).
+//  * Anchored slots (Sec. 3.3, Alg. 1/3) keep the same mode state and differ only in
+//    the readout: with u = Q Z'_k^T + G conj(E) as above and P the chunk's absolute
+//    start, the anchored query-mode products are rho^P o conj(u) instead of E o u, and
+//    the readout weights (a + i b) o conj(rho^P) instead of (a - i b) o E.  With -B in
+//    the slot matrix both are the rotating twiddles of steps (3) and (7) applied with
+//    the one row [cos | sin](m w P) for every token of the chunk.
 //  * Sequences are split into segments.  summary_pair_kernel reduces every segment
 //    but the last to its summary (step (10) alone from a zero state); a unit then
 //    starts from the preceding summaries combined in its prologue,
@@ -66,11 +72,12 @@ template <int D, int MP, int SP> struct Pair {
     static constexpr int LQ = D + 4;         // Q:         [C][LQ]
     static constexpr int LZK = D + 4;        // Z'_k:      [2MP][LZK]  (Re rows, then Im rows)
     static constexpr int LZ = 2 * MP + 4;    // Z'_v:      [D][LZ]     (Re | Im along the row)
+    // per unit, after Z'_v: the anchored twiddle row [cos | sin](m w P) of the chunk, [2MP]
     static constexpr size_t AB_ELEMS = (size_t)SP * LAB;
     static constexpr size_t E_ELEMS = (size_t)C * LE;
     static constexpr size_t SHARED_BYTES = 2 * (AB_ELEMS + E_ELEMS) + 3 * 2 * MP * 4 + SP * 4;
     static constexpr size_t UNIT_ELEMS =
-        2 * (size_t)C * LK + (size_t)C * LQ + (size_t)2 * MP * LZK + (size_t)D * LZ;
+        2 * (size_t)C * LK + (size_t)C * LQ + (size_t)2 * MP * LZK + (size_t)D * LZ + (size_t)2 * MP;
     static constexpr size_t UNIT_BYTES = 2 * UNIT_ELEMS;
     // two units per workgroup (two waves per SIMD) when their tiles fit in LDS and their
     // registers in half of the file (at most four owned state tiles per wave)
@@ -572,6 +579,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     bf16* Qs = Vs + (size_t)C * P::LK;
     bf16* ZkT = Qs + (size_t)C * P::LQ;
     bf16* ZvT = ZkT + (size_t)2 * MP * P::LZK;
+    bf16* sPh = ZvT + (size_t)D * P::LZ;
 
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     // ---- shared tables
@@ -598,6 +606,19 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     auto stage_chunk = [&](PStage<D, MP, SP>& st, int n) {
         const int tn = (ch0 + min(n, last)) * C, cn = min(C, a.L - tn);
         pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn, ut);
+    };
+
+    // anchored slots: the twiddle row of chunk n at its absolute start t0 + (ch0 + n) C
+    const double rT = a.anchor ? a.rperiod[h] : 0.0;
+    auto phase_row = [&](int n) {
+        if (a.anchor) {
+            for (int m = ut; m < MP; m += 256) {
+                float cs = 0.f, sn = 0.f;
+                if (m < a.M) anchor_phase(m, a.t0 + (long long)(ch0 + n) * C, rT, cs, sn);
+                sPh[m] = (bf16)cs;
+                sPh[MP + m] = (bf16)sn;
+            }
+        }
     };
 
     __syncthreads();  // tables visible
@@ -693,6 +714,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     pair_write_zk<D, MP, SP>(ZkT, Zk, wl, g, r);
     pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
     pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, nch > 0 ? min(C, a.L - ch0 * C) : 0, ut);
+    phase_row(0);
     stage_chunk(st, 1);
     __syncthreads();  // chunk 0 and the initial state visible
 
@@ -707,6 +729,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         // ================= phase 1: the token chain of tile tt (steps 1-9)
         {
             const int j = 16 * tt + r;
+            const bf16* tw = a.anchor ? sPh : sE + (size_t)j * P::LE;  // twiddle row of steps (3), (7)
             F qf[P::KBD];
 #pragma unroll
             for (int kb = 0; kb < P::KBD; ++kb) qf[kb] = ld_frag<bf16>(Qs + (size_t)j * P::LQ, 32 * kb, g);
@@ -745,11 +768,11 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     }
                 }
             }
-            // (3) U = E o X
+            // (3) U = E o X  (anchored: [Re | -Im] of rho^P o conj(X))
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
-                const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                const floatx4 cs = to_f4(ld4<bf16>(tw + 16 * mt + 4 * g));
+                const floatx4 ns = to_f4(ld4<bf16>(tw + MP + 16 * mt + 4 * g));
                 const floatx4 re = ua[mt], im = ua[NMT + mt];
                 ua[mt] = cs * re + ns * im;
                 ua[NMT + mt] = cs * im - ns * re;
@@ -817,11 +840,11 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 #pragma unroll
                 for (int kb = 0; kb < P::KBS; ++kb) wa[t] = mma(ld_frag_tr(sAB, P::LAB, 16 * t, kb, g, r), pf[kb], wa[t]);
             }
-            // (7) [Re W'' | -Im W''] with W'' = (a - i b) o E
+            // (7) [Re W'' | -Im W''] with W'' = (a - i b) o E  (anchored: (a + i b) o conj(rho^P))
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + 16 * mt + 4 * g));
-                const floatx4 ns = to_f4(ld4<bf16>(sE + (size_t)j * P::LE + MP + 16 * mt + 4 * g));
+                const floatx4 cs = to_f4(ld4<bf16>(tw + 16 * mt + 4 * g));
+                const floatx4 ns = to_f4(ld4<bf16>(tw + MP + 16 * mt + 4 * g));
                 const floatx4 am = wa[mt], bm = wa[NMT + mt];
                 wa[mt] = am * cs - bm * ns;
                 wa[NMT + mt] = am * ns + bm * cs;
@@ -883,6 +906,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         }
         const int cn = n + 1 < nch ? min(C, a.L - (tok0 + C)) : 0;
         pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, cn, ut);
+        phase_row(n + 1);
         stage_chunk(st, n + 2);
         __syncthreads();  // chunk n + 1 and its state visible
     }

@@ -24,11 +24,12 @@ struct Plan {
     int nseg, cps;       // segments per sequence, chunks per segment
     int upw;             // sequence units per forward workgroup (1, or 2 for the pair kernel)
     int pair;            // 1 if the bf16 pair kernel runs the forward pass
+    int anchor;          // 1: slots anchored at absolute phase 0 (Sec. 3.3), 0: at the current token
     int cpb, nbs;        // chunks per summarised block, summarised blocks per sequence
     size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
     // workspace byte offsets
     size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_theta,
-        off_rotblk, off_trig, off_summ, off_carry, total;
+        off_rotblk, off_trig, off_rperiod, off_summ, off_carry, total;
 };
 
 struct TableArgs {
@@ -41,10 +42,12 @@ struct TableArgs {
     int* theta;     // [H][SP]        start-mask thresholds (INT32_MAX for padded slots)
     float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
     float* trig;    // [2][SP]        cos | sin of 2 pi k / S, k < S (zero past S)
+    double* rperiod; // [H]           1 / T of each head (clamped period)
     int M, S, MP, SP, C, Lblk, h0, nh, with_shared;
     int conj_tab;   // Etab holds conj(rho^i) (the bf16 pair kernels' convention)
     int jrows;      // phase rows j = 0..jrows-1 computed (C + 1; 2 for a decode step)
     float scale;    // factor folded into ABs (1 when the kernel applies the score scale itself)
+    int negB;       // store -B in ABs / ABm (the slot matrix of the anchored readout)
     double T[kMaxHeadsPerTableLaunch];  // clamped periods of heads h0..h0+nh-1
 };
 
@@ -67,10 +70,12 @@ struct FwdArgs {
     float* summ;
     float* carry;
     const float* rotblk;
+    const double* rperiod;  // [H] 1 / T (anchored readout only)
     int B, H, L, M;
     int nch, nseg, cps, cpb, nbs;
     long long t0;
     float scale;  // score scale (applied by the pair kernel; folded into ABs otherwise)
+    int anchor;   // 1: slots anchored at absolute phase 0 (Sec. 3.3)
 };
 
 struct StepArgs {
@@ -84,9 +89,11 @@ struct StepArgs {
     const float* E32;
     const float* trig;
     const int* theta;
+    const double* rperiod;  // [H] 1 / T (anchored readout only)
     int B, H, M, S, SP;
     long long t0;
     float scale;
+    int anchor;   // 1: slots anchored at absolute phase 0 (Sec. 3.3)
 };
 
 // Launchers (defined in the .hip translation units).  They return a HIP error.

@@ -12,6 +12,11 @@
 // (Eq. for the interpolation at tau_s = s T / S) are generated from one table of
 // cos | sin(2 pi k / S), k < S, held in LDS; the slot and mode sums are split over
 // all waves of the workgroup.
+//
+// Anchored slots (Sec. 3.3, Alg. 1) read the same mode state at the absolute phase of the
+// token: with rho^p = exp(i m w p), the anchored mode state is rho^p conj(Z), so
+//   u <- rho^p conj(u)                         before the scores, and
+//   (a_m, b_m) <- (a c + b s, a s - b c)        (c + i s = rho^p) before the output sum.
 #include <math.h>
 #include <stdint.h>
 
@@ -96,6 +101,13 @@ __global__ __launch_bounds__((StepGeo<D, MP>::NT)) void step_kernel(StepArgs a)
             us += __shfl_xor(us, off);
         }
         if (qd == 0 && m < MP) {
+            if (a.anchor) {
+                float c = 0.f, s = 0.f;
+                if (m < M) anchor_phase(m, pos, a.rperiod[h], c, s);
+                const float rc_ = c * uc + s * us, rs_ = s * uc - c * us;
+                uc = rc_;
+                us = rs_;
+            }
             su[m] = uc;
             su[MP + m] = us;
         }
@@ -173,6 +185,13 @@ __global__ __launch_bounds__((StepGeo<D, MP>::NT)) void step_kernel(StepArgs a)
             cb += spart[NT + p * MP + tid];
         }
         const float c = tid == 0 ? cnorm : 2.f * cnorm;
+        if (a.anchor) {
+            float pc = 0.f, ps = 0.f;
+            if (tid < M) anchor_phase(tid, pos, a.rperiod[h], pc, ps);
+            const float na = pc * ca + ps * cb, nb = ps * ca - pc * cb;
+            ca = na;
+            cb = nb;
+        }
         sab[tid] = c * ca;
         sab[MP + tid] = c * cb;
     }

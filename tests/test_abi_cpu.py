@@ -38,9 +38,23 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_params_struct_layout():
-    # int32 x8, then int64 t0 (8-aligned), float, int32 -> 48 bytes as in bla.h
-    assert ctypes.sizeof(bla.Params) == 48
+    # int32 x8, then int64 t0 (8-aligned), float, int32, int32 (+4 tail pad) -> 56 bytes as in bla.h
+    assert ctypes.sizeof(bla.Params) == 56
     assert bla.Params.t0.offset == 32 and bla.Params.io_dtype.offset == 44
+    assert bla.Params.phase_anchor.offset == 48
+
+
+def test_phase_anchor_flag(lib):
+    """phase_anchor selects the anchored slots (1) or the rotating ones (0); anything else is
+    an argument error.  The workspace does not depend on the form."""
+    p = P()
+    for val, expect in ((0, OK), (1, OK), (2, INVALID), (-1, INVALID)):
+        p.phase_anchor = val
+        assert bla.supported(p) == expect
+    p.phase_anchor = 1
+    a = bla.workspace_size(p)
+    p.phase_anchor = 0
+    assert a == bla.workspace_size(p) and a > 0
 
 
 def test_status_strings(lib):
