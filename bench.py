@@ -10,6 +10,12 @@ Prints ONE JSON line: tokens/s (B*L per step), the roofline of the dominant kern
 between the library's launches on the same stream), the float64 CPU oracle timed on
 the host on the same workload, and the decode step (bla_step) on the decode
 workload (B=512, H=16, d=M=S=64 after a 2048-token prefill).
+
+The headline is the operator with slots at lags behind the current token (Sec. 3.1).
+The anchored-slot form (Sec. 3.3, Alg. 1/3; phase_anchor = 1) is measured the same way
+on the same workload and reported under "anchored", with its own oracle timed on a
+bounded sample.  --form anchored makes the anchored form the only forward that runs
+(for profiling it alone).
 """
 from __future__ import annotations
 
@@ -95,7 +101,7 @@ class Hip:
         return ms.value
 
 
-def bench_forward(args, hip):
+def bench_forward(args, hip, inputs, anchor):
     import numpy as np
     import torch
 
@@ -104,10 +110,10 @@ def bench_forward(args, hip):
 
     w = bi.WORKLOADS[3]
     T = bi.periods(w.M, w.H)
-    q, k, v = bi.generate(3)
+    q, k, v = inputs
     dev = torch.device("cuda:0")
     tq, tk, tv = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v))
-    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16)
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, phase_anchor=anchor)
     ws = torch.empty(bla.workspace_size(p), dtype=torch.uint8, device=dev)
     o = torch.empty_like(tq)
     sk = torch.empty((w.B, w.H, 2, w.M, w.d), dtype=torch.float32, device=dev)
@@ -155,7 +161,8 @@ def bench_forward(args, hip):
     t_fwd = phase_ms["forward"] * 1e-3
     achieved_gbs = nbytes / t_fwd / 1e9
     digest = kernel_sources_digest()
-    traffic = read_traffic(os.path.join(ROOT, "profiles", "forward_pair_kernel_lm_layer_traffic.txt"), digest)
+    tname = "forward_pair_kernel_lm_layer_anchored_traffic.txt" if anchor else "forward_pair_kernel_lm_layer_traffic.txt"
+    traffic = read_traffic(os.path.join(ROOT, "profiles", tname), digest)
     roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
     t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
@@ -170,7 +177,8 @@ def bench_forward(args, hip):
         "operator_roofline_frac": round(t_ideal / (ms * 1e-3), 4),
         "kernel_sources_sha": digest,
     }
-    return w, T, (q, k, v), ms, tokens / (ms * 1e-3), roofline, extra
+    del tq, tk, tv, o, sk, sv, ws
+    return w, T, ms, tokens / (ms * 1e-3), roofline, extra
 
 
 def bench_decode(args, hip):
@@ -211,6 +219,21 @@ def bench_decode(args, hip):
                          "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}}
 
 
+def cpu_baseline_anchored(w, T, inputs):
+    """Alg. 1 oracle (token by token, slot states as cumulative sums) on the whole workload."""
+    import oracle
+
+    q, k, v = inputs
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    threads = max(1, min(threads, w.B * w.H))
+    t = time.perf_counter()
+    oracle.forward_anchored(q, k, v, T, w.M, w.S, nthreads=threads)
+    dt = time.perf_counter() - t
+    return {"value": round(w.B * w.L / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"the whole LM-layer workload ({w.B}x{w.H} sequences of {w.L} tokens), float64 "
+                      f"Alg. 1 with slot states, OpenMP over (b,h); {dt:.2f} s wall"}
+
+
 def cpu_baseline(w, T, inputs):
     import oracle
 
@@ -232,6 +255,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-anchored", action="store_true", help="skip the anchored-slot measurement")
+    ap.add_argument("--form", choices=("rotating", "anchored"), default="rotating",
+                    help="the form of the headline forward; with 'anchored' no other forward runs")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="first run one plain device copy of this many bytes (reference kernel for "
                          "scaling the HBM byte counters of a rocprofv3 --pmc run)")
@@ -252,16 +278,31 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    w, T, inputs, ms, value, roofline, extra = bench_forward(args, hip)
-    decode = None if args.no_decode else bench_decode(args, hip)
-    cpu = None if args.no_cpu_baseline else cpu_baseline(w, T, inputs)
+    import bla_inputs as bi
+    inputs = bi.generate(3)
+    head_anchor = args.form == "anchored"
+    w, T, ms, value, roofline, extra = bench_forward(args, hip, inputs, head_anchor)
+    anchored = None
+    if not head_anchor and not args.no_anchored:
+        _, _, a_ms, a_value, a_roof, a_extra = bench_forward(args, hip, inputs, True)
+        anchored = {"form": "anchored slots (Sec. 3.3, Alg. 1/3), phase_anchor=1", "value": round(a_value, 1),
+                    "unit": "tokens/s", "ms_per_step": round(a_ms, 5), "roofline": a_roof,
+                    "forward_detail": a_extra,
+                    "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_anchored(w, T, inputs)}
+    decode = None if args.no_decode or head_anchor else bench_decode(args, hip)
+    if args.no_cpu_baseline:
+        cpu = None
+    else:
+        cpu = cpu_baseline_anchored(w, T, inputs) if head_anchor else cpu_baseline(w, T, inputs)
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "lm_layer", "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": w.M, "S": w.S,
-                   "chunk": w.chunk, "periods": "T_h=(1+h%2)(2M-1)", "state": "fp32"},
+                   "chunk": w.chunk, "periods": "T_h=(1+h%2)(2M-1)", "state": "fp32",
+                   "phase_anchor": head_anchor},
         "roofline": roofline, "cpu_baseline": cpu, "forward_detail": extra, "decode_step": decode,
+        "anchored": anchored,
     }
     print(json.dumps(line), flush=True)
 
