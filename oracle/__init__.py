@@ -10,7 +10,9 @@ Eq. compressed and the masked slot softmax of Eq. output) token by token in
 double precision.  ``interp`` exposes its interpolation matrices (Eq. translated
 evaluated on the dilated slot grid) so the tests can pin them.
 ``forward_anchored`` runs the absolute-phase form of Sec. 3.3 (Alg. 1: slots
-anchored at phase 0, slot states accumulated as a cumulative sum) token by token.
+anchored at phase 0, slot states accumulated as a cumulative sum) token by token;
+``forward_decay`` the same with the state decay of Sec. 3.4 (previous slot state
+multiplied by 1 - D before each write).
 
 Parity status of each function (what pins it) is listed in the tests
 (``tests/test_oracle_pins.py``); every function here is pinned.
@@ -61,7 +63,7 @@ def _load():
         lib.bla_oracle_step.restype = ctypes.c_int
         lib.bla_oracle_forward_anchored.argtypes = [ctypes.c_int] * 7 + [
             _dp, ctypes.c_int64, ctypes.c_double, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp,
-            ctypes.c_int]
+            ctypes.c_int, ctypes.c_int]
         lib.bla_oracle_forward_anchored.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -135,10 +137,11 @@ def step(q, k, v, T, M: int, S: int, state_k, state_v, pos, scale=None, nthreads
 
 
 def forward_anchored(q, k, v, T, M: int, S: int, t0: int = 0, scale=None, slot_k=None,
-                     slot_v=None, nthreads: int = 0):
+                     slot_v=None, nthreads: int = 0, decay: bool = False):
     """Alg. 1 (absolute-phase slots, Sec. 3.3) over q,k [B,H,L,dk], v [B,H,L,dv].
 
     slot_k / slot_v [B,H,S,d] are the slot states before token 0 (None = zero).
+    decay applies the state decay of Sec. 3.4.
     Returns (o [B,H,L,dv], slot_k [B,H,S,dk], slot_v [B,H,S,dv]) in float64.
     """
     q, k, v = _f64(q), _f64(k), _f64(v)
@@ -155,7 +158,15 @@ def forward_anchored(q, k, v, T, M: int, S: int, t0: int = 0, scale=None, slot_k
     rc = _load().bla_oracle_forward_anchored(Bn, H, L, dk, dv, M, S, _ptr(T), int(t0),
                                              float(scale), _ptr(q), _ptr(k), _ptr(v),
                                              _ptr(kt_in), _ptr(vt_in), _ptr(o), _ptr(kt),
-                                             _ptr(vt), int(nthreads))
+                                             _ptr(vt), 1 if decay else 0, int(nthreads))
     if rc != 0:
         raise ValueError("bla_oracle_forward_anchored rejected its arguments")
     return o, kt, vt
+
+
+def forward_decay(q, k, v, T, M: int, S: int, t0: int = 0, scale=None, slot_k=None,
+                  slot_v=None, nthreads: int = 0):
+    """Anchored slots with the state decay of Sec. 3.4; same arguments and results as
+    forward_anchored."""
+    return forward_anchored(q, k, v, T, M, S, t0=t0, scale=scale, slot_k=slot_k, slot_v=slot_v,
+                            nthreads=nthreads, decay=True)

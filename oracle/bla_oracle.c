@@ -279,6 +279,12 @@ int bla_oracle_step(int Bn, int H, int dk, int dv, int M, int S, const double* T
  *   output:   z_s = scale <q_t, Kt[s]> if p >= theta_s else -inf,
  *             o_t = sum_s softmax(z)_s Vt[s]
  *
+ * With decay (Sec. 3.4, the GSA-style gated update with gate 1 - D): the previous
+ * slot state is multiplied by (1 - g[s]) before the write,
+ *             Kt[s] = (1 - g[s]) Kt[s] + g[s] k_t,  Vt[s] likewise,
+ * which at T = S = 2M-1 replaces exactly the slot of the current residue class
+ * (a ring buffer of the last 2M-1 tokens: sliding-window attention).
+ *
  * m w p is reduced as w * fmod(m p, T): m p is an exact integer in double and fmod is
  * exact, so long positions lose no phase accuracy.  States are the slot states
  * [Bn][H][S][d] of Alg. 1 (K_prev, V_prev), not mode states.  Same argument rules
@@ -287,7 +293,7 @@ int bla_oracle_step(int Bn, int H, int dk, int dv, int M, int S, const double* T
 static void run_sequence_anchored(int L, int dk, int dv, int M, int S, double T_in,
                                   int64_t t0, double scale, const double* q, const double* k,
                                   const double* v, double* Kt, double* Vt, double* o,
-                                  double* work)
+                                  int decay, double* work)
 {
     double T = clamp_period(T_in, M);
     double w = 2.0 * ORACLE_PI / T;
@@ -319,8 +325,11 @@ static void run_sequence_anchored(int L, int dk, int dv, int M, int S, double T_
             g[s] = acc;
         }
         for (int s = 0; s < S; ++s) {
-            for (int d = 0; d < dk; ++d) Kt[(size_t)s * dk + d] += g[s] * kt[d];
-            for (int d = 0; d < dv; ++d) Vt[(size_t)s * dv + d] += g[s] * vt[d];
+            double keep = decay ? 1.0 - g[s] : 1.0;
+            for (int d = 0; d < dk; ++d)
+                Kt[(size_t)s * dk + d] = keep * Kt[(size_t)s * dk + d] + g[s] * kt[d];
+            for (int d = 0; d < dv; ++d)
+                Vt[(size_t)s * dv + d] = keep * Vt[(size_t)s * dv + d] + g[s] * vt[d];
         }
 
         double zmax = -INFINITY;
@@ -343,11 +352,12 @@ static void run_sequence_anchored(int L, int dk, int dv, int M, int S, double T_
     }
 }
 
+/* decay = 0: Alg. 1 (Sec. 3.3); decay = 1: with the state decay of Sec. 3.4. */
 int bla_oracle_forward_anchored(int Bn, int H, int L, int dk, int dv, int M, int S,
                                 const double* T, int64_t t0, double scale, const double* q,
                                 const double* k, const double* v, const double* kt_in,
                                 const double* vt_in, double* o, double* kt_out,
-                                double* vt_out, int nthreads)
+                                double* vt_out, int decay, int nthreads)
 {
     if (Bn < 0 || H < 0 || L < 0 || dk <= 0 || dv <= 0 || M <= 0 || S <= 0 || t0 < 0) return -1;
     size_t nseq = (size_t)Bn * H;
@@ -377,7 +387,7 @@ int bla_oracle_forward_anchored(int Bn, int H, int L, int dk, int dv, int M, int
             else memset(st + skl, 0, svl * sizeof(double));
             run_sequence_anchored(L, dk, dv, M, S, T[h], t0, scale, q + i * (size_t)L * dk,
                                   k + i * (size_t)L * dk, v + i * (size_t)L * dv, st, st + skl,
-                                  o + i * (size_t)L * dv, work);
+                                  o + i * (size_t)L * dv, decay, work);
             if (kt_out) memcpy(kt_out + i * skl, st, skl * sizeof(double));
             if (vt_out) memcpy(vt_out + i * svl, st + skl, svl * sizeof(double));
         }

@@ -482,3 +482,106 @@ def test_p6_anchored_long_positions():
     a, _, _ = oracle.forward_anchored(q, k, v, [T], M, S, t0=40)
     b, _, _ = oracle.forward_anchored(q, k, v, [T], M, S, t0=40 + 23 * 100003)
     assert _relerr(a, b) < 1e-13
+
+
+# ---------------------------------------------------------------- P12: state decay (Sec. 3.4)
+def sliding_window_attention(q, k, v, W, scale):
+    """Causal softmax attention over the last W keys (torch, float64 CPU)."""
+    L = q.shape[-2]
+    i = torch.arange(L)
+    mask = (i[None, :] <= i[:, None]) & (i[None, :] > i[:, None] - W)
+    return torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v), attn_mask=mask,
+        scale=scale).numpy()
+
+
+@pytest.mark.parametrize("M", [2, 4, 8])
+def test_p12_decay_is_sliding_window_attention(M):
+    """Sec. 3.4: with the decay 1 - D and T = S = 2M-1, each write replaces the slot of
+    the current residue class, so BLA is exactly sliding-window softmax attention with
+    window 2M-1 (torch's float64 CPU attention with a banded causal mask as reference)."""
+    rng = np.random.default_rng(30)
+    W = 2 * M - 1
+    L = 4 * W + 3
+    q, k, v = _inputs(rng, 2, 2, L, 6, 4)
+    o, _, _ = oracle.forward_decay(q, k, v, [float(W)] * 2, M, W)
+    ref = sliding_window_attention(q, k, v, W, 1.0 / math.sqrt(6))
+    assert _relerr(o, ref) < 1e-12
+
+
+def brute_force_decay(q, k, v, M, S, T, t0=0, scale=None):
+    """Sec. 3.4 written as a direct sum: slot s at absolute position p holds
+    sum_{t'<=t} D(p' - tau_s) prod_{t'<l<=t} (1 - D(p_l - tau_s)) k_t' with the closed-form
+    Dirichlet kernel; no recursion over a state."""
+    L, d = q.shape
+    Tc = max(T, 2 * M - 1)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    tau = np.arange(S) * Tc / S
+    theta = np.rint(tau)
+    Dk = dirichlet_closed((t0 + np.arange(L))[None, :] - tau[:, None], M, Tc)   # [S, L]
+    o = np.zeros((L, v.shape[1]))
+    for t in range(L):
+        Wt = np.zeros((S, t + 1))
+        for tp in range(t + 1):
+            Wt[:, tp] = Dk[:, tp] * np.prod(1.0 - Dk[:, tp + 1: t + 1], axis=1)
+        ks = Wt @ k[: t + 1]
+        vs = Wt @ v[: t + 1]
+        z = scale * (ks @ q[t])
+        z = np.where(t0 + t >= theta, z, -np.inf)
+        p = np.exp(z - z.max())
+        p /= p.sum()
+        o[t] = p @ vs
+    return o
+
+
+@pytest.mark.parametrize("M,S,T,L,t0", [(4, 7, 14.0, 30, 0), (5, 9, 18.5, 36, 3), (3, 8, 5.0, 19, 0),
+                                        (6, 6, 22.0, 31, 7), (4, 7, 7.0, 25, 0)])
+def test_p12_decay_brute_force(M, S, T, L, t0):
+    """The decayed slot states against the O(L^2 S) product form with the closed-form kernel.
+
+    Catches a decay applied after the write instead of before, a gate 1 - D on the wrong
+    token, and the phase origin."""
+    rng = np.random.default_rng(31)
+    q, k, v = _inputs(rng, 1, 2, L, 5, 3)
+    Ts = [T, T + 2.75]
+    o, _, _ = oracle.forward_decay(q, k, v, Ts, M, S, t0=t0)
+    for h in range(2):
+        ref = brute_force_decay(q[0, h], k[0, h], v[0, h], M, S, Ts[h], t0=t0)
+        assert _relerr(o[0, h], ref) < 1e-11
+
+
+def test_p12_decay_single_mode():
+    """M = 1: D = 1 everywhere, so every slot is overwritten by the current token and
+    o_t = v_t whatever q and k are."""
+    rng = np.random.default_rng(32)
+    q, k, v = _inputs(rng, 2, 2, 21, 4, 3)
+    o, _, _ = oracle.forward_decay(q, k, v, [1.0, 6.5], 1, 5)
+    assert _relerr(o, v) < 1e-13
+
+
+@pytest.mark.parametrize("L1", [1, 17, 40])
+def test_p12_decay_split_call(L1):
+    """The decayed slot states carry a sequence across calls: L tokens at once equal L1
+    tokens, then L - L1 more from the returned slot states with t0 = L1."""
+    rng = np.random.default_rng(33)
+    M, S, L = 5, 7, 57
+    q, k, v = _inputs(rng, 2, 2, L, 4, 3)
+    Ts = [9.0, 13.5]
+    o, kt, vt = oracle.forward_decay(q, k, v, Ts, M, S)
+    o1, kt1, vt1 = oracle.forward_decay(q[:, :, :L1], k[:, :, :L1], v[:, :, :L1], Ts, M, S)
+    o2, kt2, vt2 = oracle.forward_decay(q[:, :, L1:], k[:, :, L1:], v[:, :, L1:], Ts, M, S, t0=L1,
+                                        slot_k=kt1, slot_v=vt1)
+    assert _relerr(np.concatenate([o1, o2], axis=2), o) < 1e-13
+    assert _relerr(kt2, kt) < 1e-13 and _relerr(vt2, vt) < 1e-13
+
+
+def test_p12_decay_forgets_the_past_at_T_equal_2M_minus_1():
+    """Ring-buffer property: at T = S = 2M-1 the slot states after L >= 2M-1 tokens hold
+    exactly the last 2M-1 keys, each in the slot of its residue class."""
+    rng = np.random.default_rng(34)
+    M, L = 4, 40
+    W = 2 * M - 1
+    q, k, v = _inputs(rng, 1, 1, L, 5, 3)
+    _, kt, _ = oracle.forward_decay(q, k, v, [float(W)], M, W)
+    for tp in range(L - W, L):
+        assert np.allclose(kt[0, 0, tp % W], k[0, 0, tp], atol=1e-13)
