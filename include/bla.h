@@ -152,6 +152,44 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
                     const void* v, const int64_t* pos, float* state_k, float* state_v, void* o,
                     void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * State-decay form (Sec. 3.4).  Anchored slots (Sec. 3.3) whose previous state is
+ * multiplied by 1 - D before each write, the gated recurrence the paper relates to GSA:
+ *        K~[s] <- (1 - g[s]) K~[s] + g[s] k_t,   V~[s] likewise,
+ *        g[s] = D_M(p - tau_s) = sum_m c_m cos(m w (p - tau_s))
+ * at the token's absolute position p, followed by step 3 of the operator (masked slot
+ * softmax and readout) on the decayed slots.  At T = S = 2M-1 a write replaces exactly the
+ * slot of the current residue class, so the form is sliding-window attention with window
+ * 2M-1.  The decay is diagonal in slots, so the state is the slot state itself:
+ *        slot_k, slot_v: float32 [B, H, S, d] (row s of head (b,h) is slot s).
+ * p->phase_anchor is ignored (the form is anchored by definition).  Shapes, dtypes, T,
+ * alignment, ownership, streams and errors follow the conventions above (p->chunk is
+ * accepted as for bla_forward; the kernels work in sub-blocks of min(16, floor(T)) tokens).
+ */
+
+/* Bytes of device workspace bla_decay_forward and bla_decay_step need for *p. */
+size_t bla_decay_workspace_size(const bla_params* p);
+
+/*
+ * Decay-form forward over L tokens: o [B,H,L,d_v]; slot_k_in / slot_v_in [B,H,S,d] are the
+ * slot states before token 0 (NULL = zero), slot_k_out / slot_v_out receive the states after
+ * token L-1 (NULL = not wanted; they must not alias the inputs).  L = 0 copies the input
+ * states (or zeros) to the outputs.
+ */
+bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q, const void* k,
+                             const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
+                             float* slot_k_out, float* slot_v_out, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/*
+ * One decay-form decode step for every (b,h): q, k [B,H,d_k], v, o [B,H,d_v], the token of
+ * row b at absolute position pos[b] (device int64 [B]; NULL = p->t0); slot_k / slot_v
+ * [B,H,S,d] are updated in place.
+ */
+bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, const void* k,
+                          const void* v, const int64_t* pos, float* slot_k, float* slot_v, void* o,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

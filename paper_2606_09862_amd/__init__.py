@@ -65,6 +65,12 @@ def lib():
                                         ctypes.POINTER(ctypes.c_int32)]
         L.bla_interp_tables.restype = ctypes.c_int
         L.bla_step.restype = ctypes.c_int
+        L.bla_decay_workspace_size.argtypes = [P]
+        L.bla_decay_workspace_size.restype = ctypes.c_size_t
+        L.bla_decay_forward.argtypes = [P, _dp] + [_vp] * 9 + [ctypes.c_size_t, _vp]
+        L.bla_decay_forward.restype = ctypes.c_int
+        L.bla_decay_step.argtypes = [P, _dp] + [_vp] * 8 + [ctypes.c_size_t, _vp]
+        L.bla_decay_step.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -188,3 +194,63 @@ def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
 
 def default_scale(d: int) -> float:
     return 1.0 / math.sqrt(d)
+
+
+def decay_workspace_size(p: Params) -> int:
+    return lib().bla_decay_workspace_size(ctypes.byref(p))
+
+
+def decay_forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
+                  slot_k=None, slot_v=None, want_state: bool = True, workspace=None, out=None):
+    """bla_decay_forward (state-decay form, Sec. 3.4) on q, k, v [B,H,L,d].
+
+    Returns (o, slot_k_out, slot_v_out); slot states are float32 [B,H,S,d].
+    """
+    B, H, L, d = q.shape
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, (B, H, L, d), dt, name)
+    for name, t in (("slot_k", slot_k), ("slot_v", slot_v)):
+        if t is not None:
+            _check(t, (B, H, S, d), torch.float32, name)
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    dev = q.device
+    o = torch.empty_like(q) if out is None else out
+    sk = torch.empty((B, H, S, d), dtype=torch.float32, device=dev) if want_state else None
+    sv = torch.empty((B, H, S, d), dtype=torch.float32, device=dev) if want_state else None
+    need = decay_workspace_size(p)
+    if need == 0 and supported(p) != 0:
+        raise BlaError(supported(p), "bla_decay_forward (shape check)")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib().bla_decay_forward(ctypes.byref(p), _periods(T, H), _ptr(q), _ptr(k), _ptr(v), _ptr(slot_k),
+                                 _ptr(slot_v), _ptr(o), _ptr(sk), _ptr(sv), _ptr(workspace),
+                                 workspace.numel(), _stream(dev))
+    if st != 0:
+        raise BlaError(st, "bla_decay_forward")
+    return o, sk, sv
+
+
+def decay_step(q, k, v, T, M: int, S: int, slot_k, slot_v, pos=None, t0: int = 0,
+               scale: float | None = None, workspace=None, out=None):
+    """bla_decay_step: one decode token per row; q,k,v [B,H,d]; updates slot_k/slot_v in place."""
+    B, H, d = q.shape
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, (B, H, d), dt, name)
+    _check(slot_k, (B, H, S, d), torch.float32, "slot_k")
+    _check(slot_v, (B, H, S, d), torch.float32, "slot_v")
+    if pos is not None:
+        _check(pos, (B,), torch.int64, "pos")
+    p = make_params(B, H, 1, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    dev = q.device
+    o = torch.empty_like(q) if out is None else out
+    need = decay_workspace_size(p)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = lib().bla_decay_step(ctypes.byref(p), _periods(T, H), _ptr(q), _ptr(k), _ptr(v), _ptr(pos),
+                              _ptr(slot_k), _ptr(slot_v), _ptr(o), _ptr(workspace), workspace.numel(),
+                              _stream(dev))
+    if st != 0:
+        raise BlaError(st, "bla_decay_step")
+    return o

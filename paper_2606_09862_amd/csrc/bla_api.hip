@@ -132,6 +132,7 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->off_rotblk = off; off = align_up(off + H * MP2 * 4);
     pl->off_trig = off;   off = align_up(off + 2 * SP * 4);
     pl->off_rperiod = off; off = align_up(off + H * 8);
+    pl->off_period = off; off = align_up(off + H * 8);
     pl->off_summ = off;   off = align_up(off + (size_t)units * pl->nbs * pl->unit_floats * 4);
     const size_t ncarry = pl->pair ? 0 : (size_t)(pl->nseg - 1);  // the pair kernel needs no carries
     pl->off_carry = off;  off = align_up(off + (size_t)units * ncarry * pl->unit_floats * 4);
@@ -165,6 +166,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.jrows = step ? 2 : kChunk + 1;
         a.trig = (float*)(ws + pl.off_trig);
         a.rperiod = (double*)(ws + pl.off_rperiod);
+        a.period = (double*)(ws + pl.off_period);
         a.negB = pl.anchor;
         a.scale = pl.pair ? 1.f : pl.scale;  // the pair kernel reads A | B unscaled
         for (int i = 0; i < a.nh; ++i) {
@@ -366,6 +368,113 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
     a.t0 = pl.t0;
     a.scale = pl.scale;
     if (launch_step(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
+    return BLA_OK;
+}
+
+// ---------------------------------------------------------------- state-decay form (Sec. 3.4)
+
+size_t bla_decay_workspace_size(const bla_params* p)
+{
+    if (check_shape(p, true) != BLA_OK) return 0;
+    Plan pl;
+    make_plan(p, true, &pl);
+    return pl.total;
+}
+
+bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q, const void* k,
+                             const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
+                             float* slot_k_out, float* slot_v_out, void* workspace, size_t workspace_bytes,
+                             void* stream)
+{
+    bla_status st = check_shape(p, true);
+    if (st != BLA_OK) return st;
+    if (p->L < 0) return BLA_ERR_INVALID_ARG;
+    if ((st = check_periods(p, T)) != BLA_OK) return st;
+    const long long units = (long long)p->B * p->H;
+    if (units == 0) return BLA_OK;
+    if (p->L > 0) {
+        if (!q || !k || !v || !o) return BLA_ERR_INVALID_ARG;
+        if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return BLA_ERR_INVALID_ARG;
+    }
+    const float* sptr[4] = {slot_k_in, slot_v_in, slot_k_out, slot_v_out};
+    for (int i = 0; i < 4; ++i)
+        if (sptr[i] && !aligned16(sptr[i])) return BLA_ERR_INVALID_ARG;
+    if ((slot_k_out && slot_k_out == slot_k_in) || (slot_v_out && slot_v_out == slot_v_in))
+        return BLA_ERR_INVALID_ARG;
+    Plan pl;
+    make_plan(p, true, &pl);
+    if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if (p->L == 0) {
+        const size_t n = (size_t)units * p->S * p->d_k;
+        if (launch_state_copy(slot_k_in, slot_k_out, n, s) != hipSuccess) return BLA_ERR_HIP;
+        if (launch_state_copy(slot_v_in, slot_v_out, n, s) != hipSuccess) return BLA_ERR_HIP;
+        return BLA_OK;
+    }
+    if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
+    DecayArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.sk_in = slot_k_in;
+    a.sv_in = slot_v_in;
+    a.sk_out = slot_k_out;
+    a.sv_out = slot_v_out;
+    a.theta = (const int*)(ws + pl.off_theta);
+    a.period = (const double*)(ws + pl.off_period);
+    a.rperiod = (const double*)(ws + pl.off_rperiod);
+    a.B = p->B;
+    a.H = p->H;
+    a.L = p->L;
+    a.M = p->M;
+    a.S = p->S;
+    a.t0 = p->t0;
+    a.scale = pl.scale;
+    if (launch_decay_forward(pl.bf16, pl.D, pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;
+    return BLA_OK;
+}
+
+bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, const void* k,
+                          const void* v, const int64_t* pos, float* slot_k, float* slot_v, void* o,
+                          void* workspace, size_t workspace_bytes, void* stream)
+{
+    bla_status st = check_shape(p, true);
+    if (st != BLA_OK) return st;
+    if ((st = check_periods(p, T)) != BLA_OK) return st;
+    const long long units = (long long)p->B * p->H;
+    if (units == 0) return BLA_OK;
+    if (!q || !k || !v || !o || !slot_k || !slot_v) return BLA_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(slot_k) ||
+        !aligned16(slot_v))
+        return BLA_ERR_INVALID_ARG;
+    if (pos && ((uintptr_t)pos & 7u)) return BLA_ERR_INVALID_ARG;
+    Plan pl;
+    make_plan(p, true, &pl);
+    if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
+    DecayStepArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.o = o;
+    a.pos = pos;
+    a.sk = slot_k;
+    a.sv = slot_v;
+    a.theta = (const int*)(ws + pl.off_theta);
+    a.rperiod = (const double*)(ws + pl.off_rperiod);
+    a.B = p->B;
+    a.H = p->H;
+    a.M = p->M;
+    a.S = p->S;
+    a.t0 = p->t0;
+    a.scale = pl.scale;
+    if (launch_decay_step(pl.bf16, pl.D, pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;
     return BLA_OK;
 }
 

@@ -64,7 +64,10 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
         const double Tp = a.T[hl];
         if (k < a.SP) {
             a.theta[(size_t)h * a.SP + k] = k < a.S ? (int)rint((double)k * Tp / (double)a.S) : INT32_MAX;
-            if (k == 0) a.rperiod[h] = 1.0 / Tp;
+            if (k == 0) {
+                a.rperiod[h] = 1.0 / Tp;
+                a.period[h] = Tp;
+            }
         } else {
             const int m = k - a.SP;
             double sn = 0.0, cs = 0.0;

@@ -29,7 +29,7 @@ struct Plan {
     size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
     // workspace byte offsets
     size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_theta,
-        off_rotblk, off_trig, off_rperiod, off_summ, off_carry, total;
+        off_rotblk, off_trig, off_rperiod, off_period, off_summ, off_carry, total;
 };
 
 struct TableArgs {
@@ -43,6 +43,7 @@ struct TableArgs {
     float* rotblk;  // [H][2MP]       cos | sin of m w Lblk
     float* trig;    // [2][SP]        cos | sin of 2 pi k / S, k < S (zero past S)
     double* rperiod; // [H]           1 / T of each head (clamped period)
+    double* period;  // [H]           the clamped period T of each head
     int M, S, MP, SP, C, Lblk, h0, nh, with_shared;
     int conj_tab;   // Etab holds conj(rho^i) (the bf16 pair kernels' convention)
     int jrows;      // phase rows j = 0..jrows-1 computed (C + 1; 2 for a decode step)
@@ -96,6 +97,39 @@ struct StepArgs {
     int anchor;   // 1: slots anchored at absolute phase 0 (Sec. 3.3)
 };
 
+// State-decay form (Sec. 3.4): slot states [B][H][S][d] float32.
+struct DecayArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    const float* sk_in;
+    const float* sv_in;
+    float* sk_out;
+    float* sv_out;
+    const int* theta;       // [H][SP] start-mask thresholds (INT32_MAX for padded slots)
+    const double* period;   // [H] clamped period T
+    const double* rperiod;  // [H] 1 / T
+    int B, H, L, M, S;
+    long long t0;
+    float scale;
+};
+
+struct DecayStepArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* o;
+    const int64_t* pos;
+    float* sk;
+    float* sv;
+    const int* theta;
+    const double* rperiod;
+    int B, H, M, S;
+    long long t0;
+    float scale;
+};
+
 // Launchers (defined in the .hip translation units).  They return a HIP error.
 hipError_t launch_tables(const TableArgs& a, int bf16, hipStream_t s);
 hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s);
@@ -103,6 +137,8 @@ hipError_t launch_scan(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_state_copy(const float* src, float* dst, size_t n, hipStream_t s);
 hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
+hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s);
+hipError_t launch_decay_step(int bf16_io, int D, int SP, const DecayStepArgs& a, hipStream_t s);
 
 // Whether a forward kernel exists for (bf16, D, MP, SP).
 bool forward_supported(int bf16, int D, int MP, int SP);

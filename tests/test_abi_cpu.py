@@ -169,6 +169,36 @@ def test_step_errors(lib):
     assert lib.bla_step(ctypes.byref(p), nan, *args, _fake(0x100000), 1 << 40, None) == INVALID
 
 
+def test_decay_errors(lib):
+    """Argument checks of the decay entry points run before any launch (no GPU needed)."""
+    p = P(L=10)
+    H = 2
+    arr = (ctypes.c_double * H)(31.0, 62.0)
+    assert bla.decay_workspace_size(p) > 0
+    fwd = [_fake(0x10000), _fake(0x20000), _fake(0x30000), None, None, _fake(0x40000), None, None]
+    assert lib.bla_decay_forward(ctypes.byref(p), arr, *fwd, _fake(0x100000), 16, None) == WORKSPACE
+    bad = list(fwd)
+    bad[0] = None              # q missing
+    assert lib.bla_decay_forward(ctypes.byref(p), arr, *bad, _fake(0x100000), 1 << 40, None) == INVALID
+    bad = list(fwd)
+    bad[2] = _fake(0x30008)    # v not 16-byte aligned
+    assert lib.bla_decay_forward(ctypes.byref(p), arr, *bad, _fake(0x100000), 1 << 40, None) == INVALID
+    bad = list(fwd)
+    bad[3] = _fake(0x50000)    # slot_k_out aliasing slot_k_in
+    bad[6] = _fake(0x50000)
+    assert lib.bla_decay_forward(ctypes.byref(p), arr, *bad, _fake(0x100000), 1 << 40, None) == INVALID
+    nan = (ctypes.c_double * H)(math.nan, 1.0)
+    assert lib.bla_decay_forward(ctypes.byref(p), nan, *fwd, _fake(0x100000), 1 << 40, None) == INVALID
+    step = [_fake(0x10000), _fake(0x20000), _fake(0x30000), None, _fake(0x40000), _fake(0x50000),
+            _fake(0x60000)]
+    assert lib.bla_decay_step(ctypes.byref(p), arr, *step, _fake(0x100000), 16, None) == WORKSPACE
+    bad = list(step)
+    bad[4] = None              # slot_k missing
+    assert lib.bla_decay_step(ctypes.byref(p), arr, *bad, _fake(0x100000), 1 << 40, None) == INVALID
+    q = P(d=48)
+    assert bla.decay_workspace_size(q) == 0
+
+
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(bla, "LIB_PATH", str(tmp_path / "nope.so"))
     monkeypatch.setattr(bla, "_lib", None)

@@ -45,8 +45,17 @@ def gates(P, c, M, S, T):
     return np.cos(ph) @ A.T + np.sin(ph) @ B.T
 
 
+def cut_length(P, cmax, M, S, T, eps=EPS, floor_log2=-100.0):
+    """Sub-block length the kernels take at P: at most cmax tokens, ending before any slot's
+    gate product drops below 2^floor_log2, and at least one token."""
+    g = gates(P, cmax, M, S, T)
+    lg = np.cumsum(np.log2(np.maximum(1.0 - g, eps)), axis=0)     # [cmax, S]
+    bad = np.nonzero((lg < floor_log2).any(axis=1))[0]
+    return max(1, int(bad[0]) if bad.size else cmax)
+
+
 def subblock_sequence(q, k, v, T, M, S, sub=16, t0=0, scale=None, kt=None, vt=None, eps=EPS,
-                      out=True):
+                      out=True, adaptive=False):
     """One (b,h) sequence through the sub-block form; returns (o, K~, V~, A_total)."""
     L, d = q.shape
     Tc = max(T, 2 * M - 1)
@@ -56,8 +65,11 @@ def subblock_sequence(q, k, v, T, M, S, sub=16, t0=0, scale=None, kt=None, vt=No
     vt = np.zeros((S, v.shape[1])) if vt is None else vt.copy()
     o = np.zeros((L, v.shape[1]))
     a_total = np.ones(S)
-    for b0 in range(0, L, sub):
+    b0 = 0
+    while b0 < L:
         c = min(sub, L - b0)
+        if adaptive:
+            c = cut_length(t0 + b0, c, M, S, T, eps)
         g = gates(t0 + b0, c, M, S, T)                           # [c, S]
         E = np.cumprod(np.maximum(1.0 - g, eps), axis=0)         # [c, S]
         Bq = g / E
@@ -74,6 +86,7 @@ def subblock_sequence(q, k, v, T, M, S, sub=16, t0=0, scale=None, kt=None, vt=No
         kt = E[-1][:, None] * (kt + Bq.T @ Kb)
         vt = E[-1][:, None] * (vt + Bq.T @ Vb)
         a_total *= E[-1]
+        b0 += c
     return o, kt, vt, a_total
 
 
@@ -135,3 +148,19 @@ def test_segments_combine_by_summaries():
                                            kt=xk, vt=xv)
             outs.append(o)
         assert _relerr(np.concatenate(outs), ref[0, 0]) < 1e-9
+
+
+@pytest.mark.parametrize("M,S,T,L", [(2, 8, 500.0, 80), (1, 5, 6.5, 30), (3, 5, 300.0, 64), (64, 64, 127.0, 64)])
+def test_adaptive_cut_keeps_the_range(M, S, T, L):
+    """Small M against a long period makes many consecutive gates small (the main lobe of
+    D_M is T / (2M - 1) tokens wide); the gate-driven cut keeps every E above 2^-100 and the
+    result equal to the recurrence.  On the workload shapes (M = 64) the cut stays at 16."""
+    rng = np.random.default_rng(43)
+    q = rng.standard_normal((1, 1, L, 4)) / 2
+    k = rng.standard_normal((1, 1, L, 4)) / 2
+    v = rng.standard_normal((1, 1, L, 3))
+    ref_o, ref_k, _ = oracle.forward_decay(q, k, v, [T], M, S)
+    o, kt, _, _ = subblock_sequence(q[0, 0], k[0, 0], v[0, 0], T, M, S, adaptive=True)
+    assert _relerr(o, ref_o[0, 0]) < 1e-9 and _relerr(kt, ref_k[0, 0]) < 1e-9
+    if M == 64:
+        assert all(cut_length(p, 16, M, S, T) == 16 for p in range(0, 4096, 16))
