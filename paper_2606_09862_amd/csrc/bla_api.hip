@@ -178,6 +178,46 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
     return BLA_OK;
 }
 
+// Decay form: the tables of a decode-step plan plus the segment summaries.  Sequences are
+// cut into segments (a multiple of 16 tokens, at least 32) until the forward launch has
+// about two waves per SIMD, within a 512 MB cap on the summaries.
+struct DecayPlan {
+    Plan pl;
+    int nseg, seg_len;
+    size_t off_summ, total;
+};
+
+void make_decay_plan(const bla_params* p, DecayPlan* dp)
+{
+    make_plan(p, true, &dp->pl);
+    const int L = p->L > 0 ? p->L : 0;
+    const long long units = (long long)p->B * p->H;
+    const int SP = dp->pl.SP, D = dp->pl.D;
+    const size_t sf_bytes = ((size_t)2 * SP * D + SP) * sizeof(float);
+    int nseg = 1, seg_len = L > 0 ? L : 1;
+    if (units > 0 && L > 32) {
+        const long long waves = 8ll * device_cu_count();
+        const long long per_unit = units * decay_waves(D, SP);
+        long long want = (waves + per_unit - 1) / per_unit;
+        const long long maxseg = (L + 31) / 32;
+        if (want > maxseg) want = maxseg;
+        nseg = want < 1 ? 1 : (int)want;
+        while (nseg > 1 && (size_t)units * (nseg - 1) * sf_bytes > (size_t(512) << 20)) nseg = (nseg + 1) / 2;
+        if (nseg > 1) {
+            seg_len = ((L + nseg - 1) / nseg + 15) / 16 * 16;
+            nseg = (L + seg_len - 1) / seg_len;
+        }
+        if (nseg <= 1) {
+            nseg = 1;
+            seg_len = L;
+        }
+    }
+    dp->nseg = nseg;
+    dp->seg_len = seg_len;
+    dp->off_summ = align_up(dp->pl.total);
+    dp->total = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
+}
+
 }  // namespace
 
 extern "C" {
@@ -375,10 +415,10 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
 
 size_t bla_decay_workspace_size(const bla_params* p)
 {
-    if (check_shape(p, true) != BLA_OK) return 0;
-    Plan pl;
-    make_plan(p, true, &pl);
-    return pl.total;
+    if (check_shape(p, true) != BLA_OK || p->L < 0) return 0;
+    DecayPlan dp;
+    make_decay_plan(p, &dp);
+    return dp.total;
 }
 
 bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q, const void* k,
@@ -401,9 +441,10 @@ bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q
         if (sptr[i] && !aligned16(sptr[i])) return BLA_ERR_INVALID_ARG;
     if ((slot_k_out && slot_k_out == slot_k_in) || (slot_v_out && slot_v_out == slot_v_in))
         return BLA_ERR_INVALID_ARG;
-    Plan pl;
-    make_plan(p, true, &pl);
-    if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
+    DecayPlan dp;
+    make_decay_plan(p, &dp);
+    const Plan& pl = dp.pl;
+    if (!workspace || workspace_bytes < dp.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
     if (p->L == 0) {
@@ -426,11 +467,14 @@ bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q
     a.theta = (const int*)(ws + pl.off_theta);
     a.period = (const double*)(ws + pl.off_period);
     a.rperiod = (const double*)(ws + pl.off_rperiod);
+    a.summ = (float*)(ws + dp.off_summ);
     a.B = p->B;
     a.H = p->H;
     a.L = p->L;
     a.M = p->M;
     a.S = p->S;
+    a.nseg = dp.nseg;
+    a.seg_len = dp.seg_len;
     a.t0 = p->t0;
     a.scale = pl.scale;
     if (launch_decay_forward(pl.bf16, pl.D, pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;

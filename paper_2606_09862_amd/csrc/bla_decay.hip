@@ -18,6 +18,13 @@
 // the lengths depend on positions only (16 tokens unless many small gates follow each
 // other, as when M is small against T).
 //
+// Sequences are split into segments run by separate workgroups.  The recurrence is linear
+// with data-independent gates, so a segment maps its entering state X to A_g o X + S_g:
+// decay_forward_kernel<SUM = true> computes S_g (from a zero state) and A_g (the product
+// of the segment's gates) for every segment but the last, decay_scan_kernel turns them in
+// place into the entering states, and decay_forward_kernel<SUM = false> runs every segment
+// from its entering state.
+//
 // Tiles are (slot x token) so that the softmax over the slots of a token is a reduction
 // over the rows of the wave's tiles.  A workgroup of NWU waves runs one (b, h) sequence;
 // wave w owns NSTW slot tiles and their fp32 state in registers (K~ as d x slot tiles, V~
@@ -47,6 +54,28 @@ template <int D, int SP> struct DecayGeo {
     static_assert(NST % NSTW == 0, "slot tiles split evenly over the waves");
 };
 
+// sin(pi x) for |x| <= 1/2: the odd Taylor series of sin(pi x) through x^11, evaluated in
+// float32 (relative error below 2e-7 on the whole range, so the Dirichlet ratio stays
+// accurate near x = 0).
+__device__ __forceinline__ float sinpi_half(float x)
+{
+    const float x2 = x * x;
+    float p = -0.0073704309457143504f;           // -pi^11 / 11!
+    p = p * x2 + 0.082145886611128228f;          //  pi^9 / 9!
+    p = p * x2 - 0.59926452932079209f;           // -pi^7 / 7!
+    p = p * x2 + 2.5501640398773455f;            //  pi^5 / 5!
+    p = p * x2 - 5.1677127800499703f;            // -pi^3 / 3!
+    p = p * x2 + 3.1415926535897932f;            //  pi
+    return x * p;
+}
+
+// sin(pi a) for a in (-1, 1] from the half-range series (sin(pi a) = sin(pi (1 - a)), odd).
+__device__ __forceinline__ float sinpi_one(float a)
+{
+    const float b = a > 0.5f ? 1.f - a : (a < -0.5f ? -1.f - a : a);
+    return sinpi_half(b);
+}
+
 // Dirichlet kernel D_M at x = p - tau_s for the slot grid tau_s = s T / S, from the
 // fractional revolutions fx = frac(p / T) (double): the closed form
 // sin(N pi f) / (N sin(pi f)) with N = 2M - 1 and f = x / T reduced to (-1/2, 1/2].
@@ -60,7 +89,10 @@ __device__ __forceinline__ float dirichlet_at(double fx, int s, double rS, int N
     return sinpif((float)a) / ((float)N * sinpif((float)f));
 }
 
-template <typename T, int D, int SP>
+// Floats of one segment summary: K~ [SP][D], V~ [SP][D], gate product [SP].
+template <int D, int SP> constexpr size_t decay_summary_floats() { return (size_t)2 * SP * D + SP; }
+
+template <typename T, int D, int SP, bool SUM>
 __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(DecayArgs a)
 {
     using G = DecayGeo<D, SP>;
@@ -82,9 +114,12 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     const int tid = threadIdx.x;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63, g = lane >> 4, r = lane & 15;
-    const int bh = blockIdx.x, h = bh % a.H;
+    const int nsu = SUM ? a.nseg - 1 : a.nseg;  // segments per sequence in this launch
+    const int bh = blockIdx.x / nsu, seg = blockIdx.x % nsu, h = bh % a.H;
+    constexpr size_t SF = decay_summary_floats<D, SP>();
     const int s0w = 16 * NSTW * wv;  // first slot of the wave
     const int S = a.S, L = a.L;
+    const int tbeg = seg * a.seg_len, tend = min(L, tbeg + a.seg_len);
     const int N = 2 * a.M - 1;
     const double rT = a.rperiod[h], rS = 1.0 / (double)S;
     const T* qb = (const T*)a.q + (size_t)bh * L * D;
@@ -109,6 +144,16 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         for (int dt = 0; dt < NDT; ++dt) {
             Kst[t][dt] = zero4();
             Vst[t][dt] = zero4();
+            if (SUM) continue;
+            if (seg > 0) {
+                // entering state of the segment from the scanned summaries
+                const float* cy = a.summ + ((size_t)bh * (a.nseg - 1) + (seg - 1)) * SF;
+                Kst[t][dt] = ld4f(cy + (size_t)sc * D + 16 * dt + 4 * g);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    Vst[t][dt][e] = cy[(size_t)SP * D + (size_t)(s0w + 16 * t + 4 * g + e) * D + 16 * dt + r];
+                continue;
+            }
             if (a.sk_in && sc < S) Kst[t][dt] = ld4f(a.sk_in + ((size_t)bh * S + sc) * D + 16 * dt + 4 * g);
             if (a.sv_in) {
 #pragma unroll
@@ -170,35 +215,46 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         }
     };
 
-    if (L > 0) stage_load(0, min(16, L));
+    if (tbeg < tend) stage_load(tbeg, min(16, tend - tbeg));
+    float aprod[NSTW];  // product of the segment's gates for the K~^T column slot (summaries)
+#pragma unroll
+    for (int t = 0; t < NSTW; ++t) aprod[t] = 1.f;
     const float k2 = a.scale * 1.44269504088896341f;
 
     // The sub-blocks are at most 16 tokens long and end before any slot's gate product
     // falls below 2^-100 (so E and 1/E stay inside the float32 range); their lengths depend
     // only on the positions, and at least one token is taken.
-    for (int tb = 0; tb < L;) {
+    for (int tb = tbeg; tb < tend;) {
         const long long P = a.t0 + tb;  // absolute position of the sub-block's first token
-        const int cmax = min(16, L - tb);
+        const int cmax = min(16, tend - tb);
 
         // ---- gates in the G layout: lane (g, r) holds slot s0w + 16 t + r, tokens 4g..4g+3
         float gt[NSTW][4], al[NSTW][4];
         int cw = 16;
         {
-            double fx[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const double x = (double)(P + 4 * g + e) * rT;
-                fx[e] = x - floor(x);
-            }
+            // phase in revolutions of the lane's first token, reduced in double; each token's
+            // f and N f are formed in double from it and rounded once, so the numerator and
+            // the denominator of the ratio carry the same f
+            const double x0 = (double)(P + 4 * g) * rT;
+            const double fx0 = x0 - floor(x0);
+            const float rN = 1.f / (float)N;
 #pragma unroll
             for (int t = 0; t < NSTW; ++t) {
                 const int s = s0w + 16 * t + r;
+                const double fb = fx0 - (double)s * rS;
                 float lg[4];
                 float run = 0.f;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const bool valid = 4 * g + e < cmax && s < S;
-                    gt[t][e] = valid ? dirichlet_at(fx[e], s, rS, N) : 0.f;
+                    double fd = fb + (double)e * rT;
+                    fd -= rint(fd);
+                    double ad = (double)N * fd;
+                    ad -= 2.0 * rint(0.5 * ad);
+                    const float f = (float)fd, aa = (float)ad;
+                    const float den = sinpi_half(f);
+                    const float dv = den == 0.f ? 1.f : sinpi_one(aa) * rN * __builtin_amdgcn_rcpf(den);
+                    gt[t][e] = valid ? dv : 0.f;
                     al[t][e] = valid ? fmaxf(1.f - gt[t][e], kDecayEps) : 1.f;
                     run += __log2f(al[t][e]);
                     lg[e] = run;
@@ -230,7 +286,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         cs = max(1, min(cs, cmax));
         stage_store(cs);
         __syncthreads();  // K, V visible
-        if (tb + cs < L) stage_load(tb + cs, min(16, L - tb - cs));
+        if (tb + cs < tend) stage_load(tb + cs, min(16, tend - tb - cs));
 
         // ---- E and Bq of the sub-block's cs tokens (tokens past cs: gate 0, factor 1)
         float bq[NSTW][4];
@@ -264,6 +320,20 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         }
         // (the gate tables are read below only by the wave that wrote them)
 
+        // K^T and V^T fragments (rows: d, reduction: the sub-block's tokens)
+        F vtf[NDT], ktf[NDT];
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            if constexpr (BF) {
+                vtf[dt] = join(ld_tr(Vs + (4 * g + (r >> 2)) * G::LK + 16 * dt + 4 * (r & 3)), zero_half<T>());
+                ktf[dt] = join(ld_tr(Ks + (4 * g + (r >> 2)) * G::LK + 16 * dt + 4 * (r & 3)), zero_half<T>());
+            } else {
+                vtf[dt] = ld_frag_lo<T>(VT + (16 * dt + r) * G::LKT, 0, g);
+                ktf[dt] = ld_frag_lo<T>(KT + (16 * dt + r) * G::LKT, 0, g);
+            }
+        }
+
+        if constexpr (!SUM) {
         // ---- Q fragments (columns: tokens) straight from global memory
         const int qrow = tb + min(r, cs - 1);
         F qf[KBD];
@@ -361,16 +431,8 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
 
         // ---- O^T (d rows, tokens columns) = V~^T (P o E)^T + V^T H^T
         floatx4 oT[NDT];
-        F vtf[NDT], ktf[NDT];
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-            if constexpr (BF) {
-                vtf[dt] = join(ld_tr(Vs + (4 * g + (r >> 2)) * G::LK + 16 * dt + 4 * (r & 3)), zero_half<T>());
-                ktf[dt] = join(ld_tr(Ks + (4 * g + (r >> 2)) * G::LK + 16 * dt + 4 * (r & 3)), zero_half<T>());
-            } else {
-                vtf[dt] = ld_frag_lo<T>(VT + (16 * dt + r) * G::LKT, 0, g);
-                ktf[dt] = ld_frag_lo<T>(KT + (16 * dt + r) * G::LKT, 0, g);
-            }
             floatx4 acc = zero4();
 #pragma unroll
             for (int kp = 0; kp < NPF; ++kp) {
@@ -400,6 +462,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
                 if (tok < cs) ob[(size_t)(tb + tok) * D + d] = (T)acc;
             }
         }
+        }  // !SUM
 
         // ---- state update: K~^T += K^T Bq, V~ += Bq^T V, then the decay E_{c-1} of the sub-block
 #pragma unroll
@@ -407,6 +470,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
             const F bqa = join(cvt4(floatx4{bq[t][0], bq[t][1], bq[t][2], bq[t][3]}, T()), zero_half<T>());
             const float ecol = sE[(cs - 1) * LG + s0w + 16 * t + r];
             const floatx4 erow = ld4f(sE + (cs - 1) * LG + s0w + 16 * t + 4 * g);
+            aprod[t] *= ecol;
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
                 Kst[t][dt] = mma(ktf[dt], bqa, Kst[t][dt]) * ecol;
@@ -416,6 +480,24 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         tb += cs;
     }
 
+    if constexpr (SUM) {
+        // ---- segment summary: K~ rows, V~ rows, gate product
+        float* sm = a.summ + ((size_t)bh * (a.nseg - 1) + seg) * SF;
+#pragma unroll
+        for (int t = 0; t < NSTW; ++t) {
+            const int sc = s0w + 16 * t + r;
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                st4f(sm + (size_t)sc * D + 16 * dt + 4 * g, Kst[t][dt]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    sm[(size_t)SP * D + (size_t)(s0w + 16 * t + 4 * g + e) * D + 16 * dt + r] = Vst[t][dt][e];
+            }
+            if (g == 0) sm[(size_t)2 * SP * D + sc] = aprod[t];
+        }
+        return;
+    }
+    if (seg != a.nseg - 1) return;
     // ---- final slot states
 #pragma unroll
     for (int t = 0; t < NSTW; ++t) {
@@ -431,6 +513,29 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
                 }
             }
         }
+    }
+}
+
+// Entering states of the segments, in place over the summaries: thread (b,h, element)
+// walks the segments, carry_{g+1} = A_g o carry_g + S_g from carry_0 = the input state,
+// and stores carry_{g+1} where S_g was.
+template <int D, int SP>
+__global__ __launch_bounds__(256) void decay_scan_kernel(DecayArgs a)
+{
+    constexpr size_t PER = (size_t)2 * SP * D, SF = decay_summary_floats<D, SP>();
+    const size_t gid = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (gid >= (size_t)a.B * a.H * PER) return;
+    const size_t bh = gid / PER, e = gid % PER;
+    const int half = (int)(e / ((size_t)SP * D));
+    const int rem = (int)(e % ((size_t)SP * D)), s = rem / D, d = rem % D;
+    float x = 0.f;
+    const float* in = half ? a.sv_in : a.sk_in;
+    if (in && s < a.S) x = in[(bh * a.S + s) * D + d];
+    float* base = a.summ + bh * (size_t)(a.nseg - 1) * SF;
+    for (int g = 0; g < a.nseg - 1; ++g) {
+        float* sg = base + (size_t)g * SF;
+        x = sg[PER + s] * x + sg[e];
+        sg[e] = x;
     }
 }
 
@@ -531,15 +636,26 @@ __global__ __launch_bounds__((decay_step_threads<D, SP>())) void decay_step_kern
     }
 }
 
+template <typename T, int D, int SP>
+static hipError_t launch_decay_sp(const DecayArgs& a, hipStream_t s)
+{
+    const unsigned units = (unsigned)(a.B * a.H);
+    if (a.nseg > 1) {
+        hipLaunchKernelGGL((decay_forward_kernel<T, D, SP, true>), dim3(units * (a.nseg - 1)),
+                           dim3(DecayGeo<D, SP>::NTH), 0, s, a);
+        const size_t n = (size_t)units * 2 * SP * D;
+        hipLaunchKernelGGL((decay_scan_kernel<D, SP>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+    }
+    hipLaunchKernelGGL((decay_forward_kernel<T, D, SP, false>), dim3(units * a.nseg), dim3(DecayGeo<D, SP>::NTH),
+                       0, s, a);
+    return hipGetLastError();
+}
+
 template <typename T, int D>
 static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s)
 {
-    const dim3 grid((unsigned)(a.B * a.H));
-#define BLA_DECAY_SP(SSP)                                                                                   \
-    if (SP == SSP) {                                                                                        \
-        hipLaunchKernelGGL((decay_forward_kernel<T, D, SSP>), grid, dim3(DecayGeo<D, SSP>::NTH), 0, s, a); \
-        return hipGetLastError();                                                                           \
-    }
+#define BLA_DECAY_SP(SSP) \
+    if (SP == SSP) return launch_decay_sp<T, D, SSP>(a, s);
     BLA_DECAY_SP(32)
     BLA_DECAY_SP(64)
     BLA_DECAY_SP(128)

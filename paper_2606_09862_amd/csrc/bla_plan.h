@@ -110,10 +110,20 @@ struct DecayArgs {
     const int* theta;       // [H][SP] start-mask thresholds (INT32_MAX for padded slots)
     const double* period;   // [H] clamped period T
     const double* rperiod;  // [H] 1 / T
+    float* summ;            // [B*H][nseg-1] segment summaries, scanned in place into entering states
     int B, H, L, M, S;
+    int nseg, seg_len;      // segments per sequence and their length (a multiple of 16 tokens)
     long long t0;
     float scale;
 };
+
+// Waves per workgroup of the decay forward kernel for (d, padded S) (its slot tiles over the
+// waves: each wave holds at most 16 / (d / 16) slot tiles of state).
+inline int decay_waves(int D, int SP)
+{
+    const int ndt = D / 16, nst = SP / 16, per = 16 / ndt < nst ? 16 / ndt : nst;
+    return nst / per;
+}
 
 struct DecayStepArgs {
     const void* q;
