@@ -12,10 +12,11 @@ the host on the same workload, and the decode step (bla_step) on the decode
 workload (B=512, H=16, d=M=S=64 after a 2048-token prefill).
 
 The headline is the operator with slots at lags behind the current token (Sec. 3.1).
-The anchored-slot form (Sec. 3.3, Alg. 1/3; phase_anchor = 1) is measured the same way
-on the same workload and reported under "anchored", with its own oracle timed on a
-bounded sample.  --form anchored makes the anchored form the only forward that runs
-(for profiling it alone).
+The anchored-slot form (Sec. 3.3, Alg. 1/3; phase_anchor = 1) and the state-decay form
+(Sec. 3.4, bla_decay_forward) are measured the same way on the same workload and reported
+under "anchored" and "decay", each with its own oracle timed on the host.  --form
+anchored / --form decay makes that form the only forward that runs (for profiling it
+alone).
 """
 from __future__ import annotations
 
@@ -42,6 +43,14 @@ def forward_flops_per_token_head(C, d, M, S):
     return 2 * (C + 1) * d + 4 * (C + 1) * M + 8 * M * S + 16 * M * d
 
 
+def decay_flops_per_token_head(d, S, sub=16):
+    """Algorithmic flops of the decay form's sub-block contractions per (token, head):
+    K~ Q^T and the readout against V~ (2 S d each), the state update of K~ and V~ (4 S d),
+    and the causal sub-block terms Bq^T G^T, tril(Bq P^T), G and V H (about S + d each per
+    token pair, (sub + 1) / 2 pairs)."""
+    return 8 * S * d + (sub + 1) * (2 * S + 2 * d)
+
+
 def forward_bytes(B, H, L, d, M, io_bytes):
     """q, k, v read + o written (io dtype) + final fp32 states written."""
     return B * H * L * d * io_bytes * 4 + B * H * 2 * (2 * M * d * 4)
@@ -50,7 +59,7 @@ def forward_bytes(B, H, L, d, M, io_bytes):
 def kernel_sources_digest():
     csrc = os.path.join(ROOT, "paper_2606_09862_amd", "csrc")
     h = hashlib.sha256()
-    for name in ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"):
+    for name in ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h", "bla_decay.hip"):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -101,7 +110,7 @@ class Hip:
         return ms.value
 
 
-def bench_forward(args, hip, inputs, anchor):
+def bench_forward(args, hip, inputs, form):
     import numpy as np
     import torch
 
@@ -113,24 +122,28 @@ def bench_forward(args, hip, inputs, anchor):
     q, k, v = inputs
     dev = torch.device("cuda:0")
     tq, tk, tv = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v))
-    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, phase_anchor=anchor)
-    ws = torch.empty(bla.workspace_size(p), dtype=torch.uint8, device=dev)
+    decay = form == "decay"
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, phase_anchor=form == "anchored")
+    ws_bytes = bla.decay_workspace_size(p) if decay else bla.workspace_size(p)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     o = torch.empty_like(tq)
-    sk = torch.empty((w.B, w.H, 2, w.M, w.d), dtype=torch.float32, device=dev)
+    state_shape = (w.B, w.H, w.S, w.d) if decay else (w.B, w.H, 2, w.M, w.d)
+    sk = torch.empty(state_shape, dtype=torch.float32, device=dev)
     sv = torch.empty_like(sk)
     stream = torch.cuda.current_stream(dev)
     sptr = ctypes.c_void_p(stream.cuda_stream)
     Tarr = (ctypes.c_double * w.H)(*T)
     L = bla.lib()
-    L.bla_forward_timed.argtypes = [ctypes.POINTER(bla.Params), ctypes.POINTER(ctypes.c_double)] + \
+    fn = L.bla_decay_forward_timed if decay else L.bla_forward_timed
+    fn.argtypes = [ctypes.POINTER(bla.Params), ctypes.POINTER(ctypes.c_double)] + \
         [ctypes.c_void_p] * 9 + [ctypes.c_size_t, ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)]
-    L.bla_forward_timed.restype = ctypes.c_int
+    fn.restype = ctypes.c_int
     ptrs = [ctypes.c_void_p(t.data_ptr()) if t is not None else None
             for t in (tq, tk, tv, None, None, o, sk, sv, ws)]
 
     def call(evs):
         arr = None if evs is None else (ctypes.c_void_p * 5)(*[e.value for e in evs])
-        st = L.bla_forward_timed(ctypes.byref(p), Tarr, *ptrs, ws.numel(), sptr, arr)
+        st = fn(ctypes.byref(p), Tarr, *ptrs, ws.numel(), sptr, arr)
         if st != 0:
             raise RuntimeError(f"bla_forward failed: {bla.STATUS.get(st, st)}")
 
@@ -156,18 +169,24 @@ def bench_forward(args, hip, inputs, anchor):
     phase_ms = {ph: float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs]))
                 for j, ph in enumerate(phases)}
     tokens = w.B * w.L
-    flops = forward_flops_per_token_head(w.chunk, w.d, w.M, w.S) * w.B * w.H * w.L
-    nbytes = forward_bytes(w.B, w.H, w.L, w.d, w.M, 2)
+    if decay:
+        flops = decay_flops_per_token_head(w.d, w.S) * w.B * w.H * w.L
+        nbytes = w.B * w.H * w.L * w.d * 2 * 4 + w.B * w.H * 2 * w.S * w.d * 4
+    else:
+        flops = forward_flops_per_token_head(w.chunk, w.d, w.M, w.S) * w.B * w.H * w.L
+        nbytes = forward_bytes(w.B, w.H, w.L, w.d, w.M, 2)
     t_fwd = phase_ms["forward"] * 1e-3
     achieved_gbs = nbytes / t_fwd / 1e9
     digest = kernel_sources_digest()
-    tname = "forward_pair_kernel_lm_layer_anchored_traffic.txt" if anchor else "forward_pair_kernel_lm_layer_traffic.txt"
+    tname = {"rotating": "forward_pair_kernel_lm_layer_traffic.txt",
+             "anchored": "forward_pair_kernel_lm_layer_anchored_traffic.txt",
+             "decay": "decay_forward_kernel_lm_layer_traffic.txt"}[form]
     traffic = read_traffic(os.path.join(ROOT, "profiles", tname), digest)
     roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
     t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
     extra = {
-        "kernel": "forward_pair_kernel<64,64,64>",
+        "kernel": "decay_forward_kernel<bf16,64,64>" if decay else "forward_pair_kernel<64,64,64>",
         "algorithmic_bytes_per_launch": nbytes,
         "algorithmic_flops_per_launch": flops,
         "forward_kernel_us": round(phase_ms["forward"] * 1e3, 2),
@@ -234,6 +253,21 @@ def cpu_baseline_anchored(w, T, inputs):
                       f"Alg. 1 with slot states, OpenMP over (b,h); {dt:.2f} s wall"}
 
 
+def cpu_baseline_decay(w, T, inputs):
+    """Decay-form oracle (token by token, decayed slot states) on the whole workload."""
+    import oracle
+
+    q, k, v = inputs
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    threads = max(1, min(threads, w.B * w.H))
+    t = time.perf_counter()
+    oracle.forward_decay(q, k, v, T, w.M, w.S, nthreads=threads)
+    dt = time.perf_counter() - t
+    return {"value": round(w.B * w.L / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"the whole LM-layer workload ({w.B}x{w.H} sequences of {w.L} tokens), float64 "
+                      f"decayed slot recurrence, OpenMP over (b,h); {dt:.2f} s wall"}
+
+
 def cpu_baseline(w, T, inputs):
     import oracle
 
@@ -256,8 +290,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-anchored", action="store_true", help="skip the anchored-slot measurement")
-    ap.add_argument("--form", choices=("rotating", "anchored"), default="rotating",
-                    help="the form of the headline forward; with 'anchored' no other forward runs")
+    ap.add_argument("--no-decay", action="store_true", help="skip the state-decay measurement")
+    ap.add_argument("--form", choices=("rotating", "anchored", "decay"), default="rotating",
+                    help="the form of the headline forward; otherwise no other forward runs")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="first run one plain device copy of this many bytes (reference kernel for "
                          "scaling the HBM byte counters of a rocprofv3 --pmc run)")
@@ -280,29 +315,31 @@ def main():
         del src, dst
     import bla_inputs as bi
     inputs = bi.generate(3)
-    head_anchor = args.form == "anchored"
-    w, T, ms, value, roofline, extra = bench_forward(args, hip, inputs, head_anchor)
-    anchored = None
-    if not head_anchor and not args.no_anchored:
-        _, _, a_ms, a_value, a_roof, a_extra = bench_forward(args, hip, inputs, True)
-        anchored = {"form": "anchored slots (Sec. 3.3, Alg. 1/3), phase_anchor=1", "value": round(a_value, 1),
-                    "unit": "tokens/s", "ms_per_step": round(a_ms, 5), "roofline": a_roof,
-                    "forward_detail": a_extra,
-                    "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_anchored(w, T, inputs)}
-    decode = None if args.no_decode or head_anchor else bench_decode(args, hip)
-    if args.no_cpu_baseline:
-        cpu = None
-    else:
-        cpu = cpu_baseline_anchored(w, T, inputs) if head_anchor else cpu_baseline(w, T, inputs)
+    head = args.form
+    w, T, ms, value, roofline, extra = bench_forward(args, hip, inputs, head)
+    baselines = {"rotating": cpu_baseline, "anchored": cpu_baseline_anchored, "decay": cpu_baseline_decay}
+    titles = {"anchored": "anchored slots (Sec. 3.3, Alg. 1/3), phase_anchor=1",
+              "decay": "state decay (Sec. 3.4), bla_decay_forward, float32 slot states [B,H,S,d]"}
+    others = {}
+    for form, skip in (("anchored", args.no_anchored), ("decay", args.no_decay)):
+        if head != "rotating" or skip:
+            others[form] = None
+            continue
+        _, _, f_ms, f_value, f_roof, f_extra = bench_forward(args, hip, inputs, form)
+        others[form] = {"form": titles[form], "value": round(f_value, 1), "unit": "tokens/s",
+                        "ms_per_step": round(f_ms, 5), "roofline": f_roof, "forward_detail": f_extra,
+                        "cpu_baseline": None if args.no_cpu_baseline else baselines[form](w, T, inputs)}
+    decode = None if args.no_decode or head != "rotating" else bench_decode(args, hip)
+    cpu = None if args.no_cpu_baseline else baselines[head](w, T, inputs)
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "lm_layer", "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": w.M, "S": w.S,
                    "chunk": w.chunk, "periods": "T_h=(1+h%2)(2M-1)", "state": "fp32",
-                   "phase_anchor": head_anchor},
+                   "form": head},
         "roofline": roofline, "cpu_baseline": cpu, "forward_detail": extra, "decode_step": decode,
-        "anchored": anchored,
+        "anchored": others["anchored"], "decay": others["decay"],
     }
     print(json.dumps(line), flush=True)
 

@@ -182,6 +182,19 @@ bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q
                              size_t workspace_bytes, void* stream);
 
 /*
+ * bla_decay_forward with phase timing, for measurement tools: events[0..4] are hipEvent_t
+ * handles created by the caller (any entry, or the array, may be NULL), recorded on
+ * `stream` before the table kernel, after it, after the segment-summary pass, after the
+ * scan of the summaries, and after the forward pass (a pass that does not run for this
+ * shape still gets its event).  Everything else is exactly bla_decay_forward;
+ * BLA_ERR_HIP is also returned if an event cannot be recorded.
+ */
+bla_status bla_decay_forward_timed(const bla_params* p, const double* T, const void* q, const void* k,
+                                   const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
+                                   float* slot_k_out, float* slot_v_out, void* workspace,
+                                   size_t workspace_bytes, void* stream, void* const* events);
+
+/*
  * One decay-form decode step for every (b,h): q, k [B,H,d_k], v, o [B,H,d_v], the token of
  * row b at absolute position pos[b] (device int64 [B]; NULL = p->t0); slot_k / slot_v
  * [B,H,S,d] are updated in place.

@@ -421,10 +421,10 @@ size_t bla_decay_workspace_size(const bla_params* p)
     return dp.total;
 }
 
-bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q, const void* k,
-                             const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
-                             float* slot_k_out, float* slot_v_out, void* workspace, size_t workspace_bytes,
-                             void* stream)
+static bla_status decay_forward_impl(const bla_params* p, const double* T, const void* q, const void* k,
+                                     const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
+                                     float* slot_k_out, float* slot_v_out, void* workspace,
+                                     size_t workspace_bytes, void* stream, void* const* events)
 {
     bla_status st = check_shape(p, true);
     if (st != BLA_OK) return st;
@@ -453,7 +453,12 @@ bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q
         if (launch_state_copy(slot_v_in, slot_v_out, n, s) != hipSuccess) return BLA_ERR_HIP;
         return BLA_OK;
     }
+    auto mark = [&](int i) -> bool {
+        return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
+    };
+    if (!mark(0)) return BLA_ERR_HIP;
     if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
+    if (!mark(1)) return BLA_ERR_HIP;
     DecayArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
@@ -477,8 +482,27 @@ bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q
     a.seg_len = dp.seg_len;
     a.t0 = p->t0;
     a.scale = pl.scale;
-    if (launch_decay_forward(pl.bf16, pl.D, pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;
+    if (launch_decay_forward(pl.bf16, pl.D, pl.SP, a, s, events ? events + 2 : nullptr) != hipSuccess)
+        return BLA_ERR_HIP;
     return BLA_OK;
+}
+
+bla_status bla_decay_forward(const bla_params* p, const double* T, const void* q, const void* k,
+                             const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
+                             float* slot_k_out, float* slot_v_out, void* workspace, size_t workspace_bytes,
+                             void* stream)
+{
+    return decay_forward_impl(p, T, q, k, v, slot_k_in, slot_v_in, o, slot_k_out, slot_v_out, workspace,
+                              workspace_bytes, stream, nullptr);
+}
+
+bla_status bla_decay_forward_timed(const bla_params* p, const double* T, const void* q, const void* k,
+                                   const void* v, const float* slot_k_in, const float* slot_v_in, void* o,
+                                   float* slot_k_out, float* slot_v_out, void* workspace,
+                                   size_t workspace_bytes, void* stream, void* const* events)
+{
+    return decay_forward_impl(p, T, q, k, v, slot_k_in, slot_v_in, o, slot_k_out, slot_v_out, workspace,
+                              workspace_bytes, stream, events);
 }
 
 bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, const void* k,

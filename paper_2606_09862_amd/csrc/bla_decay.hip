@@ -636,26 +636,36 @@ __global__ __launch_bounds__((decay_step_threads<D, SP>())) void decay_step_kern
     }
 }
 
+// ev (nullable, entries nullable): hipEvent_t recorded after the summary pass, after the scan
+// and after the forward pass.
 template <typename T, int D, int SP>
-static hipError_t launch_decay_sp(const DecayArgs& a, hipStream_t s)
+static hipError_t launch_decay_sp(const DecayArgs& a, hipStream_t s, void* const* ev)
 {
+    auto mark = [&](int i) -> hipError_t {
+        return (ev && ev[i]) ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
+    };
     const unsigned units = (unsigned)(a.B * a.H);
-    if (a.nseg > 1) {
+    if (a.nseg > 1)
         hipLaunchKernelGGL((decay_forward_kernel<T, D, SP, true>), dim3(units * (a.nseg - 1)),
                            dim3(DecayGeo<D, SP>::NTH), 0, s, a);
+    hipError_t e = mark(0);
+    if (e != hipSuccess) return e;
+    if (a.nseg > 1) {
         const size_t n = (size_t)units * 2 * SP * D;
         hipLaunchKernelGGL((decay_scan_kernel<D, SP>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
     }
+    if ((e = mark(1)) != hipSuccess) return e;
     hipLaunchKernelGGL((decay_forward_kernel<T, D, SP, false>), dim3(units * a.nseg), dim3(DecayGeo<D, SP>::NTH),
                        0, s, a);
-    return hipGetLastError();
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return mark(2);
 }
 
 template <typename T, int D>
-static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s)
+static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s, void* const* ev)
 {
 #define BLA_DECAY_SP(SSP) \
-    if (SP == SSP) return launch_decay_sp<T, D, SSP>(a, s);
+    if (SP == SSP) return launch_decay_sp<T, D, SSP>(a, s, ev);
     BLA_DECAY_SP(32)
     BLA_DECAY_SP(64)
     BLA_DECAY_SP(128)
@@ -664,16 +674,16 @@ static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s)
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s)
+hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s, void* const* ev)
 {
     if (bf16_io) {
-        if (D == 32) return launch_decay_d<bf16, 32>(a, SP, s);
-        if (D == 64) return launch_decay_d<bf16, 64>(a, SP, s);
-        if (D == 128) return launch_decay_d<bf16, 128>(a, SP, s);
+        if (D == 32) return launch_decay_d<bf16, 32>(a, SP, s, ev);
+        if (D == 64) return launch_decay_d<bf16, 64>(a, SP, s, ev);
+        if (D == 128) return launch_decay_d<bf16, 128>(a, SP, s, ev);
     } else {
-        if (D == 32) return launch_decay_d<float, 32>(a, SP, s);
-        if (D == 64) return launch_decay_d<float, 64>(a, SP, s);
-        if (D == 128) return launch_decay_d<float, 128>(a, SP, s);
+        if (D == 32) return launch_decay_d<float, 32>(a, SP, s, ev);
+        if (D == 64) return launch_decay_d<float, 64>(a, SP, s, ev);
+        if (D == 128) return launch_decay_d<float, 128>(a, SP, s, ev);
     }
     return hipErrorInvalidValue;
 }

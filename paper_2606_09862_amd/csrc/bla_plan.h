@@ -147,7 +147,8 @@ hipError_t launch_scan(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_state_copy(const float* src, float* dst, size_t n, hipStream_t s);
 hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
-hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s);
+hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s,
+                                void* const* events);
 hipError_t launch_decay_step(int bf16_io, int D, int SP, const DecayStepArgs& a, hipStream_t s);
 
 // Whether a forward kernel exists for (bf16, D, MP, SP).
