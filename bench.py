@@ -56,10 +56,19 @@ def forward_bytes(B, H, L, d, M, io_bytes):
     return B * H * L * d * io_bytes * 4 + B * H * 2 * (2 * M * d * 4)
 
 
-def kernel_sources_digest():
+KERNEL_SOURCES = {
+    "rotating": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"),
+    "anchored": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"),
+    "decay": ("bla_device.h", "bla_plan.h", "bla_decay.hip"),
+}
+
+
+def kernel_sources_digest(form):
+    """Digest of the sources the form's forward kernels are built from; a committed traffic
+    figure is used only while it matches."""
     csrc = os.path.join(ROOT, "paper_2606_09862_amd", "csrc")
     h = hashlib.sha256()
-    for name in ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h", "bla_decay.hip"):
+    for name in KERNEL_SOURCES[form]:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -177,7 +186,7 @@ def bench_forward(args, hip, inputs, form):
         nbytes = forward_bytes(w.B, w.H, w.L, w.d, w.M, 2)
     t_fwd = phase_ms["forward"] * 1e-3
     achieved_gbs = nbytes / t_fwd / 1e9
-    digest = kernel_sources_digest()
+    digest = kernel_sources_digest(form)
     tname = {"rotating": "forward_pair_kernel_lm_layer_traffic.txt",
              "anchored": "forward_pair_kernel_lm_layer_anchored_traffic.txt",
              "decay": "decay_forward_kernel_lm_layer_traffic.txt"}[form]
