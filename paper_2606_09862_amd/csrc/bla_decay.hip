@@ -43,8 +43,9 @@ constexpr float kDecayEps = 9.094947017729282e-13f;  // 2^-40
 
 template <int D, int SP> struct DecayGeo {
     static constexpr int NDT = D / 16, KBD = D / 32, NST = SP / 16;
-    // slot tiles per wave: the wave's fp32 state is 2 * NSTW * NDT tiles (128 VGPRs)
-    static constexpr int NSTW = (16 / NDT < NST) ? 16 / NDT : NST;
+    // slot tiles per wave: the wave's fp32 state is 2 * NSTW * NDT tiles (at most 64 VGPRs,
+    // so that two waves fit on a SIMD)
+    static constexpr int NSTW = decay_slot_tiles_per_wave(D, SP);
     static constexpr int NWU = NST / NSTW;  // waves per workgroup
     static constexpr int NTH = 64 * NWU;
     static constexpr int LK = D + 12;       // K, V rows [16][LK] (bf16), conflict-free transposed reads

@@ -117,13 +117,17 @@ struct DecayArgs {
     float scale;
 };
 
-// Waves per workgroup of the decay forward kernel for (d, padded S) (its slot tiles over the
-// waves: each wave holds at most 16 / (d / 16) slot tiles of state).
-inline int decay_waves(int D, int SP)
+// Slot tiles per wave of the decay forward kernel for (d, padded S): 8 / (d / 16) tiles (the
+// wave's K~ and V~ state then takes 64 VGPRs), at least 1, at most all of them, and at
+// least 1/8 of them (so a workgroup has at most 8 waves).
+constexpr int decay_slot_tiles_per_wave(int D, int SP)
 {
-    const int ndt = D / 16, nst = SP / 16, per = 16 / ndt < nst ? 16 / ndt : nst;
-    return nst / per;
+    const int nst = SP / 16, want = 8 / (D / 16) > 0 ? 8 / (D / 16) : 1;
+    const int lo = (nst + 7) / 8;
+    return want < lo ? lo : (want > nst ? nst : want);
 }
+// Waves per workgroup of the decay forward kernel.
+inline int decay_waves(int D, int SP) { return (SP / 16) / decay_slot_tiles_per_wave(D, SP); }
 
 struct DecayStepArgs {
     const void* q;
