@@ -12,7 +12,9 @@ evaluated on the dilated slot grid) so the tests can pin them.
 ``forward_anchored`` runs the absolute-phase form of Sec. 3.3 (Alg. 1: slots
 anchored at phase 0, slot states accumulated as a cumulative sum) token by token;
 ``forward_decay`` the same with the state decay of Sec. 3.4 (previous slot state
-multiplied by 1 - D before each write).
+multiplied by 1 - D before each write).  ``backward`` differentiates Alg. 2: the chain
+rule taken through the token loop in reverse, with the forward states of every token
+stored by a forward pass.
 
 Parity status of each function (what pins it) is listed in the tests
 (``tests/test_oracle_pins.py``); every function here is pinned.
@@ -65,6 +67,9 @@ def _load():
             _dp, ctypes.c_int64, ctypes.c_double, _dp, _dp, _dp, _dp, _dp, _dp, _dp, _dp,
             ctypes.c_int, ctypes.c_int]
         lib.bla_oracle_forward_anchored.restype = ctypes.c_int
+        lib.bla_oracle_backward.argtypes = [ctypes.c_int] * 7 + [
+            _dp, ctypes.c_int64, ctypes.c_double] + [_dp] * 13 + [ctypes.c_int]
+        lib.bla_oracle_backward.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -170,3 +175,34 @@ def forward_decay(q, k, v, T, M: int, S: int, t0: int = 0, scale=None, slot_k=No
     forward_anchored."""
     return forward_anchored(q, k, v, T, M, S, t0=t0, scale=scale, slot_k=slot_k, slot_v=slot_v,
                             nthreads=nthreads, decay=True)
+
+
+def backward(q, k, v, dO, T, M: int, S: int, t0: int = 0, scale=None, state_k=None, state_v=None,
+             dstate_k=None, dstate_v=None, nthreads: int = 0):
+    """Gradients of Alg. 2 (the operator of ``forward``) for the loss whose gradients are
+    dO = dLoss/dO [B,H,L,dv] and dstate_k / dstate_v = dLoss/d(final states) [B,H,2,M,d]
+    (None = zero).  state_k / state_v are the forward's input states (None = zero).
+
+    Returns (dq [B,H,L,dk], dk [B,H,L,dk], dv [B,H,L,dv], dLoss/d(state_k in),
+    dLoss/d(state_v in)) in float64.
+    """
+    q, k, v, dO = _f64(q), _f64(k), _f64(v), _f64(dO)
+    Bn, H, L, dk = q.shape
+    dv = v.shape[-1]
+    assert k.shape == q.shape and v.shape[:3] == (Bn, H, L) and dO.shape == v.shape
+    T = np.ascontiguousarray(np.broadcast_to(np.asarray(T, np.float64), (H,)))
+    if scale is None:
+        scale = 1.0 / np.sqrt(dk)
+    dq = np.zeros_like(q)
+    dkk = np.zeros_like(k)
+    dvv = np.zeros_like(v)
+    gsk = np.zeros((Bn, H, 2, M, dk), np.float64)
+    gsv = np.zeros((Bn, H, 2, M, dv), np.float64)
+    rc = _load().bla_oracle_backward(Bn, H, L, dk, dv, M, S, _ptr(T), int(t0), float(scale),
+                                     _ptr(q), _ptr(k), _ptr(v), _ptr(dO), _ptr(_f64(state_k)),
+                                     _ptr(_f64(state_v)), _ptr(_f64(dstate_k)), _ptr(_f64(dstate_v)),
+                                     _ptr(dq), _ptr(dkk), _ptr(dvv), _ptr(gsk), _ptr(gsv),
+                                     int(nthreads))
+    if rc != 0:
+        raise ValueError("bla_oracle_backward rejected its arguments")
+    return dq, dkk, dvv, gsk, gsv

@@ -396,3 +396,235 @@ int bla_oracle_forward_anchored(int Bn, int H, int L, int dk, int dv, int M, int
     }
     return err ? -1 : 0;
 }
+
+/*
+ * Gradients of Alg. 2 (reverse-mode differentiation of the token loop; the paper trains
+ * every model of Sec. 4 through this operator but states no backward pass, so this is the
+ * chain rule applied to the forward definition above, step by step in reverse).
+ *
+ * Given dO = dLoss/dO and dZk_out, dZv_out = dLoss/d(final states) (zero if absent), for
+ * t = L-1 down to 0, with the states after token t's update (stored by a forward pass) and
+ * the adjoint gK, gV = dLoss/d(state after token t):
+ *   slots:        Kt[s] = sum_m A[s][m] Kcos[m] + B[s][m] Ksin[m],  Vt likewise
+ *   softmax:      p = softmax(z) with z_s = scale <q_t, Kt[s]> (masked slots: p_s = 0)
+ *   readout:      dp_s = <dO_t, Vt[s]>,   dVt[s] = p_s dO_t
+ *   softmax grad: dz_s = p_s (dp_s - sum_s' p_s' dp_s')
+ *   scores:       dq_t = scale sum_s dz_s Kt[s],   dKt[s] = scale dz_s q_t
+ *   slot grads into the adjoint:  gKcos[m] += sum_s A[s][m] dKt[s],  gKsin[m] += sum_s B[s][m] dKt[s]
+ *                                 (gV from dVt likewise)
+ *   recurrence:   k_t was added to every cos row, so dk_t = sum_m gKcos[m] (dv_t likewise);
+ *                 the rotation (c, s) = (cos m w, sin m w) is orthogonal, so the adjoint of the
+ *                 state before the token is  gcos' = c gcos + s gsin,  gsin' = -s gcos + c gsin.
+ * After t = 0 the adjoint is dLoss/d(state_in).
+ */
+static void run_sequence_backward(int L, int dk, int dv, int M, int S, double T_in, int64_t t0,
+                                  double scale, const double* q, const double* k, const double* v,
+                                  const double* dO, const double* sk_in, const double* sv_in,
+                                  double* gK, double* gV, double* dq, double* dkk, double* dvv,
+                                  double* hist, double* work)
+{
+    double T = clamp_period(T_in, M);
+    double w = 2.0 * ORACLE_PI / T;
+    size_t skl = 2 * (size_t)M * dk, svl = 2 * (size_t)M * dv;
+    double* A = work;                        /* S*M */
+    double* Bm = A + (size_t)S * M;          /* S*M */
+    int64_t* theta = (int64_t*)(Bm + (size_t)S * M); /* S */
+    double* rc = (double*)(theta + S);       /* M */
+    double* rs = rc + M;                     /* M */
+    double* p = rs + M;                      /* S */
+    double* dz = p + S;                      /* S */
+    double* Kt = dz + S;                     /* S*dk */
+    double* Vt = Kt + (size_t)S * dk;        /* S*dv */
+
+    bla_oracle_interp(M, S, T, A, Bm, theta);
+    for (int m = 0; m < M; ++m) {
+        rc[m] = cos(m * w);
+        rs[m] = sin(m * w);
+    }
+
+    /* forward pass: hist[t] = (Kcos, Ksin, Vcos, Vsin) after token t's update */
+    for (int t = 0; t < L; ++t) {
+        const double* prev = t ? hist + (size_t)(t - 1) * (skl + svl) : NULL;
+        double* cur = hist + (size_t)t * (skl + svl);
+        for (int m = 0; m < M; ++m) {
+            for (int d = 0; d < dk; ++d) {
+                double c = prev ? prev[(size_t)m * dk + d] : (sk_in ? sk_in[(size_t)m * dk + d] : 0.0);
+                double s = prev ? prev[(size_t)(M + m) * dk + d]
+                                : (sk_in ? sk_in[(size_t)(M + m) * dk + d] : 0.0);
+                cur[(size_t)m * dk + d] = rc[m] * c - rs[m] * s + k[(size_t)t * dk + d];
+                cur[(size_t)(M + m) * dk + d] = rs[m] * c + rc[m] * s;
+            }
+            for (int d = 0; d < dv; ++d) {
+                double c = prev ? prev[skl + (size_t)m * dv + d] : (sv_in ? sv_in[(size_t)m * dv + d] : 0.0);
+                double s = prev ? prev[skl + (size_t)(M + m) * dv + d]
+                                : (sv_in ? sv_in[(size_t)(M + m) * dv + d] : 0.0);
+                cur[skl + (size_t)m * dv + d] = rc[m] * c - rs[m] * s + v[(size_t)t * dv + d];
+                cur[skl + (size_t)(M + m) * dv + d] = rs[m] * c + rc[m] * s;
+            }
+        }
+    }
+
+    /* reverse pass */
+    for (int t = L - 1; t >= 0; --t) {
+        const double* st = hist + (size_t)t * (skl + svl);
+        const double* Kc = st;
+        const double* Ks = st + (size_t)M * dk;
+        const double* Vc = st + skl;
+        const double* Vs = st + skl + (size_t)M * dv;
+        const double* qt = q + (size_t)t * dk;
+        const double* gt = dO + (size_t)t * dv;
+        int64_t pos = t0 + t;
+
+        /* slots, scores and softmax, as in the forward */
+        for (int s = 0; s < S; ++s) {
+            for (int d = 0; d < dk; ++d) {
+                double acc = 0.0;
+                for (int m = 0; m < M; ++m)
+                    acc += A[(size_t)s * M + m] * Kc[(size_t)m * dk + d] + Bm[(size_t)s * M + m] * Ks[(size_t)m * dk + d];
+                Kt[(size_t)s * dk + d] = acc;
+            }
+            for (int d = 0; d < dv; ++d) {
+                double acc = 0.0;
+                for (int m = 0; m < M; ++m)
+                    acc += A[(size_t)s * M + m] * Vc[(size_t)m * dv + d] + Bm[(size_t)s * M + m] * Vs[(size_t)m * dv + d];
+                Vt[(size_t)s * dv + d] = acc;
+            }
+            double dot = 0.0;
+            for (int d = 0; d < dk; ++d) dot += qt[d] * Kt[(size_t)s * dk + d];
+            p[s] = pos < theta[s] ? -INFINITY : scale * dot;
+        }
+        double zmax = -INFINITY;
+        for (int s = 0; s < S; ++s)
+            if (p[s] > zmax) zmax = p[s];
+        double den = 0.0;
+        for (int s = 0; s < S; ++s) {
+            p[s] = (p[s] == -INFINITY) ? 0.0 : exp(p[s] - zmax);
+            den += p[s];
+        }
+        for (int s = 0; s < S; ++s) p[s] /= den;
+
+        /* readout and softmax gradients */
+        double pdp = 0.0;
+        for (int s = 0; s < S; ++s) {
+            double dot = 0.0;
+            for (int d = 0; d < dv; ++d) dot += gt[d] * Vt[(size_t)s * dv + d];
+            dz[s] = dot;
+            pdp += p[s] * dot;
+        }
+        for (int s = 0; s < S; ++s) dz[s] = p[s] * (dz[s] - pdp);
+
+        /* query gradient */
+        for (int d = 0; d < dk; ++d) {
+            double acc = 0.0;
+            for (int s = 0; s < S; ++s) acc += dz[s] * Kt[(size_t)s * dk + d];
+            dq[(size_t)t * dk + d] = scale * acc;
+        }
+
+        /* slot gradients into the adjoint of the state after token t */
+        for (int m = 0; m < M; ++m) {
+            for (int d = 0; d < dk; ++d) {
+                double ac = 0.0, as = 0.0;
+                for (int s = 0; s < S; ++s) {
+                    double g = scale * dz[s] * qt[d];
+                    ac += A[(size_t)s * M + m] * g;
+                    as += Bm[(size_t)s * M + m] * g;
+                }
+                gK[(size_t)m * dk + d] += ac;
+                gK[(size_t)(M + m) * dk + d] += as;
+            }
+            for (int d = 0; d < dv; ++d) {
+                double ac = 0.0, as = 0.0;
+                for (int s = 0; s < S; ++s) {
+                    double g = p[s] * gt[d];
+                    ac += A[(size_t)s * M + m] * g;
+                    as += Bm[(size_t)s * M + m] * g;
+                }
+                gV[(size_t)m * dv + d] += ac;
+                gV[(size_t)(M + m) * dv + d] += as;
+            }
+        }
+
+        /* the token entered every cos row */
+        for (int d = 0; d < dk; ++d) {
+            double acc = 0.0;
+            for (int m = 0; m < M; ++m) acc += gK[(size_t)m * dk + d];
+            dkk[(size_t)t * dk + d] = acc;
+        }
+        for (int d = 0; d < dv; ++d) {
+            double acc = 0.0;
+            for (int m = 0; m < M; ++m) acc += gV[(size_t)m * dv + d];
+            dvv[(size_t)t * dv + d] = acc;
+        }
+
+        /* through the rotation to the state before the token */
+        for (int m = 0; m < M; ++m) {
+            for (int d = 0; d < dk; ++d) {
+                double c = gK[(size_t)m * dk + d], s = gK[(size_t)(M + m) * dk + d];
+                gK[(size_t)m * dk + d] = rc[m] * c + rs[m] * s;
+                gK[(size_t)(M + m) * dk + d] = -rs[m] * c + rc[m] * s;
+            }
+            for (int d = 0; d < dv; ++d) {
+                double c = gV[(size_t)m * dv + d], s = gV[(size_t)(M + m) * dv + d];
+                gV[(size_t)m * dv + d] = rc[m] * c + rs[m] * s;
+                gV[(size_t)(M + m) * dv + d] = -rs[m] * c + rc[m] * s;
+            }
+        }
+    }
+}
+
+/*
+ * Backward over Bn*H sequences: dq, dk [Bn][H][L][dk], dv [Bn][H][L][dv]; dsk_out, dsv_out
+ * (nullable) receive dLoss/d(state_in).  sk_in, sv_in (nullable: zero) are the forward's
+ * input states; dsk_in, dsv_in (nullable: zero) are dLoss/d(final states).  Same argument
+ * rules and return codes as bla_oracle_forward.
+ */
+int bla_oracle_backward(int Bn, int H, int L, int dk, int dv, int M, int S, const double* T,
+                        int64_t t0, double scale, const double* q, const double* k,
+                        const double* v, const double* dO, const double* sk_in,
+                        const double* sv_in, const double* dsk_in, const double* dsv_in,
+                        double* dq, double* dkk, double* dvv, double* dsk_out, double* dsv_out,
+                        int nthreads)
+{
+    if (Bn < 0 || H < 0 || L < 0 || dk <= 0 || dv <= 0 || M <= 0 || S <= 0 || t0 < 0) return -1;
+    size_t nseq = (size_t)Bn * H;
+    size_t wlen = 2 * (size_t)S * M + (size_t)S + 2 * (size_t)M + 2 * (size_t)S +
+                  (size_t)S * (dk + dv);
+    size_t skl = 2 * (size_t)M * dk, svl = 2 * (size_t)M * dv;
+    int err = 0;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+#pragma omp parallel
+    {
+        double* work = (double*)malloc(wlen * sizeof(double));
+        double* adj = (double*)malloc((skl + svl) * sizeof(double));
+        double* hist = (double*)malloc(((size_t)(L > 0 ? L : 1)) * (skl + svl) * sizeof(double));
+        if (!work || !adj || !hist) {
+#pragma omp atomic write
+            err = 1;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (long long i = 0; i < (long long)nseq; ++i) {
+            if (!work || !adj || !hist) continue;
+            int h = (int)(i % H);
+            if (dsk_in) memcpy(adj, dsk_in + i * skl, skl * sizeof(double));
+            else memset(adj, 0, skl * sizeof(double));
+            if (dsv_in) memcpy(adj + skl, dsv_in + i * svl, svl * sizeof(double));
+            else memset(adj + skl, 0, svl * sizeof(double));
+            run_sequence_backward(L, dk, dv, M, S, T[h], t0, scale, q + i * (size_t)L * dk,
+                                  k + i * (size_t)L * dk, v + i * (size_t)L * dv,
+                                  dO + i * (size_t)L * dv, sk_in ? sk_in + i * skl : NULL,
+                                  sv_in ? sv_in + i * svl : NULL, adj, adj + skl,
+                                  dq + i * (size_t)L * dk, dkk + i * (size_t)L * dk,
+                                  dvv + i * (size_t)L * dv, hist, work);
+            if (dsk_out) memcpy(dsk_out + i * skl, adj, skl * sizeof(double));
+            if (dsv_out) memcpy(dsv_out + i * svl, adj + skl, svl * sizeof(double));
+        }
+        free(work);
+        free(adj);
+        free(hist);
+    }
+    return err ? -1 : 0;
+}

@@ -585,3 +585,110 @@ def test_p12_decay_forgets_the_past_at_T_equal_2M_minus_1():
     _, kt, _ = oracle.forward_decay(q, k, v, [float(W)], M, W)
     for tp in range(L - W, L):
         assert np.allclose(kt[0, 0, tp % W], k[0, 0, tp], atol=1e-13)
+
+
+# ---------------------------------------------------------------- P13: backward of Alg. 2
+def _loss(q, k, v, g, gk, gv, T, M, S, t0=0, sk=None, sv=None):
+    """The scalar loss whose gradients the backward computes: <g, O> + <gk, Zk_L> + <gv, Zv_L>."""
+    o, zk, zv = oracle.forward(q, k, v, T, M, S, t0=t0, state_k=sk, state_v=sv)
+    return float((o * g).sum() + (zk * gk).sum() + (zv * gv).sum())
+
+
+def test_p13_backward_every_element_by_finite_differences():
+    """Each element of dq, dk, dv and of the state-in gradients against a central finite
+    difference of the forward oracle (float64, h = 1e-6).  Brute force on a tiny problem
+    with a ragged period, S != 2M-1, t0 > 0 and nonzero states in and out: catches any
+    dropped term, sign or transposed index of the reverse pass."""
+    rng = np.random.default_rng(40)
+    B, H, L, d, M, S, t0 = 1, 2, 9, 3, 3, 4, 2
+    q, k, v = _inputs(rng, B, H, L, d)
+    g = rng.standard_normal((B, H, L, d))
+    sk, sv = (rng.standard_normal((B, H, 2, M, d)) * 0.3 for _ in range(2))
+    gk, gv = (rng.standard_normal((B, H, 2, M, d)) * 0.2 for _ in range(2))
+    T = [6.5, 11.0]
+    dq, dk, dv, dsk, dsv = oracle.backward(q, k, v, g, T, M, S, t0=t0, state_k=sk, state_v=sv,
+                                           dstate_k=gk, dstate_v=gv)
+    args = [q, k, v, sk, sv]
+    grads = [dq, dk, dv, dsk, dsv]
+    h = 1e-6
+    for which, (x, gx) in enumerate(zip(args, grads)):
+        fd = np.zeros_like(x)
+        for idx in np.ndindex(*x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += h
+            xm[idx] -= h
+            ap, am = list(args), list(args)
+            ap[which], am[which] = xp, xm
+            fp = _loss(ap[0], ap[1], ap[2], g, gk, gv, T, M, S, t0, ap[3], ap[4])
+            fm = _loss(am[0], am[1], am[2], g, gk, gv, T, M, S, t0, am[3], am[4])
+            fd[idx] = (fp - fm) / (2 * h)
+        assert _relerr(gx, fd) < 1e-7, (which, _relerr(gx, fd))
+
+
+@pytest.mark.parametrize("M,S,T,L,t0", [(5, 9, 18.5, 70, 0), (4, 4, 9.0, 41, 5), (8, 15, 15.0, 33, 0)])
+def test_p13_backward_directional_derivative(M, S, T, L, t0):
+    """Directional derivatives at larger sizes: <grad, delta> equals the central difference
+    of the loss along a random direction of every input at once."""
+    rng = np.random.default_rng(41)
+    B, H, d = 2, 2, 5
+    q, k, v = _inputs(rng, B, H, L, d)
+    g = rng.standard_normal((B, H, L, d))
+    gk, gv = (rng.standard_normal((B, H, 2, M, d)) * 0.1 for _ in range(2))
+    Ts = [T, 2 * T]
+    dq, dk, dv, _, _ = oracle.backward(q, k, v, g, Ts, M, S, t0=t0, dstate_k=gk, dstate_v=gv)
+    dirs = [rng.standard_normal(x.shape) for x in (q, k, v)]
+    h = 1e-5
+    fp = _loss(q + h * dirs[0], k + h * dirs[1], v + h * dirs[2], g, gk, gv, Ts, M, S, t0)
+    fm = _loss(q - h * dirs[0], k - h * dirs[1], v - h * dirs[2], g, gk, gv, Ts, M, S, t0)
+    an = float((dq * dirs[0]).sum() + (dk * dirs[1]).sum() + (dv * dirs[2]).sum())
+    assert abs((fp - fm) / (2 * h) - an) <= 1e-8 * max(1.0, abs(an))
+
+
+@pytest.mark.parametrize("M", [2, 4, 8])
+def test_p13_backward_full_attention_limit(M):
+    """T = S = 2M-1 and L <= 2M-1: the operator is causal softmax attention (P5), so its
+    gradients are those of torch's autograd through scaled_dot_product_attention (float64
+    CPU math path)."""
+    rng = np.random.default_rng(42)
+    W = 2 * M - 1
+    L, d = W, 6
+    q, k, v = _inputs(rng, 2, 2, L, d)
+    g = rng.standard_normal(v.shape)
+    dq, dk, dv, _, _ = oracle.backward(q, k, v, g, [float(W)] * 2, M, W)
+    tq, tk, tv = (torch.from_numpy(x).requires_grad_(True) for x in (q, k, v))
+    o = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, is_causal=True, scale=d ** -0.5)
+    o.backward(torch.from_numpy(g))
+    for a, b in ((dq, tq.grad), (dk, tk.grad), (dv, tv.grad)):
+        assert _relerr(a, b.numpy()) < 1e-12
+
+
+def test_p13_backward_single_mode():
+    """M = 1: o_t = sum_{t' <= t} v_t' whatever q and k are (P8), so dq = dk = 0 and dv is the
+    reverse cumulative sum of dO."""
+    rng = np.random.default_rng(43)
+    q, k, v = _inputs(rng, 1, 2, 17, 4)
+    g = rng.standard_normal(v.shape)
+    dq, dk, dv, _, _ = oracle.backward(q, k, v, g, [1.0, 5.5], 1, 3)
+    assert np.abs(dq).max() < 1e-13 and np.abs(dk).max() < 1e-13
+    assert _relerr(dv, np.cumsum(g[:, :, ::-1], axis=2)[:, :, ::-1]) < 1e-14
+
+
+@pytest.mark.parametrize("L1", [1, 13, 30])
+def test_p13_backward_split_call(L1):
+    """The state gradients chain calls: the backward of L tokens equals the backward of the
+    last L - L1 tokens (from the first part's final states, t0 = L1), whose state-in gradients
+    are then the final-state gradients of the first part."""
+    rng = np.random.default_rng(44)
+    M, S, L = 5, 7, 45
+    q, k, v = _inputs(rng, 2, 2, L, 4)
+    g = rng.standard_normal(v.shape)
+    Ts = [9.0, 13.5]
+    dq, dk, dv, _, _ = oracle.backward(q, k, v, g, Ts, M, S)
+    _, zk, zv = oracle.forward(q[:, :, :L1], k[:, :, :L1], v[:, :, :L1], Ts, M, S)
+    dq2, dk2, dv2, gk, gv = oracle.backward(q[:, :, L1:], k[:, :, L1:], v[:, :, L1:], g[:, :, L1:],
+                                            Ts, M, S, t0=L1, state_k=zk, state_v=zv)
+    dq1, dk1, dv1, _, _ = oracle.backward(q[:, :, :L1], k[:, :, :L1], v[:, :, :L1], g[:, :, :L1],
+                                          Ts, M, S, dstate_k=gk, dstate_v=gv)
+    assert _relerr(np.concatenate([dq1, dq2], 2), dq) < 1e-13
+    assert _relerr(np.concatenate([dk1, dk2], 2), dk) < 1e-13
+    assert _relerr(np.concatenate([dv1, dv2], 2), dv) < 1e-13
