@@ -203,6 +203,38 @@ bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, c
                           const void* v, const int64_t* pos, float* slot_k, float* slot_v, void* o,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Backward pass (gradients of the operator above, Alg. 2 with phase_anchor = 0).  The paper
+ * trains every model through this operator (Sec. 4); the gradients are those of the loss
+ * whose partial derivatives are dO = dLoss/dO [B,H,L,d_v] and dstate_k_out / dstate_v_out =
+ * dLoss/d(final states) [B,H,2,M,d] (NULL = zero).  q, k, v, state_k_in, state_v_in are the
+ * forward call's inputs (states NULL = zero); the forward outputs are not needed (the
+ * states are rebuilt chunk by chunk).  Writes dq, dk [B,H,L,d_k] and dv [B,H,L,d_v] in the
+ * io dtype, and dLoss/d(input states) into dstate_k_in / dstate_v_in [B,H,2,M,d] float32
+ * (NULL = not wanted; they must not alias the other state arguments).  L = 0 copies the
+ * final-state gradients (or zeros) to them.
+ * Supported: phase_anchor = 0; bfloat16 with d in {32, 64} or float32 with d = 32; M <= 64
+ * (float32: M <= 32) and S <= max(32, 2 P(M)) <= 128; anything else BLA_ERR_UNSUPPORTED.
+ * Every other convention (alignment, T, ownership, streams, errors) as for bla_forward.
+ */
+size_t bla_backward_workspace_size(const bla_params* p);
+bla_status bla_backward(const bla_params* p, const double* T, const void* q, const void* k, const void* v,
+                        const void* dO, const float* state_k_in, const float* state_v_in,
+                        const float* dstate_k_out, const float* dstate_v_out, void* dq, void* dk, void* dv,
+                        float* dstate_k_in, float* dstate_v_in, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/*
+ * bla_backward with phase timing, for measurement tools: events[0..4] (hipEvent_t, created by
+ * the caller; any entry or the array may be NULL) are recorded before the table kernel, after
+ * it, after the forward-summary pass, after the adjoint-summary pass and after the reverse walk.
+ */
+bla_status bla_backward_timed(const bla_params* p, const double* T, const void* q, const void* k,
+                              const void* v, const void* dO, const float* state_k_in, const float* state_v_in,
+                              const float* dstate_k_out, const float* dstate_v_out, void* dq, void* dk,
+                              void* dv, float* dstate_k_in, float* dstate_v_in, void* workspace,
+                              size_t workspace_bytes, void* stream, void* const* events);
+
 #ifdef __cplusplus
 }
 #endif

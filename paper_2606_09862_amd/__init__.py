@@ -1,4 +1,4 @@
-"""Blurry Window Attention forward operator on MI355X (gfx950).
+"""Blurry Window Attention forward operator (and its backward pass) on MI355X (gfx950).
 
 A thin ctypes binding over ``libbla.so`` (the C ABI in ``include/bla.h``).  It
 only marshals arguments: every step of the operator runs in the library's HIP
@@ -71,6 +71,13 @@ def lib():
         L.bla_decay_forward.restype = ctypes.c_int
         L.bla_decay_step.argtypes = [P, _dp] + [_vp] * 8 + [ctypes.c_size_t, _vp]
         L.bla_decay_step.restype = ctypes.c_int
+        L.bla_backward_workspace_size.argtypes = [P]
+        L.bla_backward_workspace_size.restype = ctypes.c_size_t
+        L.bla_backward.argtypes = [P, _dp] + [_vp] * 14 + [ctypes.c_size_t, _vp]
+        L.bla_backward.restype = ctypes.c_int
+        L.bla_backward_timed.argtypes = [P, _dp] + [_vp] * 14 + [ctypes.c_size_t, _vp,
+                                                                  ctypes.POINTER(ctypes.c_void_p)]
+        L.bla_backward_timed.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -254,3 +261,42 @@ def decay_step(q, k, v, T, M: int, S: int, slot_k, slot_v, pos=None, t0: int = 0
     if st != 0:
         raise BlaError(st, "bla_decay_step")
     return o
+
+
+def backward_workspace_size(p: Params) -> int:
+    return lib().bla_backward_workspace_size(ctypes.byref(p))
+
+
+def backward(q, k, v, dO, T, M: int, S: int, t0: int = 0, scale: float | None = None,
+             state_k=None, state_v=None, dstate_k=None, dstate_v=None, want_state_grad: bool = True,
+             workspace=None):
+    """bla_backward: gradients of ``forward`` (rotating slots) for dO = dLoss/dO [B,H,L,d] and
+    dstate_k / dstate_v = dLoss/d(final states) [B,H,2,M,d] (None = zero).  state_k / state_v
+    are the forward's input states.  Returns (dq, dk, dv, dLoss/d(state_k in),
+    dLoss/d(state_v in)); the last two are None when want_state_grad is False.
+    """
+    B, H, L, d = q.shape
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v), ("dO", dO)):
+        _check(t, (B, H, L, d), dt, name)
+    for name, t in (("state_k", state_k), ("state_v", state_v), ("dstate_k", dstate_k),
+                    ("dstate_v", dstate_v)):
+        if t is not None:
+            _check(t, (B, H, 2, M, d), torch.float32, name)
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale)
+    dev = q.device
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    gsk = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state_grad else None
+    gsv = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state_grad else None
+    need = backward_workspace_size(p)
+    if need == 0:
+        raise BlaError(2, "bla_backward (shape check)")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    st = lib().bla_backward(ctypes.byref(p), _periods(T, H), _ptr(q), _ptr(k), _ptr(v), _ptr(dO),
+                            _ptr(state_k), _ptr(state_v), _ptr(dstate_k), _ptr(dstate_v), _ptr(dq),
+                            _ptr(dk), _ptr(dv), _ptr(gsk), _ptr(gsv), _ptr(workspace), workspace.numel(),
+                            _stream(dev))
+    if st != 0:
+        raise BlaError(st, "bla_backward")
+    return dq, dk, dv, gsk, gsv

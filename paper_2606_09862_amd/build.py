@@ -29,8 +29,9 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}"
           "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
-# Units whose kernels the compiler cannot build with VGPR-form accumulators.
-NO_VGPR_FORM = {"bla_fwd_bf16_d128_wide.hip", "bla_fwd_f32_d128.hip"}
+# Units whose kernels the compiler cannot build with VGPR-form accumulators (or that need the
+# accumulation registers as well: the backward kernels hold four state tiles per wave).
+NO_VGPR_FORM = {"bla_fwd_bf16_d128_wide.hip", "bla_fwd_f32_d128.hip", "bla_bwd_bf16.hip", "bla_bwd_f32.hip"}
 
 
 def _compile(src: str) -> str:

@@ -218,6 +218,53 @@ void make_decay_plan(const bla_params* p, DecayPlan* dp)
     dp->total = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
 }
 
+// Backward: the one-unit tables (conj_tab = 0, score scale folded into A | B), then the
+// forward and adjoint summaries of the segments.  A sequence is cut into segments until the
+// main pass has a workgroup per compute unit (the summaries cost one extra pass over every
+// segment but the first, so no more are taken).
+struct BwdPlan {
+    Plan pl;
+    int nseg, cps;
+    size_t off_fsum, off_asum, total;
+};
+
+bla_status check_backward_shape(const bla_params* p)
+{
+    bla_status st = check_shape(p, true);
+    if (st != BLA_OK) return st;
+    if (p->L < 0) return BLA_ERR_INVALID_ARG;
+    if (p->phase_anchor != 0) return BLA_ERR_UNSUPPORTED;
+    if (!backward_supported(p->io_dtype == BLA_BF16, p->d_k, pad_modes(p->M), pad_slots(p->S)))
+        return BLA_ERR_UNSUPPORTED;
+    return BLA_OK;
+}
+
+void make_bwd_plan(const bla_params* p, BwdPlan* bp)
+{
+    make_plan(p, false, &bp->pl);
+    Plan& pl = bp->pl;
+    pl.pair = 0;
+    pl.upw = 1;
+    const long long units = (long long)p->B * p->H;
+    int nseg = 1;
+    if (units > 0 && pl.nch > 1) {
+        const long long cus = device_cu_count();
+        if (units < cus) {
+            long long want = cus / units;
+            if (want > pl.nch) want = pl.nch;
+            nseg = want < 1 ? 1 : (int)want;
+        }
+    }
+    int cps = pl.nch > 0 ? (pl.nch + nseg - 1) / nseg : 1;
+    nseg = pl.nch > 0 ? (pl.nch + cps - 1) / cps : 1;
+    bp->nseg = nseg;
+    bp->cps = cps;
+    const size_t unit_bytes = (size_t)4 * pl.MP * pl.D * sizeof(float);
+    bp->off_fsum = pl.off_summ;
+    bp->off_asum = align_up(bp->off_fsum + (size_t)units * nseg * unit_bytes);
+    bp->total = align_up(bp->off_asum + (size_t)units * nseg * unit_bytes);
+}
+
 }  // namespace
 
 extern "C" {
@@ -544,6 +591,115 @@ bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, c
     a.scale = pl.scale;
     if (launch_decay_step(pl.bf16, pl.D, pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;
     return BLA_OK;
+}
+
+size_t bla_backward_workspace_size(const bla_params* p)
+{
+    if (check_backward_shape(p) != BLA_OK) return 0;
+    BwdPlan bp;
+    make_bwd_plan(p, &bp);
+    return bp.total;
+}
+
+static bla_status backward_impl(const bla_params* p, const double* T, const void* q, const void* k,
+                                const void* v, const void* dO, const float* state_k_in,
+                                const float* state_v_in, const float* dstate_k_out,
+                                const float* dstate_v_out, void* dq, void* dk, void* dv,
+                                float* dstate_k_in, float* dstate_v_in, void* workspace,
+                                size_t workspace_bytes, void* stream, void* const* events)
+{
+    bla_status st = check_backward_shape(p);
+    if (st != BLA_OK) return st;
+    if ((st = check_periods(p, T)) != BLA_OK) return st;
+    const long long units = (long long)p->B * p->H;
+    if (units == 0) return BLA_OK;
+    if (p->L > 0) {
+        const void* t[7] = {q, k, v, dO, dq, dk, dv};
+        for (int i = 0; i < 7; ++i)
+            if (!t[i] || !aligned16(t[i])) return BLA_ERR_INVALID_ARG;
+    }
+    const float* sptr[6] = {state_k_in, state_v_in, dstate_k_out, dstate_v_out, dstate_k_in, dstate_v_in};
+    for (int i = 0; i < 6; ++i)
+        if (sptr[i] && !aligned16(sptr[i])) return BLA_ERR_INVALID_ARG;
+    if ((dstate_k_in && (dstate_k_in == dstate_k_out || dstate_k_in == state_k_in)) ||
+        (dstate_v_in && (dstate_v_in == dstate_v_out || dstate_v_in == state_v_in)))
+        return BLA_ERR_INVALID_ARG;
+    BwdPlan bp;
+    make_bwd_plan(p, &bp);
+    if (!workspace || workspace_bytes < bp.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    char* ws = (char*)workspace;
+    const Plan& pl = bp.pl;
+    const size_t n_state = (size_t)units * 2 * p->M * p->d_k;
+    if (p->L == 0) {
+        // no tokens: the input states are the final states
+        if (launch_state_copy(dstate_k_out, dstate_k_in, n_state, s) != hipSuccess) return BLA_ERR_HIP;
+        if (launch_state_copy(dstate_v_out, dstate_v_in, n_state, s) != hipSuccess) return BLA_ERR_HIP;
+        return BLA_OK;
+    }
+    auto mark = [&](int i) -> bool {
+        return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
+    };
+    if (!mark(0)) return BLA_ERR_HIP;
+    if ((st = build_tables(pl, T, ws, s, false)) != BLA_OK) return st;
+    if (!mark(1)) return BLA_ERR_HIP;
+    BwdArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.dO = dO;
+    a.sk_in = state_k_in;
+    a.sv_in = state_v_in;
+    a.gk_out = dstate_k_out;
+    a.gv_out = dstate_v_out;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.gk_in = dstate_k_in;
+    a.gv_in = dstate_v_in;
+    a.E32 = (const float*)(ws + pl.off_E32);
+    a.EbarT = ws + pl.off_EbarT;
+    a.ErevT = ws + pl.off_ErevT;
+    a.Etab = ws + pl.off_Etab;
+    a.ABs = ws + pl.off_ABs;
+    a.ABm = ws + pl.off_ABm;
+    a.theta = (const int*)(ws + pl.off_theta);
+    a.rperiod = (const double*)(ws + pl.off_rperiod);
+    a.fsum = (float*)(ws + bp.off_fsum);
+    a.asum = (float*)(ws + bp.off_asum);
+    a.B = p->B;
+    a.H = p->H;
+    a.L = p->L;
+    a.M = p->M;
+    a.nch = pl.nch;
+    a.nseg = bp.nseg;
+    a.cps = bp.cps;
+    a.t0 = p->t0;
+    a.scale = pl.scale;
+    void* ev3[3] = {events ? events[2] : nullptr, events ? events[3] : nullptr, events ? events[4] : nullptr};
+    if (launch_backward(pl.bf16, pl.D, pl.MP, pl.SP, a, s, ev3) != hipSuccess) return BLA_ERR_HIP;
+    return BLA_OK;
+}
+
+bla_status bla_backward(const bla_params* p, const double* T, const void* q, const void* k, const void* v,
+                        const void* dO, const float* state_k_in, const float* state_v_in,
+                        const float* dstate_k_out, const float* dstate_v_out, void* dq, void* dk, void* dv,
+                        float* dstate_k_in, float* dstate_v_in, void* workspace, size_t workspace_bytes,
+                        void* stream)
+{
+    return backward_impl(p, T, q, k, v, dO, state_k_in, state_v_in, dstate_k_out, dstate_v_out, dq, dk, dv,
+                         dstate_k_in, dstate_v_in, workspace, workspace_bytes, stream, nullptr);
+}
+
+bla_status bla_backward_timed(const bla_params* p, const double* T, const void* q, const void* k,
+                              const void* v, const void* dO, const float* state_k_in, const float* state_v_in,
+                              const float* dstate_k_out, const float* dstate_v_out, void* dq, void* dk,
+                              void* dv, float* dstate_k_in, float* dstate_v_in, void* workspace,
+                              size_t workspace_bytes, void* stream, void* const* events)
+{
+    return backward_impl(p, T, q, k, v, dO, state_k_in, state_v_in, dstate_k_out, dstate_v_out, dq, dk, dv,
+                         dstate_k_in, dstate_v_in, workspace, workspace_bytes, stream, events);
 }
 
 }  // extern "C"

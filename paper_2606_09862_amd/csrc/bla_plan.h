@@ -144,6 +144,61 @@ struct DecayStepArgs {
     float scale;
 };
 
+// Backward of the chunked operator (gradients of Alg. 2).  Every [B,H,L,d] tensor in the
+// io dtype; states and state gradients float32 [B,H,2,M,d].
+struct BwdArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const void* dO;
+    const float* sk_in;    // forward's input states (nullable: zero)
+    const float* sv_in;
+    const float* gk_out;   // dLoss / d(final states) (nullable: zero)
+    const float* gv_out;
+    void* dq;
+    void* dk;
+    void* dv;
+    float* gk_in;          // dLoss / d(input states) (nullable: not wanted)
+    float* gv_in;
+    const float* E32;      // [H][C+1][2MP]
+    const void* EbarT;     // [H][2MP][C]  conj(rho^i)
+    const void* ErevT;     // [H][2MP][C]  rho^{C-i}
+    const void* Etab;      // [H][C][2MP]  rho^i
+    const void* ABs;       // [SP][2MP]    scale * (A | B)
+    const void* ABm;       // [2MP][SP]    (A | B) transposed
+    const int* theta;      // [H][SP]
+    const double* rperiod; // [H] 1 / T
+    float* fsum;           // [B*H][nseg][2][2][MP][D] forward summaries of the segments
+    float* asum;           // [B*H][nseg][2][2][MP][D] adjoint summaries (segment 0 unused)
+    int B, H, L, M;
+    int nch, nseg, cps;    // chunks per sequence, segments, chunks per segment
+    long long t0;
+    float scale;
+};
+
+// LDS bytes of the backward kernel for an element size (2: bf16, 4: float32): token tiles
+// row-major and transposed, Gram / H tiles, readout weights, state operands, thresholds.
+constexpr size_t bwd_lds_bytes(int esz, int D, int MP, int SP)
+{
+    const size_t C = kChunk, PAD = 4, LDQ = D + PAD, LDK = C + PAD, LDU = 2 * (size_t)MP + PAD;
+    const size_t A = 4 * C * LDQ, Tt = 4 * (size_t)D * LDK, G = 2 * C * LDK;
+    const size_t Bw = 4 * (size_t)MP * LDK > 2 * C * LDU ? 4 * (size_t)MP * LDK : 2 * C * LDU;
+    const size_t Z = 2 * (size_t)D * LDU;
+    return (A + Tt + G + Bw + Z) * (size_t)esz + (size_t)SP * 4;
+}
+constexpr size_t kBwdMaxLds = 160 * 1024;
+
+// Whether a backward kernel exists for (bf16, D, MP, SP): bf16 with D in {32, 64},
+// float32 with D = 32; MP <= 64, SP <= max(32, 2 MP) <= 128, within the LDS of a workgroup.
+inline bool backward_supported(int bf16, int D, int MP, int SP)
+{
+    if (bf16 ? (D != 32 && D != 64) : D != 32) return false;
+    if (MP != 16 && MP != 32 && MP != 64) return false;
+    if (SP != 32 && SP != 64 && SP != 128) return false;
+    if (SP > (2 * MP > 32 ? 2 * MP : 32)) return false;
+    return bwd_lds_bytes(bf16 ? 2 : 4, D, MP, SP) <= kBwdMaxLds;
+}
+
 // Launchers (defined in the .hip translation units).  They return a HIP error.
 hipError_t launch_tables(const TableArgs& a, int bf16, hipStream_t s);
 hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s);
@@ -154,6 +209,11 @@ hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
 hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s,
                                 void* const* events);
 hipError_t launch_decay_step(int bf16_io, int D, int SP, const DecayStepArgs& a, hipStream_t s);
+
+// Backward passes: forward summaries of every segment, adjoint summaries (segments 1..),
+// and the reverse walk.  events[0..2] (nullable) are recorded after each pass.
+hipError_t launch_backward(int bf16, int D, int MP, int SP, const BwdArgs& a, hipStream_t s,
+                           void* const* events);
 
 // Whether a forward kernel exists for (bf16, D, MP, SP).
 bool forward_supported(int bf16, int D, int MP, int SP);
