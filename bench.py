@@ -16,7 +16,9 @@ The anchored-slot form (Sec. 3.3, Alg. 1/3; phase_anchor = 1) and the state-deca
 (Sec. 3.4, bla_decay_forward) are measured the same way on the same workload and reported
 under "anchored" and "decay", each with its own oracle timed on the host.  --form
 anchored / --form decay makes that form the only forward that runs (for profiling it
-alone).
+alone).  The backward pass (bla_backward: dq, dk, dv from dO on the same workload) is
+measured under "backward" with the matrix-core roofline of its reverse-walk kernel and the
+oracle's backward timed on a sample of the sequences; --form backward runs only it.
 """
 from __future__ import annotations
 
@@ -51,6 +53,15 @@ def decay_flops_per_token_head(d, S, sub=16):
     return 8 * S * d + (sub + 1) * (2 * S + 2 * d)
 
 
+def backward_flops_per_token_head(C, d, M, S):
+    """Algorithmic flops of the backward's reverse walk per (token, head), causal halves of the
+    C x C terms with the diagonal: the Gram tiles Q K^T, dO V^T and the tril(H) products for dq,
+    dk, dv (5(C+1)d); G conj(E), Gd conj(E), H_q, H_v (8(C+1)M); scores, dP, W'' and Wq''
+    (16MS); Q Z'_k^T, dO Z'_v^T, Re(Wq'' Z'_k), the two adjoint terms of dk and dv, the state
+    rebuilt by subtraction and the adjoint update (36Md)."""
+    return 5 * (C + 1) * d + 8 * (C + 1) * M + 16 * M * S + 36 * M * d
+
+
 def forward_bytes(B, H, L, d, M, io_bytes):
     """q, k, v read + o written (io dtype) + final fp32 states written."""
     return B * H * L * d * io_bytes * 4 + B * H * 2 * (2 * M * d * 4)
@@ -60,6 +71,7 @@ KERNEL_SOURCES = {
     "rotating": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"),
     "anchored": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"),
     "decay": ("bla_device.h", "bla_plan.h", "bla_decay.hip"),
+    "backward": ("bla_device.h", "bla_forward.h", "bla_plan.h", "bla_backward.h"),
 }
 
 
@@ -209,6 +221,101 @@ def bench_forward(args, hip, inputs, form):
     return w, T, ms, tokens / (ms * 1e-3), roofline, extra
 
 
+def bench_backward(args, hip, inputs):
+    """bla_backward on the LM-layer workload: dq, dk, dv and the input-state gradients from
+    q, k, v and dO (all resident in HBM).  One step = one bla_backward call (tables, forward
+    summaries, adjoint summaries, reverse walk)."""
+    import numpy as np
+    import torch
+
+    import bla_inputs as bi
+    import paper_2606_09862_amd as bla
+
+    w = bi.WORKLOADS[3]
+    T = bi.periods(w.M, w.H)
+    dev = torch.device("cuda:0")
+    q, k, v = inputs
+    g = bi.generate_grad(3)
+    tq, tk, tv, tg = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v, g))
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16)
+    ws = torch.empty(bla.backward_workspace_size(p), dtype=torch.uint8, device=dev)
+    dq, dk, dv = torch.empty_like(tq), torch.empty_like(tk), torch.empty_like(tv)
+    gsk = torch.empty((w.B, w.H, 2, w.M, w.d), dtype=torch.float32, device=dev)
+    gsv = torch.empty_like(gsk)
+    sptr = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    Tarr = (ctypes.c_double * w.H)(*T)
+    ptrs = [ctypes.c_void_p(t.data_ptr()) if t is not None else None
+            for t in (tq, tk, tv, tg, None, None, None, None, dq, dk, dv, gsk, gsv, ws)]
+    fn = bla.lib().bla_backward_timed
+
+    def call(evs):
+        arr = None if evs is None else (ctypes.c_void_p * 5)(*[e.value for e in evs])
+        st = fn(ctypes.byref(p), Tarr, *ptrs, ws.numel(), sptr, arr)
+        if st != 0:
+            raise RuntimeError(f"bla_backward failed: {bla.STATUS.get(st, st)}")
+
+    for _ in range(args.warmup):
+        call(None)
+    t0, t1 = hip.event(), hip.event()
+    torch.cuda.synchronize(dev)
+    hip.record(t0, sptr)
+    for _ in range(args.steps):
+        call(None)
+    hip.record(t1, sptr)
+    torch.cuda.synchronize(dev)
+    ms = hip.elapsed_ms(t0, t1) / args.steps
+    evs = [[hip.event() for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    for i in range(args.steps):
+        call(evs[i])
+    torch.cuda.synchronize(dev)
+    phases = ["tables", "forward_summaries", "adjoint_summaries", "reverse_walk"]
+    phase_ms = {ph: float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs])) for j, ph in enumerate(phases)}
+    flops = backward_flops_per_token_head(w.chunk, w.d, w.M, w.S) * w.B * w.H * w.L
+    nbytes = w.B * w.H * w.L * w.d * 2 * 7 + w.B * w.H * 2 * (2 * w.M * w.d * 4)
+    t_walk = phase_ms["reverse_walk"] * 1e-3
+    tflops = flops / t_walk / 1e12
+    digest = kernel_sources_digest("backward")
+    traffic = read_traffic(os.path.join(ROOT, "profiles", "bwd_kernel_lm_layer_traffic.txt"), digest)
+    roofline = {"bound": "mfma", "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": traffic}
+    t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
+    detail = {
+        "kernel": "bwd_kernel<bf16,64,64,64,false>",
+        "algorithmic_flops_per_launch": flops,
+        "algorithmic_bytes_per_launch": nbytes,
+        "reverse_walk_us": round(phase_ms["reverse_walk"] * 1e3, 2),
+        "reverse_walk_hbm_gbs": round(nbytes / t_walk / 1e9, 1),
+        "phase_us": {k2: round(v2 * 1e3, 2) for k2, v2 in phase_ms.items()},
+        "operator_roofline_frac": round(t_ideal / (ms * 1e-3), 4),
+        "kernel_sources_sha": digest,
+    }
+    del tq, tk, tv, tg, dq, dk, dv, gsk, gsv, ws
+    return ms, w.B * w.L / (ms * 1e-3), roofline, detail, g
+
+
+def cpu_baseline_backward(w, T, inputs, g, nseq=16):
+    """The oracle's backward (token by token, per-token states kept) on a bounded sample: the
+    first nseq of the workload's sequences, one per host thread."""
+    import numpy as np
+
+    import oracle
+
+    q, k, v = inputs
+    H = w.H
+    rows = [(i // H, i % H) for i in range(nseq)]
+    pick = lambda x: np.stack([x[b, h] for b, h in rows])[None]
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    threads = max(1, min(threads, nseq))
+    t = time.perf_counter()
+    oracle.backward(pick(q), pick(k), pick(v), pick(g), [T[h] for _, h in rows], w.M, w.S, nthreads=threads)
+    dt = time.perf_counter() - t
+    return {"value": round(nseq * w.L / H / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nseq} of the LM-layer workload's {w.B * w.H} sequences (L={w.L}), float64 reverse pass "
+                      f"through Alg. 2, one sequence per thread; {dt:.2f} s wall; tokens/s counts a token with "
+                      f"all {H} heads, as the GPU figure does"}
+
+
 def bench_decode(args, hip):
     import torch
 
@@ -300,8 +407,10 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-anchored", action="store_true", help="skip the anchored-slot measurement")
     ap.add_argument("--no-decay", action="store_true", help="skip the state-decay measurement")
-    ap.add_argument("--form", choices=("rotating", "anchored", "decay"), default="rotating",
-                    help="the form of the headline forward; otherwise no other forward runs")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
+    ap.add_argument("--form", choices=("rotating", "anchored", "decay", "backward"), default="rotating",
+                    help="the form of the headline forward; otherwise no other forward runs "
+                         "(backward: only the backward pass runs, for profiling it alone)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="first run one plain device copy of this many bytes (reference kernel for "
                          "scaling the HBM byte counters of a rocprofv3 --pmc run)")
@@ -324,6 +433,12 @@ def main():
         del src, dst
     import bla_inputs as bi
     inputs = bi.generate(3)
+    if args.form == "backward":
+        b_ms, b_value, b_roof, b_detail, _ = bench_backward(args, hip, inputs)
+        print(json.dumps({"metric": "BLA backward tokens/sec at L=4096 (1 MI355X)", "value": round(b_value, 1),
+                          "unit": "tokens/s", "ms_per_step": round(b_ms, 5), "roofline": b_roof,
+                          "detail": b_detail}), flush=True)
+        return
     head = args.form
     w, T, ms, value, roofline, extra = bench_forward(args, hip, inputs, head)
     baselines = {"rotating": cpu_baseline, "anchored": cpu_baseline_anchored, "decay": cpu_baseline_decay}
@@ -338,6 +453,15 @@ def main():
         others[form] = {"form": titles[form], "value": round(f_value, 1), "unit": "tokens/s",
                         "ms_per_step": round(f_ms, 5), "roofline": f_roof, "forward_detail": f_extra,
                         "cpu_baseline": None if args.no_cpu_baseline else baselines[form](w, T, inputs)}
+    backward = None
+    if head == "rotating" and not args.no_backward:
+        b_ms, b_value, b_roof, b_detail, g = bench_backward(args, hip, inputs)
+        w3 = bi.WORKLOADS[3]
+        backward = {"form": "gradients of the rotating form (Alg. 2): dq, dk, dv and the input-state gradients",
+                    "value": round(b_value, 1), "unit": "tokens/s", "ms_per_step": round(b_ms, 5),
+                    "roofline": b_roof, "detail": b_detail,
+                    "cpu_baseline": None if args.no_cpu_baseline else
+                    cpu_baseline_backward(w3, bi.periods(w3.M, w3.H), inputs, g)}
     decode = None if args.no_decode or head != "rotating" else bench_decode(args, hip)
     cpu = None if args.no_cpu_baseline else baselines[head](w, T, inputs)
     line = {
@@ -348,7 +472,7 @@ def main():
                    "chunk": w.chunk, "periods": "T_h=(1+h%2)(2M-1)", "state": "fp32",
                    "form": head},
         "roofline": roofline, "cpu_baseline": cpu, "forward_detail": extra, "decode_step": decode,
-        "anchored": others["anchored"], "decay": others["decay"],
+        "anchored": others["anchored"], "decay": others["decay"], "backward": backward,
     }
     print(json.dumps(line), flush=True)
 

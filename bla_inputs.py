@@ -143,6 +143,22 @@ def generate(cid: int, rows=None, L=None, B=None, H=None, d=None):
     return q, k, v
 
 
+def generate_grad(cid: int, rows=None, L=None, B=None, H=None, d=None):
+    """dLoss/dO for the backward pass: [len(rows), H, L, d] float32 holding io-dtype values,
+    N(0, 1)/sqrt(d) from the stream of tensor 3 of each batch row (an upstream gradient of the
+    same scale as the inputs; the loss itself is not modelled)."""
+    w = WORKLOADS[cid]
+    Bn = w.B if B is None else B
+    Hn = w.H if H is None else H
+    Ln = w.L if L is None else L
+    dn = w.d if d is None else d
+    rows = list(range(Bn)) if rows is None else list(rows)
+    g = np.empty((len(rows), Hn, Ln, dn), np.float32)
+    for i, b in enumerate(rows):
+        g[i] = _cast(_rng(cid, 3, b).standard_normal((Hn, Ln, dn)) / math.sqrt(dn), w.dtype)
+    return g
+
+
 def generate_decode_device(device, B=None, L=None, seed: int = 5):
     """Decode workload on a torch device: LM-layer style q,k,v [B,H,L,d] in bf16.
 

@@ -229,3 +229,38 @@ def test_interp_tables_errors(lib):
     for args in [(0, 4, 7.0), (4, 0, 7.0), (4, 4, 0.0), (4, 4, float("nan")), (4, 4, float("inf"))]:
         assert f(*args, A.ctypes.data_as(dp), A.ctypes.data_as(dp), th.ctypes.data_as(ip)) == INVALID
     assert f(4, 4, 7.0, None, A.ctypes.data_as(dp), th.ctypes.data_as(ip)) == INVALID
+
+
+def test_backward_errors(lib):
+    """Argument and shape checks of bla_backward run before any launch (no GPU needed)."""
+    p = P(L=10)
+    H = 2
+    arr = (ctypes.c_double * H)(31.0, 62.0)
+    assert bla.backward_workspace_size(p) > 0
+    # q, k, v, dO, state_k_in, state_v_in, dstate_k_out, dstate_v_out, dq, dk, dv, dstate_k_in, dstate_v_in
+    args = [_fake(0x10000), _fake(0x20000), _fake(0x30000), _fake(0x40000), None, None, None, None,
+            _fake(0x50000), _fake(0x60000), _fake(0x70000), None, None]
+    call = lambda a, nbytes=1 << 40, params=p, T=arr: lib.bla_backward(
+        ctypes.byref(params), T, *a, _fake(0x100000), nbytes, None)
+    assert call(args, nbytes=16) == WORKSPACE
+    for i in (0, 3, 8, 10):              # q, dO, dq, dv missing
+        bad = list(args)
+        bad[i] = None
+        assert call(bad) == INVALID
+    bad = list(args)
+    bad[9] = _fake(0x60008)              # dk not 16-byte aligned
+    assert call(bad) == INVALID
+    bad = list(args)
+    bad[6] = bad[11] = _fake(0x80000)    # dstate_k_in aliasing dstate_k_out
+    assert call(bad) == INVALID
+    nan = (ctypes.c_double * H)(math.nan, 1.0)
+    assert call(args, T=nan) == INVALID
+    # outside the backward's shapes: d = 128, M > 64, the anchored form
+    assert bla.backward_workspace_size(P(d=128)) == 0
+    assert bla.backward_workspace_size(P(M=100, S=100)) == 0
+    pa = P(L=10)
+    pa.phase_anchor = 1
+    assert bla.backward_workspace_size(pa) == 0
+    assert call(args, params=pa) == UNSUPPORTED
+    assert bla.backward_workspace_size(P(dtype="f32", d=32, M=32, S=64)) > 0
+    assert bla.backward_workspace_size(P(dtype="f32", d=64)) == 0

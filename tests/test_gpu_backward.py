@@ -141,8 +141,6 @@ def test_backward_workload3_sampled_rows():
     w = bi.WORKLOADS[3]
     T = bi.periods(w.M, w.H)
     q, k, v = bi.generate(3)
-    rng = np.random.default_rng(3)
-    g = bi.round_bf16((rng.standard_normal(q.shape) / math.sqrt(w.d)).astype(np.float32))
-    q, k, v = (bi.round_bf16(x) for x in (q, k, v))
+    g = bi.generate_grad(3)
     rows = [(0, 0), (3, 5), (7, 14), (7, 15)]
     run_bwd(q, k, v, g, T, w.M, w.S, torch.bfloat16, label="workload 3", rows=rows)
