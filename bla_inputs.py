@@ -159,6 +159,24 @@ def generate_grad(cid: int, rows=None, L=None, B=None, H=None, d=None):
     return g
 
 
+def generate_layer(cid: int, rows=None, L=None, B=None, H=None, d=None):
+    """Hidden states and projections of a whole layer: x [len(rows), L, D] ~ N(0, 1) and
+    W_qkv [D, 3D], W_o [D, D] ~ N(0, 1/D) (D = H d), float32 arrays holding bf16 values."""
+    w = WORKLOADS[cid]
+    Bn = w.B if B is None else B
+    Hn = w.H if H is None else H
+    Ln = w.L if L is None else L
+    dn = w.d if d is None else d
+    D = Hn * dn
+    rows = list(range(Bn)) if rows is None else list(rows)
+    x = np.empty((len(rows), Ln, D), np.float32)
+    for i, b in enumerate(rows):
+        x[i] = _cast(_rng(cid, 30, b).standard_normal((Ln, D)), "bf16")
+    w_qkv = _cast(_rng(cid, 31).standard_normal((D, 3 * D)) / math.sqrt(D), "bf16")
+    w_o = _cast(_rng(cid, 32).standard_normal((D, D)) / math.sqrt(D), "bf16")
+    return x, w_qkv, w_o
+
+
 def generate_decode_device(device, B=None, L=None, seed: int = 5):
     """Decode workload on a torch device: LM-layer style q,k,v [B,H,L,d] in bf16.
 

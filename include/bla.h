@@ -235,6 +235,37 @@ bla_status bla_backward_timed(const bla_params* p, const double* T, const void* 
                               void* dv, float* dstate_k_in, float* dstate_v_in, void* workspace,
                               size_t workspace_bytes, void* stream, void* const* events);
 
+/*
+ * A whole BLA layer on hidden states (bfloat16 only).  The queries, keys and values are
+ * linear projections of the hidden states (the attention layer of Sec. 2.1 whose softmax BLA
+ * replaces), the H heads run the operator (bla_forward, either form by p->phase_anchor), and
+ * an output projection mixes the heads back into the model width D = H * d_k:
+ *     [q | k | v] = x W_qkv,   o = BLA(q, k, v),   y = o W_o
+ * with x, y [B, L, D] row-major, W_qkv [D, 3D] (columns h d_k .. h d_k + d_k - 1 of block 0,
+ * 1, 2 are head h's query, key and value projections), W_o [D, D] (row h d_k + e takes element
+ * e of head h's output), all bf16; the products accumulate in float32 (hipBLASLt) and q, k, v
+ * and o are rounded to bf16 between the steps.  p describes the operator (p->d_k = p->d_v is
+ * the head width, p->L the tokens); states as for bla_forward.  The workspace holds the
+ * projected tensors, the operator's workspace and 32 MB of GEMM scratch.  The first call on
+ * a device creates a hipBLASLt handle that lives until the process ends.  Errors as for
+ * bla_forward; a failing GEMM is BLA_ERR_HIP.
+ */
+size_t bla_layer_workspace_size(const bla_params* p);
+bla_status bla_layer_forward(const bla_params* p, const double* T, const void* x, const void* w_qkv,
+                             const void* w_o, const float* state_k_in, const float* state_v_in, void* y,
+                             float* state_k_out, float* state_v_out, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
+ * bla_layer_forward with phase timing: events[0..5] (hipEvent_t or NULL) are recorded before
+ * the QKV projection, after it, after the head split, after the operator, after the head merge
+ * and after the output projection.
+ */
+bla_status bla_layer_forward_timed(const bla_params* p, const double* T, const void* x, const void* w_qkv,
+                                   const void* w_o, const float* state_k_in, const float* state_v_in, void* y,
+                                   float* state_k_out, float* state_v_out, void* workspace,
+                                   size_t workspace_bytes, void* stream, void* const* events);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,7 +14,9 @@ anchored at phase 0, slot states accumulated as a cumulative sum) token by token
 ``forward_decay`` the same with the state decay of Sec. 3.4 (previous slot state
 multiplied by 1 - D before each write).  ``backward`` differentiates Alg. 2: the chain
 rule taken through the token loop in reverse, with the forward states of every token
-stored by a forward pass.
+stored by a forward pass.  ``layer_forward`` puts the operator between the projections of
+an attention layer (queries, keys and values projected from the hidden states, an output
+projection after the heads), with numpy's float64 matrix products for the projections.
 
 Parity status of each function (what pins it) is listed in the tests
 (``tests/test_oracle_pins.py``); every function here is pinned.
@@ -206,3 +208,22 @@ def backward(q, k, v, dO, T, M: int, S: int, t0: int = 0, scale=None, state_k=No
     if rc != 0:
         raise ValueError("bla_oracle_backward rejected its arguments")
     return dq, dkk, dvv, gsk, gsv
+
+
+def layer_forward(x, w_qkv, w_o, T, H: int, M: int, S: int, t0: int = 0, scale=None, state_k=None,
+                  state_v=None, nthreads: int = 0):
+    """A BLA layer on hidden states x [B, L, D] (D = H d): [q | k | v] = x W_qkv (W_qkv [D, 3D],
+    head h's columns h d .. h d + d - 1 of each block), the operator (``forward``) per head,
+    y = concat_h(o_h) W_o (W_o [D, D]).  Everything in float64.
+
+    Returns (y [B, L, D], state_k, state_v) as ``forward`` does.
+    """
+    x = _f64(x)
+    Bn, L, D = x.shape
+    d = D // H
+    qkv = x @ _f64(w_qkv)                                     # [B, L, 3D]
+    heads = qkv.reshape(Bn, L, 3, H, d).transpose(2, 0, 3, 1, 4)  # [3, B, H, L, d]
+    o, sk, sv = forward(heads[0], heads[1], heads[2], T, M, S, t0=t0, scale=scale, state_k=state_k,
+                        state_v=state_v, nthreads=nthreads)
+    y = o.transpose(0, 2, 1, 3).reshape(Bn, L, D) @ _f64(w_o)
+    return y, sk, sv

@@ -78,6 +78,13 @@ def lib():
         L.bla_backward_timed.argtypes = [P, _dp] + [_vp] * 14 + [ctypes.c_size_t, _vp,
                                                                   ctypes.POINTER(ctypes.c_void_p)]
         L.bla_backward_timed.restype = ctypes.c_int
+        L.bla_layer_workspace_size.argtypes = [P]
+        L.bla_layer_workspace_size.restype = ctypes.c_size_t
+        L.bla_layer_forward.argtypes = [P, _dp] + [_vp] * 9 + [ctypes.c_size_t, _vp]
+        L.bla_layer_forward.restype = ctypes.c_int
+        L.bla_layer_forward_timed.argtypes = [P, _dp] + [_vp] * 9 + [ctypes.c_size_t, _vp,
+                                                                       ctypes.POINTER(ctypes.c_void_p)]
+        L.bla_layer_forward_timed.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -300,3 +307,41 @@ def backward(q, k, v, dO, T, M: int, S: int, t0: int = 0, scale: float | None = 
     if st != 0:
         raise BlaError(st, "bla_backward")
     return dq, dk, dv, gsk, gsv
+
+
+def layer_workspace_size(p: Params) -> int:
+    return lib().bla_layer_workspace_size(ctypes.byref(p))
+
+
+def layer_forward(x, w_qkv, w_o, T, H: int, M: int, S: int, t0: int = 0, scale: float | None = None,
+                  state_k=None, state_v=None, want_state: bool = True, workspace=None, out=None,
+                  phase_anchor: bool = False):
+    """bla_layer_forward: y = BLA(x W_qkv) W_o on hidden states x [B, L, D] (bf16, D = H d);
+    w_qkv [D, 3D] and w_o [D, D] bf16.  Returns (y [B, L, D], state_k_out, state_v_out)."""
+    B, L, D = x.shape
+    d = D // H
+    dt = x.dtype
+    if dt != torch.bfloat16 or d * H != D:
+        raise ValueError("layer_forward: bf16 hidden states with D = H * d")
+    _check(x, (B, L, D), dt, "x")
+    _check(w_qkv, (D, 3 * D), dt, "w_qkv")
+    _check(w_o, (D, D), dt, "w_o")
+    for name, t in (("state_k", state_k), ("state_v", state_v)):
+        if t is not None:
+            _check(t, (B, H, 2, M, d), torch.float32, name)
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale, phase_anchor=phase_anchor)
+    dev = x.device
+    y = torch.empty_like(x) if out is None else out
+    sk = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
+    sv = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
+    need = layer_workspace_size(p)
+    if need == 0:
+        raise BlaError(supported(p) or 2, "bla_layer_forward (shape check)")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    st = lib().bla_layer_forward(ctypes.byref(p), _periods(T, H), _ptr(x), _ptr(w_qkv), _ptr(w_o), _ptr(state_k),
+                                 _ptr(state_v), _ptr(y), _ptr(sk), _ptr(sv), _ptr(workspace), workspace.numel(),
+                                 _stream(dev))
+    if st != 0:
+        raise BlaError(st, "bla_layer_forward")
+    return y, sk, sv

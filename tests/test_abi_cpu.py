@@ -264,3 +264,36 @@ def test_backward_errors(lib):
     assert call(args, params=pa) == UNSUPPORTED
     assert bla.backward_workspace_size(P(dtype="f32", d=32, M=32, S=64)) > 0
     assert bla.backward_workspace_size(P(dtype="f32", d=64)) == 0
+
+
+def test_layer_errors(lib):
+    """Shape and argument checks of bla_layer_forward before any launch (no GPU needed)."""
+    p = P(L=10, d=64, H=2)
+    arr = (ctypes.c_double * 2)(31.0, 62.0)
+    assert bla.layer_workspace_size(p) > 0
+    assert bla.layer_workspace_size(P(dtype="f32")) == 0          # the layer is bf16 only
+    args = [_fake(0x10000), _fake(0x20000), _fake(0x30000), None, None, _fake(0x40000), None, None]
+    call = lambda a, nbytes=1 << 40: lib.bla_layer_forward(ctypes.byref(p), arr, *a, _fake(0x100000), nbytes, None)
+    assert call(args, nbytes=16) == WORKSPACE
+    for i in (0, 1, 2, 5):                                      # x, W_qkv, W_o, y missing
+        bad = list(args)
+        bad[i] = None
+        assert call(bad) == INVALID
+    bad = list(args)
+    bad[1] = _fake(0x20008)                                      # misaligned W_qkv
+    assert call(bad) == INVALID
+
+
+def test_binding_argument_counts_match_the_header(lib):
+    """Every entry point the binding declares argument types for takes as many arguments as
+    its C declaration in include/bla.h."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    seen = 0
+    for m in re.finditer(r"\b(bla_[a-z_]+)\s*\(([^;{]*?)\)\s*;", text):
+        name, params = m.group(1), m.group(2).strip()
+        n = 0 if params in ("", "void") else params.count(",") + 1
+        at = getattr(getattr(lib, name), "argtypes", None)
+        if at is not None:
+            seen += 1
+            assert len(at) == n, f"{name}: binding has {len(at)} argument types, the header {n} parameters"
+    assert seen >= 10

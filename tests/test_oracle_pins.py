@@ -692,3 +692,39 @@ def test_p13_backward_split_call(L1):
     assert _relerr(np.concatenate([dq1, dq2], 2), dq) < 1e-13
     assert _relerr(np.concatenate([dk1, dk2], 2), dk) < 1e-13
     assert _relerr(np.concatenate([dv1, dv2], 2), dv) < 1e-13
+
+
+# ---------------------------------------------------------------- P14: the layer around the operator
+def test_p14_layer_with_identity_projections_is_the_operator():
+    """One head, W_qkv = [I | I | I] and W_o = I: the layer is the operator applied to x
+    itself as queries, keys and values."""
+    rng = np.random.default_rng(60)
+    B, L, D, M, S = 2, 37, 6, 4, 7
+    x = rng.standard_normal((B, L, D))
+    eye = np.eye(D)
+    y, sk, _ = oracle.layer_forward(x, np.concatenate([eye, eye, eye], 1), eye, [9.5], 1, M, S)
+    xh = x[:, None]
+    o, rk, _ = oracle.forward(xh, xh, xh, [9.5], M, S)
+    assert _relerr(y, o[:, 0]) < 1e-14 and _relerr(sk, rk) < 1e-14
+
+
+@pytest.mark.parametrize("H,M", [(2, 3), (4, 2)])
+def test_p14_layer_attention_limit_is_multi_head_attention(H, M):
+    """T = S = 2M-1 and L <= 2M-1: every head is causal softmax attention (P5), so the layer is
+    multi-head attention with the same projections (torch float64: per-head
+    scaled_dot_product_attention between the projections)."""
+    rng = np.random.default_rng(61)
+    W = 2 * M - 1
+    B, L, d = 3, W, 4
+    D = H * d
+    x = rng.standard_normal((B, L, D))
+    wqkv = rng.standard_normal((D, 3 * D)) / math.sqrt(D)
+    wo = rng.standard_normal((D, D)) / math.sqrt(D)
+    y, _, _ = oracle.layer_forward(x, wqkv, wo, [float(W)] * H, H, M, W)
+    tx = torch.from_numpy(x)
+    q, k, v = (tx @ torch.from_numpy(wqkv[:, i * D:(i + 1) * D]) for i in range(3))
+    split = lambda t: t.reshape(B, L, H, d).transpose(1, 2)
+    o = torch.nn.functional.scaled_dot_product_attention(split(q), split(k), split(v), is_causal=True,
+                                                         scale=d ** -0.5)
+    ref = o.transpose(1, 2).reshape(B, L, D) @ torch.from_numpy(wo)
+    assert _relerr(y, ref.numpy()) < 1e-12
