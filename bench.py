@@ -18,7 +18,9 @@ under "anchored" and "decay", each with its own oracle timed on the host.  --for
 anchored / --form decay makes that form the only forward that runs (for profiling it
 alone).  The backward pass (bla_backward: dq, dk, dv from dO on the same workload) is
 measured under "backward" with the matrix-core roofline of its reverse-walk kernel and the
-oracle's backward timed on a sample of the sequences; --form backward runs only it.
+oracle's backward timed on a sample of the sequences; --form backward runs only it.  The
+whole layer (bla_layer_forward: projections, operator, output projection) is measured under
+"layer" at the recall workload's shape.
 """
 from __future__ import annotations
 
@@ -316,6 +318,81 @@ def cpu_baseline_backward(w, T, inputs, g, nseq=16):
                       f"all {H} heads, as the GPU figure does"}
 
 
+def bench_layer(args, hip):
+    """bla_layer_forward at the recall workload's shape (B=64, H=4, L=512, d=64, D=256, M=S=32):
+    x [B, L, D] -> y [B, L, D] through the QKV projection, the operator and the output
+    projection.  One step = one layer call."""
+    import numpy as np
+    import torch
+
+    import bla_inputs as bi
+    import paper_2606_09862_amd as bla
+
+    w = bi.WORKLOADS[2]
+    T = bi.periods(w.M, w.H)
+    D = w.H * w.d
+    dev = torch.device("cuda:0")
+    x, wqkv, wo = bi.generate_layer(2)
+    tx, tw, to = (torch.from_numpy(a).to(dev).to(torch.bfloat16) for a in (x, wqkv, wo))
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16)
+    ws = torch.empty(bla.layer_workspace_size(p), dtype=torch.uint8, device=dev)
+    y = torch.empty_like(tx)
+    sk = torch.empty((w.B, w.H, 2, w.M, w.d), dtype=torch.float32, device=dev)
+    sv = torch.empty_like(sk)
+    sptr = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    Tarr = (ctypes.c_double * w.H)(*T)
+    ptrs = [ctypes.c_void_p(t.data_ptr()) if t is not None else None for t in (tx, tw, to, None, None, y, sk, sv, ws)]
+    fn = bla.lib().bla_layer_forward_timed
+
+    def call(evs):
+        arr = None if evs is None else (ctypes.c_void_p * 6)(*[e.value for e in evs])
+        st = fn(ctypes.byref(p), Tarr, *ptrs, ws.numel(), sptr, arr)
+        if st != 0:
+            raise RuntimeError(f"bla_layer_forward failed: {bla.STATUS.get(st, st)}")
+
+    for _ in range(args.warmup):
+        call(None)
+    e0, e1 = hip.event(), hip.event()
+    torch.cuda.synchronize(dev)
+    hip.record(e0, sptr)
+    for _ in range(args.steps):
+        call(None)
+    hip.record(e1, sptr)
+    torch.cuda.synchronize(dev)
+    ms = hip.elapsed_ms(e0, e1) / args.steps
+    evs = [[hip.event() for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    for i in range(args.steps):
+        call(evs[i])
+    torch.cuda.synchronize(dev)
+    phases = ["qkv_projection", "head_split", "operator", "head_merge", "output_projection"]
+    phase_us = {ph: round(float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs])) * 1e3, 2)
+                for j, ph in enumerate(phases)}
+    tokens = w.B * w.L
+    gemm_flops = 8 * tokens * D * D
+    op_flops = forward_flops_per_token_head(w.chunk, w.d, w.M, w.S) * w.B * w.H * w.L
+    # the layer's own inputs and outputs: x, y, the weights and the final states
+    nbytes = 2 * tokens * D * 2 + 4 * D * D * 2 + w.B * w.H * 2 * (2 * w.M * w.d * 4)
+    t_ideal = max((gemm_flops + op_flops) / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
+    gemm_s = (phase_us["qkv_projection"] + phase_us["output_projection"]) * 1e-6
+    out = {"workload": f"recall shape: B={w.B} H={w.H} L={w.L} d={w.d} (D={D}) M={w.M} S={w.S}, bf16",
+           "value": round(tokens / (ms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms, 5),
+           "phase_us": phase_us, "flops_per_launch": gemm_flops + op_flops,
+           "projection_tflops": round(gemm_flops / gemm_s / 1e12, 1),
+           "layer_roofline_frac": round(t_ideal / (ms * 1e-3), 4)}
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+        t = time.perf_counter()
+        oracle.layer_forward(x, wqkv, wo, T, w.H, w.M, w.S, nthreads=threads)
+        dt = time.perf_counter() - t
+        out["cpu_baseline"] = {"value": round(tokens / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+                               "sample": f"the whole layer workload: float64 numpy projections and the "
+                                         f"token-by-token operator over {w.B * w.H} sequences; {dt:.2f} s wall"}
+    del tx, tw, to, y, sk, sv, ws
+    return out
+
+
 def bench_decode(args, hip):
     import torch
 
@@ -408,6 +485,7 @@ def main():
     ap.add_argument("--no-anchored", action="store_true", help="skip the anchored-slot measurement")
     ap.add_argument("--no-decay", action="store_true", help="skip the state-decay measurement")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
+    ap.add_argument("--no-layer", action="store_true", help="skip the whole-layer measurement")
     ap.add_argument("--form", choices=("rotating", "anchored", "decay", "backward"), default="rotating",
                     help="the form of the headline forward; otherwise no other forward runs "
                          "(backward: only the backward pass runs, for profiling it alone)")
@@ -462,6 +540,7 @@ def main():
                     "roofline": b_roof, "detail": b_detail,
                     "cpu_baseline": None if args.no_cpu_baseline else
                     cpu_baseline_backward(w3, bi.periods(w3.M, w3.H), inputs, g)}
+    layer = None if args.no_layer or head != "rotating" else bench_layer(args, hip)
     decode = None if args.no_decode or head != "rotating" else bench_decode(args, hip)
     cpu = None if args.no_cpu_baseline else baselines[head](w, T, inputs)
     line = {
@@ -472,7 +551,7 @@ def main():
                    "chunk": w.chunk, "periods": "T_h=(1+h%2)(2M-1)", "state": "fp32",
                    "form": head},
         "roofline": roofline, "cpu_baseline": cpu, "forward_detail": extra, "decode_step": decode,
-        "anchored": others["anchored"], "decay": others["decay"], "backward": backward,
+        "anchored": others["anchored"], "decay": others["decay"], "backward": backward, "layer": layer,
     }
     print(json.dumps(line), flush=True)
 
