@@ -73,7 +73,8 @@ KERNEL_SOURCES = {
     "rotating": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"),
     "anchored": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h"),
     "decay": ("bla_device.h", "bla_plan.h", "bla_decay.hip"),
-    "backward": ("bla_device.h", "bla_forward.h", "bla_plan.h", "bla_backward.h"),
+    "backward": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h", "bla_backward.h",
+                 "bla_backward_bf16.h"),
 }
 
 
@@ -283,7 +284,7 @@ def bench_backward(args, hip, inputs):
                 "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": traffic}
     t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
     detail = {
-        "kernel": "bwd_kernel<bf16,64,64,64,false>",
+        "kernel": "bwd16_kernel<64,64,64,false>",
         "algorithmic_flops_per_launch": flops,
         "algorithmic_bytes_per_launch": nbytes,
         "reverse_walk_us": round(phase_ms["reverse_walk"] * 1e3, 2),
