@@ -426,10 +426,26 @@ def bench_decode(args, hip):
     state_bytes = w.B * w.H * 2 * (2 * w.M * w.d * 4)        # k and v states
     nbytes = 2 * state_bytes + w.B * w.H * w.d * 2 * 4       # read + write states, q,k,v,o
     gbs = nbytes / (ms * 1e-3) / 1e9
+    # a plain device-to-device copy of the same state size (read + write), for the rate a
+    # streaming read-modify-write can reach on this device
+    src = torch.empty(state_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    c0, c1 = hip.event(), hip.event()
+    torch.cuda.synchronize(dev)
+    hip.record(c0, sptr)
+    for _ in range(args.steps):
+        dst.copy_(src)
+    hip.record(c1, sptr)
+    torch.cuda.synchronize(dev)
+    copy_gbs = 2 * state_bytes / (hip.elapsed_ms(c0, c1) / args.steps * 1e-3) / 1e9
+    del src, dst
     return {"workload": "decode", "B": w.B, "H": w.H, "d": w.d, "M": w.M, "S": w.S, "position": w.L,
             "ms_per_step": round(ms, 4), "tokens_per_s": round(w.B / (ms * 1e-3), 1),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None}}
+                         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+            "device_copy_gbs": round(copy_gbs, 1), "frac_of_device_copy": round(gbs / copy_gbs, 4)}
 
 
 def cpu_baseline_anchored(w, T, inputs):
