@@ -188,13 +188,6 @@ __device__ __forceinline__ void rotate_dm(StateTiles<T, D, MP>& Z, const float* 
     }
 }
 
-// A uniform pointer the optimiser cannot see through (no code is emitted).
-template <typename P> __device__ __forceinline__ const P* opaque(const P* p)
-{
-    asm volatile("" : "+s"(p));
-    return p;
-}
-
 // Pre-rotated phase (cos, sin) of m w n for one mode, n an exact token count.
 __device__ __forceinline__ void bwd_phase(int m, long long n, double rT, float& c, float& s)
 {

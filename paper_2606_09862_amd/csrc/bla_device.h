@@ -47,6 +47,15 @@ __device__ __forceinline__ floatx4 mma(floatx8 a, floatx8 b, floatx4 c)
 
 __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
 
+// A uniform pointer the optimiser cannot see through (no code is emitted).  Re-deriving a
+// table pointer this way once per loop iteration keeps the table's fragments from being
+// hoisted out of the loop into registers (which spills when the tables are large).
+template <typename P> __device__ __forceinline__ const P* opaque(const P* p)
+{
+    asm volatile("" : "+s"(p));
+    return p;
+}
+
 template <typename T> __device__ __forceinline__ typename Frag<T>::type zero_frag()
 {
     typename Frag<T>::type f;

@@ -15,7 +15,7 @@
 //   (7-9)  O   = Re(W'' Z'_v) + tril(Re(W'' conj(E)^T)) V
 //   (10)   Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i]
 //
-// Work split inside a 256-thread workgroup (4 waves): contractions that produce
+// Work split inside a 256-thread workgroup (4 waves; 8 for d = M = 128, see Geo): contractions that produce
 // per-mode rows (1+3, 10) are split by mode tiles, the Gram tile (2) by key
 // tiles, and the per-token chain (4-9) by token tiles, so that the chain passes
 // its intermediates in registers (see bla_device.h).  The fp32 state of the
@@ -53,7 +53,11 @@ constexpr size_t kMaxLds = 160 * 1024;
 template <typename T, int D, int MP> struct Geo {
     static constexpr int C = kChunk;
     static constexpr int NT = C / 16;           // token tiles per chunk
-    static constexpr int NW = kThreads / 64;    // waves
+    // Threads per workgroup: 4 waves, or 8 for d = M = 128, where four waves would each hold
+    // two mode tiles of both states (256 registers) and spill; the token chain then runs on
+    // waves 0..NT-1 and the other four take part in the mode-tile phases only.
+    static constexpr int NTHR = (D == 128 && MP == 128) ? 2 * kThreads : kThreads;
+    static constexpr int NW = NTHR / 64;        // waves
     static constexpr int NMT = MP / 16;         // mode tiles
     static constexpr int NDT = D / 16;          // head-dim tiles
     static constexpr int KBD = D / 32;          // reduction blocks over d
@@ -73,9 +77,9 @@ template <typename T, int D, int MP> struct Geo {
     // staging units: Q rows in pieces of 8 elements, K/V in 4-token x 8-element blocks
     static constexpr int QU = C * D / 8;
     static constexpr int KVU = 2 * (C / 4) * (D / 8);
-    static constexpr int QPT = (QU + kThreads - 1) / kThreads;
-    static constexpr int KVPT = (KVU + kThreads - 1) / kThreads;
-    static_assert(NT == NW, "one token tile per wave");
+    static constexpr int QPT = (QU + NTHR - 1) / NTHR;
+    static constexpr int KVPT = (KVU + NTHR - 1) / NTHR;
+    static_assert(NT <= NW, "one token tile per wave, for the first NT waves");
     static_assert(D % 32 == 0 && MP % 16 == 0, "tile shapes");
 };
 
@@ -128,9 +132,9 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
     constexpr int DO = D / 8;
 #pragma unroll
     for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
-        const int u = tid + i * kThreads;
+        const int u = tid + i * GG::NTHR;
         const int t = min(u / DO, c - 1), dq = u % DO;
-        if (GG::QU % kThreads == 0 || u < GG::QU) {
+        if (GG::QU % GG::NTHR == 0 || u < GG::QU) {
             st.q[i][0] = ld4<T>(qc + (size_t)t * D + 8 * dq);
             st.q[i][1] = ld4<T>(qc + (size_t)t * D + 8 * dq + 4);
         }
@@ -138,10 +142,10 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
     constexpr int UNITS = GG::KVU / 2;
 #pragma unroll
     for (int i = 0; i < GG::KVPT; ++i) {
-        const int u = tid + i * kThreads;
+        const int u = tid + i * GG::NTHR;
         const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
         const T* src = (which ? vc : kc) + 8 * dq;
-        if (GG::KVU % kThreads == 0 || u < GG::KVU) {
+        if (GG::KVU % GG::NTHR == 0 || u < GG::KVU) {
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int row = min(4 * tq + t, c - 1);
@@ -161,8 +165,8 @@ __device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T*
     const H z = zero_half<T>();
 #pragma unroll
     for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
-        const int u = tid + i * kThreads;
-        if (GG::QU % kThreads == 0 || u < GG::QU) {
+        const int u = tid + i * GG::NTHR;
+        if (GG::QU % GG::NTHR == 0 || u < GG::QU) {
             const int t = u / DO, dq = u % DO;
             const bool ok = t < c;
             *reinterpret_cast<H*>(Qs + (size_t)t * GG::LDQ + 8 * dq) = ok ? st.q[i][0] : z;
@@ -172,8 +176,8 @@ __device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T*
     constexpr int UNITS = GG::KVU / 2;
 #pragma unroll
     for (int i = 0; i < GG::KVPT; ++i) {
-        const int u = tid + i * kThreads;
-        if (GG::KVU % kThreads == 0 || u < GG::KVU) {
+        const int u = tid + i * GG::NTHR;
+        if (GG::KVU % GG::NTHR == 0 || u < GG::KVU) {
             const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
             T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
             H x[4][2];
@@ -196,30 +200,30 @@ __device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T*
 
 // A table copied from the workspace into LDS: ROWS x COLS elements of E, source
 // rows contiguous, destination row stride DSTRIDE (COLS * sizeof(E) a multiple of 8).
-template <typename E, int ROWS, int COLS, int DSTRIDE> struct TabCopy {
+template <typename E, int ROWS, int COLS, int DSTRIDE, int NTHR = kThreads> struct TabCopy {
     static constexpr int PER = 8 / (int)sizeof(E);        // elements per 8-byte piece
     static constexpr int PIECES = ROWS * COLS / PER;
-    static constexpr int ITER = (PIECES + kThreads - 1) / kThreads;
+    static constexpr int ITER = (PIECES + NTHR - 1) / NTHR;
 };
 
 // Copy up to two tables with every load of the thread in flight before the first
 // store (the copies run once per workgroup, so their latency is paid only once).
-template <typename E, int ROWS, int COLS, int DSTRIDE>
+template <typename E, int ROWS, int COLS, int DSTRIDE, int NTHR = kThreads>
 __device__ __forceinline__ void copy_table(E* dst, const E* src, int tid)
 {
     typedef int intx2 __attribute__((ext_vector_type(2)));
-    using TC = TabCopy<E, ROWS, COLS, DSTRIDE>;
+    using TC = TabCopy<E, ROWS, COLS, DSTRIDE, NTHR>;
     intx2 buf[TC::ITER];
 #pragma unroll
     for (int i = 0; i < TC::ITER; ++i) {
-        const int u = tid + i * kThreads;
-        if (TC::PIECES % kThreads == 0 || u < TC::PIECES)
+        const int u = tid + i * NTHR;
+        if (TC::PIECES % NTHR == 0 || u < TC::PIECES)
             buf[i] = reinterpret_cast<const intx2*>(src)[u];
     }
 #pragma unroll
     for (int i = 0; i < TC::ITER; ++i) {
-        const int u = tid + i * kThreads;
-        if (TC::PIECES % kThreads == 0 || u < TC::PIECES) {
+        const int u = tid + i * NTHR;
+        if (TC::PIECES % NTHR == 0 || u < TC::PIECES) {
             const int rr = u / (COLS / TC::PER), cc = (u % (COLS / TC::PER)) * TC::PER;
             *reinterpret_cast<intx2*>(dst + (size_t)rr * DSTRIDE + cc) = buf[i];
         }
@@ -324,7 +328,7 @@ __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTil
 // ---------------------------------------------------------------------------------
 // Block summaries: the pre-rotated state after cpb full chunks, from zero.
 template <typename T, int D, int MP>
-__global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
+__global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs a)
 {
     using GG = Geo<T, D, MP>;
     __shared__ __attribute__((aligned(16))) T lds[2 * GG::KT_ELEMS];
@@ -387,7 +391,7 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(FwdArgs a)
 // One workgroup per (b, h, segment): the chunk loop over the segment.  AN: anchored slots
 // (a separate instantiation, so that the rotating form keeps its own register allocation).
 template <typename T, int D, int MP, int SP, bool AN>
-__global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
+__global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs a)
 {
     using P = Fwd<T, D, MP, SP>;
     using GG = Geo<T, D, MP>;
@@ -438,14 +442,14 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         T* lErev = lEbar + (size_t)2 * MP * P::LDR;
         float* lRho = reinterpret_cast<float*>(lErev + (size_t)2 * MP * P::LDR);
         int* lTheta = reinterpret_cast<int*>(lRho + 4 * MP);
-        copy_table<T, SP, 2 * MP, P::LDAS>(lABs, (const T*)a.ABs, tid);
-        copy_table<T, 2 * MP, SP, P::LDAM>(lABm, (const T*)a.ABm, tid);
-        copy_table<T, C, 2 * MP, P::LDE>(lEtab, gEtab, tid);
-        copy_table<T, 2 * MP, C, P::LDR>(lEbar, gEbar, tid);
-        copy_table<T, 2 * MP, C, P::LDR>(lErev, gErev, tid);
-        copy_table<float, 1, 2 * MP, 2 * MP>(lRho, E32h + 2 * MP, tid);                    // rho
-        copy_table<float, 1, 2 * MP, 2 * MP>(lRho + 2 * MP, E32h + (size_t)C * 2 * MP, tid);  // rho^C
-        copy_table<int, 1, SP, SP>(lTheta, thh, tid);
+        copy_table<T, SP, 2 * MP, P::LDAS, GG::NTHR>(lABs, (const T*)a.ABs, tid);
+        copy_table<T, 2 * MP, SP, P::LDAM, GG::NTHR>(lABm, (const T*)a.ABm, tid);
+        copy_table<T, C, 2 * MP, P::LDE, GG::NTHR>(lEtab, gEtab, tid);
+        copy_table<T, 2 * MP, C, P::LDR, GG::NTHR>(lEbar, gEbar, tid);
+        copy_table<T, 2 * MP, C, P::LDR, GG::NTHR>(lErev, gErev, tid);
+        copy_table<float, 1, 2 * MP, 2 * MP, GG::NTHR>(lRho, E32h + 2 * MP, tid);                    // rho
+        copy_table<float, 1, 2 * MP, 2 * MP, GG::NTHR>(lRho + 2 * MP, E32h + (size_t)C * 2 * MP, tid);  // rho^C
+        copy_table<int, 1, SP, SP, GG::NTHR>(lTheta, thh, tid);
         tABs = lABs;
         tABm = lABm;
         tEtab = lEtab;
@@ -539,10 +543,18 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
     for (int n = 0; n < nch; ++n) {
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
+        if constexpr (!P::TL) {
+            // tables in global memory: re-read per chunk rather than held in registers
+            tABs = opaque(tABs);
+            tABm = opaque(tABm);
+            tEtab = opaque(tEtab);
+            tEbar = opaque(tEbar);
+            tErev = opaque(tErev);
+        }
         __syncthreads();  // previous chunk done with Qs / Kt / Vt and the twiddle row
         stage_store<T, D, MP, true>(st, Qs, Kt, Vt, c, tid);
         if constexpr (AN) {
-            for (int m = tid; m < MP; m += kThreads) {
+            for (int m = tid; m < MP; m += GG::NTHR) {
                 float cs = 0.f, sn = 0.f;
                 if (m < a.M) anchor_phase(m, a.t0 + tok0, rT, cs, sn);
                 lPh[m] = (T)cs;
@@ -644,7 +656,7 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
         __syncthreads();
 
         // ---- per-token chain on token tile w: scores, softmax, readout, output
-        {
+        if (w < NT) {
             const int j = 16 * w + r;
             const long long pos = a.t0 + tok0 + j;
             F uf[GG::KBM];
@@ -684,31 +696,49 @@ __global__ __launch_bounds__(kThreads) void forward_kernel(FwdArgs a)
 #pragma unroll
             for (int kb = 0; kb < P::KBS; ++kb) pf[kb] = frag_from_acc<T>(sc[2 * kb] * inv, sc[2 * kb + 1] * inv);
 
-            floatx4 wa[2 * NMT];
-#pragma unroll
-            for (int t = 0; t < 2 * NMT; ++t) {
-                wa[t] = zero4();
-#pragma unroll
-                for (int kb = 0; kb < P::KBS; ++kb)
-                    wa[t] = mma(ld_frag<T>(tABm + (size_t)(16 * t + r) * sABm, 32 * kb, g), pf[kb], wa[t]);
-            }
-#pragma unroll
-            for (int mt = 0; mt < NMT; ++mt) {
-                floatx4 cs, sn;
-                if constexpr (AN) {
-                    cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
-                    sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
-                } else {
-                    cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
-                    sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
-                }
-                const floatx4 am = wa[mt], bm = wa[NMT + mt];
-                wa[mt] = am * cs + bm * sn;
-                wa[NMT + mt] = am * sn - bm * cs;
-            }
+            // W'' by groups of MG mode tiles: the Re and Im tiles of a group are produced,
+            // twiddled and packed into their fragments together, so that only 2 MG accumulator
+            // tiles are live at a time.  Fragment kb holds combined tiles 2kb, 2kb + 1 of
+            // [Re tiles | Im tiles]: for MG = 2 those are Re (wf[kb']) and Im (wf[NMT/2 + kb'])
+            // of the group's two mode tiles; for a single mode tile (NMT = 1) wf[0] = [Re | Im].
+            constexpr int MG = (NMT % 2 == 0) ? 2 : 1;
+            static_assert(MG == 2 || NMT == 1, "mode-tile grouping");
             F wf[GG::KBM];
 #pragma unroll
-            for (int kb = 0; kb < GG::KBM; ++kb) wf[kb] = frag_from_acc<T>(wa[2 * kb], wa[2 * kb + 1]);
+            for (int kb = 0; kb < NMT / MG; ++kb) {
+                floatx4 wa[2][MG];  // [Re, Im][mode tile MG kb + u]
+#pragma unroll
+                for (int p = 0; p < 2; ++p)
+#pragma unroll
+                    for (int u = 0; u < MG; ++u) {
+                        const int t = p * NMT + MG * kb + u;
+                        wa[p][u] = zero4();
+#pragma unroll
+                        for (int ks = 0; ks < P::KBS; ++ks)
+                            wa[p][u] = mma(ld_frag<T>(tABm + (size_t)(16 * t + r) * sABm, 32 * ks, g), pf[ks], wa[p][u]);
+                    }
+#pragma unroll
+                for (int u = 0; u < MG; ++u) {
+                    const int mt = MG * kb + u;
+                    floatx4 cs, sn;
+                    if constexpr (AN) {
+                        cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
+                        sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
+                    } else {
+                        cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
+                        sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                    }
+                    const floatx4 am = wa[0][u], bm = wa[1][u];
+                    wa[0][u] = am * cs + bm * sn;
+                    wa[1][u] = am * sn - bm * cs;
+                }
+                if constexpr (MG == 2) {
+                    wf[kb] = frag_from_acc<T>(wa[0][0], wa[0][1]);
+                    wf[NMT / 2 + kb] = frag_from_acc<T>(wa[1][0], wa[1][1]);
+                } else {
+                    wf[0] = frag_from_acc<T>(wa[0][0], wa[1][0]);
+                }
+            }
 
             floatx4 oa[NDT];
 #pragma unroll

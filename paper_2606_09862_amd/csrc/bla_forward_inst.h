@@ -65,9 +65,9 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
         } else if constexpr (fits<T, D, MP, SP>()) {                                                    \
             const dim3 grid((unsigned)(p.B * p.H * p.nseg));                                            \
             if (a.anchor)                                                                               \
-                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, true>), grid, dim3(kThreads), 0, s, a); \
+                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, true>), grid, dim3(Geo<T, D, MP>::NTHR), 0, s, a); \
             else                                                                                        \
-                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, false>), grid, dim3(kThreads), 0, s, a); \
+                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, false>), grid, dim3(Geo<T, D, MP>::NTHR), 0, s, a); \
             return hipGetLastError();                                                                   \
         } else {                                                                                        \
             return hipErrorInvalidValue;                                                                \
@@ -81,7 +81,7 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
                                dim3(summary_threads<D, MP>()), 0, s, a);                                \
         } else {                                                                                        \
             hipLaunchKernelGGL((summary_kernel<T, D, MP>), dim3((unsigned)(p.B * p.H * p.nbs)),         \
-                               dim3(kThreads), 0, s, a);                                                \
+                               dim3(Geo<T, D, MP>::NTHR), 0, s, a);                                     \
         }                                                                                               \
         return hipGetLastError();                                                                       \
     }                                                                                                   \

@@ -6,4 +6,3 @@ BLA_INSTANTIATE(bf16, 128, 32, 64)
 BLA_INSTANTIATE(bf16, 128, 64, 32)
 BLA_INSTANTIATE(bf16, 128, 64, 64)
 BLA_INSTANTIATE(bf16, 128, 64, 128)
-BLA_INSTANTIATE(bf16, 128, 128, 128)

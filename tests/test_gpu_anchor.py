@@ -66,6 +66,19 @@ def test_anchor_segments(dtype, B, H, L, d, M, S, T):
     assert_close(ov, ref_v, tol, "state_v")
 
 
+def test_anchor_eight_waves():
+    """bf16, d = M = 128 (eight waves per workgroup), several segments, ragged tail."""
+    B, H, L, d, M, S, T = 1, 2, 64 * 11 + 9, 128, 128, 128, (255.0, 510.0)
+    q, k, v = gauss(L + 29, B, H, L, d, torch.bfloat16)
+    o, ok, ov = run_anchored(q, k, v, T, M, S, torch.bfloat16, label=f"eight waves {B}x{H}x{L}")
+    ref_o, _, _ = oracle.forward_anchored(q, k, v, T, M, S)
+    _, ref_k, ref_v = oracle.forward(q, k, v, T, M, S)
+    tol = TOL[torch.bfloat16]
+    assert_close(o, ref_o, tol, "O")
+    assert_close(ok, ref_k, tol, "state_k")
+    assert_close(ov, ref_v, tol, "state_v")
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_anchor_continuation(dtype):
     """Two calls: the second continues from the first one's state at t0 = L1 (the state

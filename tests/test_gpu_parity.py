@@ -119,6 +119,19 @@ def test_bf16_unit_layouts(B, H, L, d, M, S, T):
     run_case(q, k, v, T[:H], M, S, torch.bfloat16, label=f"layout {B}x{H}x{L}x{d} M={M}")
 
 
+@pytest.mark.parametrize("B,H,L,d,M,S,T", [
+    (1, 2, 64 * 11 + 9, 128, 128, 128, (255.0, 510.0)),  # d = M = 128: eight waves, one mode tile each
+    (2, 1, 300, 128, 100, 256, (199.0,)),                 # modes padded 100 -> 128, slots 256
+])
+def test_wide_state_eight_waves(B, H, L, d, M, S, T):
+    """bf16, d = M = 128 runs eight waves per workgroup (the token chain on the first four);
+    float32 I/O at this size does not fit the LDS tiles and is rejected."""
+    q, k, v = gauss(L + 5 * M + S, B, H, L, d, torch.bfloat16)
+    run_case(q, k, v, T[:H], M, S, torch.bfloat16, label=f"eight waves {B}x{H}x{L}x{d} M={M} S={S}")
+    bla = _bla()
+    assert bla.supported(bla.make_params(B, H, L, d, M, S, torch.float32)) != 0
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_state_in_and_offset(dtype):
     """Continue a sequence: state_in from the oracle, t0 > 0 (start mask at absolute positions)."""
