@@ -346,7 +346,7 @@ def bench_layer(args, hip):
     fn = bla.lib().bla_layer_forward_timed
 
     def call(evs):
-        arr = None if evs is None else (ctypes.c_void_p * 6)(*[e.value for e in evs])
+        arr = None if evs is None else (ctypes.c_void_p * 4)(*[e.value for e in evs])
         st = fn(ctypes.byref(p), Tarr, *ptrs, ws.numel(), sptr, arr)
         if st != 0:
             raise RuntimeError(f"bla_layer_forward failed: {bla.STATUS.get(st, st)}")
@@ -361,12 +361,12 @@ def bench_layer(args, hip):
     hip.record(e1, sptr)
     torch.cuda.synchronize(dev)
     ms = hip.elapsed_ms(e0, e1) / args.steps
-    evs = [[hip.event() for _ in range(6)] for _ in range(args.steps)]
+    evs = [[hip.event() for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
     for i in range(args.steps):
         call(evs[i])
     torch.cuda.synchronize(dev)
-    phases = ["qkv_projection", "head_split", "operator", "head_merge", "output_projection"]
+    phases = ["qkv_projection", "operator", "output_projection"]
     phase_us = {ph: round(float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs])) * 1e3, 2)
                 for j, ph in enumerate(phases)}
     tokens = w.B * w.L

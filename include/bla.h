@@ -245,8 +245,10 @@ bla_status bla_backward_timed(const bla_params* p, const double* T, const void* 
  * 1, 2 are head h's query, key and value projections), W_o [D, D] (row h d_k + e takes element
  * e of head h's output), all bf16; the products accumulate in float32 (hipBLASLt) and q, k, v
  * and o are rounded to bf16 between the steps.  p describes the operator (p->d_k = p->d_v is
- * the head width, p->L the tokens); states as for bla_forward.  The workspace holds the
- * projected tensors, the operator's workspace and 32 MB of GEMM scratch.  The first call on
+ * the head width, p->L the tokens); states as for bla_forward.  The operator reads q, k, v in
+ * place from the projection output [B, L, 3, H, d_k] and writes o in place as [B, L, H, d_k],
+ * the output projection's input.  The workspace holds those two tensors, the operator's
+ * workspace and 32 MB of GEMM scratch.  The first call on
  * a device creates a hipBLASLt handle that lives until the process ends.  Errors as for
  * bla_forward; a failing GEMM is BLA_ERR_HIP.
  */
@@ -257,9 +259,8 @@ bla_status bla_layer_forward(const bla_params* p, const double* T, const void* x
                              void* stream);
 
 /*
- * bla_layer_forward with phase timing: events[0..5] (hipEvent_t or NULL) are recorded before
- * the QKV projection, after it, after the head split, after the operator, after the head merge
- * and after the output projection.
+ * bla_layer_forward with phase timing: events[0..3] (hipEvent_t or NULL) are recorded before
+ * the QKV projection, after it, after the operator and after the output projection.
  */
 bla_status bla_layer_forward_timed(const bla_params* p, const double* T, const void* x, const void* w_qkv,
                                    const void* w_o, const float* state_k_in, const float* state_v_in, void* y,

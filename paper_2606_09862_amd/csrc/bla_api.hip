@@ -315,9 +315,12 @@ size_t bla_step_workspace_size(const bla_params* p)
     return pl.total;
 }
 
+// in_strides / out_strides: {batch, head, token} element strides of q, k, v and of o
+// (nullable: contiguous [B, H, L, d]).
 static bla_status forward_impl(const bla_params* p, const double* T, const void* q, const void* k,
-                               const void* v, const float* state_k_in, const float* state_v_in,
-                               void* o, float* state_k_out, float* state_v_out, void* workspace,
+                               const void* v, const long long* in_strides, const float* state_k_in,
+                               const float* state_v_in, void* o, const long long* out_strides,
+                               float* state_k_out, float* state_v_out, void* workspace,
                                size_t workspace_bytes, void* stream, void* const* events)
 {
     bla_status st = check_shape(p, false);
@@ -325,6 +328,13 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     if ((st = check_periods(p, T)) != BLA_OK) return st;
     const long long units = (long long)p->B * p->H;
     if (units == 0) return BLA_OK;
+    const long long Ld = (long long)p->L * p->d_k;
+    const long long contiguous[3] = {(long long)p->H * Ld, Ld, p->d_k};
+    const long long* si = in_strides ? in_strides : contiguous;
+    const long long* so = out_strides ? out_strides : contiguous;
+    for (int i = 0; i < 3; ++i)
+        if (si[i] < 0 || so[i] < 0 || si[i] % 8 || so[i] % 8) return BLA_ERR_INVALID_ARG;
+    if (si[2] < p->d_k || so[2] < p->d_k || si[2] > INT32_MAX || so[2] > INT32_MAX) return BLA_ERR_INVALID_ARG;
     if (p->L > 0) {
         if (!q || !k || !v || !o) return BLA_ERR_INVALID_ARG;
         if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return BLA_ERR_INVALID_ARG;
@@ -386,6 +396,12 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     a.nbs = pl.nbs;
     a.t0 = pl.t0;
     a.scale = pl.scale;
+    a.in_b = si[0];
+    a.in_h = si[1];
+    a.in_t = (int)si[2];
+    a.out_b = so[0];
+    a.out_h = so[1];
+    a.out_t = (int)so[2];
     if (pl.nseg > 1 && launch_summary(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
     if (!mark(2)) return BLA_ERR_HIP;
     if (pl.nseg > 1 && !pl.pair && launch_scan(pl, a, s) != hipSuccess) return BLA_ERR_HIP;
@@ -400,8 +416,8 @@ bla_status bla_forward(const bla_params* p, const double* T, const void* q, cons
                        float* state_k_out, float* state_v_out, void* workspace,
                        size_t workspace_bytes, void* stream)
 {
-    return forward_impl(p, T, q, k, v, state_k_in, state_v_in, o, state_k_out, state_v_out, workspace,
-                        workspace_bytes, stream, nullptr);
+    return forward_impl(p, T, q, k, v, nullptr, state_k_in, state_v_in, o, nullptr, state_k_out, state_v_out,
+                        workspace, workspace_bytes, stream, nullptr);
 }
 
 bla_status bla_forward_timed(const bla_params* p, const double* T, const void* q, const void* k,
@@ -409,8 +425,8 @@ bla_status bla_forward_timed(const bla_params* p, const double* T, const void* q
                              float* state_k_out, float* state_v_out, void* workspace,
                              size_t workspace_bytes, void* stream, void* const* events)
 {
-    return forward_impl(p, T, q, k, v, state_k_in, state_v_in, o, state_k_out, state_v_out, workspace,
-                        workspace_bytes, stream, events);
+    return forward_impl(p, T, q, k, v, nullptr, state_k_in, state_v_in, o, nullptr, state_k_out, state_v_out,
+                        workspace, workspace_bytes, stream, events);
 }
 
 bla_status bla_step(const bla_params* p, const double* T, const void* q, const void* k,
@@ -703,3 +719,16 @@ bla_status bla_backward_timed(const bla_params* p, const double* T, const void* 
 }
 
 }  // extern "C"
+
+namespace bla {
+
+bla_status forward_strided(const bla_params* p, const double* T, const void* q, const void* k, const void* v,
+                           const long long* in_strides, const float* state_k_in, const float* state_v_in, void* o,
+                           const long long* out_strides, float* state_k_out, float* state_v_out, void* workspace,
+                           size_t workspace_bytes, void* stream, void* const* events)
+{
+    return forward_impl(p, T, q, k, v, in_strides, state_k_in, state_v_in, o, out_strides, state_k_out,
+                        state_v_out, workspace, workspace_bytes, stream, events);
+}
+
+}  // namespace bla

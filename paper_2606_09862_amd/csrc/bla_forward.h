@@ -126,7 +126,7 @@ template <typename T, int D, int MP> struct Stage {
 // while they are in flight.
 template <typename T, int D, int MP, bool WQ>
 __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, const T* kc, const T* vc,
-                                           int c, int tid)
+                                           int ts, int c, int tid)
 {
     using GG = Geo<T, D, MP>;
     constexpr int DO = D / 8;
@@ -135,8 +135,8 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
         const int u = tid + i * GG::NTHR;
         const int t = min(u / DO, c - 1), dq = u % DO;
         if (GG::QU % GG::NTHR == 0 || u < GG::QU) {
-            st.q[i][0] = ld4<T>(qc + (size_t)t * D + 8 * dq);
-            st.q[i][1] = ld4<T>(qc + (size_t)t * D + 8 * dq + 4);
+            st.q[i][0] = ld4<T>(qc + (size_t)t * ts + 8 * dq);
+            st.q[i][1] = ld4<T>(qc + (size_t)t * ts + 8 * dq + 4);
         }
     }
     constexpr int UNITS = GG::KVU / 2;
@@ -149,8 +149,8 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int row = min(4 * tq + t, c - 1);
-                st.kv[i][t][0] = ld4<T>(src + (size_t)row * D);
-                st.kv[i][t][1] = ld4<T>(src + (size_t)row * D + 4);
+                st.kv[i][t][0] = ld4<T>(src + (size_t)row * ts);
+                st.kv[i][t][1] = ld4<T>(src + (size_t)row * ts + 4);
             }
         }
     }
@@ -337,8 +337,9 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in a scalar register
     const int blk = blockIdx.x % a.nbs, bh = blockIdx.x / a.nbs, h = bh % a.H;
-    const T* kbase = (const T*)a.k + (size_t)bh * a.L * D;
-    const T* vbase = (const T*)a.v + (size_t)bh * a.L * D;
+    const T* kbase = (const T*)a.k + fwd_in_base(a, bh);
+    const T* vbase = (const T*)a.v + fwd_in_base(a, bh);
+    const int ts = a.in_t;
     const float* E32h = a.E32 + (size_t)h * (GG::C + 1) * 2 * MP;
 
     const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C;
@@ -355,9 +356,9 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs 
     // little arithmetic per byte, so it is bound by how much load latency it hides.
     Stage<T, D, MP> st0, st1;
     const size_t first = (size_t)blk * a.cpb * GG::C;
-    stage_load<T, D, MP, false>(st0, nullptr, kbase + first * D, vbase + first * D, GG::C, tid);
+    stage_load<T, D, MP, false>(st0, nullptr, kbase + first * ts, vbase + first * ts, ts, GG::C, tid);
     if (a.cpb > 1)
-        stage_load<T, D, MP, false>(st1, nullptr, kbase + (first + GG::C) * D, vbase + (first + GG::C) * D,
+        stage_load<T, D, MP, false>(st1, nullptr, kbase + (first + GG::C) * ts, vbase + (first + GG::C) * ts, ts,
                                     GG::C, tid);
     for (int n = 0; n < a.cpb; ++n) {
         __syncthreads();
@@ -365,7 +366,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs 
         st0 = st1;
         if (n + 2 < a.cpb) {
             const size_t tok = first + (size_t)(n + 2) * GG::C;
-            stage_load<T, D, MP, false>(st1, nullptr, kbase + tok * D, vbase + tok * D, GG::C, tid);
+            stage_load<T, D, MP, false>(st1, nullptr, kbase + tok * ts, vbase + tok * ts, ts, GG::C, tid);
         }
         __syncthreads();
         advance_state<T, D, MP>(Zk, Zv, Kt, Vt, rhoC, E32h, ErevTh, GG::C, GG::C, w, g, r);
@@ -411,10 +412,11 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
     const int seg = blockIdx.x % a.nseg, bh = blockIdx.x / a.nseg, h = bh % a.H;
     const int ch0 = seg * a.cps;
     const int nch = min(a.cps, a.nch - ch0);
-    const T* qb = (const T*)a.q + (size_t)bh * a.L * D;
-    const T* kb_ = (const T*)a.k + (size_t)bh * a.L * D;
-    const T* vb = (const T*)a.v + (size_t)bh * a.L * D;
-    T* ob = (T*)a.o + (size_t)bh * a.L * D;
+    const T* qb = (const T*)a.q + fwd_in_base(a, bh);
+    const T* kb_ = (const T*)a.k + fwd_in_base(a, bh);
+    const T* vb = (const T*)a.v + fwd_in_base(a, bh);
+    T* ob = (T*)a.o + fwd_out_base(a, bh);
+    const int ts = a.in_t, tso = a.out_t;
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     const int* thh = a.theta + (size_t)h * SP;
 
@@ -474,10 +476,10 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
     F kpf[GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand), unmasked
     {
         const int tok0 = ch0 * C, c0 = min(C, a.L - tok0), i = min(16 * w + r, c0 - 1);
-        stage_load<T, D, MP, true>(st, qb + (size_t)tok0 * D, kb_ + (size_t)tok0 * D, vb + (size_t)tok0 * D, c0,
-                                   tid);
+        stage_load<T, D, MP, true>(st, qb + (size_t)tok0 * ts, kb_ + (size_t)tok0 * ts, vb + (size_t)tok0 * ts,
+                                   ts, c0, tid);
 #pragma unroll
-        for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tok0 + i) * D, 32 * kb, g);
+        for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tok0 + i) * ts, 32 * kb, g);
     }
     if constexpr (P::TL) __syncthreads();  // LDS tables visible
 
@@ -566,10 +568,10 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
         for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = (16 * w + r < c) ? kpf[kb] : zero_frag<T>();
         if (n + 1 < nch) {
             const int tn = tok0 + C, cn = min(C, a.L - tn), i = min(16 * w + r, cn - 1);
-            stage_load<T, D, MP, true>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn,
-                                       tid);
+            stage_load<T, D, MP, true>(st, qb + (size_t)tn * ts, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts,
+                                       cn, tid);
 #pragma unroll
-            for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tn + i) * D, 32 * kb, g);
+            for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tn + i) * ts, 32 * kb, g);
         }
         __syncthreads();  // staging and ZvT visible
 
@@ -774,7 +776,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
             }
             if (j < c) {
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) st4<T>(ob + (size_t)(tok0 + j) * D + 16 * dt + 4 * g, oa[dt]);
+                for (int dt = 0; dt < NDT; ++dt) st4<T>(ob + (size_t)(tok0 + j) * tso + 16 * dt + 4 * g, oa[dt]);
             }
         }
         __syncthreads();  // everyone done reading ZvT

@@ -95,9 +95,10 @@ template <int D, int MP, int SP> using PState = PStateDM<D, MP>;
 template <int D, int MP, int SP> using PStage = bf16x8[Pair<D, MP, SP>::PPT];
 
 // ut: thread index within the unit (0..255); q, k, v: the chunk's first rows.
+// ts: token stride of q, k, v (elements).
 template <int D, int MP, int SP>
 __device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf16* q,
-                                                const bf16* k, const bf16* v, int c, int ut)
+                                                const bf16* k, const bf16* v, int ts, int c, int ut)
 {
     using P = Pair<D, MP, SP>;
     constexpr int PR = D / 8;  // pieces per row
@@ -107,7 +108,7 @@ __device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf1
         if (P::PIECES % 256 == 0 || u < P::PIECES) {
             const int which = u / (P::C * PR), rem = u % (P::C * PR);
             const int row = min(rem / PR, c - 1), pc = rem % PR;
-            const unsigned off = (unsigned)(row * D + 8 * pc);  // within one chunk
+            const unsigned off = (unsigned)(row * ts + 8 * pc);  // within one chunk
             const bf16* src = (which == 0 ? q : which == 1 ? k : v) + off;
             st[i] = *reinterpret_cast<const bf16x8*>(src);
         }
@@ -279,9 +280,9 @@ template <int D, int MP> using SStage = bf16x8[SumPair<D, MP>::PPT];
 template <int D, int MP> using SState = floatx4[SumPair<D, MP>::OMT][SumPair<D, MP>::ODT][2];
 template <int D, int MP> using SEFrag = bf16x8[SumPair<D, MP>::EREG ? SumPair<D, MP>::OMT : 1][SumPair<D, MP>::KBC][2];
 
-// k, v: first row of the chunk, column offset of the workgroup's slice applied
+// k, v: first row of the chunk, column offset of the workgroup's slice applied; ts: token stride
 template <int D, int MP>
-__device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k, const bf16* v, int tid)
+__device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k, const bf16* v, int ts, int tid)
 {
     using P = SumPair<D, MP>;
 #pragma unroll
@@ -289,7 +290,7 @@ __device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k,
         const int u = tid + P::NTHR * i;
         if (P::PIECES % P::NTHR == 0 || u < P::PIECES) {
             const int which = u / (P::C * P::PR), rem = u % (P::C * P::PR);
-            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + (size_t)(rem / P::PR) * D +
+            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + (size_t)(rem / P::PR) * ts +
                                                      8 * (rem % P::PR));
         }
     }
@@ -338,8 +339,9 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
     const int h = blockIdx.y, ds = blockIdx.x % DS, blk = (blockIdx.x / DS) % a.nbs, b = blockIdx.x / (DS * a.nbs);
     const int bh = b * a.H + h;
     const size_t first = (size_t)blk * a.cpb * C;
-    const bf16* kb_ = (const bf16*)a.k + ((size_t)bh * a.L + first) * D + ds * P::DW;
-    const bf16* vb = (const bf16*)a.v + ((size_t)bh * a.L + first) * D + ds * P::DW;
+    const int ts = a.in_t;
+    const bf16* kb_ = (const bf16*)a.k + fwd_in_base(a, bh) + first * ts + ds * P::DW;
+    const bf16* vb = (const bf16*)a.v + fwd_in_base(a, bh) + first * ts + ds * P::DW;
 
     // tables first: their loads are then the oldest in flight when they are stored
     pair_copy<C, 2 * MP, P::LE, P::NTHR>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
@@ -355,13 +357,13 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
     SStage<D, MP> st[NPF];
 #pragma unroll
     for (int i = 0; i < NPF; ++i) {
-        const size_t off = (size_t)min(i, last) * C * D;
-        sum_stage_load<D, MP>(st[i], kb_ + off, vb + off, tid);
+        const size_t off = (size_t)min(i, last) * C * ts;
+        sum_stage_load<D, MP>(st[i], kb_ + off, vb + off, ts, tid);
     }
     sum_stage_store<D, MP>(st[0], KV, KV + P::KV_ELEMS, tid);
     {
-        const size_t off = (size_t)min(NPF, last) * C * D;
-        sum_stage_load<D, MP>(st[0], kb_ + off, vb + off, tid);
+        const size_t off = (size_t)min(NPF, last) * C * ts;
+        sum_stage_load<D, MP>(st[0], kb_ + off, vb + off, ts, tid);
     }
     __syncthreads();  // tables and chunk 0 visible
 
@@ -402,8 +404,8 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
                 const int s1 = (s + 1) % NPF;  // a constant once the loop is unrolled
                 bf16* Kn = KV + (size_t)(s1 & 1) * 2 * P::KV_ELEMS;
                 sum_stage_store<D, MP>(st[s1], Kn, Kn + P::KV_ELEMS, tid);
-                const size_t off = (size_t)min(n + 1 + NPF, last) * C * D;
-                sum_stage_load<D, MP>(st[s1], kb_ + off, vb + off, tid);
+                const size_t off = (size_t)min(n + 1 + NPF, last) * C * ts;
+                sum_stage_load<D, MP>(st[s1], kb_ + off, vb + off, ts, tid);
             }
             if (n < a.cpb) {
                 F ktf[P::KBC][ODT], vtf[P::KBC][ODT];
@@ -595,17 +597,19 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 
     const int ch0 = seg * a.cps;
     const int nch = active ? min(a.cps, a.nch - ch0) : 0;
-    const bf16* qb = (const bf16*)a.q + (size_t)bh * a.L * D;
-    const bf16* kb_ = (const bf16*)a.k + (size_t)bh * a.L * D;
-    const bf16* vb = (const bf16*)a.v + (size_t)bh * a.L * D;
-    bf16* ob = (bf16*)a.o + (size_t)bh * a.L * D;
+    const bf16* qb = (const bf16*)a.q + fwd_in_base(a, bh);
+    const bf16* kb_ = (const bf16*)a.k + fwd_in_base(a, bh);
+    const bf16* vb = (const bf16*)a.v + fwd_in_base(a, bh);
+    bf16* ob = (bf16*)a.o + fwd_out_base(a, bh);
+    const int ts = a.in_t, tso = a.out_t;
     // Chunk n + 1 is loaded into registers during chunk n; every load is unconditional
     // (an exhausted or idle unit re-reads a chunk that exists), so the wait before each
     // store to LDS covers only that stage's loads.
     const int last = max(nch - 1, 0);
     auto stage_chunk = [&](PStage<D, MP, SP>& st, int n) {
         const int tn = (ch0 + min(n, last)) * C, cn = min(C, a.L - tn);
-        pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * D, kb_ + (size_t)tn * D, vb + (size_t)tn * D, cn, ut);
+        pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * ts, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts, cn,
+                                   ut);
     };
 
     // anchored slots: the twiddle row of chunk n at its absolute start t0 + (ch0 + n) C
@@ -887,9 +891,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 }
             }
             if (j < c) {
-                bf16* oc = ob + (size_t)tok0 * D;
+                bf16* oc = ob + (size_t)tok0 * tso;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) st4<bf16>(oc + (unsigned)(j * D + 16 * dt + 4 * g), oa[dt]);
+                for (int dt = 0; dt < NDT; ++dt) st4<bf16>(oc + (unsigned)(j * tso + 16 * dt + 4 * g), oa[dt]);
             }
         }
         // ================= phase 1 (independent of the chain): step (10) on the owned mode tiles

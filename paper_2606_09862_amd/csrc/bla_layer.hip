@@ -4,13 +4,13 @@
 // output projection mixes the heads back into the model width.
 //
 //   qkv = x W_qkv        x [B*L, D], W_qkv [D, 3D]   (hipBLASLt, bf16 in, float32 accumulation)
-//   q, k, v <- qkv       [B, L, 3, H, d] -> three [B, H, L, d] tensors (permute kernel)
-//   o = bla_forward(q, k, v)                          ([B, H, L, d], states in / out)
-//   o' <- o              [B, H, L, d] -> [B, L, H, d] (permute kernel)
-//   y = o' W_o           W_o [D, D]                   (hipBLASLt)
+//   o = BLA(q, k, v)     q, k, v read in place from qkv, viewed as [B, L, 3, H, d], and o
+//                        written in place as [B, L, H, d] (the operator's strided form)
+//   y = o W_o            W_o [D, D]                   (hipBLASLt)
 //
-// The two products are plain dense GEMMs, so they go to the vendor library; every other
-// step runs in this library's kernels.
+// The two products are plain dense GEMMs, so they go to the vendor library; the operator
+// runs in this library's kernels and reads and writes the GEMMs' row-major tensors
+// directly, so no head split or merge pass touches memory.
 #include <stdint.h>
 #include <string.h>
 
@@ -28,49 +28,6 @@ constexpr size_t kLayerAlign = 256;
 constexpr size_t kGemmWorkspace = size_t(32) << 20;  // hipBLASLt scratch inside the caller's workspace
 
 size_t lalign(size_t x) { return (x + kLayerAlign - 1) / kLayerAlign * kLayerAlign; }
-
-// qkv [B, L, 3, H, d] -> q, k, v [B, H, L, d]; one thread moves 8 elements (16 bytes), in the
-// order of the destination so that the stores are contiguous.
-__global__ __launch_bounds__(256) void split_heads_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ q,
-                                                          bf16* __restrict__ k, bf16* __restrict__ v, int B, int L,
-                                                          int H, int d)
-{
-    const int d8 = d / 8;
-    const long long per = (long long)B * H * L * d8;  // 8-element pieces per destination tensor
-    const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (gid >= 3 * per) return;
-    const int which = (int)(gid / per);
-    long long r = gid % per;
-    const int e8 = (int)(r % d8);
-    r /= d8;
-    const int l = (int)(r % L);
-    r /= L;
-    const int h = (int)(r % H);
-    const int b = (int)(r / H);
-    const size_t D = (size_t)H * d;
-    const uint4 x = *reinterpret_cast<const uint4*>(qkv + (((size_t)b * L + l) * 3 + which) * D + (size_t)h * d + 8 * e8);
-    bf16* dst = which == 0 ? q : (which == 1 ? k : v);
-    *reinterpret_cast<uint4*>(dst + (((size_t)b * H + h) * L + l) * d + 8 * e8) = x;
-}
-
-// o [B, H, L, d] -> [B, L, H, d]
-__global__ __launch_bounds__(256) void merge_heads_kernel(const bf16* __restrict__ o, bf16* __restrict__ out, int B,
-                                                          int L, int H, int d)
-{
-    const int d8 = d / 8;
-    const long long n = (long long)B * L * H * d8;
-    const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
-    if (gid >= n) return;
-    long long r = gid;
-    const int e8 = (int)(r % d8);
-    r /= d8;
-    const int h = (int)(r % H);
-    r /= H;
-    const int l = (int)(r % L);
-    const int b = (int)(r / L);
-    const uint4 x = *reinterpret_cast<const uint4*>(o + (((size_t)b * H + h) * L + l) * d + 8 * e8);
-    *reinterpret_cast<uint4*>(out + (((size_t)b * L + l) * H + h) * d + 8 * e8) = x;
-}
 
 // One hipBLASLt handle per device, created on first use and kept for the process.
 hipblasLtHandle_t gemm_handle()
@@ -126,7 +83,7 @@ bool gemm_rowmajor(const bf16* X, const bf16* W, bf16* Y, long long m, long long
 }
 
 struct LayerPlan {
-    size_t off_qkv, off_q, off_k, off_v, off_o, off_fwd, off_gemm, total;
+    size_t off_qkv, off_o, off_fwd, off_gemm, total;
     size_t fwd_bytes;
 };
 
@@ -137,14 +94,10 @@ bla_status layer_plan(const bla_params* p, LayerPlan* lp)
     const bla_status st = bla_supported(p);
     if (st != BLA_OK) return st;
     const size_t tok = (size_t)p->B * p->L, D = (size_t)p->H * p->d_k;
-    const size_t one = (size_t)p->B * p->H * p->L * p->d_k * 2;  // one [B,H,L,d] bf16 tensor
     lp->fwd_bytes = bla_workspace_size(p);
     size_t off = 0;
-    lp->off_qkv = off; off = lalign(off + tok * 3 * D * 2);   // later the merged heads [B, L, D]
-    lp->off_q = off;   off = lalign(off + one);
-    lp->off_k = off;   off = lalign(off + one);
-    lp->off_v = off;   off = lalign(off + one);
-    lp->off_o = off;   off = lalign(off + one);
+    lp->off_qkv = off; off = lalign(off + tok * 3 * D * 2);  // [B, L, 3, H, d]
+    lp->off_o = off;   off = lalign(off + tok * D * 2);      // [B, L, H, d]
     lp->off_fwd = off; off = lalign(off + lp->fwd_bytes);
     lp->off_gemm = off; off = lalign(off + kGemmWorkspace);
     lp->total = off;
@@ -186,29 +139,22 @@ static bla_status layer_impl(const bla_params* p, const double* T, const void* x
         return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
     };
     bf16* qkv = (bf16*)(ws + lp.off_qkv);
-    bf16* q = (bf16*)(ws + lp.off_q);
-    bf16* k = (bf16*)(ws + lp.off_k);
-    bf16* v = (bf16*)(ws + lp.off_v);
     bf16* o = (bf16*)(ws + lp.off_o);
     void* gws = ws + lp.off_gemm;
+    const long long L = p->L, d = p->d_k;
+    const long long in_strides[3] = {L * 3 * D, d, 3 * D};  // [B, L, 3, H, d]
+    const long long out_strides[3] = {L * D, d, D};         // [B, L, H, d]
 
     if (!mark(0)) return BLA_ERR_HIP;
     if (!gemm_rowmajor((const bf16*)x, (const bf16*)w_qkv, qkv, tok, 3 * D, D, gws, kGemmWorkspace, s))
         return BLA_ERR_HIP;
     if (!mark(1)) return BLA_ERR_HIP;
-    const long long pieces = tok * 3 * D / 8;
-    hipLaunchKernelGGL(split_heads_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s, qkv, q, k, v,
-                       p->B, p->L, p->H, p->d_k);
-    if (hipGetLastError() != hipSuccess || !mark(2)) return BLA_ERR_HIP;
-    st = bla_forward(p, T, q, k, v, state_k_in, state_v_in, o, state_k_out, state_v_out, ws + lp.off_fwd,
-                     lp.fwd_bytes, stream);
+    st = forward_strided(p, T, qkv, qkv + D, qkv + 2 * D, in_strides, state_k_in, state_v_in, o, out_strides,
+                         state_k_out, state_v_out, ws + lp.off_fwd, lp.fwd_bytes, stream, nullptr);
     if (st != BLA_OK) return st;
+    if (!mark(2)) return BLA_ERR_HIP;
+    if (!gemm_rowmajor(o, (const bf16*)w_o, (bf16*)y, tok, D, D, gws, kGemmWorkspace, s)) return BLA_ERR_HIP;
     if (!mark(3)) return BLA_ERR_HIP;
-    hipLaunchKernelGGL(merge_heads_kernel, dim3((unsigned)((tok * D / 8 + 255) / 256)), dim3(256), 0, s, o, qkv, p->B,
-                       p->L, p->H, p->d_k);
-    if (hipGetLastError() != hipSuccess || !mark(4)) return BLA_ERR_HIP;
-    if (!gemm_rowmajor(qkv, (const bf16*)w_o, (bf16*)y, tok, D, D, gws, kGemmWorkspace, s)) return BLA_ERR_HIP;
-    if (!mark(5)) return BLA_ERR_HIP;
     return BLA_OK;
 }
 

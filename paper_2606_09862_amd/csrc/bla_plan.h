@@ -6,6 +6,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "bla.h"
+
 namespace bla {
 
 constexpr int kChunk = 64;      // tokens per chunk of the parallel form
@@ -77,7 +79,22 @@ struct FwdArgs {
     long long t0;
     float scale;  // score scale (applied by the pair kernel; folded into ABs otherwise)
     int anchor;   // 1: slots anchored at absolute phase 0 (Sec. 3.3)
+    // Element strides of q, k, v (in_*) and o (out_*): row (b, h) starts at b * x_b + h * x_h,
+    // token t of it at + t * x_t, and its d elements are contiguous.  [B, H, L, d] is
+    // (H L d, L d, d); a fused projection output [B, L, 3, H, d] is (3 L H d, d, 3 H d).
+    long long in_b, in_h, out_b, out_h;
+    int in_t, out_t;
 };
+
+// Where row (b, h) = bh of q, k, v (in) or o (out) starts, in elements.
+__host__ __device__ inline size_t fwd_in_base(const FwdArgs& a, int bh)
+{
+    return (size_t)(bh / a.H) * (size_t)a.in_b + (size_t)(bh % a.H) * (size_t)a.in_h;
+}
+__host__ __device__ inline size_t fwd_out_base(const FwdArgs& a, int bh)
+{
+    return (size_t)(bh / a.H) * (size_t)a.out_b + (size_t)(bh % a.H) * (size_t)a.out_h;
+}
 
 struct StepArgs {
     const void* q;
@@ -217,6 +234,15 @@ hipError_t launch_backward(int bf16, int D, int MP, int SP, const BwdArgs& a, hi
 
 // Whether a forward kernel exists for (bf16, D, MP, SP).
 bool forward_supported(int bf16, int D, int MP, int SP);
+
+// bla_forward on q, k, v and o with the element strides of FwdArgs: in_strides and
+// out_strides are {batch, head, token} (nullable: contiguous [B, H, L, d]).  Each stride
+// must be a multiple of 8 elements.  Used by the layer to read the projection output and
+// write the head-merged output in place.
+bla_status forward_strided(const bla_params* p, const double* T, const void* q, const void* k, const void* v,
+                           const long long* in_strides, const float* state_k_in, const float* state_v_in, void* o,
+                           const long long* out_strides, float* state_k_out, float* state_v_out, void* workspace,
+                           size_t workspace_bytes, void* stream, void* const* events);
 // Sequence units per workgroup of the bf16 pair kernel (0: the one-unit forward kernel runs).
 int forward_units_per_wg(int bf16, int D, int MP, int SP);
 
