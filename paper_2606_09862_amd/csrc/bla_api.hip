@@ -184,7 +184,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
 struct DecayPlan {
     Plan pl;
     int nseg, seg_len;
-    size_t off_summ, total;
+    size_t off_summ, off_gate, total;
 };
 
 void make_decay_plan(const bla_params* p, DecayPlan* dp)
@@ -215,7 +215,8 @@ void make_decay_plan(const bla_params* p, DecayPlan* dp)
     dp->nseg = nseg;
     dp->seg_len = seg_len;
     dp->off_summ = align_up(dp->pl.total);
-    dp->total = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
+    dp->off_gate = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
+    dp->total = dp->off_gate + align_up((size_t)p->H * L * SP * sizeof(float));
 }
 
 // Backward: the one-unit tables (conj_tab = 0, score scale folded into A | B), then the
@@ -521,7 +522,6 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     };
     if (!mark(0)) return BLA_ERR_HIP;
     if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
-    if (!mark(1)) return BLA_ERR_HIP;
     DecayArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
@@ -536,6 +536,7 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     a.period = (const double*)(ws + pl.off_period);
     a.rperiod = (const double*)(ws + pl.off_rperiod);
     a.summ = (float*)(ws + dp.off_summ);
+    a.gate = (float*)(ws + dp.off_gate);
     a.B = p->B;
     a.H = p->H;
     a.L = p->L;
@@ -545,6 +546,8 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     a.seg_len = dp.seg_len;
     a.t0 = p->t0;
     a.scale = pl.scale;
+    if (launch_decay_gates(pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;
+    if (!mark(1)) return BLA_ERR_HIP;
     if (launch_decay_forward(pl.bf16, pl.D, pl.SP, a, s, events ? events + 2 : nullptr) != hipSuccess)
         return BLA_ERR_HIP;
     return BLA_OK;

@@ -93,6 +93,34 @@ __device__ __forceinline__ float dirichlet_at(double fx, int s, double rS, int N
 // Floats of one segment summary: K~ [SP][D], V~ [SP][D], gate product [SP].
 template <int D, int SP> constexpr size_t decay_summary_floats() { return (size_t)2 * SP * D + SP; }
 
+// Gate of slot s (s < S) at absolute position P: the interpolation weight D_M(P - tau_s) of
+// Eq. compressed_simplified, with the phase f = (P - tau_s) / T reduced to (-1/2, 1/2] in
+// double (P / T first, so that a position far past the period keeps a small one's accuracy)
+// and the ratio sin(N pi f) / (N sin(pi f)) evaluated in float32 (D_M(0) = 1).
+__device__ __forceinline__ float decay_gate(long long P, int s, double rT, double rS, int N)
+{
+    const double x = (double)P * rT;
+    double fd = (x - floor(x)) - (double)s * rS;
+    fd -= rint(fd);
+    double ad = (double)N * fd;
+    ad -= 2.0 * rint(0.5 * ad);
+    const float den = sinpi_half((float)fd);
+    return den == 0.f ? 1.f : sinpi_one((float)ad) * (1.f / (float)N) * __builtin_amdgcn_rcpf(den);
+}
+
+// The gate table of one forward call: gate[h][t][s] = g_{t0 + t}[s] for t < L, 0 for the
+// padded slots s >= S.  The gates depend on the head's period and the position only, so
+// every batch row of a head reads the same table.
+// Grid: (ceil(L SP / 256), H); SP is a power of two, rS = 1 / S.
+__global__ __launch_bounds__(256) void decay_gate_kernel(DecayArgs a, int SP, double rS)
+{
+    const int h = blockIdx.y;
+    const unsigned i = blockIdx.x * 256u + threadIdx.x;  // t SP + s within the head
+    if (i >= (unsigned)a.L * (unsigned)SP) return;
+    const int s = (int)(i & (unsigned)(SP - 1)), t = (int)(i / (unsigned)SP);
+    a.gate[(size_t)h * a.L * SP + i] = s < a.S ? decay_gate(a.t0 + t, s, a.rperiod[h], rS, 2 * a.M - 1) : 0.f;
+}
+
 template <typename T, int D, int SP, bool SUM>
 __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(DecayArgs a)
 {
@@ -121,8 +149,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     const int s0w = 16 * NSTW * wv;  // first slot of the wave
     const int S = a.S, L = a.L;
     const int tbeg = seg * a.seg_len, tend = min(L, tbeg + a.seg_len);
-    const int N = 2 * a.M - 1;
-    const double rT = a.rperiod[h], rS = 1.0 / (double)S;
+    const float* gh = a.gate + (size_t)h * L * SP;  // the head's gate table [L][SP]
     const T* qb = (const T*)a.q + (size_t)bh * L * D;
     const T* kb_ = (const T*)a.k + (size_t)bh * L * D;
     const T* vb = (const T*)a.v + (size_t)bh * L * D;
@@ -216,7 +243,29 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         }
     };
 
-    if (tbeg < tend) stage_load(tbeg, min(16, tend - tbeg));
+    // gates of the next sub-block's first 16 tokens, loaded a sub-block ahead
+    float gpf[NSTW][4];
+    auto gate_load = [&](int t0s) {
+#pragma unroll
+        for (int t = 0; t < NSTW; ++t)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) gpf[t][e] = gh[(size_t)min(t0s + 4 * g + e, L - 1) * SP + s0w + 16 * t + r];
+    };
+    // query rows of the next sub-block (columns: tokens), loaded a sub-block ahead; rows past
+    // the sub-block's cut are other tokens of the sequence, whose columns are never stored
+    F qpf[SUM ? 1 : KBD];
+    auto q_load = [&](int t0s) {
+        if constexpr (!SUM) {
+            const int qrow = min(t0s + r, L - 1);
+#pragma unroll
+            for (int kb = 0; kb < KBD; ++kb) qpf[kb] = ld_frag<T>(qb + (size_t)qrow * D, 32 * kb, g);
+        }
+    };
+    if (tbeg < tend) {
+        stage_load(tbeg, min(16, tend - tbeg));
+        gate_load(tbeg);
+        q_load(tbeg);
+    }
     float aprod[NSTW];  // product of the segment's gates for the K~^T column slot (summaries)
 #pragma unroll
     for (int t = 0; t < NSTW; ++t) aprod[t] = 1.f;
@@ -228,35 +277,24 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     for (int tb = tbeg; tb < tend;) {
         const long long P = a.t0 + tb;  // absolute position of the sub-block's first token
         const int cmax = min(16, tend - tb);
+        F qf[SUM ? 1 : KBD];
+#pragma unroll
+        for (int kb = 0; kb < (SUM ? 0 : KBD); ++kb) qf[kb] = qpf[kb];
 
         // ---- gates in the G layout: lane (g, r) holds slot s0w + 16 t + r, tokens 4g..4g+3
         float gt[NSTW][4], al[NSTW][4];
         int cw = 16;
         {
-            // phase in revolutions of the lane's first token, reduced in double; each token's
-            // f and N f are formed in double from it and rounded once, so the numerator and
-            // the denominator of the ratio carry the same f
-            const double x0 = (double)(P + 4 * g) * rT;
-            const double fx0 = x0 - floor(x0);
-            const float rN = 1.f / (float)N;
 #pragma unroll
             for (int t = 0; t < NSTW; ++t) {
-                const int s = s0w + 16 * t + r;
-                const double fb = fx0 - (double)s * rS;
                 float lg[4];
                 float run = 0.f;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const bool valid = 4 * g + e < cmax && s < S;
-                    double fd = fb + (double)e * rT;
-                    fd -= rint(fd);
-                    double ad = (double)N * fd;
-                    ad -= 2.0 * rint(0.5 * ad);
-                    const float f = (float)fd, aa = (float)ad;
-                    const float den = sinpi_half(f);
-                    const float dv = den == 0.f ? 1.f : sinpi_one(aa) * rN * __builtin_amdgcn_rcpf(den);
-                    gt[t][e] = valid ? dv : 0.f;
-                    al[t][e] = valid ? fmaxf(1.f - gt[t][e], kDecayEps) : 1.f;
+                    const bool valid = 4 * g + e < cmax;
+                    const float gv = gpf[t][e];
+                    gt[t][e] = valid ? gv : 0.f;
+                    al[t][e] = valid ? fmaxf(1.f - gv, kDecayEps) : 1.f;
                     run += __log2f(al[t][e]);
                     lg[e] = run;
                 }
@@ -287,7 +325,11 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         cs = max(1, min(cs, cmax));
         stage_store(cs);
         __syncthreads();  // K, V visible
-        if (tb + cs < tend) stage_load(tb + cs, min(16, tend - tb - cs));
+        if (tb + cs < tend) {
+            stage_load(tb + cs, min(16, tend - tb - cs));
+            gate_load(tb + cs);
+            q_load(tb + cs);
+        }
 
         // ---- E and Bq of the sub-block's cs tokens (tokens past cs: gate 0, factor 1)
         float bq[NSTW][4];
@@ -335,12 +377,6 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         }
 
         if constexpr (!SUM) {
-        // ---- Q fragments (columns: tokens) straight from global memory
-        const int qrow = tb + min(r, cs - 1);
-        F qf[KBD];
-#pragma unroll
-        for (int kb = 0; kb < KBD; ++kb) qf[kb] = ld_frag<T>(qb + (size_t)qrow * D, 32 * kb, g);
-
         // G^T = K Q^T (keys j rows, queries i columns), causal
         floatx4 gT = zero4();
         {
@@ -673,6 +709,16 @@ static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s, void
     BLA_DECAY_SP(256)
 #undef BLA_DECAY_SP
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_decay_gates(int SP, const DecayArgs& a, hipStream_t s)
+{
+    const long long n = (long long)a.L * SP;  // per head; L SP < 2^32 (L < 2^31, SP <= 256 -> checked)
+    if (n == 0 || a.H == 0) return hipSuccess;
+    if (n >= (1ll << 32) || (SP & (SP - 1))) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(decay_gate_kernel, dim3((unsigned)((n + 255) / 256), (unsigned)a.H), dim3(256), 0, s, a, SP,
+                       1.0 / (double)a.S);
+    return hipGetLastError();
 }
 
 hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s, void* const* ev)

@@ -128,6 +128,7 @@ struct DecayArgs {
     const double* period;   // [H] clamped period T
     const double* rperiod;  // [H] 1 / T
     float* summ;            // [B*H][nseg-1] segment summaries, scanned in place into entering states
+    float* gate;            // [H][L][SP] gates g_t[s] at the call's positions (0 for padded slots)
     int B, H, L, M, S;
     int nseg, seg_len;      // segments per sequence and their length (a multiple of 16 tokens)
     long long t0;
@@ -226,6 +227,8 @@ hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
 hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s,
                                 void* const* events);
 hipError_t launch_decay_step(int bf16_io, int D, int SP, const DecayStepArgs& a, hipStream_t s);
+// The gate table of a decay forward call (a.gate): H L SP values, shared by every batch row.
+hipError_t launch_decay_gates(int SP, const DecayArgs& a, hipStream_t s);
 
 // Backward passes: forward summaries of every segment, adjoint summaries (segments 1..),
 // and the reverse walk.  events[0..2] (nullable) are recorded after each pass.
