@@ -184,7 +184,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
 struct DecayPlan {
     Plan pl;
     int nseg, seg_len;
-    size_t off_summ, off_gate, total;
+    size_t off_summ, off_gmap, off_gate, total;
 };
 
 void make_decay_plan(const bla_params* p, DecayPlan* dp)
@@ -215,8 +215,9 @@ void make_decay_plan(const bla_params* p, DecayPlan* dp)
     dp->nseg = nseg;
     dp->seg_len = seg_len;
     dp->off_summ = align_up(dp->pl.total);
-    dp->off_gate = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
-    dp->total = dp->off_gate + align_up((size_t)p->H * L * SP * sizeof(float));
+    dp->off_gmap = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
+    dp->off_gate = dp->off_gmap + align_up((size_t)p->H * sizeof(int));
+    dp->total = dp->off_gate + align_up((size_t)p->H * L * SP * sizeof(float));  // at most one table per head
 }
 
 // Backward: the one-unit tables (conj_tab = 0, score scale folded into A | B), then the
@@ -537,6 +538,7 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     a.rperiod = (const double*)(ws + pl.off_rperiod);
     a.summ = (float*)(ws + dp.off_summ);
     a.gate = (float*)(ws + dp.off_gate);
+    a.gmap = (const int*)(ws + dp.off_gmap);
     a.B = p->B;
     a.H = p->H;
     a.L = p->L;
@@ -546,7 +548,40 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     a.seg_len = dp.seg_len;
     a.t0 = p->t0;
     a.scale = pl.scale;
-    if (launch_decay_gates(pl.SP, a, s) != hipSuccess) return BLA_ERR_HIP;
+    // gate tables: one per distinct clamped period within each group of heads
+    {
+        int ubase = 0;
+        for (int h0 = 0; h0 < p->H; h0 += kMaxHeadsPerTableLaunch) {
+            GateArgs g;
+            memset(&g, 0, sizeof(g));
+            g.gate = a.gate;
+            g.gmap = (int*)(ws + dp.off_gmap);
+            g.L = p->L;
+            g.SP = pl.SP;
+            g.S = p->S;
+            g.M = p->M;
+            g.h0 = h0;
+            g.nh = p->H - h0 < kMaxHeadsPerTableLaunch ? p->H - h0 : kMaxHeadsPerTableLaunch;
+            g.ubase = ubase;
+            g.t0 = p->t0;
+            g.rS = 1.0 / (double)p->S;
+            double per[kMaxHeadsPerTableLaunch];
+            for (int i = 0; i < g.nh; ++i) {
+                const double tmin = 2.0 * p->M - 1.0;
+                const double Tp = T[h0 + i] < tmin ? tmin : T[h0 + i];  // clamped as the tables kernel does
+                int u = 0;
+                while (u < g.nu && per[u] != Tp) ++u;
+                if (u == g.nu) {
+                    per[g.nu] = Tp;
+                    g.rT[g.nu] = 1.0 / Tp;
+                    ++g.nu;
+                }
+                g.map[i] = ubase + u;
+            }
+            if (launch_decay_gates(g, s) != hipSuccess) return BLA_ERR_HIP;
+            ubase += g.nu;
+        }
+    }
     if (!mark(1)) return BLA_ERR_HIP;
     if (launch_decay_forward(pl.bf16, pl.D, pl.SP, a, s, events ? events + 2 : nullptr) != hipSuccess)
         return BLA_ERR_HIP;

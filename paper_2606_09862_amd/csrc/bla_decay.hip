@@ -108,17 +108,20 @@ __device__ __forceinline__ float decay_gate(long long P, int s, double rT, doubl
     return den == 0.f ? 1.f : sinpi_one((float)ad) * (1.f / (float)N) * __builtin_amdgcn_rcpf(den);
 }
 
-// The gate table of one forward call: gate[h][t][s] = g_{t0 + t}[s] for t < L, 0 for the
-// padded slots s >= S.  The gates depend on the head's period and the position only, so
-// every batch row of a head reads the same table.
-// Grid: (ceil(L SP / 256), H); SP is a power of two, rS = 1 / S.
-__global__ __launch_bounds__(256) void decay_gate_kernel(DecayArgs a, int SP, double rS)
+// The gate tables of one forward call: gate[u][t][s] = g_{t0 + t}[s] of period u for t < L,
+// 0 for the padded slots s >= S.  The gates depend on the period and the position only, so
+// every batch row, and every head of one period, reads the same table.  Grid:
+// (ceil(L SP / 256), nu); SP is a power of two.  Block (0, 0) also writes the head map.
+__global__ __launch_bounds__(256) void decay_gate_kernel(GateArgs a)
 {
-    const int h = blockIdx.y;
-    const unsigned i = blockIdx.x * 256u + threadIdx.x;  // t SP + s within the head
-    if (i >= (unsigned)a.L * (unsigned)SP) return;
-    const int s = (int)(i & (unsigned)(SP - 1)), t = (int)(i / (unsigned)SP);
-    a.gate[(size_t)h * a.L * SP + i] = s < a.S ? decay_gate(a.t0 + t, s, a.rperiod[h], rS, 2 * a.M - 1) : 0.f;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < (unsigned)a.nh)
+        a.gmap[a.h0 + threadIdx.x] = a.map[threadIdx.x];
+    const int u = blockIdx.y;
+    const unsigned i = blockIdx.x * 256u + threadIdx.x;  // t SP + s within the table
+    if (i >= (unsigned)a.L * (unsigned)a.SP) return;
+    const int s = (int)(i & (unsigned)(a.SP - 1)), t = (int)(i / (unsigned)a.SP);
+    a.gate[(size_t)(a.ubase + u) * a.L * a.SP + i] =
+        s < a.S ? decay_gate(a.t0 + t, s, a.rT[u], a.rS, 2 * a.M - 1) : 0.f;
 }
 
 template <typename T, int D, int SP, bool SUM>
@@ -138,7 +141,8 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     __shared__ __attribute__((aligned(16))) int sTheta[SP];
     __shared__ float sRed[2][NWU][16];
     __shared__ int sCut[NWU];
-    __shared__ __attribute__((aligned(16))) float sO[NWU > 1 ? NWU * D * 16 : 4];
+    constexpr int LO = D + 4;  // sO row stride (floats)
+    __shared__ __attribute__((aligned(16))) float sO[NWU > 1 ? NWU * 16 * LO : 4];
 
     const int tid = threadIdx.x;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -149,7 +153,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     const int s0w = 16 * NSTW * wv;  // first slot of the wave
     const int S = a.S, L = a.L;
     const int tbeg = seg * a.seg_len, tend = min(L, tbeg + a.seg_len);
-    const float* gh = a.gate + (size_t)h * L * SP;  // the head's gate table [L][SP]
+    const float* gh = a.gate + (size_t)a.gmap[h] * L * SP;  // the head's gate table [L][SP]
     const T* qb = (const T*)a.q + (size_t)bh * L * D;
     const T* kb_ = (const T*)a.k + (size_t)bh * L * D;
     const T* vb = (const T*)a.v + (size_t)bh * L * D;
@@ -356,7 +360,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const float E = excl * ex[e];
-                bq[t][e] = gt[t][e] / E;
+                bq[t][e] = gt[t][e] * __builtin_amdgcn_rcpf(E);  // E >= 2^-100: a normal float
                 sE[(4 * g + e) * LG + s] = E;
                 sB[(4 * g + e) * LG + s] = bq[t][e];
             }
@@ -485,18 +489,25 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
                 for (int dt = 0; dt < NDT; ++dt) st4<T>(ob + (size_t)(tb + r) * D + 16 * dt + 4 * g, oT[dt]);
             }
         } else {
-            // partial outputs of every wave through LDS: sO[w][d][token]
+            // partial outputs of every wave through LDS: sO[w][token][d]; then each thread
+            // sums eight consecutive d of one token over the waves and stores them at once
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) sO[((size_t)wv * D + 16 * dt + 4 * g + e) * 16 + r] = oT[dt][e];
+            for (int dt = 0; dt < NDT; ++dt) st4f(sO + ((size_t)wv * 16 + r) * LO + 16 * dt + 4 * g, oT[dt]);
             __syncthreads();
-            for (int u = tid; u < 16 * D; u += NTH) {
-                const int tok = u / D, d = u % D;
-                float acc = 0.f;
+            constexpr int P8 = 16 * D / 8;  // 8-element pieces of the sub-block's output
+            for (int u = tid; u < P8; u += NTH) {
+                const int tok = u / (D / 8), d0 = 8 * (u % (D / 8));
+                floatx4 lo = zero4(), hi = zero4();
 #pragma unroll
-                for (int w = 0; w < NWU; ++w) acc += sO[((size_t)w * D + d) * 16 + tok];
-                if (tok < cs) ob[(size_t)(tb + tok) * D + d] = (T)acc;
+                for (int w = 0; w < NWU; ++w) {
+                    lo += ld4f(sO + ((size_t)w * 16 + tok) * LO + d0);
+                    hi += ld4f(sO + ((size_t)w * 16 + tok) * LO + d0 + 4);
+                }
+                if (tok < cs) {
+                    T* dst = ob + (size_t)(tb + tok) * D + d0;
+                    st4<T>(dst, lo);
+                    st4<T>(dst + 4, hi);
+                }
             }
         }
         }  // !SUM
@@ -711,13 +722,13 @@ static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s, void
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_decay_gates(int SP, const DecayArgs& a, hipStream_t s)
+hipError_t launch_decay_gates(const GateArgs& g, hipStream_t s)
 {
-    const long long n = (long long)a.L * SP;  // per head; L SP < 2^32 (L < 2^31, SP <= 256 -> checked)
-    if (n == 0 || a.H == 0) return hipSuccess;
-    if (n >= (1ll << 32) || (SP & (SP - 1))) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(decay_gate_kernel, dim3((unsigned)((n + 255) / 256), (unsigned)a.H), dim3(256), 0, s, a, SP,
-                       1.0 / (double)a.S);
+    const long long n = (long long)g.L * g.SP;  // per table
+    if (n == 0 || g.nu == 0) return hipSuccess;
+    if (n >= (1ll << 32) || (g.SP & (g.SP - 1)) || g.nh > kMaxHeadsPerTableLaunch || g.nu > g.nh)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(decay_gate_kernel, dim3((unsigned)((n + 255) / 256), (unsigned)g.nu), dim3(256), 0, s, g);
     return hipGetLastError();
 }
 

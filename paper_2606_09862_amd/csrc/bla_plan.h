@@ -128,7 +128,8 @@ struct DecayArgs {
     const double* period;   // [H] clamped period T
     const double* rperiod;  // [H] 1 / T
     float* summ;            // [B*H][nseg-1] segment summaries, scanned in place into entering states
-    float* gate;            // [H][L][SP] gates g_t[s] at the call's positions (0 for padded slots)
+    float* gate;            // [U][L][SP] gates g_t[s] at the call's positions (0 for padded slots)
+    const int* gmap;        // [H] head -> its gate table (heads with one period share a table)
     int B, H, L, M, S;
     int nseg, seg_len;      // segments per sequence and their length (a multiple of 16 tokens)
     long long t0;
@@ -227,8 +228,18 @@ hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
 hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s,
                                 void* const* events);
 hipError_t launch_decay_step(int bf16_io, int D, int SP, const DecayStepArgs& a, hipStream_t s);
-// The gate table of a decay forward call (a.gate): H L SP values, shared by every batch row.
-hipError_t launch_decay_gates(int SP, const DecayArgs& a, hipStream_t s);
+// The gate tables of a decay forward call: one [L][SP] table per distinct period, shared by
+// every batch row and every head of that period, and the head map.
+struct GateArgs {
+    float* gate;  // tables ubase .. ubase + nu - 1 of [L][SP] each
+    int* gmap;    // [H]; entries h0 .. h0 + nh - 1 written from map
+    int L, SP, S, M, h0, nh, ubase, nu;
+    long long t0;
+    double rS;                                 // 1 / S
+    double rT[kMaxHeadsPerTableLaunch];        // 1 / T of table ubase + u
+    int map[kMaxHeadsPerTableLaunch];          // table of head h0 + i
+};
+hipError_t launch_decay_gates(const GateArgs& g, hipStream_t s);
 
 // Backward passes: forward summaries of every segment, adjoint summaries (segments 1..),
 // and the reverse walk.  events[0..2] (nullable) are recorded after each pass.

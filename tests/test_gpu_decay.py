@@ -48,6 +48,17 @@ def test_decay_small_shapes(dtype, B, H, L, d, M, S, T, t0):
     run_decay(q, k, v, T, M, S, dtype, t0=t0, label=f"{B}x{H}x{L}x{d}")
 
 
+def test_decay_many_heads_shared_periods():
+    """70 heads whose clamped periods repeat (heads of one period share a gate table; more
+    than 64 heads take two table launches), including a period below 2M-1 that clamps onto
+    another head's."""
+    B, H, L, d, M, S = 2, 70, 45, 32, 4, 7
+    base = (7.0, 14.0, 9.5, 3.0)  # 3.0 clamps to 2M-1 = 7, the first period
+    T = tuple(base[h % 4] if h != 66 else 11.25 for h in range(H))
+    q, k, v = gauss(L + H, B, H, L, d, torch.float32)
+    run_decay(q, k, v, T, M, S, torch.float32, t0=13, label=f"{B}x{H}x{L}x{d} shared periods")
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_decay_is_sliding_window_on_the_gpu(dtype):
     """T = S = 2M-1 (Sec. 3.4): the GPU decay form equals sliding-window attention with
