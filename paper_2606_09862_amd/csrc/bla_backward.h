@@ -85,8 +85,8 @@ __device__ __forceinline__ void bstage_load(BStage<T, D, NTEN>& st, const T* con
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int row = min(4 * tq + t, c - 1);
-                st.x[i][t][0] = ld4<T>(base + (size_t)row * D);
-                st.x[i][t][1] = ld4<T>(base + (size_t)row * D + 4);
+                st.x[i][t][0] = ld_global<typename Frag<T>::half>(base + (size_t)row * D);
+                st.x[i][t][1] = ld_global<typename Frag<T>::half>(base + (size_t)row * D + 4);
             }
         }
     }
@@ -115,8 +115,8 @@ __device__ __forceinline__ void bstage_store(const BStage<T, D, NTEN>& st, T* co
                 T* rd = rowdst[ten] + 8 * dq;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    *reinterpret_cast<H*>(rd + (size_t)(4 * tq + t) * ldq) = x[t][0];
-                    *reinterpret_cast<H*>(rd + (size_t)(4 * tq + t) * ldq + 4) = x[t][1];
+                    st_lds<H>(rd + (size_t)(4 * tq + t) * ldq, x[t][0]);
+                    st_lds<H>(rd + (size_t)(4 * tq + t) * ldq + 4, x[t][1]);
                 }
             }
             T* td = trdst[ten] + (size_t)(8 * dq) * ldk + 4 * tq;
@@ -124,8 +124,8 @@ __device__ __forceinline__ void bstage_store(const BStage<T, D, NTEN>& st, T* co
             for (int e = 0; e < 4; ++e) {
                 H lo{x[0][0][e], x[1][0][e], x[2][0][e], x[3][0][e]};
                 H hi{x[0][1][e], x[1][1][e], x[2][1][e], x[3][1][e]};
-                *reinterpret_cast<H*>(td + (size_t)e * ldk) = lo;
-                *reinterpret_cast<H*>(td + (size_t)(e + 4) * ldk) = hi;
+                st_lds<H>(td + (size_t)e * ldk, lo);
+                st_lds<H>(td + (size_t)(e + 4) * ldk, hi);
             }
         }
     }

@@ -70,8 +70,8 @@ __device__ __forceinline__ void bstage_store_rows(const BStage<bf16, D, NTEN>& s
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const bool ok = 4 * tq + t < c;
-                *reinterpret_cast<H*>(rd + (size_t)(4 * tq + t) * ld) = ok ? st.x[i][t][0] : z;
-                *reinterpret_cast<H*>(rd + (size_t)(4 * tq + t) * ld + 4) = ok ? st.x[i][t][1] : z;
+                st_lds<H>(rd + (size_t)(4 * tq + t) * ld, ok ? st.x[i][t][0] : z);
+                st_lds<H>(rd + (size_t)(4 * tq + t) * ld + 4, ok ? st.x[i][t][1] : z);
             }
         }
     }

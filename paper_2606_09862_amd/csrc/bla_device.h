@@ -56,6 +56,19 @@ template <typename P> __device__ __forceinline__ const P* opaque(const P* p)
     return p;
 }
 
+// Stores and loads through a generic pointer that is known to address LDS (or global
+// memory): the explicit address space gives ds_write / global_load instructions instead of
+// flat ones (a flat access counts against both the LDS and the memory wait counters, so
+// each wait for one waits for the other as well).
+template <typename V, typename P> __device__ __forceinline__ void st_lds(P* p, V x)
+{
+    *(__attribute__((address_space(3))) V*)p = x;
+}
+template <typename V, typename P> __device__ __forceinline__ V ld_global(const P* p)
+{
+    return *(const __attribute__((address_space(1))) V*)p;
+}
+
 template <typename T> __device__ __forceinline__ typename Frag<T>::type zero_frag()
 {
     typename Frag<T>::type f;
