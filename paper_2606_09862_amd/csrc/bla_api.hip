@@ -184,7 +184,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
 struct DecayPlan {
     Plan pl;
     int nseg, seg_len;
-    size_t off_summ, off_gmap, off_gate, total;
+    size_t off_summ, off_gmap, off_glen, off_gE, off_gB, total;
 };
 
 void make_decay_plan(const bla_params* p, DecayPlan* dp)
@@ -215,9 +215,13 @@ void make_decay_plan(const bla_params* p, DecayPlan* dp)
     dp->nseg = nseg;
     dp->seg_len = seg_len;
     dp->off_summ = align_up(dp->pl.total);
+    // sub-block schedules: at most one per head
+    const size_t HL = (size_t)(p->H > 0 ? p->H : 0) * L;
     dp->off_gmap = dp->off_summ + align_up((size_t)units * (nseg - 1) * sf_bytes);
-    dp->off_gate = dp->off_gmap + align_up((size_t)p->H * sizeof(int));
-    dp->total = dp->off_gate + align_up((size_t)p->H * L * SP * sizeof(float));  // at most one table per head
+    dp->off_glen = dp->off_gmap + align_up((size_t)(p->H > 0 ? p->H : 0) * sizeof(int));
+    dp->off_gE = dp->off_glen + align_up(HL * sizeof(int));
+    dp->off_gB = dp->off_gE + align_up(HL * SP * sizeof(float));
+    dp->total = dp->off_gB + align_up(HL * SP * sizeof(float));
 }
 
 // Backward: the one-unit tables (conj_tab = 0, score scale folded into A | B), then the
@@ -537,7 +541,9 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     a.period = (const double*)(ws + pl.off_period);
     a.rperiod = (const double*)(ws + pl.off_rperiod);
     a.summ = (float*)(ws + dp.off_summ);
-    a.gate = (float*)(ws + dp.off_gate);
+    a.gE = (const float*)(ws + dp.off_gE);
+    a.gB = (const float*)(ws + dp.off_gB);
+    a.glen = (const int*)(ws + dp.off_glen);
     a.gmap = (const int*)(ws + dp.off_gmap);
     a.B = p->B;
     a.H = p->H;
@@ -548,13 +554,15 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
     a.seg_len = dp.seg_len;
     a.t0 = p->t0;
     a.scale = pl.scale;
-    // gate tables: one per distinct clamped period within each group of heads
+    // sub-block schedules: one per distinct clamped period within each group of heads
     {
         int ubase = 0;
         for (int h0 = 0; h0 < p->H; h0 += kMaxHeadsPerTableLaunch) {
             GateArgs g;
             memset(&g, 0, sizeof(g));
-            g.gate = a.gate;
+            g.gE = (float*)(ws + dp.off_gE);
+            g.gB = (float*)(ws + dp.off_gB);
+            g.glen = (int*)(ws + dp.off_glen);
             g.gmap = (int*)(ws + dp.off_gmap);
             g.L = p->L;
             g.SP = pl.SP;

@@ -13,10 +13,12 @@
 //     O^T  = V~_b^T (P o E)^T + V^T tril(Bq (P o E)^T)
 //     K~  <- E_{c-1} o (K~_b + Bq^T K),  V~ likewise.
 // A gate is clamped at eps = 2^-40 where the decay flushes a slot (a = 0); the flushed
-// state then survives with weight eps instead of 0.  A sub-block ends before any slot's
-// gate product drops below 2^-100, so E and 1/E stay inside the float32 (and bf16) range;
-// the lengths depend on positions only (16 tokens unless many small gates follow each
-// other, as when M is small against T).
+// state then survives with weight eps instead of 0.  Sub-blocks never cross a 16-token
+// window of the sequence, and one ends before any slot's gate product drops below 2^-100,
+// so E and 1/E stay inside the float32 (and bf16) range; the lengths depend on positions
+// only (a whole window unless many small gates follow each other, as when M is small
+// against T).  The gates, the sub-block lengths, E and Bq are the same for every batch row
+// and every head of one period: decay_sched_kernel computes them once per call.
 //
 // Sequences are split into segments run by separate workgroups.  The recurrence is linear
 // with data-independent gates, so a segment maps its entering state X to A_g o X + S_g:
@@ -108,20 +110,74 @@ __device__ __forceinline__ float decay_gate(long long P, int s, double rT, doubl
     return den == 0.f ? 1.f : sinpi_one((float)ad) * (1.f / (float)N) * __builtin_amdgcn_rcpf(den);
 }
 
-// The gate tables of one forward call: gate[u][t][s] = g_{t0 + t}[s] of period u for t < L,
-// 0 for the padded slots s >= S.  The gates depend on the period and the position only, so
-// every batch row, and every head of one period, reads the same table.  Grid:
-// (ceil(L SP / 256), nu); SP is a power of two.  Block (0, 0) also writes the head map.
-__global__ __launch_bounds__(256) void decay_gate_kernel(GateArgs a)
+// The sub-block schedule of one forward call for period u and one 16-token window of the
+// sequence (tokens w0 .. w0 + 15): the gates g_t[s] of Eq. compressed_simplified, the
+// sub-blocks (greedy from the window start: each ends before any slot's product of
+// a = max(1 - g, eps) falls below 2^-100, and takes at least one token), and per token the
+// product E of a over its sub-block so far and Bq = g / E.  One workgroup of 256 threads per
+// (window, period): all threads evaluate the window's gates into LDS, then wave 0 walks the
+// sub-blocks with lane l holding slots l, l + 64, ...  Block (0, 0) also writes the head map.
+template <int SPL>  // slots per lane: max(1, SP / 64)
+__global__ __launch_bounds__(256) void decay_sched_kernel(GateArgs a)
 {
+    constexpr int MAXSPL = SPL;
+    __shared__ float sg[16 * 64 * SPL];
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < (unsigned)a.nh)
         a.gmap[a.h0 + threadIdx.x] = a.map[threadIdx.x];
-    const int u = blockIdx.y;
-    const unsigned i = blockIdx.x * 256u + threadIdx.x;  // t SP + s within the table
-    if (i >= (unsigned)a.L * (unsigned)a.SP) return;
-    const int s = (int)(i & (unsigned)(a.SP - 1)), t = (int)(i / (unsigned)a.SP);
-    a.gate[(size_t)(a.ubase + u) * a.L * a.SP + i] =
-        s < a.S ? decay_gate(a.t0 + t, s, a.rT[u], a.rS, 2 * a.M - 1) : 0.f;
+    const int u = blockIdx.y, w0 = 16 * blockIdx.x, tid = threadIdx.x;
+    const int nt = min(16, a.L - w0);
+    const int N = 2 * a.M - 1;
+    const double rT = a.rT[u];
+    for (int x = tid; x < 16 * a.SP; x += 256) {
+        const int i = x / a.SP, s = x % a.SP;
+        sg[x] = (i < nt && s < a.S) ? decay_gate(a.t0 + w0 + i, s, rT, a.rS, N) : 0.f;
+    }
+    __syncthreads();
+    if (tid >= 64) return;
+    const int lane = tid;
+    const size_t row0 = (size_t)(a.ubase + u) * a.L + w0;  // table row of the window's first token
+    float gv[16][MAXSPL];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int k = 0; k < MAXSPL; ++k) {
+            const int s = lane + 64 * k;
+            gv[i][k] = s < a.SP ? sg[i * a.SP + s] : 0.f;
+        }
+    for (int i0 = 0; i0 < nt;) {
+        // first token of [i0, nt) whose prefix (from i0) of log2 a drops below -100
+        int cut = nt;
+#pragma unroll
+        for (int k = 0; k < MAXSPL; ++k) {
+            float lg = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                if (i >= i0 && i < nt) {
+                    lg += __log2f(fmaxf(1.f - gv[i][k], kDecayEps));
+                    if (lg < -100.f) cut = min(cut, i);
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) cut = min(cut, __shfl_xor(cut, off));
+        const int cs = max(1, cut - i0);
+#pragma unroll
+        for (int k = 0; k < MAXSPL; ++k) {
+            const int s = lane + 64 * k;
+            float run = 1.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                if (i >= i0 && i < i0 + cs && s < a.SP) {
+                    run *= fmaxf(1.f - gv[i][k], kDecayEps);
+                    const size_t idx = (row0 + i) * a.SP + s;
+                    a.gE[idx] = run;
+                    a.gB[idx] = gv[i][k] * __builtin_amdgcn_rcpf(run);  // run >= 2^-100: a normal float
+                }
+            }
+        }
+        if (lane == 0) a.glen[row0 + i0] = cs;
+        i0 += cs;
+    }
 }
 
 template <typename T, int D, int SP, bool SUM>
@@ -140,7 +196,6 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     __shared__ __attribute__((aligned(16))) float sB[16 * LG];
     __shared__ __attribute__((aligned(16))) int sTheta[SP];
     __shared__ float sRed[2][NWU][16];
-    __shared__ int sCut[NWU];
     constexpr int LO = D + 4;  // sO row stride (floats)
     __shared__ __attribute__((aligned(16))) float sO[NWU > 1 ? NWU * 16 * LO : 4];
 
@@ -153,7 +208,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     const int s0w = 16 * NSTW * wv;  // first slot of the wave
     const int S = a.S, L = a.L;
     const int tbeg = seg * a.seg_len, tend = min(L, tbeg + a.seg_len);
-    const float* gh = a.gate + (size_t)a.gmap[h] * L * SP;  // the head's gate table [L][SP]
+    const size_t grow = (size_t)a.gmap[h] * L;  // the head's schedule: rows grow + t of [L][SP]
     const T* qb = (const T*)a.q + (size_t)bh * L * D;
     const T* kb_ = (const T*)a.k + (size_t)bh * L * D;
     const T* vb = (const T*)a.v + (size_t)bh * L * D;
@@ -247,13 +302,20 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         }
     };
 
-    // gates of the next sub-block's first 16 tokens, loaded a sub-block ahead
-    float gpf[NSTW][4];
-    auto gate_load = [&](int t0s) {
+    // schedule of the next sub-block (length, E and Bq of its first 16 tokens in the G
+    // layout), loaded a sub-block ahead
+    int lpf = 1;
+    float Epf[NSTW][4], Bpf[NSTW][4];
+    auto sched_load = [&](int t0s) {
+        lpf = a.glen[grow + t0s];
 #pragma unroll
         for (int t = 0; t < NSTW; ++t)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) gpf[t][e] = gh[(size_t)min(t0s + 4 * g + e, L - 1) * SP + s0w + 16 * t + r];
+            for (int e = 0; e < 4; ++e) {
+                const size_t idx = (grow + min(t0s + 4 * g + e, L - 1)) * SP + s0w + 16 * t + r;
+                Epf[t][e] = a.gE[idx];
+                Bpf[t][e] = a.gB[idx];
+            }
     };
     // query rows of the next sub-block (columns: tokens), loaded a sub-block ahead; rows past
     // the sub-block's cut are other tokens of the sequence, whose columns are never stored
@@ -267,7 +329,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     };
     if (tbeg < tend) {
         stage_load(tbeg, min(16, tend - tbeg));
-        gate_load(tbeg);
+        sched_load(tbeg);
         q_load(tbeg);
     }
     float aprod[NSTW];  // product of the segment's gates for the K~^T column slot (summaries)
@@ -275,97 +337,45 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     for (int t = 0; t < NSTW; ++t) aprod[t] = 1.f;
     const float k2 = a.scale * 1.44269504088896341f;
 
-    // The sub-blocks are at most 16 tokens long and end before any slot's gate product
-    // falls below 2^-100 (so E and 1/E stay inside the float32 range); their lengths depend
-    // only on the positions, and at least one token is taken.
+    // Sub-blocks as scheduled (at most 16 tokens, never across a 16-token window); segment
+    // starts are window starts.
     for (int tb = tbeg; tb < tend;) {
         const long long P = a.t0 + tb;  // absolute position of the sub-block's first token
         const int cmax = min(16, tend - tb);
+        const int cs = max(1, min(lpf, cmax));
         F qf[SUM ? 1 : KBD];
 #pragma unroll
         for (int kb = 0; kb < (SUM ? 0 : KBD); ++kb) qf[kb] = qpf[kb];
-
-        // ---- gates in the G layout: lane (g, r) holds slot s0w + 16 t + r, tokens 4g..4g+3
-        float gt[NSTW][4], al[NSTW][4];
-        int cw = 16;
-        {
+        // E and Bq of the sub-block's tokens in the G layout (lane (g, r): slot s0w + 16 t + r,
+        // tokens 4g..4g+3); tokens past cs: factor 1, Bq 0
+        float Ecur[NSTW][4], bq[NSTW][4];
 #pragma unroll
-            for (int t = 0; t < NSTW; ++t) {
-                float lg[4];
-                float run = 0.f;
+        for (int t = 0; t < NSTW; ++t)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const bool valid = 4 * g + e < cmax;
-                    const float gv = gpf[t][e];
-                    gt[t][e] = valid ? gv : 0.f;
-                    al[t][e] = valid ? fmaxf(1.f - gv, kDecayEps) : 1.f;
-                    run += __log2f(al[t][e]);
-                    lg[e] = run;
-                }
-                // inclusive log2 prefix over the lane groups below (tokens 0..4g-1)
-                float inc = lg[3];
-                float up = __shfl(inc, (lane + 48) & 63);  // group g - 1
-                if (g >= 1) inc += up;
-                up = __shfl(inc, (lane + 32) & 63);        // group g - 2
-                if (g >= 2) inc += up;
-                float excl = __shfl(inc, (lane + 48) & 63);
-                if (g == 0) excl = 0.f;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (excl + lg[e] < -100.f) cw = min(cw, 4 * g + e);
+            for (int e = 0; e < 4; ++e) {
+                const bool live = 4 * g + e < cs;
+                Ecur[t][e] = live ? Epf[t][e] : 1.f;
+                bq[t][e] = live ? Bpf[t][e] : 0.f;
             }
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) cw = min(cw, __shfl_xor(cw, off));
-        }
-        if constexpr (NWU > 1) {
-            if (lane == 0) sCut[wv] = cw;
-        }
-        __syncthreads();  // previous sub-block done with the LDS tiles; the cut visible
-        int cs = cw;
-        if constexpr (NWU > 1) {
-#pragma unroll
-            for (int w = 0; w < NWU; ++w) cs = min(cs, sCut[w]);
-        }
-        cs = max(1, min(cs, cmax));
+        __syncthreads();  // previous sub-block done with the LDS tiles
         stage_store(cs);
         __syncthreads();  // K, V visible
         if (tb + cs < tend) {
             stage_load(tb + cs, min(16, tend - tb - cs));
-            gate_load(tb + cs);
+            sched_load(tb + cs);
             q_load(tb + cs);
         }
-
-        // ---- E and Bq of the sub-block's cs tokens (tokens past cs: gate 0, factor 1)
-        float bq[NSTW][4];
+        // the sub-block's E and Bq rows in LDS, each wave on its own slots (read below only by
+        // the wave that wrote them)
 #pragma unroll
         for (int t = 0; t < NSTW; ++t) {
             const int s = s0w + 16 * t + r;
-            float ex[4];
-            float run = 1.f;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const bool live = 4 * g + e < cs;
-                if (!live) gt[t][e] = 0.f;
-                run *= live ? al[t][e] : 1.f;
-                ex[e] = run;
-            }
-            // exclusive product over the lower lane groups (tokens 0..4g-1)
-            float inc = ex[3];
-            float up = __shfl(inc, (lane + 48) & 63);
-            if (g >= 1) inc *= up;
-            up = __shfl(inc, (lane + 32) & 63);
-            if (g >= 2) inc *= up;
-            float excl = __shfl(inc, (lane + 48) & 63);
-            if (g == 0) excl = 1.f;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float E = excl * ex[e];
-                bq[t][e] = gt[t][e] * __builtin_amdgcn_rcpf(E);  // E >= 2^-100: a normal float
-                sE[(4 * g + e) * LG + s] = E;
+                sE[(4 * g + e) * LG + s] = Ecur[t][e];
                 sB[(4 * g + e) * LG + s] = bq[t][e];
             }
         }
-        // (the gate tables are read below only by the wave that wrote them)
 
         // K^T and V^T fragments (rows: d, reduction: the sub-block's tokens)
         F vtf[NDT], ktf[NDT];
@@ -724,11 +734,15 @@ static hipError_t launch_decay_d(const DecayArgs& a, int SP, hipStream_t s, void
 
 hipError_t launch_decay_gates(const GateArgs& g, hipStream_t s)
 {
-    const long long n = (long long)g.L * g.SP;  // per table
-    if (n == 0 || g.nu == 0) return hipSuccess;
-    if (n >= (1ll << 32) || (g.SP & (g.SP - 1)) || g.nh > kMaxHeadsPerTableLaunch || g.nu > g.nh)
-        return hipErrorInvalidValue;
-    hipLaunchKernelGGL(decay_gate_kernel, dim3((unsigned)((n + 255) / 256), (unsigned)g.nu), dim3(256), 0, s, g);
+    if (g.L <= 0 || g.nu == 0) return hipSuccess;
+    if (g.SP > 256 || g.nh > kMaxHeadsPerTableLaunch || g.nu > g.nh) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((g.L + 15) / 16), (unsigned)g.nu);
+    if (g.SP <= 64)
+        hipLaunchKernelGGL(decay_sched_kernel<1>, grid, dim3(256), 0, s, g);
+    else if (g.SP == 128)
+        hipLaunchKernelGGL(decay_sched_kernel<2>, grid, dim3(256), 0, s, g);
+    else
+        hipLaunchKernelGGL(decay_sched_kernel<4>, grid, dim3(256), 0, s, g);
     return hipGetLastError();
 }
 

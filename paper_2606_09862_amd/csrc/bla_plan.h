@@ -128,8 +128,14 @@ struct DecayArgs {
     const double* period;   // [H] clamped period T
     const double* rperiod;  // [H] 1 / T
     float* summ;            // [B*H][nseg-1] segment summaries, scanned in place into entering states
-    float* gate;            // [U][L][SP] gates g_t[s] at the call's positions (0 for padded slots)
-    const int* gmap;        // [H] head -> its gate table (heads with one period share a table)
+    // Sub-block schedule of the call, per distinct period u (heads map to it through gmap):
+    // sub-blocks never cross a 16-token window of the sequence; glen[u][t] is the length of
+    // the sub-block that starts at token t, gE[u][t][s] the gate product E of token t within
+    // its sub-block and gB[u][t][s] = g_t[s] / E (0 for padded slots).
+    const float* gE;
+    const float* gB;
+    const int* glen;
+    const int* gmap;        // [H] head -> its schedule (heads with one period share one)
     int B, H, L, M, S;
     int nseg, seg_len;      // segments per sequence and their length (a multiple of 16 tokens)
     long long t0;
@@ -228,10 +234,12 @@ hipError_t launch_step(const Plan& p, const StepArgs& a, hipStream_t s);
 hipError_t launch_decay_forward(int bf16_io, int D, int SP, const DecayArgs& a, hipStream_t s,
                                 void* const* events);
 hipError_t launch_decay_step(int bf16_io, int D, int SP, const DecayStepArgs& a, hipStream_t s);
-// The gate tables of a decay forward call: one [L][SP] table per distinct period, shared by
-// every batch row and every head of that period, and the head map.
+// The sub-block schedules of a decay forward call: one per distinct period, shared by every
+// batch row and every head of that period, and the head map.
 struct GateArgs {
-    float* gate;  // tables ubase .. ubase + nu - 1 of [L][SP] each
+    float* gE;    // schedules ubase .. ubase + nu - 1: [L][SP] each
+    float* gB;    // [L][SP] each
+    int* glen;    // [L] each
     int* gmap;    // [H]; entries h0 .. h0 + nh - 1 written from map
     int L, SP, S, M, h0, nh, ubase, nu;
     long long t0;
