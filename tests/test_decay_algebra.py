@@ -56,7 +56,9 @@ def cut_length(P, cmax, M, S, T, eps=EPS, floor_log2=-100.0):
 
 def subblock_sequence(q, k, v, T, M, S, sub=16, t0=0, scale=None, kt=None, vt=None, eps=EPS,
                       out=True, adaptive=False):
-    """One (b,h) sequence through the sub-block form; returns (o, K~, V~, A_total)."""
+    """One (b,h) sequence through the sub-block form; returns (o, K~, V~, A_total).  The
+    sub-blocks tile windows of `sub` tokens from the sequence start (with adaptive cuts, a
+    window may hold several), as the kernels schedule them."""
     L, d = q.shape
     Tc = max(T, 2 * M - 1)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
@@ -67,7 +69,7 @@ def subblock_sequence(q, k, v, T, M, S, sub=16, t0=0, scale=None, kt=None, vt=No
     a_total = np.ones(S)
     b0 = 0
     while b0 < L:
-        c = min(sub, L - b0)
+        c = min(sub - b0 % sub, L - b0)  # sub-blocks never cross a window of `sub` tokens
         if adaptive:
             c = cut_length(t0 + b0, c, M, S, T, eps)
         g = gates(t0 + b0, c, M, S, T)                           # [c, S]
