@@ -75,6 +75,7 @@ KERNEL_SOURCES = {
     "decay": ("bla_device.h", "bla_plan.h", "bla_decay.hip"),
     "backward": ("bla_device.h", "bla_forward.h", "bla_forward_pair.h", "bla_plan.h", "bla_backward.h",
                  "bla_backward_bf16.h"),
+    "step": ("bla_device.h", "bla_plan.h", "bla_step.hip"),
 }
 
 
@@ -441,10 +442,12 @@ def bench_decode(args, hip):
     torch.cuda.synchronize(dev)
     copy_gbs = 2 * state_bytes / (hip.elapsed_ms(c0, c1) / args.steps * 1e-3) / 1e9
     del src, dst
+    traffic = read_traffic(os.path.join(ROOT, "profiles", "step_kernel_decode_traffic.txt"),
+                           kernel_sources_digest("step"))
     return {"workload": "decode", "B": w.B, "H": w.H, "d": w.d, "M": w.M, "S": w.S, "position": w.L,
             "ms_per_step": round(ms, 4), "tokens_per_s": round(w.B / (ms * 1e-3), 1),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+                         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic},
             "device_copy_gbs": round(copy_gbs, 1), "frac_of_device_copy": round(gbs / copy_gbs, 4)}
 
 
