@@ -297,27 +297,30 @@ __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTil
             }
         }
     }
+    // per reduction block: the phase fragments of the owned mode tiles first, then one
+    // head-dim tile of K and V at a time (few fragments live next to the state)
 #pragma unroll
     for (int kb = 0; kb < GG::KBC; ++kb) {
-        F kf[GG::NDT], vf[GG::NDT];
-#pragma unroll
-        for (int dt = 0; dt < GG::NDT; ++dt) {
-            kf[dt] = ld_frag<T>(Kt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
-            vf[dt] = ld_frag<T>(Vt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
-        }
+        F ef[GG::OWN][2];
 #pragma unroll
         for (int o = 0; o < GG::OWN; ++o) {
-            const int mt = w + GG::NW * o;
-            if (mt < GG::NMT) {
+            const int mt = min(w + GG::NW * o, GG::NMT - 1);
 #pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    const F ef = (c == GG::C)
-                                     ? ld_frag<T>(Erev + (size_t)(16 * (p * GG::NMT + mt) + r) * ldR, 32 * kb, g)
-                                     : erev_frag<T, MP>(E32, 2 * MP, c, p, mt, kb, g, r);
+            for (int p = 0; p < 2; ++p)
+                ef[o][p] = (c == GG::C) ? ld_frag<T>(Erev + (size_t)(16 * (p * GG::NMT + mt) + r) * ldR, 32 * kb, g)
+                                        : erev_frag<T, MP>(E32, 2 * MP, c, p, mt, kb, g, r);
+        }
 #pragma unroll
-                    for (int dt = 0; dt < GG::NDT; ++dt) {
-                        Zk[o][p][dt] = mma(kf[dt], ef, Zk[o][p][dt]);
-                        Zv[o][p][dt] = mma(ef, vf[dt], Zv[o][p][dt]);
+        for (int dt = 0; dt < GG::NDT; ++dt) {
+            const F kf = ld_frag<T>(Kt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
+            const F vf = ld_frag<T>(Vt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
+#pragma unroll
+            for (int o = 0; o < GG::OWN; ++o) {
+                if (w + GG::NW * o < GG::NMT) {
+#pragma unroll
+                    for (int p = 0; p < 2; ++p) {
+                        Zk[o][p][dt] = mma(kf, ef[o][p], Zk[o][p][dt]);
+                        Zv[o][p][dt] = mma(ef[o][p], vf, Zv[o][p][dt]);
                     }
                 }
             }
@@ -471,15 +474,20 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
         tTheta = thh;
     }
 
+    // Eight-wave geometry (bf16): the Gram tile's key rows are read transposed from the staged
+    // K^T tile instead of being held in registers a chunk ahead.
+    constexpr bool KROWS = GG::NTHR > kThreads && sizeof(T) == 2;
     // first chunk's staging loads go out before the state set-up
     Stage<T, D, MP> st;
-    F kpf[GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand), unmasked
+    F kpf[KROWS ? 1 : GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand), unmasked
     {
         const int tok0 = ch0 * C, c0 = min(C, a.L - tok0), i = min(16 * w + r, c0 - 1);
         stage_load<T, D, MP, true>(st, qb + (size_t)tok0 * ts, kb_ + (size_t)tok0 * ts, vb + (size_t)tok0 * ts,
                                    ts, c0, tid);
+        if constexpr (!KROWS) {
 #pragma unroll
-        for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tok0 + i) * ts, 32 * kb, g);
+            for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tok0 + i) * ts, 32 * kb, g);
+        }
     }
     if constexpr (P::TL) __syncthreads();  // LDS tables visible
 
@@ -563,19 +571,30 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
                 lPh[MP + m] = (T)(-sn);
             }
         }
-        F kcur[GG::KBD];
+        F kcur[KROWS ? 1 : GG::KBD];
+        if constexpr (!KROWS) {
 #pragma unroll
-        for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = (16 * w + r < c) ? kpf[kb] : zero_frag<T>();
+            for (int kb = 0; kb < GG::KBD; ++kb) kcur[kb] = (16 * w + r < c) ? kpf[kb] : zero_frag<T>();
+        }
         if (n + 1 < nch) {
             const int tn = tok0 + C, cn = min(C, a.L - tn), i = min(16 * w + r, cn - 1);
             stage_load<T, D, MP, true>(st, qb + (size_t)tn * ts, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts,
                                        cn, tid);
+            if constexpr (!KROWS) {
 #pragma unroll
-            for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tn + i) * ts, 32 * kb, g);
+                for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tn + i) * ts, 32 * kb, g);
+            }
         }
         __syncthreads();  // staging and ZvT visible
 
         // ---- phase A: Gram tile (key tile w) and Q Z'_k^T on owned mode tiles
+        floatx4 U[OWN][2][NT];
+#pragma unroll
+        for (int o = 0; o < OWN; ++o)
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int ct = 0; ct < NT; ++ct) U[o][p][ct] = zero4();
         F zkf[OWN][2][GG::KBD];  // Z'_k^T tiles as A fragments (rows m, reduction over d)
 #pragma unroll
         for (int o = 0; o < OWN; ++o)
@@ -584,13 +603,6 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
 #pragma unroll
                 for (int kb = 0; kb < GG::KBD; ++kb)
                     zkf[o][p][kb] = frag_from_acc<T>(Zk[o][p][2 * kb], Zk[o][p][2 * kb + 1]);
-        floatx4 U[OWN][2][NT];
-#pragma unroll
-        for (int o = 0; o < OWN; ++o)
-#pragma unroll
-            for (int p = 0; p < 2; ++p)
-#pragma unroll
-                for (int ct = 0; ct < NT; ++ct) U[o][p][ct] = zero4();
 #pragma unroll
         for (int ct = 0; ct < NT; ++ct) {
             const int j = 16 * ct + r;
@@ -600,7 +612,12 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
             if (ct >= w) {
                 floatx4 acc = zero4();
 #pragma unroll
-                for (int kb = 0; kb < GG::KBD; ++kb) acc = mma(kcur[kb], qf[kb], acc);
+                for (int kb = 0; kb < GG::KBD; ++kb) {
+                    if constexpr (KROWS)
+                        acc = mma(ld_frag_tr(Kt, GG::LDK, 16 * w, kb, g, r), qf[kb], acc);  // rows past c are 0
+                    else
+                        acc = mma(kcur[kb], qf[kb], acc);
+                }
                 if (ct == w) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)

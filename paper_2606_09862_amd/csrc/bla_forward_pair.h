@@ -38,25 +38,6 @@
 
 namespace bla {
 
-typedef short shortx4 __attribute__((ext_vector_type(4)));
-
-// Transposing LDS read: within each 16-lane group, lane 4a+b supplies the address
-// of 4 consecutive elements; lane 4b'+c receives element c of lane 4a+b' for a = 0..3.
-__device__ __forceinline__ bf16x4 ld_tr(const bf16* p)
-{
-    shortx4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) shortx4*)p);
-    return __builtin_bit_cast(bf16x4, v);
-}
-
-// Operand fragment for rows x0..x0+15 (lane r) and reduction block kb from an LDS
-// tile stored reduction-major, M[k][x] with row length ld: the fragment's element e
-// of lane (g, r) is M[k(e)][x0 + r], k(e) = 32kb + 16(e/4) + 4g + e%4.
-__device__ __forceinline__ bf16x8 ld_frag_tr(const bf16* M, int ld, int x0, int kb, int g, int r)
-{
-    const bf16* p = M + (size_t)(32 * kb + 4 * g + (r >> 2)) * ld + x0 + 4 * (r & 3);
-    return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
-}
-
 template <int D, int MP, int SP> struct Pair {
     static constexpr int C = kChunk, NT = C / 16, WPU = 4;
     static constexpr int NMT = MP / 16, NDT = D / 16, NST = SP / 16;
