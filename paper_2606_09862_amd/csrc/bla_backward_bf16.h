@@ -29,20 +29,24 @@ template <int D, int MP, int SP> struct Bwd16 {
     static constexpr int OWN = (NMT + NW - 1) / NW;   // mode tiles of the forward state per wave
     static constexpr int ODT = (NDT + NW - 1) / NW;   // head-dim tiles of the adjoint per wave
     static constexpr int LDQ = D + 12;                // token tiles [C][LDQ] (read both ways)
-    static constexpr int LDK = C + 4;                 // Gram / H tiles [C][LDK]; weights [2MP][LDK]
-    static constexpr int LDU = 2 * MP + 4;            // U, Y [C][LDU]; Z'_k [D][LDU]
+    static constexpr int LDK = C + 4;                 // Gram tiles [C][LDK]
+    static constexpr int LDU = 2 * MP + 4;            // U, Y [C][LDU]
     static constexpr int LE = 2 * MP + 12;            // phase table [C][LE]; slot matrix [SP][LE]
+    // Tiles written row-major by the wave that produces them (8-byte stores) and read
+    // transposed (ds_read_b64_tr_b16):
+    static constexpr int LDH = C + 4;                 // H tiles [query][key]
+    static constexpr int LDW = 2 * MP + 4;            // readout weights [token][Re m | Im m]
+    static constexpr int LDZ = D + 4;                 // Z'_k [Re m | Im m][d]
     static constexpr size_t A_ELEMS = (size_t)4 * C * LDQ;
-    static constexpr size_t G_ELEMS = (size_t)2 * C * LDK;
-    static constexpr size_t B_ELEMS = (size_t)2 * C * LDU > (size_t)4 * MP * LDK ? (size_t)2 * C * LDU
-                                                                                  : (size_t)4 * MP * LDK;
-    static constexpr size_t Z_ELEMS = (size_t)D * LDU;
+    static constexpr size_t G_ELEMS = (size_t)2 * C * (LDH > LDK ? LDH : LDK);
+    static constexpr size_t B_ELEMS = (size_t)2 * C * (LDW > LDU ? LDW : LDU);
+    static constexpr size_t Z_ELEMS = (size_t)2 * MP * LDZ;
     static constexpr size_t E_ELEMS = (size_t)C * LE;
     static constexpr size_t S_ELEMS = (size_t)SP * LE;
     static constexpr size_t LDS_BYTES =
         (A_ELEMS + G_ELEMS + B_ELEMS + Z_ELEMS + E_ELEMS + S_ELEMS) * 2 + (size_t)SP * 4 + (size_t)2 * MP * 4;
     static_assert(LDS_BYTES <= kBwdMaxLds, "backward tiles fit in LDS");
-    static_assert((size_t)2 * C * LDK <= G_ELEMS, "H tiles fit in the Gram region");
+    static_assert((size_t)2 * C * LDH <= G_ELEMS, "H tiles fit in the Gram region");
 };
 
 __device__ __forceinline__ bf16x8 neg_frag(bf16x8 f)
@@ -208,13 +212,13 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
     bf16* dOs = Qs + (size_t)C * LDQ;
     bf16* GT = Ks + P::A_ELEMS;                              // region G: Gram tiles, then H tiles
     bf16* GdT = GT + (size_t)C * LDK;
-    bf16* HqT = GT;
-    bf16* HvT = GdT;
+    bf16* HqT = GT;                                          // [query][key], LDH
+    bf16* HvT = GT + (size_t)C * P::LDH;
     bf16* UT = GT + P::G_ELEMS;                              // region B: U, Y, then the weights
     bf16* YT = UT + (size_t)C * LDU;
-    bf16* WqT = UT;
-    bf16* WvT = WqT + (size_t)2 * MP * LDK;
-    bf16* ZkT = UT + P::B_ELEMS;                             // [d][Re m | Im m] of Z'_k
+    bf16* WqT = UT;                                          // [token][Re m | Im m], LDW
+    bf16* WvT = WqT + (size_t)C * P::LDW;
+    bf16* ZkT = UT + P::B_ELEMS;                             // [Re m | Im m][d] of Z'_k, LDZ
     bf16* sE = ZkT + P::Z_ELEMS;                             // conj(rho^i) rows
     bf16* sAB = sE + P::E_ELEMS;                             // scale (A | B) rows
     int* sTheta = reinterpret_cast<int*>(sAB + P::S_ELEMS);
@@ -430,11 +434,9 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const size_t row = (size_t)(16 * dt + 4 * g + e) * LDU;
-                            ZkT[row + 16 * mt + r] = (bf16)Zk[o][0][dt][e];
-                            ZkT[row + MP + 16 * mt + r] = (bf16)Zk[o][1][dt][e];
-                        }
+                        for (int p = 0; p < 2; ++p)
+                            st_lds<bf16x4>(ZkT + (size_t)(p * MP + 16 * mt + r) * P::LDZ + 16 * dt + 4 * g,
+                                           cvt4(Zk[o][p][dt], bf16()));
                 }
             }
         }
@@ -605,12 +607,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     const floatx4 am = wa[mt], bm = wa[NMT + mt];
                     wa[mt] = am * cs - bm * ns;
                     wa[NMT + mt] = am * ns + bm * cs;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const size_t re = (size_t)(16 * mt + 4 * g + e) * LDK + j;
-                        WvT[re] = (bf16)wa[mt][e];
-                        WvT[re + (size_t)MP * LDK] = (bf16)wa[NMT + mt][e];
-                    }
+                    st_lds<bf16x4>(WvT + (size_t)j * P::LDW + 16 * mt + 4 * g, cvt4(wa[mt], bf16()));
+                    st_lds<bf16x4>(WvT + (size_t)j * P::LDW + MP + 16 * mt + 4 * g, cvt4(wa[NMT + mt], bf16()));
                 }
                 if constexpr (!SUM) {
                     F wf[KBM];
@@ -629,8 +627,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                                     if (4 * g + e > r) hv[e] = 0.f;
                             }
                         }
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) HvT[(size_t)(16 * kt + 4 * g + e) * LDK + j] = (bf16)hv[e];
+                        st_lds<bf16x4>(HvT + (size_t)j * P::LDH + 16 * kt + 4 * g, cvt4(hv, bf16()));
                     }
                 }
             }
@@ -650,12 +647,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     const floatx4 am = wq[mt], bm = wq[NMT + mt];
                     wq[mt] = am * cs - bm * ns;
                     wq[NMT + mt] = am * ns + bm * cs;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const size_t re = (size_t)(16 * mt + 4 * g + e) * LDK + j;
-                        WqT[re] = (bf16)wq[mt][e];
-                        WqT[re + (size_t)MP * LDK] = (bf16)wq[NMT + mt][e];
-                    }
+                    st_lds<bf16x4>(WqT + (size_t)j * P::LDW + 16 * mt + 4 * g, cvt4(wq[mt], bf16()));
+                    st_lds<bf16x4>(WqT + (size_t)j * P::LDW + MP + 16 * mt + 4 * g, cvt4(wq[NMT + mt], bf16()));
                 }
                 if constexpr (!SUM) {
                     F qf2[KBM];
@@ -667,7 +660,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                         oa[dt] = zero4();
 #pragma unroll
                         for (int kb = 0; kb < KBM; ++kb)
-                            oa[dt] = mma(ld_frag<bf16>(ZkT + (size_t)(16 * dt + r) * LDU, 32 * kb, g), qf2[kb], oa[dt]);
+                            oa[dt] = mma(ld_frag_tr(ZkT, P::LDZ, 16 * dt, kb, g, r), qf2[kb], oa[dt]);
                     }
                     floatx4 hq[NT];
 #pragma unroll
@@ -683,8 +676,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                                     if (4 * g + e > r) hq[kt][e] = 0.f;
                             }
                         }
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) HqT[(size_t)(16 * kt + 4 * g + e) * LDK + j] = (bf16)hq[kt][e];
+                        st_lds<bf16x4>(HqT + (size_t)j * P::LDH + 16 * kt + 4 * g, cvt4(hq[kt], bf16()));
                     }
 #pragma unroll
                     for (int kb = 0; kb < KBC; ++kb) {
@@ -744,8 +736,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     floatx4 ka = zero4(), va = zero4();
 #pragma unroll
                     for (int kb = 0; kb < KBC; ++kb) {
-                        ka = mma(qtf[kb], ld_frag<bf16>(HqT + (size_t)j * LDK, 32 * kb, g), ka);
-                        va = mma(otf[kb], ld_frag<bf16>(HvT + (size_t)j * LDK, 32 * kb, g), va);
+                        ka = mma(qtf[kb], ld_frag_tr(HqT, P::LDH, 16 * kt, kb, g, r), ka);
+                        va = mma(otf[kb], ld_frag_tr(HvT, P::LDH, 16 * kt, kb, g, r), va);
                     }
 #pragma unroll
                     for (int kb = 0; kb < KBM; ++kb) {
@@ -769,10 +761,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                 for (int p = 0; p < 2; ++p)
 #pragma unroll
                     for (int mt = 0; mt < NMT; ++mt) {
-                        Gk[od][p][mt] = mma(ld_frag<bf16>(WqT + (size_t)(p * MP + 16 * mt + r) * LDK, 32 * kb, g), qtf,
-                                            Gk[od][p][mt]);
-                        Gv[od][p][mt] = mma(ld_frag<bf16>(WvT + (size_t)(p * MP + 16 * mt + r) * LDK, 32 * kb, g), otf,
-                                            Gv[od][p][mt]);
+                        Gk[od][p][mt] = mma(ld_frag_tr(WqT, P::LDW, p * MP + 16 * mt, kb, g, r), qtf, Gk[od][p][mt]);
+                        Gv[od][p][mt] = mma(ld_frag_tr(WvT, P::LDW, p * MP + 16 * mt, kb, g, r), otf, Gv[od][p][mt]);
                     }
             }
         }
