@@ -164,10 +164,14 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
  *        slot_k, slot_v: float32 [B, H, S, d] (row s of head (b,h) is slot s).
  * p->phase_anchor is ignored (the form is anchored by definition).  Shapes, dtypes, T,
  * alignment, ownership, streams and errors follow the conventions above (p->chunk is
- * accepted as for bla_forward; the kernels work in sub-blocks of min(16, floor(T)) tokens).
+ * accepted as for bla_forward; the kernels work in sub-blocks of at most 16 tokens that never
+ * cross a 16-token window of the sequence and end early where a slot's product of decay
+ * factors would fall below 2^-100).
  */
 
-/* Bytes of device workspace bla_decay_forward and bla_decay_step need for *p. */
+/* Bytes of device workspace bla_decay_forward and bla_decay_step need for *p.  For a forward
+ * call it grows with L: the segment summaries plus a sub-block schedule of about
+ * 8 * P(S) + 4 bytes per token and head (P(S): S padded as for bla_forward). */
 size_t bla_decay_workspace_size(const bla_params* p);
 
 /*
