@@ -192,8 +192,9 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
     // float32: K row-major plus K^T, V^T), gate tables, thresholds, cross-wave buffers
     constexpr int KV_ELEMS = BF ? 2 * 16 * G::LK : 16 * G::LKF + 2 * D * G::LKT;
     __shared__ __attribute__((aligned(16))) T sKV[KV_ELEMS];
-    __shared__ __attribute__((aligned(16))) float sE[16 * LG];
-    __shared__ __attribute__((aligned(16))) float sB[16 * LG];
+    // E and Bq rows of the sub-block for the outputs (the summary pass reads E from the schedule)
+    __shared__ __attribute__((aligned(16))) float sE[SUM ? 4 : 16 * LG];
+    __shared__ __attribute__((aligned(16))) float sB[SUM ? 4 : 16 * LG];
     __shared__ __attribute__((aligned(16))) int sTheta[SP];
     __shared__ float sRed[2][NWU][16];
     constexpr int LO = D + 4;  // sO row stride (floats)
@@ -313,7 +314,7 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const size_t idx = (grow + min(t0s + 4 * g + e, L - 1)) * SP + s0w + 16 * t + r;
-                Epf[t][e] = a.gE[idx];
+                if constexpr (!SUM) Epf[t][e] = a.gE[idx];
                 Bpf[t][e] = a.gB[idx];
             }
     };
@@ -354,9 +355,20 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const bool live = 4 * g + e < cs;
-                Ecur[t][e] = live ? Epf[t][e] : 1.f;
+                if constexpr (!SUM) Ecur[t][e] = live ? Epf[t][e] : 1.f;
                 bq[t][e] = live ? Bpf[t][e] : 0.f;
             }
+        // the summary pass: E of the sub-block's last token straight from the schedule
+        float ecs[NSTW];
+        floatx4 ers[NSTW];
+        if constexpr (SUM) {
+            const size_t last = (grow + tb + cs - 1) * SP + s0w;
+#pragma unroll
+            for (int t = 0; t < NSTW; ++t) {
+                ecs[t] = a.gE[last + 16 * t + r];
+                ers[t] = ld4f(a.gE + last + 16 * t + 4 * g);
+            }
+        }
         __syncthreads();  // previous sub-block done with the LDS tiles
         stage_store(cs);
         __syncthreads();  // K, V visible
@@ -367,13 +379,15 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
         }
         // the sub-block's E and Bq rows in LDS, each wave on its own slots (read below only by
         // the wave that wrote them)
+        if constexpr (!SUM) {
 #pragma unroll
-        for (int t = 0; t < NSTW; ++t) {
-            const int s = s0w + 16 * t + r;
+            for (int t = 0; t < NSTW; ++t) {
+                const int s = s0w + 16 * t + r;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                sE[(4 * g + e) * LG + s] = Ecur[t][e];
-                sB[(4 * g + e) * LG + s] = bq[t][e];
+                for (int e = 0; e < 4; ++e) {
+                    sE[(4 * g + e) * LG + s] = Ecur[t][e];
+                    sB[(4 * g + e) * LG + s] = bq[t][e];
+                }
             }
         }
 
@@ -526,8 +540,8 @@ __global__ __launch_bounds__((DecayGeo<D, SP>::NTH)) void decay_forward_kernel(D
 #pragma unroll
         for (int t = 0; t < NSTW; ++t) {
             const F bqa = join(cvt4(floatx4{bq[t][0], bq[t][1], bq[t][2], bq[t][3]}, T()), zero_half<T>());
-            const float ecol = sE[(cs - 1) * LG + s0w + 16 * t + r];
-            const floatx4 erow = ld4f(sE + (cs - 1) * LG + s0w + 16 * t + 4 * g);
+            const float ecol = SUM ? ecs[t] : sE[(cs - 1) * LG + s0w + 16 * t + r];
+            const floatx4 erow = SUM ? ers[t] : ld4f(sE + (cs - 1) * LG + s0w + 16 * t + 4 * g);
             aprod[t] *= ecol;
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
