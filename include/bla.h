@@ -82,6 +82,18 @@ typedef struct {
     int32_t phase_anchor; /* 0: slots at lags behind the current token (the operator above,
                             Sec. 3.1, Alg. 2); 1: slots anchored at absolute phase 0 (Sec. 3.3,
                             Alg. 1 / Alg. 3); any other value is BLA_ERR_INVALID_ARG        */
+    int32_t reuse_tables; /* 0: build the phase and slot tables in the workspace (every call).
+                            1: reuse them if this workspace already holds them.  Alg. 1 and
+                            Alg. 3 take the interpolation matrices A, B as precomputed inputs;
+                            with this flag the tables of an earlier call are kept.  The library
+                            records, per device and workspace address, the key of the tables it
+                            last built there (entry point, every field of *p that the tables
+                            depend on, and the periods T); a call with reuse_tables = 1 skips
+                            the table kernel only when that record matches, and builds the
+                            tables otherwise.  The caller guarantees that nothing else has
+                            written the workspace since that call (a workspace freed and
+                            allocated again at the same address holds stale bytes: pass 0
+                            then).  Any value other than 0 or 1 is BLA_ERR_INVALID_ARG.     */
 } bla_params;
 
 /* Human-readable name of a status code (static string, never NULL). */

@@ -8,7 +8,6 @@ library has not been built, importing works but every call raises.
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 
 import torch
@@ -33,7 +32,7 @@ class Params(ctypes.Structure):
                 ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("M", ctypes.c_int32),
                 ("S", ctypes.c_int32), ("chunk", ctypes.c_int32), ("t0", ctypes.c_int64),
                 ("scale", ctypes.c_float), ("io_dtype", ctypes.c_int32),
-                ("phase_anchor", ctypes.c_int32)]
+                ("phase_anchor", ctypes.c_int32), ("reuse_tables", ctypes.c_int32)]
 
 
 _lib = None
@@ -89,9 +88,11 @@ def lib():
     return _lib
 
 
-def make_params(B, H, L, d, M, S, dtype, t0=0, scale=0.0, chunk=0, phase_anchor=False) -> Params:
+def make_params(B, H, L, d, M, S, dtype, t0=0, scale=0.0, chunk=0, phase_anchor=False,
+                reuse_tables=False) -> Params:
     io = BLA_BF16 if dtype == torch.bfloat16 else BLA_F32
-    return Params(B, H, L, d, d, M, S, chunk, int(t0), float(scale), io, int(phase_anchor))
+    return Params(B, H, L, d, d, M, S, chunk, int(t0), float(scale), io, int(phase_anchor),
+                  int(reuse_tables))
 
 
 def _periods(T, H):
@@ -143,14 +144,27 @@ def _check(t, shape, dtype, name):
                          f"got {t.dtype} {tuple(t.shape)} on {t.device}")
 
 
+def _out(out, like, shape):
+    """A fresh output like `like`, or the caller's `out` after the same checks as the inputs
+    (shape, dtype, contiguity, device), so that a wrong buffer fails before any launch."""
+    if out is None:
+        return torch.empty_like(like)
+    _check(out, shape, like.dtype, "out")
+    if out.device != like.device:
+        raise ValueError(f"out: expected a tensor on {like.device}, got {out.device}")
+    return out
+
+
 def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
             state_k=None, state_v=None, want_state: bool = True, workspace=None, out=None,
-            phase_anchor: bool = False):
+            phase_anchor: bool = False, reuse_tables: bool = False):
     """bla_forward on q, k, v [B,H,L,d] (float32 or bfloat16 cuda tensors).
 
     Returns (o, state_k_out, state_v_out); the states are float32 [B,H,2,M,d]
     (None when want_state is False).  phase_anchor selects the anchored slots of
     Sec. 3.3 (Alg. 1 / Alg. 3); the state is the same mode state in both forms.
+    reuse_tables: keep the tables an earlier call built in the same `workspace`
+    (bla_params.reuse_tables; only meaningful with a caller-kept workspace).
     """
     B, H, L, d = q.shape
     dt = q.dtype
@@ -158,12 +172,12 @@ def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
         _check(t, (B, H, L, d), dt, name)
     _check(q, (B, H, L, d), dt, "q")
     p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale,
-                    phase_anchor=phase_anchor)
+                    phase_anchor=phase_anchor, reuse_tables=reuse_tables)
     for name, t in (("state_k", state_k), ("state_v", state_v)):
         if t is not None:
             _check(t, (B, H, 2, M, d), torch.float32, name)
     dev = q.device
-    o = torch.empty_like(q) if out is None else out
+    o = _out(out, q, (B, H, L, d))
     sk = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
     sv = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
     need = workspace_size(p)
@@ -180,7 +194,8 @@ def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
 
 
 def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
-         scale: float | None = None, workspace=None, out=None, phase_anchor: bool = False):
+         scale: float | None = None, workspace=None, out=None, phase_anchor: bool = False,
+         reuse_tables: bool = False):
     """bla_step: one decode token per row; q,k,v [B,H,d]; updates state_k/state_v in place."""
     B, H, d = q.shape
     dt = q.dtype
@@ -192,9 +207,9 @@ def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
     if pos is not None:
         _check(pos, (B,), torch.int64, "pos")
     p = make_params(B, H, 1, d, M, S, dt, t0, 0.0 if scale is None else scale,
-                    phase_anchor=phase_anchor)
+                    phase_anchor=phase_anchor, reuse_tables=reuse_tables)
     dev = q.device
-    o = torch.empty_like(q) if out is None else out
+    o = _out(out, q, (B, H, d))
     need = step_workspace_size(p)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
@@ -204,10 +219,6 @@ def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
     if st != 0:
         raise BlaError(st, "bla_step")
     return o
-
-
-def default_scale(d: int) -> float:
-    return 1.0 / math.sqrt(d)
 
 
 def decay_workspace_size(p: Params) -> int:
@@ -229,7 +240,7 @@ def decay_forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None =
             _check(t, (B, H, S, d), torch.float32, name)
     p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale)
     dev = q.device
-    o = torch.empty_like(q) if out is None else out
+    o = _out(out, q, (B, H, L, d))
     sk = torch.empty((B, H, S, d), dtype=torch.float32, device=dev) if want_state else None
     sv = torch.empty((B, H, S, d), dtype=torch.float32, device=dev) if want_state else None
     need = decay_workspace_size(p)
@@ -258,7 +269,7 @@ def decay_step(q, k, v, T, M: int, S: int, slot_k, slot_v, pos=None, t0: int = 0
         _check(pos, (B,), torch.int64, "pos")
     p = make_params(B, H, 1, d, M, S, dt, t0, 0.0 if scale is None else scale)
     dev = q.device
-    o = torch.empty_like(q) if out is None else out
+    o = _out(out, q, (B, H, d))
     need = decay_workspace_size(p)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
@@ -331,7 +342,7 @@ def layer_forward(x, w_qkv, w_o, T, H: int, M: int, S: int, t0: int = 0, scale: 
             _check(t, (B, H, 2, M, d), torch.float32, name)
     p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale, phase_anchor=phase_anchor)
     dev = x.device
-    y = torch.empty_like(x) if out is None else out
+    y = _out(out, x, (B, L, D))
     sk = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
     sv = torch.empty((B, H, 2, M, d), dtype=torch.float32, device=dev) if want_state else None
     need = layer_workspace_size(p)

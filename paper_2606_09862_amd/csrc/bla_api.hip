@@ -4,6 +4,9 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
+
 #include <hip/hip_runtime.h>
 
 #include "bla.h"
@@ -15,24 +18,67 @@ using namespace bla;
 
 constexpr size_t kAlign = 256;
 constexpr size_t kMaxSummaryBytes = size_t(256) << 20;  // cap on per-block summary scratch
+constexpr int kMaxPairSegments = 16;                     // segments per sequence on the pair kernel
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 int pad_modes(int M) { return M <= 16 ? 16 : M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : -1; }
 int pad_slots(int S) { return S <= 32 ? 32 : S <= 64 ? 64 : S <= 128 ? 128 : S <= 256 ? 256 : -1; }
 
+// Compute units of the current device, cached per device.  Concurrent first calls may both
+// query the runtime; they store the same value, and the atomic makes that race benign.
 int device_cu_count()
 {
-    static int cache[128] = {0};
+    static std::atomic<int> cache[128];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 128) return 256;
-    if (cache[dev] == 0) {
-        int n = 0;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
             n = 256;
-        cache[dev] = n;
+        cache[dev].store(n, std::memory_order_relaxed);
     }
-    return cache[dev];
+    return n;
+}
+
+// Record of the tables last built into each workspace: (device, workspace address) -> key of
+// the tables' contents.  A call with reuse_tables = 1 skips the table kernel when the record
+// of its workspace matches its key.  A fixed ring of records; the oldest is overwritten.
+struct TableRecord {
+    int dev;
+    const void* ws;
+    uint64_t key;
+};
+constexpr int kTableRecords = 64;
+std::mutex g_table_mu;
+TableRecord g_table_rec[kTableRecords];
+int g_table_next = 0;
+
+uint64_t fnv_mix(uint64_t h, const void* data, size_t n)
+{
+    const unsigned char* c = (const unsigned char*)data;
+    for (size_t i = 0; i < n; ++i) h = (h ^ c[i]) * 1099511628211ull;
+    return h;
+}
+
+bool tables_recorded(int dev, const void* ws, uint64_t key)
+{
+    std::lock_guard<std::mutex> lk(g_table_mu);
+    for (int i = 0; i < kTableRecords; ++i)
+        if (g_table_rec[i].ws == ws && g_table_rec[i].dev == dev) return g_table_rec[i].key == key;
+    return false;
+}
+
+void tables_record(int dev, const void* ws, uint64_t key)
+{
+    std::lock_guard<std::mutex> lk(g_table_mu);
+    for (int i = 0; i < kTableRecords; ++i)
+        if (g_table_rec[i].ws == ws && g_table_rec[i].dev == dev) {
+            g_table_rec[i].key = key;
+            return;
+        }
+    g_table_rec[g_table_next] = TableRecord{dev, ws, key};
+    g_table_next = (g_table_next + 1) % kTableRecords;
 }
 
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
@@ -46,6 +92,7 @@ bla_status check_shape(const bla_params* p, bool step)
     if (p->io_dtype != BLA_F32 && p->io_dtype != BLA_BF16) return BLA_ERR_INVALID_ARG;
     if (!isfinite(p->scale)) return BLA_ERR_INVALID_ARG;
     if (p->phase_anchor != 0 && p->phase_anchor != 1) return BLA_ERR_INVALID_ARG;
+    if (p->reuse_tables != 0 && p->reuse_tables != 1) return BLA_ERR_INVALID_ARG;
     if (p->chunk != 0 && p->chunk != kChunk) return BLA_ERR_UNSUPPORTED;
     if (p->d_k != p->d_v) return BLA_ERR_UNSUPPORTED;
     if (p->d_k != 32 && p->d_k != 64 && p->d_k != 128) return BLA_ERR_UNSUPPORTED;
@@ -97,6 +144,14 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     }
     if (!step && units > 0 && pl->nch > 1) {
         const int cus = device_cu_count();
+        // The pair kernel combines every preceding segment summary in each unit's prologue,
+        // which reads O(nseg^2) summaries per sequence.  Where filling the device would take
+        // more than kMaxPairSegments segments (few, long sequences), the one-unit kernels run
+        // instead: per-block summaries and a scan, linear in the number of segments.
+        if (pl->pair && units * kMaxPairSegments < (long long)cus * pl->upw) {
+            pl->pair = 0;
+            pl->upw = 1;
+        }
         const long long target = (long long)cus * pl->upw;  // units that fill every CU once
         if (units < target) {
             long long want = (target + units - 1) / units;
@@ -139,9 +194,23 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->total = off;
 }
 
-// step: a decode step needs the phase rows j = 0, 1 only
-bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s, bool step)
+// step: a decode step needs the phase rows j = 0, 1 only.  reuse: skip the launch when the
+// library's record says this workspace already holds exactly these tables.
+bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s, bool step, int reuse)
 {
+    // key: everything the tables' contents and layout depend on
+    int32_t f[14] = {pl.H, pl.M, pl.S, pl.MP, pl.SP, kChunk, pl.bf16, pl.anchor, pl.pair, step ? 2 : kChunk + 1,
+                     pl.cpb * kChunk, 0, 0, 0};
+    const float tab_scale = pl.pair ? 1.f : pl.scale;
+    memcpy(&f[11], &tab_scale, sizeof(float));
+    uint64_t key = fnv_mix(1469598103934665603ull, f, sizeof(f));
+    for (int h = 0; h < pl.H; ++h) {
+        const double tmin = 2.0 * pl.M - 1.0, Tc = T[h] < tmin ? tmin : T[h];
+        key = fnv_mix(key, &Tc, sizeof(Tc));
+    }
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return BLA_ERR_HIP;
+    if (reuse && tables_recorded(dev, ws, key)) return BLA_OK;
     for (int h0 = 0; h0 < pl.H; h0 += kMaxHeadsPerTableLaunch) {
         TableArgs a;
         memset(&a, 0, sizeof(a));
@@ -175,6 +244,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         }
         if (launch_tables(a, pl.bf16, s) != hipSuccess) return BLA_ERR_HIP;
     }
+    tables_record(dev, ws, key);
     return BLA_OK;
 }
 
@@ -366,7 +436,7 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
         return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
     };
     if (!mark(0)) return BLA_ERR_HIP;
-    if ((st = build_tables(pl, T, ws, s, false)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, false, p->reuse_tables)) != BLA_OK) return st;
     if (!mark(1)) return BLA_ERR_HIP;
 
     FwdArgs a;
@@ -454,7 +524,7 @@ bla_status bla_step(const bla_params* p, const double* T, const void* q, const v
     if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, true, p->reuse_tables)) != BLA_OK) return st;
     StepArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
@@ -526,7 +596,7 @@ static bla_status decay_forward_impl(const bla_params* p, const double* T, const
         return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
     };
     if (!mark(0)) return BLA_ERR_HIP;
-    if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, true, p->reuse_tables)) != BLA_OK) return st;
     DecayArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
@@ -633,7 +703,7 @@ bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, c
     if (!workspace || workspace_bytes < pl.total || !aligned16(workspace)) return BLA_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     char* ws = (char*)workspace;
-    if ((st = build_tables(pl, T, ws, s, true)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, true, p->reuse_tables)) != BLA_OK) return st;
     DecayStepArgs a;
     memset(&a, 0, sizeof(a));
     a.q = q;
@@ -703,7 +773,7 @@ static bla_status backward_impl(const bla_params* p, const double* T, const void
         return !events || !events[i] || hipEventRecord((hipEvent_t)events[i], s) == hipSuccess;
     };
     if (!mark(0)) return BLA_ERR_HIP;
-    if ((st = build_tables(pl, T, ws, s, false)) != BLA_OK) return st;
+    if ((st = build_tables(pl, T, ws, s, false, p->reuse_tables)) != BLA_OK) return st;
     if (!mark(1)) return BLA_ERR_HIP;
     BwdArgs a;
     memset(&a, 0, sizeof(a));

@@ -58,11 +58,14 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
     template <> hipError_t Launch<T, D, MP, SP>::forward(const Plan& p, const FwdArgs& a, hipStream_t s) \
     {                                                                                                   \
         if constexpr (pair_units<T, D, MP, SP>() > 0) {                                                 \
-            constexpr int UU = pair_units<T, D, MP, SP>();                                              \
-            dim3 grid((unsigned)((p.B * p.nseg + UU - 1) / UU), (unsigned)p.H);                         \
-            hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP>), grid, dim3(256 * UU), 0, s, a);        \
-            return hipGetLastError();                                                                   \
-        } else if constexpr (fits<T, D, MP, SP>()) {                                                    \
+            if (p.pair) {                                                                               \
+                constexpr int UU = pair_units<T, D, MP, SP>();                                          \
+                dim3 grid((unsigned)((p.B * p.nseg + UU - 1) / UU), (unsigned)p.H);                     \
+                hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP>), grid, dim3(256 * UU), 0, s, a);    \
+                return hipGetLastError();                                                               \
+            }                                                                                           \
+        }                                                                                               \
+        if constexpr (fits<T, D, MP, SP>()) {                                                           \
             const dim3 grid((unsigned)(p.B * p.H * p.nseg));                                            \
             if (a.anchor)                                                                               \
                 hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, true>), grid, dim3(Geo<T, D, MP>::NTHR), 0, s, a); \
@@ -76,10 +79,14 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
     template <> hipError_t Launch<T, D, MP, SP>::summary(const Plan& p, const FwdArgs& a, hipStream_t s) \
     {                                                                                                   \
         if constexpr (pair_units<T, D, MP, SP>() > 0) {                                                 \
-            hipLaunchKernelGGL((summary_pair_kernel<D, MP>),                                            \
-                               dim3((unsigned)(p.B * p.nbs * summary_splits<D, MP>()), (unsigned)p.H),   \
-                               dim3(summary_threads<D, MP>()), 0, s, a);                                \
-        } else {                                                                                        \
+            if (p.pair) {                                                                               \
+                hipLaunchKernelGGL((summary_pair_kernel<D, MP>),                                        \
+                                   dim3((unsigned)(p.B * p.nbs * summary_splits<D, MP>()), (unsigned)p.H), \
+                                   dim3(summary_threads<D, MP>()), 0, s, a);                            \
+                return hipGetLastError();                                                               \
+            }                                                                                           \
+        }                                                                                               \
+        {                                                                                               \
             hipLaunchKernelGGL((summary_kernel<T, D, MP>), dim3((unsigned)(p.B * p.H * p.nbs)),         \
                                dim3(Geo<T, D, MP>::NTHR), 0, s, a);                                     \
         }                                                                                               \

@@ -41,7 +41,19 @@ def test_params_struct_layout():
     # int32 x8, then int64 t0 (8-aligned), float, int32, int32 (+4 tail pad) -> 56 bytes as in bla.h
     assert ctypes.sizeof(bla.Params) == 56
     assert bla.Params.t0.offset == 32 and bla.Params.io_dtype.offset == 44
-    assert bla.Params.phase_anchor.offset == 48
+    assert bla.Params.phase_anchor.offset == 48 and bla.Params.reuse_tables.offset == 52
+
+
+def test_reuse_tables_flag(lib):
+    """reuse_tables is 0 or 1 (anything else is an argument error); it does not change the
+    workspace size."""
+    p = P()
+    base = bla.workspace_size(p)
+    for val, expect in ((0, OK), (1, OK), (2, INVALID), (-1, INVALID)):
+        p.reuse_tables = val
+        assert bla.supported(p) == expect
+    p.reuse_tables = 1
+    assert bla.workspace_size(p) == base
 
 
 def test_phase_anchor_flag(lib):

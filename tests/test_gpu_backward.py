@@ -3,7 +3,8 @@ reverse pass through Alg. 2 (itself pinned by finite differences, autograd throu
 softmax attention and closed forms).
 
 Bars as for the forward: rel-L2 <= 1e-4 (float32 inputs) and <= 2e-2 (bfloat16 inputs), on
-dq, dk, dv and the input-state gradients; with the same per-element guard.  The bf16 bar
+dq, dk, dv and the input-state gradients; with the same per-element guard, and a per-row
+guard at 10x the rel-L2 bar.  The bf16 bar
 holds with margin: every operand of the backward's contractions is rounded to bf16 once, as
 in the forward, and the measured errors sit near the forward's (a few 1e-3).
 """
@@ -64,7 +65,9 @@ def run_bwd(q, k, v, g, T, M, S, dtype, t0=0, sk=None, sv=None, gk=None, gv=None
             _say(f"  {name}: zero reference, max-abs {emax:.3e} (scale {scale:.3e})")
             assert emax <= tol * scale, name
         else:
-            assert_close(sel(a), b, tol, name)
+            # gradients of the softmax are differences of nearly equal terms (dz = P o (dP -
+            # rowsum(P o dP))), so single rows carry more relative rounding than the forward's
+            assert_close(sel(a), b, tol, name, row_tol=10 * tol)
     return got
 
 

@@ -1,6 +1,7 @@
-"""GPU parity of the whole layer: bla_layer_forward (hipBLASLt projections, the head split and
-merge kernels and the operator) against the oracle's float64 layer (numpy projections around
-the token-by-token operator).  Bar: rel-L2 <= 2e-2 (bf16), with the per-element guard; the
+"""GPU parity of the whole layer: bla_layer_forward (hipBLASLt projections around the operator,
+which reads q, k, v in place from the projection output and writes o in the output projection's
+layout) against the oracle's float64 layer (numpy projections around the token-by-token
+operator).  Bar: rel-L2 <= 2e-2 (bf16), with the per-element guard; the
 projected q, k, v and the operator's output are rounded to bf16 on the GPU path only.
 """
 import numpy as np

@@ -2,8 +2,15 @@
 
 Bar (from the operator's specification): relative L2 error <= 1e-4 for float32
 inputs and <= 2e-2 for bfloat16 inputs, on the outputs and on the final states.
-A looser per-element check (max |err| <= 25 x bar x RMS) guards against errors
-confined to a few tokens that an L2 norm would dilute.
+Two local guards catch errors confined to a few tokens (one chunk boundary, one
+segment start) that an L2 norm over the whole tensor would dilute:
+  * per row (one token's output vector, one mode's state row): the relative error
+    of the row, ||got_t - ref_t|| / ||ref_t||, at most 2.5x the bar for bfloat16
+    (5e-2) and 10x the bar for float32 (1e-3); rows whose reference norm is below
+    a tenth of the typical (RMS) row norm are measured against that floor instead
+    (a row that is zero in exact arithmetic carries rounding noise of the size of
+    the terms that cancel in it);
+  * per element: max |err| <= 25 x bar x RMS.
 """
 import math
 import sys
@@ -38,7 +45,26 @@ def relerr(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
 
 
-def assert_close(got, ref, tol, what):
+def row_tolerance(tol):
+    """Bar on the worst row's relative error for a rel-L2 bar `tol`."""
+    return 10 * tol if tol <= 1e-4 else 2.5 * tol
+
+
+def worst_row_error(got, ref):
+    """(max over rows of ||got_r - ref_r|| / max(||ref_r||, floor), index of that row); a row
+    is the last axis (one token's output, one mode's state row)."""
+    d = ref.shape[-1] if ref.ndim else 1
+    g = got.reshape(-1, d)
+    r = ref.reshape(-1, d)
+    rn = np.linalg.norm(r, axis=1)
+    en = np.linalg.norm(g - r, axis=1)
+    floor = 0.1 * math.sqrt(float(np.mean(rn ** 2))) if rn.size else 0.0
+    rel = en / np.maximum(rn, max(floor, 1e-300))
+    i = int(np.argmax(rel)) if rel.size else 0
+    return (float(rel[i]) if rel.size else 0.0), i
+
+
+def assert_close(got, ref, tol, what, row_tol=None):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
@@ -46,8 +72,12 @@ def assert_close(got, ref, tol, what):
     e = relerr(got, ref)
     rms = math.sqrt(float(np.mean(ref ** 2))) if ref.size else 0.0
     emax = float(np.max(np.abs(got - ref))) if ref.size else 0.0
-    _say(f"  {what}: rel-L2 {e:.3e} (bar {tol:.0e}), max-abs {emax:.3e}, rms {rms:.3e}")
+    row_tol = row_tolerance(tol) if row_tol is None else row_tol
+    er, ir = worst_row_error(got, ref)
+    _say(f"  {what}: rel-L2 {e:.3e} (bar {tol:.0e}), worst row {er:.3e} at row {ir} (bar {row_tol:.1e}), "
+         f"max-abs {emax:.3e}, rms {rms:.3e}")
     assert e <= tol, f"{what}: rel-L2 {e:.3e} > {tol:.0e}"
+    assert er <= row_tol, f"{what}: row {ir} relative error {er:.3e} > {row_tol:.1e}"
     assert emax <= 25 * tol * max(rms, 1e-30), f"{what}: max-abs {emax:.3e}"
 
 
@@ -205,7 +235,10 @@ def test_workload2_recall_bf16():
 
 def test_workload3_lm_layer_sampled_rows():
     """Full LM-layer workload on the GPU (the benchmark's launch configuration); the oracle
-    checks every head of two batch rows, first and last."""
+    checks every head and every token of three batch rows: first, middle and last.  The
+    sequences run as several segments (their entering states combined from the preceding
+    segments' summaries); the tokens around every quarter of the sequence and every chunk
+    start are also checked on their own."""
     bla = _bla()
     w = bi.WORKLOADS[3]
     T = bi.periods(w.M, w.H)
@@ -214,9 +247,13 @@ def test_workload3_lm_layer_sampled_rows():
     tq, tk, tv = (to_dev(x, torch.bfloat16) for x in (q, k, v))
     o, sk, sv = bla.forward(tq, tk, tv, T, w.M, w.S)
     torch.cuda.synchronize()
-    for b in (0, w.B - 1):
+    starts = sorted({t for j in range(4) for t in (j * w.L // 4 - 1, j * w.L // 4, j * w.L // 4 + 1) if t >= 0} |
+                    set(range(0, w.L, w.chunk)))
+    for b in (0, w.B // 2, w.B - 1):
         ref_o, ref_k, ref_v = oracle.forward(q[b:b + 1], k[b:b + 1], v[b:b + 1], T, w.M, w.S)
-        assert_close(o[b:b + 1].float().cpu().numpy(), ref_o, 2e-2, f"O row {b}")
+        got = o[b:b + 1].float().cpu().numpy()
+        assert_close(got, ref_o, 2e-2, f"O row {b}")
+        assert_close(got[:, :, starts], ref_o[:, :, starts], 2e-2, f"O row {b}, segment and chunk starts")
         assert_close(sk[b:b + 1].cpu().numpy(), ref_k, 2e-2, f"state_k row {b}")
         assert_close(sv[b:b + 1].cpu().numpy(), ref_v, 2e-2, f"state_v row {b}")
 

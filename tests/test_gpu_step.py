@@ -55,7 +55,7 @@ def test_step_first_token_mask():
 
 def test_workload5_decode():
     """Decode workload: B=512, H=16, d=M=S=64.  Prefill 2048 tokens with bla_forward, then
-    bla_step at position 2048.  Checked on two batch rows (all heads): (a) the whole GPU path
+    bla_step at position 2048.  Checked on three batch rows (all heads): (a) the whole GPU path
     against the oracle's prefill + step; (b) the step alone from the oracle's prefill state."""
     bla = _bla()
     w = bi.WORKLOADS[5]
@@ -69,7 +69,7 @@ def test_workload5_decode():
     del pq, pk, pv
     o = bla.step(sq, sk_, sv_, T, w.M, w.S, gk, gv, t0=L)
     torch.cuda.synchronize()
-    for b in (0, w.B - 1):
+    for b in (0, w.B // 2 + 1, w.B - 1):
         hq = q[b:b + 1].float().cpu().numpy()
         hk = k[b:b + 1].float().cpu().numpy()
         hv = v[b:b + 1].float().cpu().numpy()
