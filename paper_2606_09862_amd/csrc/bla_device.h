@@ -28,6 +28,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef int intx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
 
 template <typename T> struct Frag;
 template <> struct Frag<bf16> { typedef bf16x8 type; typedef bf16x4 half; };
@@ -198,6 +199,24 @@ __device__ __forceinline__ float rows_sum(float x)
     const unsigned v = __float_as_uint(y);
     const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Complex twiddle of four accumulator rows with a half-precision phase (c, n):
+//     (re, im) <- (c re + n im, c im - n re)        (NEG: n replaced by -n)
+// Each product takes its half-precision factor as a mixed-precision FMA operand, so the
+// phase needs no conversion (the product with the zero addend stays an FMA).
+template <bool NEG>
+__device__ __forceinline__ void twiddle_h(halfx4 c, halfx4 n, floatx4& re, floatx4& im)
+{
+    floatx4 r, i;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float cf = (float)c[e], nf = NEG ? -(float)n[e] : (float)n[e];
+        r[e] = __builtin_fmaf(cf, re[e], __builtin_fmaf(nf, im[e], 0.f));
+        i[e] = __builtin_fmaf(cf, im[e], __builtin_fmaf(-nf, re[e], 0.f));
+    }
+    re = r;
+    im = i;
 }
 
 // cos and sin of the absolute phase m w P (w = 2 pi / T) for the anchored slots of

@@ -61,7 +61,10 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
             if (p.pair) {                                                                               \
                 constexpr int UU = pair_units<T, D, MP, SP>();                                          \
                 dim3 grid((unsigned)((p.B * p.nseg + UU - 1) / UU), (unsigned)p.H);                     \
-                hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP>), grid, dim3(256 * UU), 0, s, a);    \
+                if (a.anchor)                                                                           \
+                    hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP, true>), grid, dim3(256 * UU), 0, s, a); \
+                else                                                                                    \
+                    hipLaunchKernelGGL((forward_pair_kernel<D, MP, SP, false>), grid, dim3(256 * UU), 0, s, a); \
                 return hipGetLastError();                                                               \
             }                                                                                           \
         }                                                                                               \

@@ -96,7 +96,8 @@ __device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf1
     }
 }
 
-template <int D, int MP, int SP>
+// FULL: the chunk has all C rows (no zero fill past c).
+template <int D, int MP, int SP, bool FULL>
 __device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf16* Qs,
                                                  bf16* Ks, bf16* Vs, int c, int ut)
 {
@@ -109,7 +110,7 @@ __device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf
             const int which = u / (P::C * PR), rem = u % (P::C * PR);
             const int row = rem / PR, pc = rem % PR;
             bf16* dst = which == 0 ? Qs + (size_t)row * P::LQ : (which == 1 ? Ks : Vs) + (size_t)row * P::LK;
-            const bf16x8 x = (c == P::C || row < c) ? st[i] : bf16x8{};
+            const bf16x8 x = (FULL || row < c) ? st[i] : bf16x8{};
             *reinterpret_cast<bf16x4*>(dst + 8 * pc) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
             *reinterpret_cast<bf16x4*>(dst + 8 * pc + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
         }
@@ -528,7 +529,7 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
 //   2. each wave publishes its state tiles for the next chunk and stages the next chunk.
 // The second unit takes the token tiles in reverse order, so that every SIMD runs one
 // short and one long causal tile.
-template <int D, int MP, int SP>
+template <int D, int MP, int SP, bool ANCHOR>
 __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kernel(FwdArgs a)
 {
     using P = Pair<D, MP, SP>;
@@ -562,7 +563,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     bf16* Qs = Vs + (size_t)C * P::LK;
     bf16* ZkT = Qs + (size_t)C * P::LQ;
     bf16* ZvT = ZkT + (size_t)2 * MP * P::LZK;
-    bf16* sPh = ZvT + (size_t)D * P::LZ;
+    _Float16* sPh = reinterpret_cast<_Float16*>(ZvT + (size_t)D * P::LZ);  // anchored twiddle row
 
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     // ---- shared tables
@@ -594,15 +595,25 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     };
 
     // anchored slots: the twiddle row of chunk n at its absolute start t0 + (ch0 + n) C
-    const double rT = a.anchor ? a.rperiod[h] : 0.0;
+    const double rT = ANCHOR ? a.rperiod[h] : 0.0;
     auto phase_row = [&](int n) {
-        if (a.anchor) {
+        if constexpr (ANCHOR) {
             for (int m = ut; m < MP; m += 256) {
                 float cs = 0.f, sn = 0.f;
                 if (m < a.M) anchor_phase(m, a.t0 + (long long)(ch0 + n) * C, rT, cs, sn);
-                sPh[m] = (bf16)cs;
-                sPh[MP + m] = (bf16)sn;
+                sPh[m] = (_Float16)cs;
+                sPh[MP + m] = (_Float16)sn;
             }
+        }
+    };
+    halfx4 twc[NMT], tws[NMT];
+    auto twiddle_row = [&](int mt, halfx4& c, halfx4& n) {
+        if constexpr (ANCHOR) {
+            c = *reinterpret_cast<const halfx4*>(sPh + 16 * mt + 4 * g);
+            n = *reinterpret_cast<const halfx4*>(sPh + MP + 16 * mt + 4 * g);
+        } else {
+            c = twc[mt];
+            n = tws[mt];
         }
     };
 
@@ -694,11 +705,34 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             }
         }
     }
+    // Rotating slots: the twiddle row of steps (3) and (7) is the lane's own phase row
+    // conj(rho^j) = [cos | -sin](m w j) of its token j = 16 tt + r, the same in every chunk,
+    // so it is held in registers as half precision for the whole segment (modes 16 mt + 4 g
+    // .. + 3 of each mode tile mt).  Loaded after the summary combination, whose buffers
+    // need the registers.
+    if constexpr (!ANCHOR) {
+        const float* Ej = E32h + (size_t)(16 * tt + r) * 2 * MP;
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) {
+            const floatx4 cv = ld4f(Ej + 16 * mt + 4 * g), sv = ld4f(Ej + MP + 16 * mt + 4 * g);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                twc[mt][e] = (_Float16)cv[e];
+                tws[mt][e] = (_Float16)(-sv[e]);
+            }
+        }
+    }
     PStage<D, MP, SP> st;
     stage_chunk(st, 0);
     pair_write_zk<D, MP, SP>(ZkT, Zk, wl, g, r);
     pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
-    pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, nch > 0 ? min(C, a.L - ch0 * C) : 0, ut);
+    {
+        const int c0 = nch > 0 ? min(C, a.L - ch0 * C) : 0;
+        if (c0 == C)
+            pair_stage_store<D, MP, SP, true>(st, Qs, Ks, Vs, c0, ut);
+        else
+            pair_stage_store<D, MP, SP, false>(st, Qs, Ks, Vs, c0, ut);
+    }
     phase_row(0);
     stage_chunk(st, 1);
     __syncthreads();  // chunk 0 and the initial state visible
@@ -714,7 +748,6 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         // ================= phase 1: the token chain of tile tt (steps 1-9)
         {
             const int j = 16 * tt + r;
-            const bf16* tw = a.anchor ? sPh : sE + (size_t)j * P::LE;  // twiddle row of steps (3), (7)
             F qf[P::KBD];
 #pragma unroll
             for (int kb = 0; kb < P::KBD; ++kb) qf[kb] = ld_frag<bf16>(Qs + (size_t)j * P::LQ, 32 * kb, g);
@@ -756,11 +789,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             // (3) U = E o X  (anchored: [Re | -Im] of rho^P o conj(X))
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = to_f4(ld4<bf16>(tw + 16 * mt + 4 * g));
-                const floatx4 ns = to_f4(ld4<bf16>(tw + MP + 16 * mt + 4 * g));
-                const floatx4 re = ua[mt], im = ua[NMT + mt];
-                ua[mt] = cs * re + ns * im;
-                ua[NMT + mt] = cs * im - ns * re;
+                halfx4 cs, ns;
+                twiddle_row(mt, cs, ns);
+                twiddle_h<false>(cs, ns, ua[mt], ua[NMT + mt]);
             }
             F uf[P::KBM];
 #pragma unroll
@@ -781,8 +812,26 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             // the slot and padded slots carry INT32_MAX, so a chunk whose first position
             // reaches the last threshold needs no mask.
             const float k2 = a.scale * 1.44269504088896341f;
-            float mx = -INFINITY;
-            if (a.t0 + tok0 < (long long)sTheta[SP - 1]) {
+            float sum = 0.f;
+            if (k2 > 0.f && a.t0 + tok0 >= (long long)sTheta[SP - 1]) {
+                // no slot masked and a positive scale: the maximum of the raw scores, and the
+                // scale folded into the exponent's argument, exp2(k2 z - k2 max z)
+                float mx = -INFINITY;
+#pragma unroll
+                for (int s4 = 0; s4 < P::NST; ++s4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[s4][e]);
+                const float nm = -k2 * rows_max(mx);
+#pragma unroll
+                for (int s4 = 0; s4 < P::NST; ++s4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float ex = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[s4][e], k2, nm));
+                        sc[s4][e] = ex;
+                        sum += ex;
+                    }
+            } else {
+                float mx = -INFINITY;
 #pragma unroll
                 for (int s4 = 0; s4 < P::NST; ++s4) {
                     const intx4 th = *reinterpret_cast<const intx4*>(sTheta + 16 * s4 + 4 * g);
@@ -792,25 +841,16 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                         mx = fmaxf(mx, sc[s4][e]);
                     }
                 }
-            } else {
+                mx = rows_max(mx);
 #pragma unroll
                 for (int s4 = 0; s4 < P::NST; ++s4)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        sc[s4][e] *= k2;
-                        mx = fmaxf(mx, sc[s4][e]);
+                        const float ex = __builtin_amdgcn_exp2f(sc[s4][e] - mx);
+                        sc[s4][e] = ex;
+                        sum += ex;
                     }
             }
-            mx = rows_max(mx);
-            float sum = 0.f;
-#pragma unroll
-            for (int s4 = 0; s4 < P::NST; ++s4)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float ex = __builtin_amdgcn_exp2f(sc[s4][e] - mx);
-                    sc[s4][e] = ex;
-                    sum += ex;
-                }
             sum = rows_sum(sum);
             const float inv = __builtin_amdgcn_rcpf(sum);  // sum >= 1: the maximum slot contributes exp(0)
             F pf[P::KBS];
@@ -825,14 +865,13 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 #pragma unroll
                 for (int kb = 0; kb < P::KBS; ++kb) wa[t] = mma(ld_frag_tr(sAB, P::LAB, 16 * t, kb, g, r), pf[kb], wa[t]);
             }
-            // (7) [Re W'' | -Im W''] with W'' = (a - i b) o E  (anchored: (a + i b) o conj(rho^P))
+            // (7) [Re W'' | -Im W''] with W'' = (a - i b) o E  (anchored: (a + i b) o conj(rho^P)):
+            //     (a, b) <- (a c - b n, b c + a n)
 #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const floatx4 cs = to_f4(ld4<bf16>(tw + 16 * mt + 4 * g));
-                const floatx4 ns = to_f4(ld4<bf16>(tw + MP + 16 * mt + 4 * g));
-                const floatx4 am = wa[mt], bm = wa[NMT + mt];
-                wa[mt] = am * cs - bm * ns;
-                wa[NMT + mt] = am * ns + bm * cs;
+                halfx4 cs, ns;
+                twiddle_row(mt, cs, ns);
+                twiddle_h<true>(cs, ns, wa[mt], wa[NMT + mt]);
             }
             F wf[P::KBM];
 #pragma unroll
@@ -890,7 +929,10 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
         }
         const int cn = n + 1 < nch ? min(C, a.L - (tok0 + C)) : 0;
-        pair_stage_store<D, MP, SP>(st, Qs, Ks, Vs, cn, ut);
+        if (cn == C)
+            pair_stage_store<D, MP, SP, true>(st, Qs, Ks, Vs, cn, ut);
+        else
+            pair_stage_store<D, MP, SP, false>(st, Qs, Ks, Vs, cn, ut);
         phase_row(n + 1);
         stage_chunk(st, n + 2);
         __syncthreads();  // chunk n + 1 and its state visible
