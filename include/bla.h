@@ -150,6 +150,25 @@ bla_status bla_forward_timed(const bla_params* p, const double* T, const void* q
                              float* state_k_out, float* state_v_out, void* workspace,
                              size_t workspace_bytes, void* stream, void* const* events);
 
+/*
+ * bla_forward for callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops and harnesses that forbid hipMalloc).  The workspace is a fixed array inside
+ * the library, BLA_NOALLOC_SCRATCH_BYTES bytes per device (each device the library runs on
+ * holds its own copy until the process ends; its address is taken once per device, on the
+ * first call there).  The call allocates nothing: no hipMalloc, hipFree or allocating library
+ * routine.  Arguments and results are exactly those of bla_forward without the workspace
+ * arguments; a shape whose bla_workspace_size exceeds BLA_NOALLOC_SCRATCH_BYTES returns
+ * BLA_ERR_WORKSPACE before anything is launched.  Every call on a device shares that
+ * device's array, which keeps the last call's contents (the forward writes every byte it
+ * reads, so nothing needs clearing): calls that overlap in time on one device race, so
+ * order them on one stream.  reuse_tables = 1 keeps the tables of the previous call
+ * through this entry point, under the same rules as for a caller's workspace.
+ */
+#define BLA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+bla_status bla_forward_noalloc(const bla_params* p, const double* T, const void* q, const void* k,
+                               const void* v, const float* state_k_in, const float* state_v_in, void* o,
+                               float* state_k_out, float* state_v_out, void* stream);
+
 /* Bytes of device workspace bla_step needs for *p (L is ignored). */
 size_t bla_step_workspace_size(const bla_params* p);
 

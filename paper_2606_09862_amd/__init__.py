@@ -60,6 +60,8 @@ def lib():
         L.bla_forward.argtypes = [P, _dp] + [_vp] * 9 + [ctypes.c_size_t, _vp]
         L.bla_forward.restype = ctypes.c_int
         L.bla_step.argtypes = [P, _dp] + [_vp] * 8 + [ctypes.c_size_t, _vp]
+        L.bla_forward_noalloc.argtypes = [P, _dp] + [_vp] * 8 + [_vp]
+        L.bla_forward_noalloc.restype = ctypes.c_int
         L.bla_interp_tables.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dp, _dp,
                                         ctypes.POINTER(ctypes.c_int32)]
         L.bla_interp_tables.restype = ctypes.c_int
@@ -191,6 +193,33 @@ def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
     if st != 0:
         raise BlaError(st, "bla_forward")
     return o, sk, sv
+
+
+def forward_noalloc(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
+                    state_k=None, state_v=None, out=None, state_k_out=None, state_v_out=None,
+                    phase_anchor: bool = False, reuse_tables: bool = False):
+    """bla_forward_noalloc: bla_forward with the library's own fixed device workspace.  The
+    library allocates nothing; the caller passes every output (`out`, and `state_k_out` /
+    `state_v_out` float32 [B,H,2,M,d], None = not wanted).  Returns (o, state_k_out, state_v_out)."""
+    B, H, L, d = q.shape
+    dt = q.dtype
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check(t, (B, H, L, d), dt, name)
+    if out is None:
+        raise ValueError("out: bla_forward_noalloc needs the caller's output buffer")
+    o = _out(out, q, (B, H, L, d))
+    for name, t in (("state_k", state_k), ("state_v", state_v), ("state_k_out", state_k_out),
+                    ("state_v_out", state_v_out)):
+        if t is not None:
+            _check(t, (B, H, 2, M, d), torch.float32, name)
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale,
+                    phase_anchor=phase_anchor, reuse_tables=reuse_tables)
+    st = lib().bla_forward_noalloc(ctypes.byref(p), _periods(T, H), _ptr(q), _ptr(k), _ptr(v), _ptr(state_k),
+                                   _ptr(state_v), _ptr(o), _ptr(state_k_out), _ptr(state_v_out),
+                                   _stream(q.device))
+    if st != 0:
+        raise BlaError(st, "bla_forward_noalloc")
+    return o, state_k_out, state_v_out
 
 
 def step(q, k, v, T, M: int, S: int, state_k, state_v, pos=None, t0: int = 0,
