@@ -114,6 +114,45 @@ __device__ __forceinline__ bf16x8 ld_frag_tr(const bf16* M, int ld, int x0, int 
     return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
 }
 
+// Fragment-ordered rows.  An operand fragment takes the reduction indices 32kb + 4g .. + 3
+// and 32kb + 16 + 4g .. + 3 of a row (the order two stacked accumulator tiles give).  A table
+// whose rows are stored with the 4-column group 16h + 4j (h = 0, 1; j = 0..3) of every block
+// of 32 columns moved to 8j + 4h holds those eight indices next to each other, so the
+// fragment is one 16-byte LDS read instead of two 8-byte reads 32 bytes apart (which gfx950
+// serves at a quarter of the 16-byte rate).  frag_col maps a logical column (a multiple of 4)
+// to its stored position.
+__host__ __device__ constexpr int frag_col(int c)
+{
+    return (c & ~31) | (((c >> 2) & 3) << 3) | (((c >> 4) & 1) << 2);
+}
+
+// Fragment from a fragment-ordered row, or from a natural row with the reduction order
+// k(e) = 32kb + 8g + e (both operands of a contraction must use the same order): one
+// 16-byte read at 32kb + 8g.
+__device__ __forceinline__ bf16x8 ld_frag16(const bf16* row, int kb, int g)
+{
+    return *reinterpret_cast<const bf16x8*>(row + 32 * kb + 8 * g);
+}
+
+// Fragment of a natural row for the accumulator order (32kb + 4g .. + 3, 32kb + 16 + 4g ..
+// + 3) as two separate 8-byte LDS reads.  The second read is volatile so that the two are not
+// merged into one ds_read2_b64, which gfx950 serves at a quarter to half of the rate of two
+// ds_read_b64 at these addresses.
+__device__ __forceinline__ bf16x8 ld_frag_2x8(const bf16* row, int kb, int g)
+{
+    typedef const __attribute__((address_space(3))) bf16x4 lds4;
+    lds4* a = (lds4*)(row + 32 * kb + 4 * g);
+    return join(*a, *(const volatile __attribute__((address_space(3))) bf16x4*)(a + 4));
+}
+
+// ld_frag_tr on a tile whose columns are fragment-ordered (4-column groups stay contiguous,
+// so each lane's 4 consecutive elements are still one 8-byte read).
+__device__ __forceinline__ bf16x8 ld_frag_tr_fo(const bf16* M, int ld, int x0, int kb, int g, int r)
+{
+    const bf16* p = M + (size_t)(32 * kb + 4 * g + (r >> 2)) * ld + frag_col(x0 + 4 * (r & 3));
+    return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
+}
+
 // Four consecutive elements as a vector (pointer 4-element aligned).
 template <typename T> __device__ __forceinline__ typename Frag<T>::half ld4(const T* p)
 {

@@ -43,30 +43,37 @@ template <int D, int MP, int SP> struct Pair {
     static constexpr int NMT = MP / 16, NDT = D / 16, NST = SP / 16;
     static constexpr int KBD = D / 32, KBM = 2 * MP / 32, KBC = C / 32, KBS = SP / 32;
     static constexpr int OWN = (NMT + WPU - 1) / WPU;
-    // Row strides (elements).  Tiles read both row-wise and transposed use a
-    // 12-element pad (stride = 6 words mod 32 banks): row-wise fragment reads are
-    // conflict-free and transposed reads have at most 2-way conflicts.  Tiles read
-    // row-wise only use a 4-element pad (stride = 2 words mod 32).
-    static constexpr int LAB = 2 * MP + 12;  // [A|B]:     [SP][LAB]
-    static constexpr int LE = 2 * MP + 12;   // phase tab: [C][LE]
-    static constexpr int LK = D + 12;        // K, V:      [C][LK]
-    static constexpr int LQ = D + 4;         // Q:         [C][LQ]
-    static constexpr int LZK = D + 4;        // Z'_k:      [2MP][LZK]  (Re rows, then Im rows)
-    static constexpr int LZ = 2 * MP + 4;    // Z'_v:      [D][LZ]     (Re | Im along the row)
+    // Row strides (elements): every row is 16 elements longer than its data, i.e. the stride
+    // is 8 (mod 32) dwords.  With that stride a 16-lane group's 16-byte row-fragment reads
+    // (16 rows, same columns) and its transposed reads (4 rows x 32 bytes) both run at the
+    // full LDS rate on gfx950 (about 230 and 180 B/clk per compute unit, against about 120 at
+    // strides of 2, 4 or 6 (mod 32) dwords).  Z'_v, read only row-wise against accumulator-
+    // derived fragments, is stored fragment-ordered (frag_col: one 16-byte read per
+    // fragment).  K, V and Z'_k, whose row fragments pair with the query rows, keep the
+    // natural order and use the reduction order 32kb + 8g + e (16-byte reads as well).  The
+    // slot matrix and the phase table are read transposed more often than row-wise, so they
+    // keep the natural order, whose transposed reads are conflict-free at this stride, and
+    // their row fragments are two separate 8-byte reads.
+    static constexpr int LAB = 2 * MP + 16;  // [A|B]:     [SP][LAB]
+    static constexpr int LE = 2 * MP + 16;   // phase tab: [C][LE]
+    static constexpr int LK = D + 16;        // K, V:      [C][LK]
+    static constexpr int LZK = D + 16;       // Z'_k:      [2MP][LZK]  (Re rows, then Im rows)
+    static constexpr int LZ = 2 * MP + 16;   // Z'_v:      [D][LZ]     (Re | Im along the row, fragment-ordered)
     // per unit, after Z'_v: the anchored twiddle row [cos | sin](m w P) of the chunk, [2MP]
+    // (the queries do not pass through LDS: each lane loads its own token's fragments)
     static constexpr size_t AB_ELEMS = (size_t)SP * LAB;
     static constexpr size_t E_ELEMS = (size_t)C * LE;
     static constexpr size_t SHARED_BYTES = 2 * (AB_ELEMS + E_ELEMS) + 3 * 2 * MP * 4 + SP * 4;
     static constexpr size_t UNIT_ELEMS =
-        2 * (size_t)C * LK + (size_t)C * LQ + (size_t)2 * MP * LZK + (size_t)D * LZ + (size_t)2 * MP;
+        2 * (size_t)C * LK + (size_t)2 * MP * LZK + (size_t)D * LZ + (size_t)2 * MP;
     static constexpr size_t UNIT_BYTES = 2 * UNIT_ELEMS;
     // two units per workgroup (two waves per SIMD) when their tiles fit in LDS and their
     // registers in half of the file (at most four owned state tiles per wave)
     static constexpr int U = (SHARED_BYTES + 2 * UNIT_BYTES <= kMaxLds && D <= 64 && MP <= 64) ? 2 : 1;
     static constexpr bool FITS = SHARED_BYTES + U * UNIT_BYTES <= kMaxLds;
     static constexpr size_t LDS_BYTES = SHARED_BYTES + U * UNIT_BYTES;
-    // staging: Q, K, V of one chunk in 16-byte pieces, spread over the unit's 256 threads
-    static constexpr int PIECES = 3 * C * D / 8;
+    // staging: K and V of one chunk in 16-byte pieces, spread over the unit's 256 threads
+    static constexpr int PIECES = 2 * C * D / 8;
     static constexpr int PPT = (PIECES + 255) / 256;
     static_assert(NT == WPU, "one token tile per wave of a unit");
 };
@@ -75,11 +82,11 @@ template <int D, int MP> using PStateDM = floatx4[(MP / 16 + 3) / 4][2][D / 16];
 template <int D, int MP, int SP> using PState = PStateDM<D, MP>;
 template <int D, int MP, int SP> using PStage = bf16x8[Pair<D, MP, SP>::PPT];
 
-// ut: thread index within the unit (0..255); q, k, v: the chunk's first rows.
-// ts: token stride of q, k, v (elements).
+// ut: thread index within the unit (0..255); k, v: the chunk's first rows.
+// ts: token stride of k, v (elements).
 template <int D, int MP, int SP>
-__device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf16* q,
-                                                const bf16* k, const bf16* v, int ts, int c, int ut)
+__device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf16* k, const bf16* v, int ts,
+                                                int c, int ut)
 {
     using P = Pair<D, MP, SP>;
     constexpr int PR = D / 8;  // pieces per row
@@ -90,36 +97,37 @@ __device__ __forceinline__ void pair_stage_load(PStage<D, MP, SP>& st, const bf1
             const int which = u / (P::C * PR), rem = u % (P::C * PR);
             const int row = min(rem / PR, c - 1), pc = rem % PR;
             const unsigned off = (unsigned)(row * ts + 8 * pc);  // within one chunk
-            const bf16* src = (which == 0 ? q : which == 1 ? k : v) + off;
+            const bf16* src = (which == 0 ? k : v) + off;
             st[i] = *reinterpret_cast<const bf16x8*>(src);
         }
     }
 }
 
-// FULL: the chunk has all C rows (no zero fill past c).
+// FULL: the chunk has all C rows (no zero fill past c).  Rows are 16-byte aligned (LK is a
+// multiple of 8 elements), so each piece is one 16-byte store.
 template <int D, int MP, int SP, bool FULL>
-__device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf16* Qs,
-                                                 bf16* Ks, bf16* Vs, int c, int ut)
+__device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf16* Ks, bf16* Vs, int c, int ut)
 {
     using P = Pair<D, MP, SP>;
     constexpr int PR = D / 8;
+    static_assert(P::LK % 8 == 0, "16-byte rows");
 #pragma unroll
     for (int i = 0; i < P::PPT; ++i) {
         const int u = ut + 256 * i;
         if (P::PIECES % 256 == 0 || u < P::PIECES) {
             const int which = u / (P::C * PR), rem = u % (P::C * PR);
             const int row = rem / PR, pc = rem % PR;
-            bf16* dst = which == 0 ? Qs + (size_t)row * P::LQ : (which == 1 ? Ks : Vs) + (size_t)row * P::LK;
+            bf16* dst = (which == 0 ? Ks : Vs) + (size_t)row * P::LK;
             const bf16x8 x = (FULL || row < c) ? st[i] : bf16x8{};
-            *reinterpret_cast<bf16x4*>(dst + 8 * pc) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
-            *reinterpret_cast<bf16x4*>(dst + 8 * pc + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
+            *reinterpret_cast<bf16x8*>(dst + 8 * pc) = x;
         }
     }
 }
 
 // Copy a table of ROWS x COLS bf16 (source rows contiguous) into LDS rows of stride DST,
-// all loads of a thread in flight before its stores.
-template <int ROWS, int COLS, int DST, int NTHR>
+// all loads of a thread in flight before its stores.  FO: store the rows fragment-ordered
+// (frag_col).
+template <int ROWS, int COLS, int DST, int NTHR, bool FO = false>
 __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
 {
     typedef int intx2 __attribute__((ext_vector_type(2)));
@@ -133,8 +141,10 @@ __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
 #pragma unroll
     for (int i = 0; i < ITER; ++i) {
         const int u = tid + i * NTHR;
-        if (PIECES % NTHR == 0 || u < PIECES)
-            *reinterpret_cast<intx2*>(dst + (size_t)(u / (COLS / 4)) * DST + 4 * (u % (COLS / 4))) = buf[i];
+        if (PIECES % NTHR == 0 || u < PIECES) {
+            const int col = 4 * (u % (COLS / 4));
+            *reinterpret_cast<intx2*>(dst + (size_t)(u / (COLS / 4)) * DST + (FO ? frag_col(col) : col)) = buf[i];
+        }
     }
 }
 
@@ -167,8 +177,8 @@ __device__ __forceinline__ void pair_write_zv(bf16* ZvT, const PState<D, MP, SP>
         if (mt < P::NMT) {
 #pragma unroll
             for (int dt = 0; dt < P::NDT; ++dt) {
-                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + 16 * mt + 4 * g, Zv[o][0][dt]);
-                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + MP + 16 * mt + 4 * g, Zv[o][1][dt]);
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + frag_col(16 * mt + 4 * g), Zv[o][0][dt]);
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + frag_col(MP + 16 * mt + 4 * g), Zv[o][1][dt]);
             }
         }
     }
@@ -560,8 +570,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     bf16* base = reinterpret_cast<bf16*>(lds_raw + P::SHARED_BYTES + (size_t)u * P::UNIT_BYTES);
     bf16* Ks = base;
     bf16* Vs = Ks + (size_t)C * P::LK;
-    bf16* Qs = Vs + (size_t)C * P::LK;
-    bf16* ZkT = Qs + (size_t)C * P::LQ;
+    bf16* ZkT = Vs + (size_t)C * P::LK;
     bf16* ZvT = ZkT + (size_t)2 * MP * P::LZK;
     _Float16* sPh = reinterpret_cast<_Float16*>(ZvT + (size_t)D * P::LZ);  // anchored twiddle row
 
@@ -590,8 +599,17 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
     const int last = max(nch - 1, 0);
     auto stage_chunk = [&](PStage<D, MP, SP>& st, int n) {
         const int tn = (ch0 + min(n, last)) * C, cn = min(C, a.L - tn);
-        pair_stage_load<D, MP, SP>(st, qb + (size_t)tn * ts, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts, cn,
-                                   ut);
+        pair_stage_load<D, MP, SP>(st, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts, cn, ut);
+    };
+    // The query fragments of the wave's own token row j = 16 tt + r of chunk n (clamped to the
+    // chunk's last token; rows past it are computed and never stored), elements 32kb + 8g ..
+    // + 7: the reduction order of steps (1)-(2), whose other operands (Z'_k and K rows) are
+    // stored in the natural order.  Loaded straight from memory one chunk ahead.
+    auto load_q = [&](bf16x8 (&qd)[P::KBD], int n) {
+        const int tn = (ch0 + min(n, last)) * C, cn = min(C, a.L - tn);
+        const bf16* src = qb + (size_t)(tn + min(16 * tt + r, cn - 1)) * ts + 8 * g;
+#pragma unroll
+        for (int kb = 0; kb < P::KBD; ++kb) qd[kb] = *reinterpret_cast<const bf16x8*>(src + 32 * kb);
     };
 
     // anchored slots: the twiddle row of chunk n at its absolute start t0 + (ch0 + n) C
@@ -723,15 +741,17 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         }
     }
     PStage<D, MP, SP> st;
+    F qf[P::KBD];
+    load_q(qf, 0);
     stage_chunk(st, 0);
     pair_write_zk<D, MP, SP>(ZkT, Zk, wl, g, r);
     pair_write_zv<D, MP, SP>(ZvT, Zv, wl, g, r);
     {
         const int c0 = nch > 0 ? min(C, a.L - ch0 * C) : 0;
         if (c0 == C)
-            pair_stage_store<D, MP, SP, true>(st, Qs, Ks, Vs, c0, ut);
+            pair_stage_store<D, MP, SP, true>(st, Ks, Vs, c0, ut);
         else
-            pair_stage_store<D, MP, SP, false>(st, Qs, Ks, Vs, c0, ut);
+            pair_stage_store<D, MP, SP, false>(st, Ks, Vs, c0, ut);
     }
     phase_row(0);
     stage_chunk(st, 1);
@@ -748,9 +768,6 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         // ================= phase 1: the token chain of tile tt (steps 1-9)
         {
             const int j = 16 * tt + r;
-            F qf[P::KBD];
-#pragma unroll
-            for (int kb = 0; kb < P::KBD; ++kb) qf[kb] = ld_frag<bf16>(Qs + (size_t)j * P::LQ, 32 * kb, g);
             // (1)-(2) X = Q Z'_k^T + G conj(E): tiles over [Re | Im] modes (rows) x tokens (columns)
             floatx4 ua[2 * NMT];
 #pragma unroll
@@ -758,7 +775,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 ua[t] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < P::KBD; ++kb)
-                    ua[t] = mma(ld_frag<bf16>(ZkT + (size_t)(16 * t + r) * P::LZK, 32 * kb, g), qf[kb], ua[t]);
+                    ua[t] = mma(ld_frag16(ZkT + (size_t)(16 * t + r) * P::LZK, kb, g), qf[kb], ua[t]);
             }
             floatx4 ga[NT];  // Gram tiles: keys (rows) x this tile's queries (columns), keys <= query
 #pragma unroll
@@ -767,7 +784,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 if (kt <= tt) {
 #pragma unroll
                     for (int kb = 0; kb < P::KBD; ++kb)
-                        ga[kt] = mma(ld_frag<bf16>(Ks + (size_t)(16 * kt + r) * P::LK, 32 * kb, g), qf[kb], ga[kt]);
+                        ga[kt] = mma(ld_frag16(Ks + (size_t)(16 * kt + r) * P::LK, kb, g), qf[kb], ga[kt]);
                     if (kt == tt) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
@@ -775,6 +792,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     }
                 }
             }
+            load_q(qf, n + 1);  // the queries of this chunk are no longer needed
 #pragma unroll
             for (int kb = 0; kb < P::KBC; ++kb) {
                 if (2 * kb <= tt) {
@@ -806,7 +824,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 sc[s4] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < P::KBM; ++kb)
-                    sc[s4] = mma(ld_frag<bf16>(sAB + (size_t)(16 * s4 + r) * P::LAB, 32 * kb, g), uf[kb], sc[s4]);
+                    sc[s4] = mma(ld_frag_2x8(sAB + (size_t)(16 * s4 + r) * P::LAB, kb, g), uf[kb], sc[s4]);
             }
             // (5) masked softmax in base-2 units (z * scale * log2 e).  Thresholds grow with
             // the slot and padded slots carry INT32_MAX, so a chunk whose first position
@@ -884,7 +902,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 oa[dt] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < P::KBM; ++kb)
-                    oa[dt] = mma(ld_frag<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ, 32 * kb, g), wf[kb], oa[dt]);
+                    oa[dt] = mma(ld_frag16(ZvT + (size_t)(16 * dt + r) * P::LZ, kb, g), wf[kb], oa[dt]);
             }
             floatx4 hh[NT];
 #pragma unroll
@@ -893,7 +911,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 if (kt <= tt) {
 #pragma unroll
                     for (int kb = 0; kb < P::KBM; ++kb)
-                        hh[kt] = mma(ld_frag<bf16>(sE + (size_t)(16 * kt + r) * P::LE, 32 * kb, g), wf[kb], hh[kt]);
+                        hh[kt] = mma(ld_frag_2x8(sE + (size_t)(16 * kt + r) * P::LE, kb, g), wf[kb], hh[kt]);
                     if (kt == tt) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
@@ -930,9 +948,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
         }
         const int cn = n + 1 < nch ? min(C, a.L - (tok0 + C)) : 0;
         if (cn == C)
-            pair_stage_store<D, MP, SP, true>(st, Qs, Ks, Vs, cn, ut);
+            pair_stage_store<D, MP, SP, true>(st, Ks, Vs, cn, ut);
         else
-            pair_stage_store<D, MP, SP, false>(st, Qs, Ks, Vs, cn, ut);
+            pair_stage_store<D, MP, SP, false>(st, Ks, Vs, cn, ut);
         phase_row(n + 1);
         stage_chunk(st, n + 2);
         __syncthreads();  // chunk n + 1 and its state visible
