@@ -2,13 +2,18 @@
 
 Workload: the LM-layer shape (B=8, H=16, L=4096, d=64, M=S=64, chunk 64, bf16 inputs,
 fp32 state), periods T_h = (1 + h mod 2)(2M-1), synthetic seeded inputs resident in
-HBM.  One step = one bla_forward call (tables, block summaries, summary scan and the
-chunked forward kernel) producing O and the final states.
+HBM.  One step = one bla_forward call (segment summaries and the chunked forward kernel;
+the phase and slot tables are built by the first call and kept in the caller's workspace,
+reuse_tables = 1, as Alg. 1 / Alg. 3 take A and B as precomputed inputs) producing O and
+the final states.
 
-Prints ONE JSON line: tokens/s (B*L per step), the roofline of the dominant kernel
-(chunked forward: algorithmic bytes / its average duration from HIP events recorded
-between the library's launches on the same stream), the float64 CPU oracle timed on
-the host on the same workload, and the decode step (bla_step) on the decode
+Prints ONE JSON line: tokens/s (B*L per step); `roofline` of the dominant kernel (chunked
+forward: algorithmic bytes / its average duration from HIP events recorded between the
+library's launches on the same stream) and `operator_roofline` of the whole step
+(algorithmic bytes / step time, HBM traffic of every kernel of the step); the float64 CPU
+oracle timed on the host on the same workload; the recall and long-context workloads
+(B=64 H=4 L=512 d=64 M=S=32, and B=1 H=16 L=65536 d=M=S=128) measured the same way with
+their own rooflines and oracle baselines; and the decode step (bla_step) on the decode
 workload (B=512, H=16, d=M=S=64 after a 2048-token prefill).
 
 The headline is the operator with slots at lags behind the current token (Sec. 3.1).
@@ -16,11 +21,12 @@ The anchored-slot form (Sec. 3.3, Alg. 1/3; phase_anchor = 1) and the state-deca
 (Sec. 3.4, bla_decay_forward) are measured the same way on the same workload and reported
 under "anchored" and "decay", each with its own oracle timed on the host.  --form
 anchored / --form decay makes that form the only forward that runs (for profiling it
-alone).  The backward pass (bla_backward: dq, dk, dv from dO on the same workload) is
-measured under "backward" with the matrix-core roofline of its reverse-walk kernel and the
-oracle's backward timed on a sample of the sequences; --form backward runs only it.  The
-whole layer (bla_layer_forward: projections, operator, output projection) is measured under
-"layer" at the recall workload's shape.
+alone); --workload recall / long_context runs only that workload's forward.  The backward
+pass (bla_backward: dq, dk, dv from dO on the same workload) is measured under "backward"
+with the matrix-core roofline of its reverse-walk kernel and the oracle's backward timed on
+a sample of the sequences; --form backward runs only it.  The whole layer
+(bla_layer_forward: projections, operator, output projection) is measured under "layer" at
+the recall workload's shape.
 """
 from __future__ import annotations
 
@@ -90,9 +96,10 @@ def kernel_sources_digest(form):
     return h.hexdigest()[:16]
 
 
-def read_traffic(path, digest):
-    """HBM bytes per launch of the forward kernel from a committed rocprofv3 --pmc summary,
-    or None if absent or taken on a different kernel source."""
+def read_traffic(path, digest, key="hbm_bytes_per_launch"):
+    """HBM bytes from a committed rocprofv3 --pmc summary: `hbm_bytes_per_launch` of the
+    dominant kernel, or `hbm_bytes_per_step` of every kernel of a step; None if the file or
+    the key is absent or the figures were taken on a different kernel source."""
     if not os.path.exists(path):
         return None
     vals = {}
@@ -103,9 +110,26 @@ def read_traffic(path, digest):
     if vals.get("kernel_sources_sha") != digest:
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals[key])
     except (KeyError, ValueError):
         return None
+
+
+def host_cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def oracle_threads(n_seq):
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    return max(1, min(threads, n_seq))
 
 
 class Hip:
@@ -135,20 +159,40 @@ class Hip:
         return ms.value
 
 
-def bench_forward(args, hip, inputs, form):
+WORKLOAD_IDS = {"recall": 2, "lm_layer": 3, "long_context": 4}
+PROFILE_STEM = {  # committed rocprofv3 summaries of each measured forward
+    ("rotating", 3): "forward_pair_kernel_lm_layer",
+    ("anchored", 3): "forward_pair_kernel_lm_layer_anchored",
+    ("decay", 3): "decay_forward_kernel_lm_layer",
+    ("rotating", 2): "forward_pair_kernel_recall",
+    ("rotating", 4): "forward_kernel_long_context",
+}
+KERNEL_NAME = {
+    ("rotating", 3): "forward_pair_kernel<64,64,64,false>",
+    ("anchored", 3): "forward_pair_kernel<64,64,64,true>",
+    ("decay", 3): "decay_forward_kernel<bf16,64,64,false>",
+    ("rotating", 2): "forward_pair_kernel<64,32,32,false>",
+    ("rotating", 4): "forward_kernel<bf16,128,128,128,false>",
+}
+
+
+def bench_forward(args, hip, inputs, form, cid=3):
+    """One workload's forward: whole steps timed back to back, then the same steps with events
+    between the library's launches for the per-phase durations."""
     import numpy as np
     import torch
 
     import bla_inputs as bi
     import paper_2606_09862_amd as bla
 
-    w = bi.WORKLOADS[3]
+    w = bi.WORKLOADS[cid]
     T = bi.periods(w.M, w.H)
     q, k, v = inputs
     dev = torch.device("cuda:0")
     tq, tk, tv = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v))
     decay = form == "decay"
-    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, phase_anchor=form == "anchored")
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, phase_anchor=form == "anchored",
+                        reuse_tables=True)
     ws_bytes = bla.decay_workspace_size(p) if decay else bla.workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     o = torch.empty_like(tq)
@@ -183,16 +227,18 @@ def bench_forward(args, hip, inputs, form):
     hip.record(t_stop, sptr)
     torch.cuda.synchronize(dev)
     ms = hip.elapsed_ms(t_start, t_stop) / args.steps
-    # the same steps again with events between the phases (the forward kernel's duration
-    # for the roofline; the intervals of the other phases include the event overhead)
+    # the same steps again with events between the library's launches: the forward kernel's
+    # duration for its roofline.  Events 1-3 bracket the segment summaries (and, on the
+    # one-unit kernels, the scan of the summaries into carried states), reported as one phase.
     evs = [[hip.event() for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
     for i in range(args.steps):
         call(evs[i])
     torch.cuda.synchronize(dev)
-    phases = ["tables", "summary", "scan", "forward"]
-    phase_ms = {ph: float(np.mean([hip.elapsed_ms(e[j], e[j + 1]) for e in evs]))
-                for j, ph in enumerate(phases)}
+    spans = {"tables": (0, 1), "segment_summaries": (1, 3), "forward": (3, 4)}
+    if decay:
+        spans = {"tables_and_schedule": (0, 1), "summaries_and_scan": (1, 3), "forward": (3, 4)}
+    phase_ms = {ph: float(np.mean([hip.elapsed_ms(e[a], e[b]) for e in evs])) for ph, (a, b) in spans.items()}
     tokens = w.B * w.L
     if decay:
         flops = decay_flops_per_token_head(w.d, w.S) * w.B * w.H * w.L
@@ -201,28 +247,44 @@ def bench_forward(args, hip, inputs, form):
         flops = forward_flops_per_token_head(w.chunk, w.d, w.M, w.S) * w.B * w.H * w.L
         nbytes = forward_bytes(w.B, w.H, w.L, w.d, w.M, 2)
     t_fwd = phase_ms["forward"] * 1e-3
-    achieved_gbs = nbytes / t_fwd / 1e9
     digest = kernel_sources_digest(form)
-    tname = {"rotating": "forward_pair_kernel_lm_layer_traffic.txt",
-             "anchored": "forward_pair_kernel_lm_layer_anchored_traffic.txt",
-             "decay": "decay_forward_kernel_lm_layer_traffic.txt"}[form]
-    traffic = read_traffic(os.path.join(ROOT, "profiles", tname), digest)
-    roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
-    t_ideal = max(flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9))
+    stem = PROFILE_STEM.get((form, cid))
+    tpath = os.path.join(ROOT, "profiles", f"{stem}_traffic.txt") if stem else ""
+    t_mfma, t_hbm = flops / (BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)
+    if t_mfma > t_hbm:   # a contraction-bound workload (the long-context shape)
+        achieved = flops / t_fwd / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                    "traffic": read_traffic(tpath, digest) if stem else None}
+        op_achieved = flops / (ms * 1e-3) / 1e12
+        operator = {"bound": "mfma", "achieved": round(op_achieved, 1), "peak": BF16_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(op_achieved / BF16_PEAK_TFLOPS, 4)}
+    else:
+        achieved = nbytes / t_fwd / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": read_traffic(tpath, digest) if stem else None}
+        op_achieved = nbytes / (ms * 1e-3) / 1e9
+        operator = {"bound": "hbm", "achieved": round(op_achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(op_achieved / HBM_PEAK_GBS, 4)}
+    operator["traffic"] = read_traffic(tpath, digest, "hbm_bytes_per_step") if stem else None
+    operator["scope"] = "the whole step (every kernel of one call): algorithmic bytes or flops / ms_per_step"
+    roofline["scope"] = f"{KERNEL_NAME.get((form, cid), 'forward kernel')} alone: algorithmic bytes or flops / " \
+                        "its average duration from events between the launches"
     extra = {
-        "kernel": "decay_forward_kernel<bf16,64,64>" if decay else "forward_pair_kernel<64,64,64>",
+        "kernel": KERNEL_NAME.get((form, cid)),
         "algorithmic_bytes_per_launch": nbytes,
         "algorithmic_flops_per_launch": flops,
         "forward_kernel_us": round(phase_ms["forward"] * 1e3, 2),
         "forward_kernel_mfma_tflops": round(flops / t_fwd / 1e12, 1),
         "forward_kernel_mfma_frac": round(flops / t_fwd / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "forward_kernel_hbm_gbs": round(nbytes / t_fwd / 1e9, 1),
         "phase_us": {k2: round(v2 * 1e3, 2) for k2, v2 in phase_ms.items()},
-        "operator_roofline_frac": round(t_ideal / (ms * 1e-3), 4),
+        "ideal_us": round(max(t_mfma, t_hbm) * 1e6, 2),
         "kernel_sources_sha": digest,
     }
     del tq, tk, tv, o, sk, sv, ws
-    return w, T, ms, tokens / (ms * 1e-3), roofline, extra
+    return w, T, ms, tokens / (ms * 1e-3), roofline, operator, extra
 
 
 def bench_backward(args, hip, inputs):
@@ -241,7 +303,7 @@ def bench_backward(args, hip, inputs):
     q, k, v = inputs
     g = bi.generate_grad(3)
     tq, tk, tv, tg = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v, g))
-    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16)
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, reuse_tables=True)
     ws = torch.empty(bla.backward_workspace_size(p), dtype=torch.uint8, device=dev)
     dq, dk, dv = torch.empty_like(tq), torch.empty_like(tk), torch.empty_like(tv)
     gsk = torch.empty((w.B, w.H, 2, w.M, w.d), dtype=torch.float32, device=dev)
@@ -336,7 +398,7 @@ def bench_layer(args, hip):
     dev = torch.device("cuda:0")
     x, wqkv, wo = bi.generate_layer(2)
     tx, tw, to = (torch.from_numpy(a).to(dev).to(torch.bfloat16) for a in (x, wqkv, wo))
-    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16)
+    p = bla.make_params(w.B, w.H, w.L, w.d, w.M, w.S, torch.bfloat16, reuse_tables=True)
     ws = torch.empty(bla.layer_workspace_size(p), dtype=torch.uint8, device=dev)
     y = torch.empty_like(tx)
     sk = torch.empty((w.B, w.H, 2, w.M, w.d), dtype=torch.float32, device=dev)
@@ -414,13 +476,13 @@ def bench_decode(args, hip):
     ws = torch.empty(bla.step_workspace_size(p), dtype=torch.uint8, device=dev)
     o = torch.empty_like(sq)
     for _ in range(args.warmup):
-        bla.step(sq, sk_, sv_, T, w.M, w.S, gk, gv, t0=w.L, workspace=ws, out=o)
+        bla.step(sq, sk_, sv_, T, w.M, w.S, gk, gv, t0=w.L, workspace=ws, out=o, reuse_tables=True)
     sptr = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
     e0, e1 = hip.event(), hip.event()
     torch.cuda.synchronize(dev)
     hip.record(e0, sptr)
     for i in range(args.steps):
-        bla.step(sq, sk_, sv_, T, w.M, w.S, gk, gv, t0=w.L + i, workspace=ws, out=o)
+        bla.step(sq, sk_, sv_, T, w.M, w.S, gk, gv, t0=w.L + i, workspace=ws, out=o, reuse_tables=True)
     hip.record(e1, sptr)
     torch.cuda.synchronize(dev)
     ms = hip.elapsed_ms(e0, e1) / args.steps
@@ -456,12 +518,12 @@ def cpu_baseline_anchored(w, T, inputs):
     import oracle
 
     q, k, v = inputs
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
-    threads = max(1, min(threads, w.B * w.H))
+    threads = oracle_threads(w.B * w.H)
     t = time.perf_counter()
     oracle.forward_anchored(q, k, v, T, w.M, w.S, nthreads=threads)
     dt = time.perf_counter() - t
     return {"value": round(w.B * w.L / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu": host_cpu_model(),
             "sample": f"the whole LM-layer workload ({w.B}x{w.H} sequences of {w.L} tokens), float64 "
                       f"Alg. 1 with slot states, OpenMP over (b,h); {dt:.2f} s wall"}
 
@@ -471,28 +533,79 @@ def cpu_baseline_decay(w, T, inputs):
     import oracle
 
     q, k, v = inputs
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
-    threads = max(1, min(threads, w.B * w.H))
+    threads = oracle_threads(w.B * w.H)
     t = time.perf_counter()
     oracle.forward_decay(q, k, v, T, w.M, w.S, nthreads=threads)
     dt = time.perf_counter() - t
     return {"value": round(w.B * w.L / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu": host_cpu_model(),
             "sample": f"the whole LM-layer workload ({w.B}x{w.H} sequences of {w.L} tokens), float64 "
                       f"decayed slot recurrence, OpenMP over (b,h); {dt:.2f} s wall"}
 
 
-def cpu_baseline(w, T, inputs):
+def _oracle_rate(w, T, q, k, v, literal, L=None, nseq=None):
+    """tokens/s (a token with all H heads) of the float64 oracle on the first `nseq` sequences
+    (b, h in order) and the first L tokens of the workload; (rate, threads, seconds, what)."""
+    import numpy as np
+
     import oracle
 
-    q, k, v = inputs
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
-    threads = max(1, min(threads, w.B * w.H))
+    L = w.L if L is None else L
+    total = w.B * w.H
+    nseq = total if nseq is None else min(nseq, total)
+    if nseq == total:
+        qs, ks, vs, Ts = q[:, :, :L], k[:, :, :L], v[:, :, :L], T
+    else:
+        rows = [(i // w.H, i % w.H) for i in range(nseq)]
+        pick = lambda x: np.stack([x[b, h, :L] for b, h in rows])[None]
+        qs, ks, vs, Ts = pick(q), pick(k), pick(v), [T[h] for _, h in rows]
+    threads = oracle_threads(nseq)
     t = time.perf_counter()
-    oracle.forward(q, k, v, T, w.M, w.S, nthreads=threads)
+    oracle.forward(qs, ks, vs, Ts, w.M, w.S, literal=literal, nthreads=threads)
     dt = time.perf_counter() - t
-    return {"value": round(w.B * w.L / dt, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"the whole LM-layer workload ({w.B}x{w.H} sequences of {w.L} tokens), float64 "
-                      f"recurrence with the factored readout, OpenMP over (b,h); {dt:.2f} s wall"}
+    what = (f"{'all' if nseq == total else nseq} of the {total} sequences" +
+            ("" if L == w.L else f", first {L} of {w.L} tokens"))
+    return nseq * L / w.H / dt, threads, dt, what
+
+
+def cpu_baseline(w, T, inputs, literal_sample=None, factored_sample=None):
+    """The float64 oracle (Alg. 2 token by token, OpenMP over (b,h)) on the host: the factored
+    readout (the same sums regrouped) on the workload or `factored_sample` = (nseq, L), and the
+    literal readout (slots materialised per token, as Eq. compressed writes them) on
+    `literal_sample` = (nseq, L) (None: the whole workload)."""
+    q, k, v = inputs
+    fs = factored_sample or (None, None)
+    rate, threads, dt, what = _oracle_rate(w, T, q, k, v, False, L=fs[1], nseq=fs[0])
+    ls = literal_sample or (None, None)
+    lrate, lthreads, ldt, lwhat = _oracle_rate(w, T, q, k, v, True, L=ls[1], nseq=ls[0])
+    return {"value": round(rate, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu": host_cpu_model(),
+            "sample": f"{what} ({w.name} workload, B={w.B} H={w.H} L={w.L} d={w.d} M={w.M} S={w.S}), float64 "
+                      f"recurrence with the factored readout, OpenMP over (b,h); {dt:.2f} s wall; tokens/s "
+                      f"counts a token with all {w.H} heads",
+            "literal_readout": {"value": round(lrate, 1), "unit": "tokens/s", "cores": lthreads,
+                                "sample": f"{lwhat}, slots materialised per token; {ldt:.2f} s wall"}}
+
+
+def bench_workload(args, hip, name):
+    """The rotating form's forward on the recall or long-context workload, with its oracle."""
+    import bla_inputs as bi
+
+    cid = WORKLOAD_IDS[name]
+    inputs = bi.generate(cid)
+    w, T, ms, value, roof, op, extra = bench_forward(args, hip, inputs, "rotating", cid)
+    out = {"workload": name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": w.M, "S": w.S, "chunk": w.chunk,
+           "value": round(value, 1), "unit": "tokens/s", "ms_per_step": round(ms, 5), "roofline": roof,
+           "operator_roofline": op, "forward_detail": extra}
+    if not args.no_cpu_baseline:
+        if cid == 4:
+            # a bounded sample: every head over the first 4096 tokens (the recurrence costs the
+            # same per token at any position)
+            out["cpu_baseline"] = cpu_baseline(w, T, inputs, literal_sample=(16, 256), factored_sample=(16, 4096))
+        else:
+            out["cpu_baseline"] = cpu_baseline(w, T, inputs)
+    del inputs
+    return out
 
 
 def main():
@@ -506,9 +619,13 @@ def main():
     ap.add_argument("--no-decay", action="store_true", help="skip the state-decay measurement")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
     ap.add_argument("--no-layer", action="store_true", help="skip the whole-layer measurement")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the recall and long-context workloads")
     ap.add_argument("--form", choices=("rotating", "anchored", "decay", "backward"), default="rotating",
                     help="the form of the headline forward; otherwise no other forward runs "
                          "(backward: only the backward pass runs, for profiling it alone)")
+    ap.add_argument("--workload", choices=("recall", "long_context"), default=None,
+                    help="run only this workload's forward (rotating slots), for profiling it alone")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="first run one plain device copy of this many bytes (reference kernel for "
                          "scaling the HBM byte counters of a rocprofv3 --pmc run)")
@@ -530,6 +647,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     import bla_inputs as bi
+    if args.workload is not None:
+        out = bench_workload(args, hip, args.workload)
+        print(json.dumps(out), flush=True)
+        return
     inputs = bi.generate(3)
     if args.form == "backward":
         b_ms, b_value, b_roof, b_detail, _ = bench_backward(args, hip, inputs)
@@ -538,18 +659,19 @@ def main():
                           "detail": b_detail}), flush=True)
         return
     head = args.form
-    w, T, ms, value, roofline, extra = bench_forward(args, hip, inputs, head)
-    baselines = {"rotating": cpu_baseline, "anchored": cpu_baseline_anchored, "decay": cpu_baseline_decay}
+    w, T, ms, value, roofline, operator, extra = bench_forward(args, hip, inputs, head)
     titles = {"anchored": "anchored slots (Sec. 3.3, Alg. 1/3), phase_anchor=1",
               "decay": "state decay (Sec. 3.4), bla_decay_forward, float32 slot states [B,H,S,d]"}
+    baselines = {"anchored": cpu_baseline_anchored, "decay": cpu_baseline_decay}
     others = {}
     for form, skip in (("anchored", args.no_anchored), ("decay", args.no_decay)):
         if head != "rotating" or skip:
             others[form] = None
             continue
-        _, _, f_ms, f_value, f_roof, f_extra = bench_forward(args, hip, inputs, form)
+        _, _, f_ms, f_value, f_roof, f_op, f_extra = bench_forward(args, hip, inputs, form)
         others[form] = {"form": titles[form], "value": round(f_value, 1), "unit": "tokens/s",
-                        "ms_per_step": round(f_ms, 5), "roofline": f_roof, "forward_detail": f_extra,
+                        "ms_per_step": round(f_ms, 5), "roofline": f_roof, "operator_roofline": f_op,
+                        "forward_detail": f_extra,
                         "cpu_baseline": None if args.no_cpu_baseline else baselines[form](w, T, inputs)}
     backward = None
     if head == "rotating" and not args.no_backward:
@@ -562,7 +684,17 @@ def main():
                     cpu_baseline_backward(w3, bi.periods(w3.M, w3.H), inputs, g)}
     layer = None if args.no_layer or head != "rotating" else bench_layer(args, hip)
     decode = None if args.no_decode or head != "rotating" else bench_decode(args, hip)
-    cpu = None if args.no_cpu_baseline else baselines[head](w, T, inputs)
+    cpu = None
+    if not args.no_cpu_baseline:
+        if head == "rotating":
+            cpu = cpu_baseline(w, T, inputs, literal_sample=(16, 512))
+        else:
+            cpu = baselines[head](w, T, inputs)
+    workloads = {}
+    if head == "rotating" and not args.no_workloads:
+        del inputs
+        for name in ("recall", "long_context"):
+            workloads[name] = bench_workload(args, hip, name)
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
@@ -570,8 +702,10 @@ def main():
         "config": {"workload": "lm_layer", "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": w.M, "S": w.S,
                    "chunk": w.chunk, "periods": "T_h=(1+h%2)(2M-1)", "state": "fp32",
                    "form": head},
-        "roofline": roofline, "cpu_baseline": cpu, "forward_detail": extra, "decode_step": decode,
-        "anchored": others["anchored"], "decay": others["decay"], "backward": backward, "layer": layer,
+        "roofline": roofline, "operator_roofline": operator, "cpu_baseline": cpu, "forward_detail": extra,
+        "recall": workloads.get("recall"), "long_context": workloads.get("long_context"),
+        "decode_step": decode, "anchored": others["anchored"], "decay": others["decay"], "backward": backward,
+        "layer": layer,
     }
     print(json.dumps(line), flush=True)
 
