@@ -46,9 +46,13 @@
  *     they are ordered on one stream.
  *   - Supported shapes: d_k == d_v in {32, 64, 128}; 1 <= M <= 128; 1 <= S <= 256
  *     and S <= max(32, 2 P(M)) where P(M) is M rounded up to 16, 32, 64 or 128 (so
- *     the paper's S = 2M-1 is always accepted); chunk in {0, 64}; float32 I/O also
- *     needs the kernel's LDS tiles to fit (d = 128 with M > 64 does not).  Anything
- *     else returns BLA_ERR_UNSUPPORTED; bla_supported() answers without launching.
+ *     the paper's S = 2M-1 is always accepted); chunk in {0 (= 64), 16, 32, 64, 128}
+ *     (Alg. 3's chunk length: the result is the same up to rounding, only the work
+ *     split changes); chunks other than 64 need P(M) <= 64 and run on the one-unit
+ *     kernels (128-token chunks with register spills: 64 is the fast default);
+ *     float32 I/O also needs the kernel's LDS tiles to fit (d = 128 with M > 64 does
+ *     not, nor float32 128-token chunks at d = 64).  Anything else returns
+ *     BLA_ERR_UNSUPPORTED; bla_supported() answers without launching.
  */
 #ifndef BLA_H
 #define BLA_H
@@ -75,7 +79,8 @@ typedef struct {
     int32_t d_k, d_v;    /* head widths of keys/queries and of values                    */
     int32_t M;           /* Fourier modes (Sec. 3.1), >= 1                               */
     int32_t S;           /* blurry slots, >= 1 (the paper's value is 2M-1)               */
-    int32_t chunk;       /* tokens per chunk of the parallel form; 0 = default (64)      */
+    int32_t chunk;       /* tokens per chunk of the parallel form (16, 32, 64, 128);
+                            0 = default (64)                                             */
     int64_t t0;          /* absolute position of token 0 (start mask only), >= 0         */
     float scale;         /* softmax scale; 0 selects 1/sqrt(d_k) (Eq. output)            */
     int32_t io_dtype;    /* bla_dtype of q, k, v, o                                      */
@@ -248,8 +253,8 @@ bla_status bla_decay_step(const bla_params* p, const double* T, const void* q, c
  * io dtype, and dLoss/d(input states) into dstate_k_in / dstate_v_in [B,H,2,M,d] float32
  * (NULL = not wanted; they must not alias the other state arguments).  L = 0 copies the
  * final-state gradients (or zeros) to them.
- * Supported: phase_anchor = 0; bfloat16 with d in {32, 64} or float32 with d = 32; M <= 64
- * (float32: M <= 32) and S <= max(32, 2 P(M)) <= 128; anything else BLA_ERR_UNSUPPORTED.
+ * Supported: phase_anchor = 0; chunk 0 or 64; bfloat16 with d in {32, 64} or float32 with d = 32;
+ * M <= 64 (float32: M <= 32) and S <= max(32, 2 P(M)) <= 128; anything else BLA_ERR_UNSUPPORTED.
  * Every other convention (alignment, T, ownership, streams, errors) as for bla_forward.
  */
 size_t bla_backward_workspace_size(const bla_params* p);

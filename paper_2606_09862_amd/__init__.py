@@ -159,21 +159,22 @@ def _out(out, like, shape):
 
 def forward(q, k, v, T, M: int, S: int, t0: int = 0, scale: float | None = None,
             state_k=None, state_v=None, want_state: bool = True, workspace=None, out=None,
-            phase_anchor: bool = False, reuse_tables: bool = False):
+            phase_anchor: bool = False, reuse_tables: bool = False, chunk: int = 0):
     """bla_forward on q, k, v [B,H,L,d] (float32 or bfloat16 cuda tensors).
 
     Returns (o, state_k_out, state_v_out); the states are float32 [B,H,2,M,d]
     (None when want_state is False).  phase_anchor selects the anchored slots of
     Sec. 3.3 (Alg. 1 / Alg. 3); the state is the same mode state in both forms.
     reuse_tables: keep the tables an earlier call built in the same `workspace`
-    (bla_params.reuse_tables; only meaningful with a caller-kept workspace).
+    (bla_params.reuse_tables; only meaningful with a caller-kept workspace).  chunk: tokens
+    per chunk of the parallel form (16, 32, 64 or 128; 0 = 64).
     """
     B, H, L, d = q.shape
     dt = q.dtype
     for name, t in (("k", k), ("v", v)):
         _check(t, (B, H, L, d), dt, name)
     _check(q, (B, H, L, d), dt, "q")
-    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale,
+    p = make_params(B, H, L, d, M, S, dt, t0, 0.0 if scale is None else scale, chunk=chunk,
                     phase_anchor=phase_anchor, reuse_tables=reuse_tables)
     for name, t in (("state_k", state_k), ("state_v", state_v)):
         if t is not None:

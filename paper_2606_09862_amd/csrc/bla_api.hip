@@ -93,13 +93,15 @@ bla_status check_shape(const bla_params* p, bool step)
     if (!isfinite(p->scale)) return BLA_ERR_INVALID_ARG;
     if (p->phase_anchor != 0 && p->phase_anchor != 1) return BLA_ERR_INVALID_ARG;
     if (p->reuse_tables != 0 && p->reuse_tables != 1) return BLA_ERR_INVALID_ARG;
-    if (p->chunk != 0 && p->chunk != kChunk) return BLA_ERR_UNSUPPORTED;
+    if (p->chunk != 0 && p->chunk != 16 && p->chunk != 32 && p->chunk != 64 && p->chunk != 128)
+        return BLA_ERR_UNSUPPORTED;
     if (p->d_k != p->d_v) return BLA_ERR_UNSUPPORTED;
     if (p->d_k != 32 && p->d_k != 64 && p->d_k != 128) return BLA_ERR_UNSUPPORTED;
     const int MP = pad_modes(p->M), SP = pad_slots(p->S);
     if (MP < 0 || SP < 0) return BLA_ERR_UNSUPPORTED;
     if (SP > (2 * MP > 32 ? 2 * MP : 32)) return BLA_ERR_UNSUPPORTED;
-    if (!step && !forward_supported(p->io_dtype == BLA_BF16, p->d_k, MP, SP)) return BLA_ERR_UNSUPPORTED;
+    if (!step && !forward_supported(p->io_dtype == BLA_BF16, p->d_k, MP, SP, p->chunk ? p->chunk : kChunk))
+        return BLA_ERR_UNSUPPORTED;
     if ((long long)p->B * p->H > (1ll << 31) / 4) return BLA_ERR_UNSUPPORTED;
     return BLA_OK;
 }
@@ -123,21 +125,22 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->S = p->S;
     pl->MP = pad_modes(p->M);
     pl->SP = pad_slots(p->S);
-    pl->C = kChunk;
+    // a decode step does not depend on the chunk length; its tables use the default's layout
+    pl->C = step || p->chunk == 0 ? kChunk : p->chunk;
     pl->bf16 = p->io_dtype == BLA_BF16;
     pl->t0 = p->t0;
     pl->anchor = p->phase_anchor;
     pl->scale = p->scale != 0.f ? p->scale : 1.f / sqrtf((float)p->d_k);
     pl->unit_floats = (size_t)4 * pl->MP * pl->D;
     const long long units = (long long)p->B * p->H;
-    pl->nch = step ? 1 : (p->L + kChunk - 1) / kChunk;
+    pl->nch = step ? 1 : (p->L + pl->C - 1) / pl->C;
     pl->nseg = 1;
     pl->cps = pl->nch;
     pl->cpb = pl->nch;
     pl->nbs = 0;
     pl->upw = 1;
     pl->pair = 0;
-    if (!step) {
+    if (!step && pl->C == kChunk) {  // the pair kernels run 64-token chunks only
         const int pu = forward_units_per_wg(pl->bf16, pl->D, pl->MP, pl->SP);
         pl->upw = pu > 0 ? pu : 1;
         pl->pair = pu > 0;
@@ -175,7 +178,7 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
         }
     }
     const size_t esz = pl->bf16 ? 2 : 4;
-    const size_t H = (size_t)p->H, C = kChunk, MP2 = 2 * (size_t)pl->MP, SP = (size_t)pl->SP;
+    const size_t H = (size_t)p->H, C = (size_t)pl->C, MP2 = 2 * (size_t)pl->MP, SP = (size_t)pl->SP;
     size_t off = 0;
     pl->off_E32 = off;    off = align_up(off + H * (C + 1) * MP2 * 4);
     pl->off_EbarT = off;  off = align_up(off + H * MP2 * C * esz);
@@ -199,8 +202,8 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
 bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s, bool step, int reuse)
 {
     // key: everything the tables' contents and layout depend on
-    int32_t f[14] = {pl.H, pl.M, pl.S, pl.MP, pl.SP, kChunk, pl.bf16, pl.anchor, pl.pair, step ? 2 : kChunk + 1,
-                     pl.cpb * kChunk, 0, 0, 0};
+    int32_t f[14] = {pl.H, pl.M, pl.S, pl.MP, pl.SP, pl.C, pl.bf16, pl.anchor, pl.pair, step ? 2 : pl.C + 1,
+                     pl.cpb * pl.C, 0, 0, 0};
     const float tab_scale = pl.pair ? 1.f : pl.scale;
     memcpy(&f[11], &tab_scale, sizeof(float));
     uint64_t key = fnv_mix(1469598103934665603ull, f, sizeof(f));
@@ -226,13 +229,13 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
         a.S = pl.S;
         a.MP = pl.MP;
         a.SP = pl.SP;
-        a.C = kChunk;
-        a.Lblk = pl.cpb * kChunk;
+        a.C = pl.C;
+        a.Lblk = pl.cpb * pl.C;
         a.h0 = h0;
         a.nh = pl.H - h0 < kMaxHeadsPerTableLaunch ? pl.H - h0 : kMaxHeadsPerTableLaunch;
         a.with_shared = h0 == 0;
         a.conj_tab = pl.pair;
-        a.jrows = step ? 2 : kChunk + 1;
+        a.jrows = step ? 2 : pl.C + 1;
         a.trig = (float*)(ws + pl.off_trig);
         a.rperiod = (double*)(ws + pl.off_rperiod);
         a.period = (double*)(ws + pl.off_period);
@@ -310,6 +313,7 @@ bla_status check_backward_shape(const bla_params* p)
     if (st != BLA_OK) return st;
     if (p->L < 0) return BLA_ERR_INVALID_ARG;
     if (p->phase_anchor != 0) return BLA_ERR_UNSUPPORTED;
+    if (p->chunk != 0 && p->chunk != kChunk) return BLA_ERR_UNSUPPORTED;  // the backward runs 64-token chunks
     if (!backward_supported(p->io_dtype == BLA_BF16, p->d_k, pad_modes(p->M), pad_slots(p->S)))
         return BLA_ERR_UNSUPPORTED;
     return BLA_OK;
@@ -465,6 +469,7 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     a.H = pl.H;
     a.L = pl.L;
     a.M = pl.M;
+    a.C = pl.C;
     a.nch = pl.nch;
     a.nseg = pl.nseg;
     a.cps = pl.cps;

@@ -150,7 +150,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(FwdArgs a, int MP, int D
         im = re + (size_t)MP * D;
         sin_ = a.sv_in;
     }
-    const float* E1 = a.E32 + ((size_t)h * (kChunk + 1) + 1) * 2 * MP;
+    const float* E1 = a.E32 + ((size_t)h * (a.C + 1) + 1) * 2 * MP;
     float zr = 0.f, zi = 0.f;
     if (sin_ && m < a.M) {
         float xr = sin_[(((size_t)bh * 2 + 0) * a.M + m) * D + d];

@@ -50,19 +50,24 @@ namespace bla {
 
 constexpr size_t kMaxLds = 160 * 1024;
 
-template <typename T, int D, int MP> struct Geo {
-    static constexpr int C = kChunk;
+// CC: tokens per chunk (16, 32, 64 or 128; Alg. 3 takes the chunk length as an input).
+template <typename T, int D, int MP, int CC = kChunk> struct Geo {
+    static constexpr int C = CC;
     static constexpr int NT = C / 16;           // token tiles per chunk
     // Threads per workgroup: 4 waves, or 8 for d = M = 128, where four waves would each hold
-    // two mode tiles of both states (256 registers) and spill; the token chain then runs on
-    // waves 0..NT-1 and the other four take part in the mode-tile phases only.
-    static constexpr int NTHR = (D == 128 && MP == 128) ? 2 * kThreads : kThreads;
+    // two mode tiles of both states (256 registers) and spill, and for 128-token chunks (one
+    // token tile per wave); the token chain runs on waves 0..NT-1 and the other waves take
+    // part in the mode-tile phases only.
+    static constexpr int NTHR = ((D == 128 && MP == 128) || NT > 4) ? 2 * kThreads : kThreads;
     static constexpr int NW = NTHR / 64;        // waves
     static constexpr int NMT = MP / 16;         // mode tiles
     static constexpr int NDT = D / 16;          // head-dim tiles
     static constexpr int KBD = D / 32;          // reduction blocks over d
     static constexpr int KBM = 2 * MP / 32;     // reduction blocks over [Re | Im] modes
-    static constexpr int KBC = C / 32;          // reduction blocks over chunk tokens
+    static constexpr int KBC = (C + 31) / 32;   // reduction blocks over chunk tokens
+    // A 16-token chunk fills only the lower half of its one token-reduction block: every
+    // fragment over chunk tokens then carries zeros in reduction indices 16..31.
+    static constexpr bool HALF = C % 32 != 0;
     static constexpr int OWN = (NMT + NW - 1) / NW;  // mode tiles owned per wave
     // Row padding in LDS: rows of a fragment read (16 lanes, one row each, 8 bytes per
     // lane for bf16) land on distinct banks when the row stride is 8 bytes past a
@@ -81,10 +86,22 @@ template <typename T, int D, int MP> struct Geo {
     static constexpr int KVPT = (KVU + NTHR - 1) / NTHR;
     static_assert(NT <= NW, "one token tile per wave, for the first NT waves");
     static_assert(D % 32 == 0 && MP % 16 == 0, "tile shapes");
+    static_assert(C == 16 || C == 32 || C == 64 || C == 128, "chunk length");
 };
 
-template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
-    using G = Geo<T, D, MP>;
+// Fragment over chunk tokens (reduction block kb) of a row-major tile whose rows hold the
+// chunk's C tokens: for a 16-token chunk only the lower half exists.
+template <typename T, int CC>
+__device__ __forceinline__ typename Frag<T>::type ld_frag_c(const T* row, int kb, int g)
+{
+    if constexpr (CC % 32 != 0)
+        return ld_frag_lo<T>(row, 32 * kb, g);
+    else
+        return ld_frag<T>(row, 32 * kb, g);
+}
+
+template <typename T, int D, int MP, int SP, int CC = kChunk> struct Fwd : Geo<T, D, MP, CC> {
+    using G = Geo<T, D, MP, CC>;
     static constexpr int NST = SP / 16;
     static constexpr int KBS = SP / 32;
     static constexpr int LDG = G::C + G::PAD;    // GT:   [C tokens][LDG]
@@ -110,11 +127,11 @@ template <typename T, int D, int MP, int SP> struct Fwd : Geo<T, D, MP> {
 };
 
 // The wave's fp32 state tiles: [owned mode tile][Re, Im][head-dim tile].
-template <typename T, int D, int MP> using StateTiles = floatx4[Geo<T, D, MP>::OWN][2][D / 16];
+template <typename T, int D, int MP, int CC = kChunk> using StateTiles = floatx4[Geo<T, D, MP, CC>::OWN][2][D / 16];
 // ---------------------------------------------------------------------------------
 // Chunk staging: global -> registers (issued a chunk ahead) -> LDS.
-template <typename T, int D, int MP> struct Stage {
-    using GG = Geo<T, D, MP>;
+template <typename T, int D, int MP, int CC = kChunk> struct Stage {
+    using GG = Geo<T, D, MP, CC>;
     using H = typename Frag<T>::half;
     H q[GG::QPT][2];
     H kv[GG::KVPT][4][2];
@@ -124,11 +141,11 @@ template <typename T, int D, int MP> struct Stage {
 // depend on c (rows past c re-read row c-1, which exists); the zero fill past c is
 // applied when the registers are written to LDS, so no wait on the loads is forced
 // while they are in flight.
-template <typename T, int D, int MP, bool WQ>
-__device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, const T* kc, const T* vc,
+template <typename T, int D, int MP, bool WQ, int CC = kChunk>
+__device__ __forceinline__ void stage_load(Stage<T, D, MP, CC>& st, const T* qc, const T* kc, const T* vc,
                                            int ts, int c, int tid)
 {
-    using GG = Geo<T, D, MP>;
+    using GG = Geo<T, D, MP, CC>;
     constexpr int DO = D / 8;
 #pragma unroll
     for (int i = 0; i < (WQ ? GG::QPT : 0); ++i) {
@@ -156,10 +173,10 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP>& st, const T* qc, con
     }
 }
 
-template <typename T, int D, int MP, bool WQ>
-__device__ __forceinline__ void stage_store(const Stage<T, D, MP>& st, T* Qs, T* Kt, T* Vt, int c, int tid)
+template <typename T, int D, int MP, bool WQ, int CC = kChunk>
+__device__ __forceinline__ void stage_store(const Stage<T, D, MP, CC>& st, T* Qs, T* Kt, T* Vt, int c, int tid)
 {
-    using GG = Geo<T, D, MP>;
+    using GG = Geo<T, D, MP, CC>;
     using H = typename Frag<T>::half;
     constexpr int DO = D / 8;
     const H z = zero_half<T>();
@@ -248,10 +265,10 @@ __device__ __forceinline__ typename Frag<T>::type erev_frag(const float* E32, in
 
 // Write the bf16/fp32 copy of Z'_v as ZvT[d][Re m | Im m] with the Im part negated
 // (the A operand of O += Re(W'' Z'_v)).
-template <typename T, int D, int MP>
-__device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP>& Zv, int w, int g, int r)
+template <typename T, int D, int MP, int CC = kChunk>
+__device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP, CC>& Zv, int w, int g, int r)
 {
-    using GG = Geo<T, D, MP>;
+    using GG = Geo<T, D, MP, CC>;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o) {
         const int mt = w + GG::NW * o;
@@ -268,13 +285,13 @@ __device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP>& Zv
 // Step 10: Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i] on the wave's own mode tiles.
 // rhoC: the row rho^C (full chunks); E32 (row stride 2MP): phase table for a ragged c;
 // Erev / ldR: the [2MP][C] table of rho^{C-i} (full chunks).
-template <typename T, int D, int MP>
-__device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTiles<T, D, MP>& Zv,
+template <typename T, int D, int MP, int CC = kChunk>
+__device__ __forceinline__ void advance_state(StateTiles<T, D, MP, CC>& Zk, StateTiles<T, D, MP, CC>& Zv,
                                               const T* Kt, const T* Vt, const float* rhoC,
                                               const float* E32, const T* Erev, int ldR, int c, int w,
                                               int g, int r)
 {
-    using GG = Geo<T, D, MP>;
+    using GG = Geo<T, D, MP, CC>;
     using F = typename Frag<T>::type;
     const float* Ec = (c == GG::C) ? rhoC : E32 + (size_t)c * 2 * MP;
 #pragma unroll
@@ -307,13 +324,13 @@ __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTil
             const int mt = min(w + GG::NW * o, GG::NMT - 1);
 #pragma unroll
             for (int p = 0; p < 2; ++p)
-                ef[o][p] = (c == GG::C) ? ld_frag<T>(Erev + (size_t)(16 * (p * GG::NMT + mt) + r) * ldR, 32 * kb, g)
+                ef[o][p] = (c == GG::C) ? ld_frag_c<T, CC>(Erev + (size_t)(16 * (p * GG::NMT + mt) + r) * ldR, kb, g)
                                         : erev_frag<T, MP>(E32, 2 * MP, c, p, mt, kb, g, r);
         }
 #pragma unroll
         for (int dt = 0; dt < GG::NDT; ++dt) {
-            const F kf = ld_frag<T>(Kt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
-            const F vf = ld_frag<T>(Vt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g);
+            const F kf = ld_frag_c<T, CC>(Kt + (size_t)(16 * dt + r) * GG::LDK, kb, g);
+            const F vf = ld_frag_c<T, CC>(Vt + (size_t)(16 * dt + r) * GG::LDK, kb, g);
 #pragma unroll
             for (int o = 0; o < GG::OWN; ++o) {
                 if (w + GG::NW * o < GG::NMT) {
@@ -330,10 +347,10 @@ __device__ __forceinline__ void advance_state(StateTiles<T, D, MP>& Zk, StateTil
 
 // ---------------------------------------------------------------------------------
 // Block summaries: the pre-rotated state after cpb full chunks, from zero.
-template <typename T, int D, int MP>
-__global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs a)
+template <typename T, int D, int MP, int CC = kChunk>
+__global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void summary_kernel(FwdArgs a)
 {
-    using GG = Geo<T, D, MP>;
+    using GG = Geo<T, D, MP, CC>;
     __shared__ __attribute__((aligned(16))) T lds[2 * GG::KT_ELEMS];
     T* Kt = lds;
     T* Vt = lds + GG::KT_ELEMS;
@@ -347,7 +364,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs 
 
     const T* ErevTh = (const T*)a.ErevT + (size_t)h * 2 * MP * GG::C;
     const float* rhoC = E32h + (size_t)GG::C * 2 * MP;
-    StateTiles<T, D, MP> Zk, Zv;
+    StateTiles<T, D, MP, CC> Zk, Zv;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o)
 #pragma unroll
@@ -357,22 +374,22 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs 
 
     // Two chunks of K/V in flight ahead of the one being reduced: this kernel does
     // little arithmetic per byte, so it is bound by how much load latency it hides.
-    Stage<T, D, MP> st0, st1;
+    Stage<T, D, MP, CC> st0, st1;
     const size_t first = (size_t)blk * a.cpb * GG::C;
-    stage_load<T, D, MP, false>(st0, nullptr, kbase + first * ts, vbase + first * ts, ts, GG::C, tid);
+    stage_load<T, D, MP, false, CC>(st0, nullptr, kbase + first * ts, vbase + first * ts, ts, GG::C, tid);
     if (a.cpb > 1)
-        stage_load<T, D, MP, false>(st1, nullptr, kbase + (first + GG::C) * ts, vbase + (first + GG::C) * ts, ts,
-                                    GG::C, tid);
+        stage_load<T, D, MP, false, CC>(st1, nullptr, kbase + (first + GG::C) * ts, vbase + (first + GG::C) * ts, ts,
+                                        GG::C, tid);
     for (int n = 0; n < a.cpb; ++n) {
         __syncthreads();
-        stage_store<T, D, MP, false>(st0, nullptr, Kt, Vt, GG::C, tid);
+        stage_store<T, D, MP, false, CC>(st0, nullptr, Kt, Vt, GG::C, tid);
         st0 = st1;
         if (n + 2 < a.cpb) {
             const size_t tok = first + (size_t)(n + 2) * GG::C;
-            stage_load<T, D, MP, false>(st1, nullptr, kbase + tok * ts, vbase + tok * ts, ts, GG::C, tid);
+            stage_load<T, D, MP, false, CC>(st1, nullptr, kbase + tok * ts, vbase + tok * ts, ts, GG::C, tid);
         }
         __syncthreads();
-        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, rhoC, E32h, ErevTh, GG::C, GG::C, w, g, r);
+        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, E32h, ErevTh, GG::C, GG::C, w, g, r);
     }
     float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
 #pragma unroll
@@ -394,11 +411,11 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void summary_kernel(FwdArgs 
 // ---------------------------------------------------------------------------------
 // One workgroup per (b, h, segment): the chunk loop over the segment.  AN: anchored slots
 // (a separate instantiation, so that the rotating form keeps its own register allocation).
-template <typename T, int D, int MP, int SP, bool AN>
-__global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs a)
+template <typename T, int D, int MP, int SP, bool AN, int CC = kChunk>
+__global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdArgs a)
 {
-    using P = Fwd<T, D, MP, SP>;
-    using GG = Geo<T, D, MP>;
+    using P = Fwd<T, D, MP, SP, CC>;
+    using GG = Geo<T, D, MP, CC>;
     using F = typename Frag<T>::type;
     constexpr int C = GG::C, NT = GG::NT, NW = GG::NW, NMT = GG::NMT, NDT = GG::NDT, OWN = GG::OWN;
     __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
@@ -478,12 +495,12 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
     // K^T tile instead of being held in registers a chunk ahead.
     constexpr bool KROWS = GG::NTHR > kThreads && sizeof(T) == 2;
     // first chunk's staging loads go out before the state set-up
-    Stage<T, D, MP> st;
+    Stage<T, D, MP, CC> st;
     F kpf[KROWS ? 1 : GG::KBD];  // key rows 16w..16w+15 of the next chunk (Gram tile A operand), unmasked
     {
         const int tok0 = ch0 * C, c0 = min(C, a.L - tok0), i = min(16 * w + r, c0 - 1);
-        stage_load<T, D, MP, true>(st, qb + (size_t)tok0 * ts, kb_ + (size_t)tok0 * ts, vb + (size_t)tok0 * ts,
-                                   ts, c0, tid);
+        stage_load<T, D, MP, true, CC>(st, qb + (size_t)tok0 * ts, kb_ + (size_t)tok0 * ts, vb + (size_t)tok0 * ts,
+                                       ts, c0, tid);
         if constexpr (!KROWS) {
 #pragma unroll
             for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tok0 + i) * ts, 32 * kb, g);
@@ -492,7 +509,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
     if constexpr (P::TL) __syncthreads();  // LDS tables visible
 
     // ---- state entering the segment (pre-rotated: Z' = rho Z)
-    StateTiles<T, D, MP> Zk, Zv;
+    StateTiles<T, D, MP, CC> Zk, Zv;
     if (seg == 0) {
         const float* E1 = rho1;
 #pragma unroll
@@ -547,7 +564,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
                 }
         }
     }
-    write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
+    write_zvt<T, D, MP, CC>(ZvT, Zv, w, g, r);
     const double rT = AN ? a.rperiod[h] : 0.0;
 
     for (int n = 0; n < nch; ++n) {
@@ -562,7 +579,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
             tErev = opaque(tErev);
         }
         __syncthreads();  // previous chunk done with Qs / Kt / Vt and the twiddle row
-        stage_store<T, D, MP, true>(st, Qs, Kt, Vt, c, tid);
+        stage_store<T, D, MP, true, CC>(st, Qs, Kt, Vt, c, tid);
         if constexpr (AN) {
             for (int m = tid; m < MP; m += GG::NTHR) {
                 float cs = 0.f, sn = 0.f;
@@ -578,8 +595,8 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
         }
         if (n + 1 < nch) {
             const int tn = tok0 + C, cn = min(C, a.L - tn), i = min(16 * w + r, cn - 1);
-            stage_load<T, D, MP, true>(st, qb + (size_t)tn * ts, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts,
-                                       cn, tid);
+            stage_load<T, D, MP, true, CC>(st, qb + (size_t)tn * ts, kb_ + (size_t)tn * ts, vb + (size_t)tn * ts, ts,
+                                           cn, tid);
             if constexpr (!KROWS) {
 #pragma unroll
                 for (int kb = 0; kb < GG::KBD; ++kb) kpf[kb] = ld_frag<T>(kb_ + (size_t)(tn + i) * ts, 32 * kb, g);
@@ -653,7 +670,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
                                                             : ld_frag_lo<T>(grow, 32 * kb, g);
 #pragma unroll
                             for (int p = 0; p < 2; ++p)
-                                U[o][p][ct] = mma(ld_frag<T>(tEbar + (size_t)(16 * (p * NMT + mt) + r) * sR, 32 * kb, g),
+                                U[o][p][ct] = mma(ld_frag_c<T, CC>(tEbar + (size_t)(16 * (p * NMT + mt) + r) * sR, kb, g),
                                                   gf, U[o][p][ct]);
                         }
                     }
@@ -767,7 +784,8 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
                 for (int kb = 0; kb < GG::KBM; ++kb)
                     oa[dt] = mma(ld_frag<T>(ZvT + (size_t)(16 * dt + r) * GG::LDZ, 32 * kb, g), wf[kb], oa[dt]);
             }
-            floatx4 hh[NT];
+            floatx4 hh[NT < 2 ? 2 : NT];  // a 16-token chunk pairs its one tile with a zero tile
+            hh[NT < 2 ? 1 : 0] = zero4();
 #pragma unroll
             for (int kt = 0; kt < NT; ++kt) {
                 hh[kt] = zero4();
@@ -788,7 +806,7 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
                     const F hf = frag_from_acc<T>(hh[2 * kb], hh[2 * kb + 1]);
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt)
-                        oa[dt] = mma(ld_frag<T>(Vt + (size_t)(16 * dt + r) * GG::LDK, 32 * kb, g), hf, oa[dt]);
+                        oa[dt] = mma(ld_frag_c<T, CC>(Vt + (size_t)(16 * dt + r) * GG::LDK, kb, g), hf, oa[dt]);
                 }
             }
             if (j < c) {
@@ -798,8 +816,8 @@ __global__ __launch_bounds__((Geo<T, D, MP>::NTHR)) void forward_kernel(FwdArgs 
         }
         __syncthreads();  // everyone done reading ZvT
 
-        advance_state<T, D, MP>(Zk, Zv, Kt, Vt, rhoC, E32h, tErev, sR, c, w, g, r);
-        write_zvt<T, D, MP>(ZvT, Zv, w, g, r);
+        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, E32h, tErev, sR, c, w, g, r);
+        write_zvt<T, D, MP, CC>(ZvT, Zv, w, g, r);
     }
 
     // ---- final state (last segment): Z = conj(rho) Z'

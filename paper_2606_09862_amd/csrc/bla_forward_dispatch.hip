@@ -7,8 +7,9 @@ namespace bla {
     if (p.D == DD && p.MP == MMP && p.SP == SSP) return Launch<TT, DD, MMP, SSP>::forward(p, a, s);
 #define BLA_SUM_CASE(TT, DD, MMP, SSP) \
     if (p.D == DD && p.MP == MMP && p.SP == SSP) return Launch<TT, DD, MMP, SSP>::summary(p, a, s);
-#define BLA_SUP_CASE(TT, DD, MMP, SSP) \
-    if (D == DD && MP == MMP && SP == SSP) return fits<TT, DD, MMP, SSP>() || pair_units<TT, DD, MMP, SSP>() > 0;
+#define BLA_SUP_CASE(TT, DD, MMP, SSP)                                                             \
+    if (D == DD && MP == MMP && SP == SSP)                                                          \
+        return one_unit_fits<TT, DD, MMP, SSP>(C) || (C == kChunk && pair_units<TT, DD, MMP, SSP>() > 0);
 
 hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s)
 {
@@ -41,7 +42,7 @@ int forward_units_per_wg(int is_bf16, int D, int MP, int SP)
     return 0;
 }
 
-bool forward_supported(int is_bf16, int D, int MP, int SP)
+bool forward_supported(int is_bf16, int D, int MP, int SP, int C)
 {
     if (is_bf16) {
         BLA_FOR_EACH_SHAPE(BLA_SUP_CASE, bf16)

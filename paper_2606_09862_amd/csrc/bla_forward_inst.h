@@ -30,9 +30,52 @@
 
 namespace bla {
 
-template <typename T, int D, int MP, int SP> constexpr bool fits()
+template <typename T, int D, int MP, int SP, int CC = kChunk> constexpr bool fits()
 {
-    return Fwd<T, D, MP, SP>::LDS_BYTES <= kMaxLds;
+    return Fwd<T, D, MP, SP, CC>::LDS_BYTES <= kMaxLds;
+}
+
+// Chunk lengths other than the default 64 run on the one-unit kernels and are built for
+// M <= 64 (padded modes up to 64), where their tiles and registers fit.
+template <int MP, int CC> constexpr bool chunk_built() { return CC == kChunk || MP <= 64; }
+
+template <typename T, int D, int MP, int SP, int CC>
+hipError_t launch_one_unit(const Plan& p, const FwdArgs& a, hipStream_t s)
+{
+    if constexpr (chunk_built<MP, CC>() && fits<T, D, MP, SP, CC>()) {
+        const dim3 grid((unsigned)(p.B * p.H * p.nseg));
+        if (a.anchor)
+            hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, true, CC>), grid, dim3(Geo<T, D, MP, CC>::NTHR), 0, s, a);
+        else
+            hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, false, CC>), grid, dim3(Geo<T, D, MP, CC>::NTHR), 0, s, a);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+template <typename T, int D, int MP, int CC>
+hipError_t launch_one_summary(const Plan& p, const FwdArgs& a, hipStream_t s)
+{
+    if constexpr (chunk_built<MP, CC>()) {
+        hipLaunchKernelGGL((summary_kernel<T, D, MP, CC>), dim3((unsigned)(p.B * p.H * p.nbs)),
+                           dim3(Geo<T, D, MP, CC>::NTHR), 0, s, a);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+// Whether the one-unit forward kernel exists for a shape and chunk length.
+template <typename T, int D, int MP, int SP> bool one_unit_fits(int C)
+{
+    switch (C) {
+    case 16: return chunk_built<MP, 16>() && fits<T, D, MP, SP, 16>();
+    case 32: return chunk_built<MP, 32>() && fits<T, D, MP, SP, 32>();
+    case 64: return fits<T, D, MP, SP, 64>();
+    case 128: return chunk_built<MP, 128>() && fits<T, D, MP, SP, 128>();
+    }
+    return false;
 }
 
 template <typename T, int D, int MP, int SP> struct Launch {
@@ -68,16 +111,13 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
                 return hipGetLastError();                                                               \
             }                                                                                           \
         }                                                                                               \
-        if constexpr (fits<T, D, MP, SP>()) {                                                           \
-            const dim3 grid((unsigned)(p.B * p.H * p.nseg));                                            \
-            if (a.anchor)                                                                               \
-                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, true>), grid, dim3(Geo<T, D, MP>::NTHR), 0, s, a); \
-            else                                                                                        \
-                hipLaunchKernelGGL((forward_kernel<T, D, MP, SP, false>), grid, dim3(Geo<T, D, MP>::NTHR), 0, s, a); \
-            return hipGetLastError();                                                                   \
-        } else {                                                                                        \
-            return hipErrorInvalidValue;                                                                \
+        switch (p.C) {                                                                                  \
+        case 16: return launch_one_unit<T, D, MP, SP, 16>(p, a, s);                                     \
+        case 32: return launch_one_unit<T, D, MP, SP, 32>(p, a, s);                                     \
+        case 64: return launch_one_unit<T, D, MP, SP, 64>(p, a, s);                                     \
+        case 128: return launch_one_unit<T, D, MP, SP, 128>(p, a, s);                                   \
         }                                                                                               \
+        return hipErrorInvalidValue;                                                                    \
     }                                                                                                   \
     template <> hipError_t Launch<T, D, MP, SP>::summary(const Plan& p, const FwdArgs& a, hipStream_t s) \
     {                                                                                                   \
@@ -89,10 +129,12 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
                 return hipGetLastError();                                                               \
             }                                                                                           \
         }                                                                                               \
-        {                                                                                               \
-            hipLaunchKernelGGL((summary_kernel<T, D, MP>), dim3((unsigned)(p.B * p.H * p.nbs)),         \
-                               dim3(Geo<T, D, MP>::NTHR), 0, s, a);                                     \
+        switch (p.C) {                                                                                  \
+        case 16: return launch_one_summary<T, D, MP, 16>(p, a, s);                                      \
+        case 32: return launch_one_summary<T, D, MP, 32>(p, a, s);                                      \
+        case 64: return launch_one_summary<T, D, MP, 64>(p, a, s);                                      \
+        case 128: return launch_one_summary<T, D, MP, 128>(p, a, s);                                    \
         }                                                                                               \
-        return hipGetLastError();                                                                       \
+        return hipErrorInvalidValue;                                                                    \
     }                                                                                                   \
     }

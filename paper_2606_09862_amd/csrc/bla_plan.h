@@ -10,7 +10,7 @@
 
 namespace bla {
 
-constexpr int kChunk = 64;      // tokens per chunk of the parallel form
+constexpr int kChunk = 64;      // default tokens per chunk of the parallel form (the pair kernels' only one)
 constexpr int kThreads = 256;   // 4 waves of 64 lanes per workgroup
 constexpr int kMaxHeadsPerTableLaunch = 64;
 
@@ -75,6 +75,7 @@ struct FwdArgs {
     const float* rotblk;
     const double* rperiod;  // [H] 1 / T (anchored readout only)
     int B, H, L, M;
+    int C;        // tokens per chunk (the per-head phase table E32 has C + 1 rows)
     int nch, nseg, cps, cpb, nbs;
     long long t0;
     float scale;  // score scale (applied by the pair kernel; folded into ABs otherwise)
@@ -254,8 +255,8 @@ hipError_t launch_decay_gates(const GateArgs& g, hipStream_t s);
 hipError_t launch_backward(int bf16, int D, int MP, int SP, const BwdArgs& a, hipStream_t s,
                            void* const* events);
 
-// Whether a forward kernel exists for (bf16, D, MP, SP).
-bool forward_supported(int bf16, int D, int MP, int SP);
+// Whether a forward kernel exists for (bf16, D, MP, SP) and chunk length C.
+bool forward_supported(int bf16, int D, int MP, int SP, int C);
 
 // bla_forward on q, k, v and o with the element strides of FwdArgs: in_strides and
 // out_strides are {batch, head, token} (nullable: contiguous [B, H, L, d]).  Each stride

@@ -95,7 +95,15 @@ def P(**kw):
     (dict(M=129), UNSUPPORTED),
     (dict(M=16, S=33), UNSUPPORTED),        # S beyond 2 * padded M
     (dict(S=257), UNSUPPORTED),
-    (dict(chunk=32), UNSUPPORTED),
+    (dict(chunk=16), OK),
+    (dict(chunk=32), OK),
+    (dict(chunk=64), OK),
+    (dict(chunk=128), OK),
+    (dict(chunk=128, d=32, dtype="f32"), OK),
+    (dict(chunk=48), UNSUPPORTED),
+    (dict(chunk=8), UNSUPPORTED),
+    (dict(chunk=32, M=100, S=100), UNSUPPORTED),   # chunks other than 64 need P(M) <= 64
+    (dict(chunk=128, d=64, M=64, S=64, dtype="f32"), UNSUPPORTED),  # float32 tiles exceed the LDS
     (dict(d=128, M=128, S=128, dtype="f32"), UNSUPPORTED),  # float32 tiles exceed the LDS
     (dict(M=0), INVALID),
     (dict(S=0), INVALID),
@@ -276,6 +284,10 @@ def test_backward_errors(lib):
     assert call(args, params=pa) == UNSUPPORTED
     assert bla.backward_workspace_size(P(dtype="f32", d=32, M=32, S=64)) > 0
     assert bla.backward_workspace_size(P(dtype="f32", d=64)) == 0
+    # the backward runs 64-token chunks only
+    assert bla.backward_workspace_size(P(chunk=64)) > 0
+    assert bla.backward_workspace_size(P(chunk=32)) == 0
+    assert call(args, params=P(L=10, chunk=32)) == UNSUPPORTED
 
 
 def test_layer_errors(lib):

@@ -17,13 +17,14 @@ from test_gpu_parity import TOL, _bla, _say, assert_close, gauss, to_dev
 pytestmark = pytest.mark.gpu
 
 
-def run_anchored(q, k, v, T, M, S, dtype, t0=0, sk=None, sv=None, label=""):
+def run_anchored(q, k, v, T, M, S, dtype, t0=0, sk=None, sv=None, label="", chunk=0):
     bla = _bla()
-    _say(f"anchored case {label}: shape {q.shape} M={M} S={S} T={list(T)} t0={t0} dtype={dtype}")
+    _say(f"anchored case {label}: shape {q.shape} M={M} S={S} T={list(T)} t0={t0} dtype={dtype} chunk={chunk}")
     tq, tk, tv = (to_dev(x, dtype) for x in (q, k, v))
     tsk = None if sk is None else torch.from_numpy(np.ascontiguousarray(sk, np.float32)).cuda()
     tsv = None if sv is None else torch.from_numpy(np.ascontiguousarray(sv, np.float32)).cuda()
-    o, ok, ov = bla.forward(tq, tk, tv, T, M, S, t0=t0, state_k=tsk, state_v=tsv, phase_anchor=True)
+    o, ok, ov = bla.forward(tq, tk, tv, T, M, S, t0=t0, state_k=tsk, state_v=tsv, phase_anchor=True,
+                            chunk=chunk)
     torch.cuda.synchronize()
     return o.float().cpu().numpy(), ok.cpu().numpy(), ov.cpu().numpy()
 
@@ -60,6 +61,22 @@ def test_anchor_segments(dtype, B, H, L, d, M, S, T):
     o, ok, ov = run_anchored(q, k, v, T[:H], M, S, dtype, label=f"segments {B}x{H}x{L}")
     ref_o, _, _ = oracle.forward_anchored(q, k, v, T[:H], M, S)
     _, ref_k, ref_v = oracle.forward(q, k, v, T[:H], M, S)
+    tol = TOL[dtype]
+    assert_close(o, ref_o, tol, "O")
+    assert_close(ok, ref_k, tol, "state_k")
+    assert_close(ov, ref_v, tol, "state_v")
+
+
+@pytest.mark.parametrize("chunk", [16, 32, 128])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_anchor_chunk_lengths(dtype, chunk):
+    """Anchored slots with chunks of 16, 32 and 128 tokens: each chunk's twiddle row at its own
+    absolute start; several segments, ragged tail, t0 > 0."""
+    B, H, L, d, M, S, T, t0 = 1, 2, 64 * 21 + 11, 32, 16, 31, (31.0, 45.5), 333
+    q, k, v = gauss(L + chunk, B, H, L, d, dtype)
+    o, ok, ov = run_anchored(q, k, v, T, M, S, dtype, t0=t0, label=f"chunk {chunk}", chunk=chunk)
+    ref_o, _, _ = oracle.forward_anchored(q, k, v, T, M, S, t0=t0)
+    _, ref_k, ref_v = oracle.forward(q, k, v, T, M, S, t0=t0)
     tol = TOL[dtype]
     assert_close(o, ref_o, tol, "O")
     assert_close(ok, ref_k, tol, "state_k")

@@ -85,14 +85,14 @@ def to_dev(x, dtype):
     return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to("cuda").to(dtype)
 
 
-def run_case(q, k, v, T, M, S, dtype, t0=0, sk=None, sv=None, literal=False, label=""):
+def run_case(q, k, v, T, M, S, dtype, t0=0, sk=None, sv=None, literal=False, label="", chunk=0):
     """q,k,v float32 numpy holding dtype-representable values; returns errors dict."""
     bla = _bla()
-    _say(f"case {label}: shape {q.shape} M={M} S={S} T={list(T)} t0={t0} dtype={dtype}")
+    _say(f"case {label}: shape {q.shape} M={M} S={S} T={list(T)} t0={t0} dtype={dtype} chunk={chunk}")
     tq, tk, tv = (to_dev(x, dtype) for x in (q, k, v))
     tsk = None if sk is None else torch.from_numpy(np.ascontiguousarray(sk, np.float32)).cuda()
     tsv = None if sv is None else torch.from_numpy(np.ascontiguousarray(sv, np.float32)).cuda()
-    o, ok, ov = bla.forward(tq, tk, tv, T, M, S, t0=t0, state_k=tsk, state_v=tsv)
+    o, ok, ov = bla.forward(tq, tk, tv, T, M, S, t0=t0, state_k=tsk, state_v=tsv, chunk=chunk)
     torch.cuda.synchronize()
     ref_o, ref_k, ref_v = oracle.forward(q, k, v, T, M, S, t0=t0,
                                          state_k=None if sk is None else np.asarray(sk, np.float64),
@@ -122,6 +122,10 @@ def test_workload1_tiny_fp32():
 
 
 # ------------------------------------------------------------------ small shapes, ragged, edge cases
+CHUNKS = [16, 32, 64, 128]   # Alg. 3's chunk length (64 is the default)
+
+
+@pytest.mark.parametrize("chunk", CHUNKS)
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("B,H,L,d,M,S,T", [
     (2, 3, 100, 32, 16, 16, (31.0, 62.0, 40.5)),     # ragged last chunk, non-integer T
@@ -131,9 +135,21 @@ def test_workload1_tiny_fp32():
     (3, 1, 130, 32, 32, 63, (3.0,)),                  # T below 2M-1 is clamped
     (1, 1, 1, 64, 4, 4, (7.0,)),                      # a single token
 ])
-def test_small_shapes(dtype, B, H, L, d, M, S, T):
+def rejected_chunk(B, H, L, d, M, S, dtype, chunk):
+    """float32 tiles of 128-token chunks at d = 64 exceed the LDS: the library rejects the
+    shape (BLA_ERR_UNSUPPORTED) before any launch."""
+    if not (dtype == torch.float32 and chunk == 128 and d == 64):
+        return False
+    bla = _bla()
+    assert bla.supported(bla.make_params(B, H, L, d, M, S, dtype, chunk=chunk)) == 2
+    return True
+
+
+def test_small_shapes(dtype, B, H, L, d, M, S, T, chunk):
+    if rejected_chunk(B, H, L, d, M, S, dtype, chunk):
+        return
     q, k, v = gauss(L * 7 + M, B, H, L, d, dtype)
-    run_case(q, k, v, T, M, S, dtype, label=f"small {B}x{H}x{L}x{d}")
+    run_case(q, k, v, T, M, S, dtype, label=f"small {B}x{H}x{L}x{d}", chunk=chunk)
 
 
 @pytest.mark.parametrize("B,H,L,d,M,S,T", [
@@ -172,25 +188,42 @@ def test_state_in_and_offset(dtype):
              label="continuation")
 
 
+@pytest.mark.parametrize("chunk", CHUNKS)
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_many_segments(dtype):
+def test_many_segments(dtype, chunk):
     """Few sequences and many chunks: the sequence is split into segments whose entering
     states come from per-block summaries and the scan; ragged tail included."""
     B, H, L, d, M, S, T = 1, 2, 64 * 37 + 5, 32, 16, 31, (31.0, 62.0)
     q, k, v = gauss(12, B, H, L, d, dtype)
-    run_case(q, k, v, T, M, S, dtype, label="segments")
+    run_case(q, k, v, T, M, S, dtype, label="segments", chunk=chunk)
 
 
+@pytest.mark.parametrize("chunk", CHUNKS)
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_segments_with_state_in(dtype):
-    B, H, L, d, M, S, T = 1, 1, 64 * 20, 64, 16, 16, (50.0,)
+def test_segments_with_state_in(dtype, chunk):
+    B, H, L, d, M, S, T = 1, 1, 64 * 20 + 7, 64, 16, 16, (50.0,)
+    if rejected_chunk(B, H, L, d, M, S, dtype, chunk):
+        return
     q, k, v = gauss(13, B, H, L, d, dtype)
     rng = np.random.default_rng(14)
     sk = rng.standard_normal((B, H, 2, M, d)).astype(np.float32)
     sv = rng.standard_normal((B, H, 2, M, d)).astype(np.float32)
     sk[:, :, 1, 0] = 0.0
     sv[:, :, 1, 0] = 0.0
-    run_case(q, k, v, T, M, S, dtype, t0=1000, sk=sk, sv=sv, label="segments+state_in")
+    run_case(q, k, v, T, M, S, dtype, t0=1000, sk=sk, sv=sv, label="segments+state_in", chunk=chunk)
+
+
+@pytest.mark.parametrize("chunk", [16, 32, 128])
+def test_chunk_lengths_lm_shape(chunk):
+    """The LM-layer head shape (d = M = S = 64, bf16, periods 127 and 254) with the other
+    chunk lengths, against the oracle and against the default 64-token chunks."""
+    bla = _bla()
+    B, H, L, d, M, S, T = 2, 2, 64 * 12 + 29, 64, 64, 64, (127.0, 254.0)
+    q, k, v = gauss(17 + chunk, B, H, L, d, torch.bfloat16)
+    o, sk, sv = run_case(q, k, v, T, M, S, torch.bfloat16, label=f"LM shape chunk {chunk}", chunk=chunk)
+    o64, sk64, sv64 = bla.forward(*(to_dev(x, torch.bfloat16) for x in (q, k, v)), T, M, S)
+    torch.cuda.synchronize()
+    assert_close(o.float().cpu().numpy(), o64.float().cpu().numpy(), 2e-2, "O against chunk 64")
 
 
 def test_empty_and_degenerate():
