@@ -122,6 +122,16 @@ def test_workload1_tiny_fp32():
 
 
 # ------------------------------------------------------------------ small shapes, ragged, edge cases
+def rejected_chunk(B, H, L, d, M, S, dtype, chunk):
+    """float32 tiles of 128-token chunks at d = 64 exceed the LDS: the library rejects the
+    shape (BLA_ERR_UNSUPPORTED) before any launch."""
+    if not (dtype == torch.float32 and chunk == 128 and d == 64):
+        return False
+    bla = _bla()
+    assert bla.supported(bla.make_params(B, H, L, d, M, S, dtype, chunk=chunk)) == 2
+    return True
+
+
 CHUNKS = [16, 32, 64, 128]   # Alg. 3's chunk length (64 is the default)
 
 
@@ -135,16 +145,6 @@ CHUNKS = [16, 32, 64, 128]   # Alg. 3's chunk length (64 is the default)
     (3, 1, 130, 32, 32, 63, (3.0,)),                  # T below 2M-1 is clamped
     (1, 1, 1, 64, 4, 4, (7.0,)),                      # a single token
 ])
-def rejected_chunk(B, H, L, d, M, S, dtype, chunk):
-    """float32 tiles of 128-token chunks at d = 64 exceed the LDS: the library rejects the
-    shape (BLA_ERR_UNSUPPORTED) before any launch."""
-    if not (dtype == torch.float32 and chunk == 128 and d == 64):
-        return False
-    bla = _bla()
-    assert bla.supported(bla.make_params(B, H, L, d, M, S, dtype, chunk=chunk)) == 2
-    return True
-
-
 def test_small_shapes(dtype, B, H, L, d, M, S, T, chunk):
     if rejected_chunk(B, H, L, d, M, S, dtype, chunk):
         return
