@@ -36,9 +36,13 @@
  *   - io_dtype selects float32 or bfloat16 for q, k, v, o; states are float32.
  *   - T is a HOST array of H periods (double).  Each is clamped to >= 2M-1, as the
  *     paper's algorithms do; NaN, infinite, non-positive or > 1e9 is an error.
- *   - Every device buffer is owned by the caller.  The library allocates no
+ *   - Every device buffer is owned by the caller.  The operator's calls allocate no
  *     device memory: scratch space (tables, per-block partial states) lives in the
- *     caller's workspace, sized by bla_workspace_size / bla_step_workspace_size.
+ *     caller's workspace, sized by bla_workspace_size / bla_step_workspace_size.  Two
+ *     exceptions, both outside the operator's own kernels: the first bla_layer_forward
+ *     on a device creates a hipBLASLt handle (hipBLASLt allocates its own memory), and
+ *     bla_forward_noalloc's workspace is a fixed device array of the library's code
+ *     object (allocated with the module, once per device).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream).
  *     Argument errors are reported synchronously before anything is launched;
  *     launch failures are reported as BLA_ERR_HIP.  Buffers must stay valid until

@@ -14,6 +14,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include <hip/hip_runtime.h>
 #include <hipblaslt/hipblaslt.h>
 
@@ -29,12 +31,15 @@ constexpr size_t kGemmWorkspace = size_t(32) << 20;  // hipBLASLt scratch inside
 
 size_t lalign(size_t x) { return (x + kLayerAlign - 1) / kLayerAlign * kLayerAlign; }
 
-// One hipBLASLt handle per device, created on first use and kept for the process.
+// One hipBLASLt handle per device, created on first use and kept for the process.  Creation
+// is serialised, so threads that reach a device's first call together share one handle.
 hipblasLtHandle_t gemm_handle()
 {
+    static std::mutex mu;
     static hipblasLtHandle_t handles[64] = {nullptr};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    std::lock_guard<std::mutex> lk(mu);
     if (!handles[dev] && hipblasLtCreate(&handles[dev]) != HIPBLAS_STATUS_SUCCESS) handles[dev] = nullptr;
     return handles[dev];
 }
