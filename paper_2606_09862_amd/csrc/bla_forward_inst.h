@@ -124,7 +124,7 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
         if constexpr (pair_units<T, D, MP, SP>() > 0) {                                                 \
             if (p.pair) {                                                                               \
                 hipLaunchKernelGGL((summary_pair_kernel<D, MP>),                                        \
-                                   dim3((unsigned)(p.B * p.nbs * summary_splits<D, MP>()), (unsigned)p.H), \
+                                   dim3((unsigned)summary_grid_x<D, MP>((long long)p.B * p.nbs), (unsigned)p.H),  \
                                    dim3(summary_threads<D, MP>()), 0, s, a);                            \
                 return hipGetLastError();                                                               \
             }                                                                                           \

@@ -238,52 +238,58 @@ __device__ __forceinline__ void pair_advance(PStateDM<D, MP>& Zk, PStateDM<D, MP
 }
 
 // ---------------------------------------------------------------------------------
-// Segment summaries: DS workgroups per (b, h, summarised block), each reducing DW = D/DS
-// columns of K and V.  Every summarised chunk is full (only the last chunk of a sequence
-// can be shorter, and the last segment is never summarised).
+// Segment summaries: DS = D/32 workgroups per (b, h, summarised block), each reducing 32
+// columns of K and V.  Every summarised chunk is full (only the last chunk of a sequence can
+// be shorter, and the last segment is never summarised).
 //
-// Wave w owns column tiles wd + WD*i of its workgroup and mode tiles wm + WM*j
-// (w = wd + WD*wm): it reads from LDS only the K/V columns of its tiles, and keeps the
-// phase-table fragments of its mode tiles in registers for the whole block when they
-// fit.  K and V are staged several chunks ahead in registers and double-buffered in LDS
-// (one barrier per chunk).
+// K and V are streamed once.  Narrow column slices make many small workgroups (four waves
+// and about 44 KB of LDS at MP = 64, three per compute unit), each staging NPF = 4 chunks
+// ahead in registers plus one in LDS, so that many loads are in flight per compute unit.
+// The DS slices of a block run on one XCD (see the index mapping in the kernel), so each
+// 128-byte line of K and V is fetched from HBM once.
+//
+// Wave w owns column tile wd = w % 2 of its slice and mode tiles wm + WM*j (wm = w / 2).
+// K and V are double-buffered in LDS (one barrier per chunk).
 template <int D, int MP> struct SumPair {
     static constexpr int C = kChunk, KBC = C / 32;
-    static constexpr int DS = D >= 128 ? 2 : 1, DW = D / DS;
+    static constexpr int DW = 32, DS = D / DW;
     static constexpr int NDT = DW / 16, NMT = MP / 16;
-    static constexpr int WD = NDT < 4 ? NDT : 4, WM = WD == 2 ? 2 : 1, NW = WD * WM;
+    static constexpr int WD = NDT, WM = NMT < 2 ? NMT : 2, NW = WD * WM;
     static constexpr int NTHR = 64 * NW;
-    static constexpr int ODT = NDT / WD, OMT = (NMT + WM - 1) / WM;
-    static constexpr bool EREG = 16 * OMT <= 64;  // phase-table fragments held in VGPRs
-    // K/V row stride: 16 elements of pad puts the four rows of a transposed read's
-    // 16-lane group 8 banks apart (conflict-free)
+    static constexpr int ODT = 1, OMT = NMT / WM;
+    static constexpr int MINB = MP <= 64 ? 3 : 2;  // workgroups per compute unit (launch bound)
+    // row strides: the four rows of a transposed read's 16-lane group, and the two groups
+    // of one LDS cycle, fall on distinct banks
     static constexpr int LK = DW + 16;
-    static constexpr int LE = 2 * MP + 12;
+    static constexpr int LE = 2 * MP + 16;
     static constexpr size_t E_ELEMS = (size_t)C * LE, KV_ELEMS = (size_t)C * LK;
     static constexpr size_t LDS_BYTES = 2 * (E_ELEMS + 4 * KV_ELEMS) + 2 * MP * 4;
     static constexpr int PR = DW / 8;                 // 16-byte pieces per row of a tile
     static constexpr int PIECES = 2 * C * PR;         // pieces of K and V per chunk
     static constexpr int PPT = (PIECES + NTHR - 1) / NTHR;
-    static constexpr int NPF = 2;  // chunks in flight in registers (plus one in LDS)
-    static_assert(NDT % WD == 0, "column tiles split evenly over the waves");
+    static constexpr int NPF = 4;  // chunks in flight in registers (plus one in LDS)
+    static_assert(D % DW == 0 && NMT % WM == 0, "column and mode tiles split evenly over the waves");
     static_assert(NPF % 2 == 0, "the LDS buffer parity follows the unrolled stage index");
 };
 template <int D, int MP> using SStage = bf16x8[SumPair<D, MP>::PPT];
 template <int D, int MP> using SState = floatx4[SumPair<D, MP>::OMT][SumPair<D, MP>::ODT][2];
-template <int D, int MP> using SEFrag = bf16x8[SumPair<D, MP>::EREG ? SumPair<D, MP>::OMT : 1][SumPair<D, MP>::KBC][2];
 
-// k, v: first row of the chunk, column offset of the workgroup's slice applied; ts: token stride
+// k, v: first row of the chunk, column offset of the workgroup's slice applied; ts: token
+// stride; w: the wave (uniform).  A wave's 64 pieces come from one of K and V, so the base
+// pointer of each load is uniform and the per-lane part a 32-bit offset.
 template <int D, int MP>
-__device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k, const bf16* v, int ts, int tid)
+__device__ __forceinline__ void sum_stage_load(SStage<D, MP>& st, const bf16* k, const bf16* v, int ts, int w,
+                                               int lane)
 {
     using P = SumPair<D, MP>;
+    static_assert((P::C * P::PR) % 64 == 0, "a wave's pieces lie in one of K and V");
 #pragma unroll
     for (int i = 0; i < P::PPT; ++i) {
-        const int u = tid + P::NTHR * i;
-        if (P::PIECES % P::NTHR == 0 || u < P::PIECES) {
-            const int which = u / (P::C * P::PR), rem = u % (P::C * P::PR);
-            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + (size_t)(rem / P::PR) * ts +
-                                                     8 * (rem % P::PR));
+        const int u0 = 64 * w + P::NTHR * i;  // the wave's first piece (uniform)
+        if (P::PIECES % P::NTHR == 0 || u0 < P::PIECES) {
+            const int which = u0 / (P::C * P::PR), rem = u0 % (P::C * P::PR) + lane;
+            const unsigned off = (unsigned)((rem / P::PR) * ts + 8 * (rem % P::PR));
+            st[i] = *reinterpret_cast<const bf16x8*>((which == 0 ? k : v) + off);
         }
     }
 }
@@ -292,43 +298,80 @@ template <int D, int MP>
 __device__ __forceinline__ void sum_stage_store(const SStage<D, MP>& st, bf16* Ks, bf16* Vs, int tid)
 {
     using P = SumPair<D, MP>;
+    static_assert(P::LK % 8 == 0, "16-byte rows");
 #pragma unroll
     for (int i = 0; i < P::PPT; ++i) {
         const int u = tid + P::NTHR * i;
         if (P::PIECES % P::NTHR == 0 || u < P::PIECES) {
             const int which = u / (P::C * P::PR), rem = u % (P::C * P::PR);
             bf16* dst = (which == 0 ? Ks : Vs) + (size_t)(rem / P::PR) * P::LK + 8 * (rem % P::PR);
-            const bf16x8 x = st[i];
-            *reinterpret_cast<bf16x4*>(dst) = __builtin_shufflevector(x, x, 0, 1, 2, 3);
-            *reinterpret_cast<bf16x4*>(dst + 4) = __builtin_shufflevector(x, x, 4, 5, 6, 7);
+            *reinterpret_cast<bf16x8*>(dst) = st[i];
+        }
+    }
+}
+
+// Z <- rot o Z for the owned mode tiles; rot = (cos | sin) of the rotation, float32 in LDS.
+// KMAJOR: the tiles hold (d rows, m columns) (Z_k); otherwise (m rows, d columns) (Z_v).
+template <int D, int MP, bool KMAJOR>
+__device__ __forceinline__ void sum_rotate(SState<D, MP>& Z, const float* rot, int wm, int g, int r)
+{
+    using P = SumPair<D, MP>;
+#pragma unroll
+    for (int j = 0; j < P::OMT; ++j) {
+        const int mt = wm + P::WM * j;
+        if constexpr (KMAJOR) {
+            const float cc = rot[16 * mt + r], ss = rot[MP + 16 * mt + r];
+#pragma unroll
+            for (int i = 0; i < P::ODT; ++i) {
+                const floatx4 kr = Z[j][i][0], ki = Z[j][i][1];
+                Z[j][i][0] = cc * kr - ss * ki;
+                Z[j][i][1] = ss * kr + cc * ki;
+            }
+        } else {
+            const floatx4 cv = ld4f(rot + 16 * mt + 4 * g), sv = ld4f(rot + MP + 16 * mt + 4 * g);
+#pragma unroll
+            for (int i = 0; i < P::ODT; ++i) {
+                const floatx4 vr = Z[j][i][0], vi = Z[j][i][1];
+                Z[j][i][0] = cv * vr - sv * vi;
+                Z[j][i][1] = sv * vr + cv * vi;
+            }
         }
     }
 }
 
 template <int D, int MP> constexpr int summary_threads() { return SumPair<D, MP>::NTHR; }
-template <int D, int MP> constexpr int summary_splits() { return SumPair<D, MP>::DS; }
+// x extent of the summary grid for `jobs` (b, block) pairs: padded to a multiple of 8, times DS
+template <int D, int MP> constexpr long long summary_grid_x(long long jobs)
+{
+    return (jobs + 7) / 8 * 8 * SumPair<D, MP>::DS;
+}
 
-// grid: (B * nbs * DS) x H workgroups of NTHR threads; workgroup x covers column slice
-// x % DS of block (x / DS) % nbs of sequence (b = x / (DS * nbs), h), i.e. chunks
+// grid: summary_grid_x(B * nbs) x H workgroups of NTHR threads; every (b, summarised block)
+// pair has DS workgroups, one per 32-column slice of K and V; the block covers chunks
 // [blk * cpb, (blk + 1) * cpb).
 template <int D, int MP>
-__global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(FwdArgs a)
+__global__ __launch_bounds__((SumPair<D, MP>::NTHR))
+__attribute__((amdgpu_waves_per_eu(SumPair<D, MP>::MINB * SumPair<D, MP>::NW / 4))) void summary_pair_kernel(FwdArgs a)
 {
     using P = SumPair<D, MP>;
     using F = bf16x8;
     constexpr int C = P::C, NMT = P::NMT, ODT = P::ODT, OMT = P::OMT, WD = P::WD, WM = P::WM, DS = P::DS;
     __shared__ __attribute__((aligned(16))) char lds_raw[P::LDS_BYTES];
-    bf16* sE = reinterpret_cast<bf16*>(lds_raw);
-    bf16* KV = sE + P::E_ELEMS;  // [buffer][K | V][C][LK]
+    bf16* sE = reinterpret_cast<bf16*>(lds_raw);  // [C][LE]: conj(rho^i) = [cos | -sin]
+    bf16* KV = sE + P::E_ELEMS;                   // [buffer][K | V][C][LK]
     float* sRhoC = reinterpret_cast<float*>(KV + 4 * P::KV_ELEMS);
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     __builtin_assume(w >= 0 && w < P::NW);
-    // with one wave row along the modes every wave owns every mode tile (known statically)
-    const int wd = WM == 1 ? w : w % WD, wm = WM == 1 ? 0 : w / WD;
+    const int wd = w % WD, wm = w / WD;
     const int g = (tid & 63) >> 4, r = tid & 15;
-    const int h = blockIdx.y, ds = blockIdx.x % DS, blk = (blockIdx.x / DS) % a.nbs, b = blockIdx.x / (DS * a.nbs);
+    // Workgroups are dealt to the eight XCDs by linear index (x mod 8 with a row length that
+    // is a multiple of 8); the DS slices of a block take indices 8 apart, so they share an
+    // XCD and its L2 and each 128-byte line of K and V is fetched from HBM once.
+    const int xq = blockIdx.x / 8, ds = xq % DS, job = (xq / DS) * 8 + blockIdx.x % 8;
+    if (job >= a.B * a.nbs) return;  // grid padding (whole workgroup, before any barrier)
+    const int h = blockIdx.y, blk = job % a.nbs, b = job / a.nbs;
     const int bh = b * a.H + h;
     const size_t first = (size_t)blk * a.cpb * C;
     const int ts = a.in_t;
@@ -350,28 +393,25 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
 #pragma unroll
     for (int i = 0; i < NPF; ++i) {
         const size_t off = (size_t)min(i, last) * C * ts;
-        sum_stage_load<D, MP>(st[i], kb_ + off, vb + off, ts, tid);
+        sum_stage_load<D, MP>(st[i], kb_ + off, vb + off, ts, w, tid & 63);
     }
     sum_stage_store<D, MP>(st[0], KV, KV + P::KV_ELEMS, tid);
     {
         const size_t off = (size_t)min(NPF, last) * C * ts;
-        sum_stage_load<D, MP>(st[0], kb_ + off, vb + off, ts, tid);
+        sum_stage_load<D, MP>(st[0], kb_ + off, vb + off, ts, w, tid & 63);
     }
     __syncthreads();  // tables and chunk 0 visible
 
-    // conj(rho^i) fragments of the owned mode tiles: [cos | -sin] with the reduction over i
-    SEFrag<D, MP> ef;
-    if constexpr (P::EREG) {
+    // conj(rho^i) fragments of the owned mode tiles ([cos | -sin], the reduction over i),
+    // the same for every chunk: held in registers for the whole block
+    F ef[OMT][P::KBC][2];
 #pragma unroll
-        for (int j = 0; j < OMT; ++j) {
-            const int mt = min(wm + WM * j, NMT - 1);
+    for (int j = 0; j < OMT; ++j)
 #pragma unroll
-            for (int kb = 0; kb < P::KBC; ++kb) {
-                ef[j][kb][0] = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
-                ef[j][kb][1] = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
-            }
+        for (int kb = 0; kb < P::KBC; ++kb) {
+            ef[j][kb][0] = ld_frag_tr(sE, P::LE, 16 * (wm + WM * j), kb, g, r);
+            ef[j][kb][1] = ld_frag_tr(sE, P::LE, MP + 16 * (wm + WM * j), kb, g, r);
         }
-    }
 
     SState<D, MP> Zk, Zv;  // [mode tile][column tile][Re, Im]
 #pragma unroll
@@ -380,10 +420,10 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
         for (int i = 0; i < ODT; ++i) Zk[j][i][0] = Zk[j][i][1] = Zv[j][i][0] = Zv[j][i][1] = zero4();
 
     // Per chunk: Zk <- rho^C o (Zk + Yk) and Zv <- rho^C o (Zv + Yv).  The rotation of Zv
-    // is deferred to the start of the next chunk, so that each block below pairs 16
-    // matrix-core products with 64 independent vector operations:
-    //   block 1: Zk += Yk (MFMA)  with  Zv <- rho^C o Zv (previous chunk's rotation)
-    //   block 2: Zv += Yv (MFMA)  with  Zk <- rho^C o Zk
+    // is deferred to the start of the next chunk, so that each half below pairs the
+    // matrix-core products of one state with the vector rotation of the other:
+    //   1: Zk += Yk  with  Zv <- rho^C o Zv (the previous chunk's rotation; Zv = 0 at n = 0)
+    //   2: Zv += Yv  with  Zk <- rho^C o Zk
     for (int n0 = 0; n0 < a.cpb; n0 += NPF) {
 #pragma unroll
         for (int s = 0; s < NPF; ++s) {
@@ -397,7 +437,7 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
                 bf16* Kn = KV + (size_t)(s1 & 1) * 2 * P::KV_ELEMS;
                 sum_stage_store<D, MP>(st[s1], Kn, Kn + P::KV_ELEMS, tid);
                 const size_t off = (size_t)min(n + 1 + NPF, last) * C * ts;
-                sum_stage_load<D, MP>(st[s1], kb_ + off, vb + off, ts, tid);
+                sum_stage_load<D, MP>(st[s1], kb_ + off, vb + off, ts, w, tid & 63);
             }
             if (n < a.cpb) {
                 F ktf[P::KBC][ODT], vtf[P::KBC][ODT];
@@ -408,120 +448,58 @@ __global__ __launch_bounds__((SumPair<D, MP>::NTHR)) void summary_pair_kernel(Fw
                         ktf[kb][i] = ld_frag_tr(Ks, P::LK, 16 * (wd + WD * i), kb, g, r);
                         vtf[kb][i] = ld_frag_tr(Vs, P::LK, 16 * (wd + WD * i), kb, g, r);
                     }
-                // block 1
+                // 1
 #pragma unroll
                 for (int kb = 0; kb < P::KBC; ++kb)
 #pragma unroll
-                    for (int j = 0; j < OMT; ++j) {
-                        const int mt = wm + WM * j;
-                        if (mt < NMT) {
-                            F ecf, esf;
-                            if constexpr (P::EREG) {
-                                ecf = ef[j][kb][0];
-                                esf = ef[j][kb][1];
-                            } else {
-                                ecf = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
-                                esf = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
-                            }
-#pragma unroll
-                            for (int i = 0; i < ODT; ++i) {
-                                Zk[j][i][0] = mma(ktf[kb][i], ecf, Zk[j][i][0]);
-                                Zk[j][i][1] = mma(ktf[kb][i], esf, Zk[j][i][1]);
-                            }
-                        }
-                    }
-#pragma unroll
-                for (int j = 0; j < OMT; ++j) {
-                    const int mt = wm + WM * j;
-                    if (mt < NMT) {
-                        const floatx4 cv = ld4f(sRhoC + 16 * mt + 4 * g), sv = ld4f(sRhoC + MP + 16 * mt + 4 * g);
+                    for (int j = 0; j < OMT; ++j)
 #pragma unroll
                         for (int i = 0; i < ODT; ++i) {
-                            const floatx4 vr = Zv[j][i][0], vi = Zv[j][i][1];
-                            Zv[j][i][0] = cv * vr - sv * vi;
-                            Zv[j][i][1] = sv * vr + cv * vi;
+                            Zk[j][i][0] = mma(ktf[kb][i], ef[j][kb][0], Zk[j][i][0]);
+                            Zk[j][i][1] = mma(ktf[kb][i], ef[j][kb][1], Zk[j][i][1]);
                         }
-                    }
-                }
+                sum_rotate<D, MP, false>(Zv, sRhoC, wm, g, r);
 #pragma unroll
-                for (int q = 0; q < 4 * ODT * OMT; ++q) {
+                for (int q = 0; q < 2 * P::KBC * ODT * OMT; ++q) {
                     __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);  // one MFMA
-                    __builtin_amdgcn_sched_group_barrier(0x2, 4, 0);  // four VALU
+                    __builtin_amdgcn_sched_group_barrier(0x2, 2, 0);  // two VALU
                 }
-                // block 2
+                // 2
 #pragma unroll
                 for (int kb = 0; kb < P::KBC; ++kb)
 #pragma unroll
-                    for (int j = 0; j < OMT; ++j) {
-                        const int mt = wm + WM * j;
-                        if (mt < NMT) {
-                            F ecf, esf;
-                            if constexpr (P::EREG) {
-                                ecf = ef[j][kb][0];
-                                esf = ef[j][kb][1];
-                            } else {
-                                ecf = ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r);
-                                esf = ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r);
-                            }
-#pragma unroll
-                            for (int i = 0; i < ODT; ++i) {
-                                Zv[j][i][0] = mma(ecf, vtf[kb][i], Zv[j][i][0]);
-                                Zv[j][i][1] = mma(esf, vtf[kb][i], Zv[j][i][1]);
-                            }
-                        }
-                    }
-#pragma unroll
-                for (int j = 0; j < OMT; ++j) {
-                    const int mt = wm + WM * j;
-                    if (mt < NMT) {
-                        const float cc = sRhoC[16 * mt + r], ss = sRhoC[MP + 16 * mt + r];
+                    for (int j = 0; j < OMT; ++j)
 #pragma unroll
                         for (int i = 0; i < ODT; ++i) {
-                            const floatx4 kr = Zk[j][i][0], ki = Zk[j][i][1];
-                            Zk[j][i][0] = cc * kr - ss * ki;
-                            Zk[j][i][1] = ss * kr + cc * ki;
+                            Zv[j][i][0] = mma(ef[j][kb][0], vtf[kb][i], Zv[j][i][0]);
+                            Zv[j][i][1] = mma(ef[j][kb][1], vtf[kb][i], Zv[j][i][1]);
                         }
-                    }
-                }
+                sum_rotate<D, MP, true>(Zk, sRhoC, wm, g, r);
 #pragma unroll
-                for (int q = 0; q < 4 * ODT * OMT; ++q) {
+                for (int q = 0; q < 2 * P::KBC * ODT * OMT; ++q) {
                     __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x2, 4, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x2, 2, 0);
                 }
             }
             __syncthreads();  // chunk n + 1 visible; chunk n's buffer free
         }
     }
     // the deferred rotation of the last chunk
-#pragma unroll
-    for (int j = 0; j < OMT; ++j) {
-        const int mt = wm + WM * j;
-        if (mt < NMT) {
-            const floatx4 cv = ld4f(sRhoC + 16 * mt + 4 * g), sv = ld4f(sRhoC + MP + 16 * mt + 4 * g);
-#pragma unroll
-            for (int i = 0; i < ODT; ++i) {
-                const floatx4 vr = Zv[j][i][0], vi = Zv[j][i][1];
-                Zv[j][i][0] = cv * vr - sv * vi;
-                Zv[j][i][1] = sv * vr + cv * vi;
-            }
-        }
-    }
+    sum_rotate<D, MP, false>(Zv, sRhoC, wm, g, r);
 
     // Zk tiles hold (d rows, m columns), Zv tiles (m rows, d columns)
     float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
 #pragma unroll
     for (int j = 0; j < OMT; ++j) {
         const int mt = wm + WM * j;
-        if (mt < NMT) {
 #pragma unroll
-            for (int i = 0; i < ODT; ++i) {
-                const int dt = ds * P::NDT + wd + WD * i;
+        for (int i = 0; i < ODT; ++i) {
+            const int dt = ds * P::NDT + wd + WD * i;
 #pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    st4f(S + ((size_t)p * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[j][i][p]);
-                    st4f(S + (size_t)2 * MP * D + ((size_t)p * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
-                         Zv[j][i][p]);
-                }
+            for (int q = 0; q < 2; ++q) {
+                st4f(S + ((size_t)q * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[j][i][q]);
+                st4f(S + (size_t)2 * MP * D + ((size_t)q * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
+                     Zv[j][i][q]);
             }
         }
     }
