@@ -145,6 +145,32 @@ __device__ __forceinline__ bf16x8 ld_frag_2x8(const bf16* row, int kb, int g)
     return join(*a, *(const volatile __attribute__((address_space(3))) bf16x4*)(a + 4));
 }
 
+// Row-swizzled tables.  A table read both as row fragments (ld_frag_2x8: 16 rows, 8 bytes per
+// lane) and transposed (ld_frag_tr: 8 consecutive rows per half wave) at a row stride of
+// 8 (mod 64) dwords has no bank conflicts in its transposed reads, but its row-fragment reads
+// put rows r and r + 8 on the same banks.  Storing the 4-element column groups of every row
+// with bit 3 set at column XOR 8 moves those rows onto the other half of the banks; the eight
+// rows of a transposed half wave share bit 3, so their reads stay conflict-free.
+__host__ __device__ constexpr int swz_col(int row, int col) { return col ^ (((row >> 3) & 1) << 3); }
+
+// ld_frag_2x8 on a swizzled table; row points at table row 16i + r.  The swizzle touches
+// bit 3 of the column only, so it applies to the lane's part 4g and the block offsets 32kb
+// and 16 stay immediate.
+__device__ __forceinline__ bf16x8 ld_frag_2x8_sw(const bf16* row, int kb, int g, int r)
+{
+    typedef const __attribute__((address_space(3))) bf16x4 lds4;
+    lds4* a = (lds4*)(row + ((4 * g) ^ ((r >> 3) << 3)) + 32 * kb);
+    return join(*a, *(const volatile __attribute__((address_space(3))) bf16x4*)(a + 4));
+}
+
+// ld_frag_tr on a swizzled table (rows 32kb + 4g + r/4 and 16 below: bit 3 is bit 1 of g;
+// x0 is a multiple of 16).
+__device__ __forceinline__ bf16x8 ld_frag_tr_sw(const bf16* M, int ld, int x0, int kb, int g, int r)
+{
+    const bf16* p = M + (size_t)(32 * kb + 4 * g + (r >> 2)) * ld + x0 + ((4 * (r & 3)) ^ ((g >> 1) << 3));
+    return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
+}
+
 // ld_frag_tr on a tile whose columns are fragment-ordered (4-column groups stay contiguous,
 // so each lane's 4 consecutive elements are still one 8-byte read).
 __device__ __forceinline__ bf16x8 ld_frag_tr_fo(const bf16* M, int ld, int x0, int kb, int g, int r)

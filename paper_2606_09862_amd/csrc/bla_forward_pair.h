@@ -126,8 +126,8 @@ __device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf
 
 // Copy a table of ROWS x COLS bf16 (source rows contiguous) into LDS rows of stride DST,
 // all loads of a thread in flight before its stores.  FO: store the rows fragment-ordered
-// (frag_col).
-template <int ROWS, int COLS, int DST, int NTHR, bool FO = false>
+// (frag_col); SW: store them row-swizzled (swz_col).
+template <int ROWS, int COLS, int DST, int NTHR, bool FO = false, bool SW = false>
 __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
 {
     typedef int intx2 __attribute__((ext_vector_type(2)));
@@ -142,8 +142,9 @@ __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
     for (int i = 0; i < ITER; ++i) {
         const int u = tid + i * NTHR;
         if (PIECES % NTHR == 0 || u < PIECES) {
-            const int col = 4 * (u % (COLS / 4));
-            *reinterpret_cast<intx2*>(dst + (size_t)(u / (COLS / 4)) * DST + (FO ? frag_col(col) : col)) = buf[i];
+            const int row = u / (COLS / 4), col = 4 * (u % (COLS / 4));
+            *reinterpret_cast<intx2*>(dst + (size_t)row * DST + (FO ? frag_col(col) : SW ? swz_col(row, col) : col)) =
+                buf[i];
         }
     }
 }
@@ -185,8 +186,8 @@ __device__ __forceinline__ void pair_write_zv(bf16* ZvT, const PState<D, MP, SP>
 }
 
 // Step (10) on the wave's owned mode tiles: Z' <- rho^c o (Z' + sum_i conj(rho^i) [k_i | v_i])
-// with K, V ([C][LK], rows past c zero) and the phase table ([C][LE]) read transposed
-// from LDS, and rho^c (cos | sin, float32) from Ec.
+// with K, V ([C][LK], rows past c zero) and the phase table ([C][LE], row-swizzled) read
+// transposed from LDS, and rho^c (cos | sin, float32) from Ec.
 template <int D, int MP, int LK, int LE>
 __device__ __forceinline__ void pair_advance(PStateDM<D, MP>& Zk, PStateDM<D, MP>& Zv, const bf16* Ks,
                                              const bf16* Vs, const bf16* sE, const float* Ec, int wl,
@@ -206,8 +207,8 @@ __device__ __forceinline__ void pair_advance(PStateDM<D, MP>& Zk, PStateDM<D, MP
         for (int o = 0; o < OWN; ++o) {
             const int mt = wl + 4 * o;
             if (mt < NMT) {
-                const F ecf = ld_frag_tr(sE, LE, 16 * mt, kb, g, r);
-                const F esf = ld_frag_tr(sE, LE, MP + 16 * mt, kb, g, r);
+                const F ecf = ld_frag_tr_sw(sE, LE, 16 * mt, kb, g, r);
+                const F esf = ld_frag_tr_sw(sE, LE, MP + 16 * mt, kb, g, r);
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) {
                     Zk[o][0][dt] = mma(ktf[dt], ecf, Zk[o][0][dt]);
@@ -554,8 +555,8 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
 
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     // ---- shared tables
-    pair_copy<SP, 2 * MP, P::LAB, 256 * P::U>(sAB, (const bf16*)a.ABs, tid);
-    pair_copy<C, 2 * MP, P::LE, 256 * P::U>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
+    pair_copy<SP, 2 * MP, P::LAB, 256 * P::U, false, true>(sAB, (const bf16*)a.ABs, tid);
+    pair_copy<C, 2 * MP, P::LE, 256 * P::U, false, true>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
     const int c_last = a.L - (a.nch - 1) * C;
     for (int i = tid; i < 2 * MP; i += 256 * P::U) {
         sRho[i] = E32h[2 * MP + i];
@@ -777,8 +778,8 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                     const F gf = frag_from_acc<bf16>(ga[2 * kb], ga[2 * kb + 1]);
 #pragma unroll
                     for (int mt = 0; mt < NMT; ++mt) {
-                        ua[mt] = mma(ld_frag_tr(sE, P::LE, 16 * mt, kb, g, r), gf, ua[mt]);
-                        ua[NMT + mt] = mma(ld_frag_tr(sE, P::LE, MP + 16 * mt, kb, g, r), gf, ua[NMT + mt]);
+                        ua[mt] = mma(ld_frag_tr_sw(sE, P::LE, 16 * mt, kb, g, r), gf, ua[mt]);
+                        ua[NMT + mt] = mma(ld_frag_tr_sw(sE, P::LE, MP + 16 * mt, kb, g, r), gf, ua[NMT + mt]);
                     }
                 }
             }
@@ -802,7 +803,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 sc[s4] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < P::KBM; ++kb)
-                    sc[s4] = mma(ld_frag_2x8(sAB + (size_t)(16 * s4 + r) * P::LAB, kb, g), uf[kb], sc[s4]);
+                    sc[s4] = mma(ld_frag_2x8_sw(sAB + (size_t)(16 * s4 + r) * P::LAB, kb, g, r), uf[kb], sc[s4]);
             }
             // (5) masked softmax in base-2 units (z * scale * log2 e).  Thresholds grow with
             // the slot and padded slots carry INT32_MAX, so a chunk whose first position
@@ -859,7 +860,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             for (int t = 0; t < 2 * NMT; ++t) {
                 wa[t] = zero4();
 #pragma unroll
-                for (int kb = 0; kb < P::KBS; ++kb) wa[t] = mma(ld_frag_tr(sAB, P::LAB, 16 * t, kb, g, r), pf[kb], wa[t]);
+                for (int kb = 0; kb < P::KBS; ++kb) wa[t] = mma(ld_frag_tr_sw(sAB, P::LAB, 16 * t, kb, g, r), pf[kb], wa[t]);
             }
             // (7) [Re W'' | -Im W''] with W'' = (a - i b) o E  (anchored: (a + i b) o conj(rho^P)):
             //     (a, b) <- (a c - b n, b c + a n)
@@ -889,7 +890,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 if (kt <= tt) {
 #pragma unroll
                     for (int kb = 0; kb < P::KBM; ++kb)
-                        hh[kt] = mma(ld_frag_2x8(sE + (size_t)(16 * kt + r) * P::LE, kb, g), wf[kb], hh[kt]);
+                        hh[kt] = mma(ld_frag_2x8_sw(sE + (size_t)(16 * kt + r) * P::LE, kb, g, r), wf[kb], hh[kt]);
                     if (kt == tt) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
