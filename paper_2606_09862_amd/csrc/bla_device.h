@@ -57,6 +57,17 @@ template <typename P> __device__ __forceinline__ const P* opaque(const P* p)
     return p;
 }
 
+// A lane value the optimiser cannot see through (no code is emitted).  Lane indices
+// re-derived this way at the top of each iteration of a chunk loop make the per-lane
+// addresses computed from them loop-variant, so they are recomputed inside the loop (a few
+// vector instructions) instead of being hoisted out and kept live across it, which spilled
+// them to scratch; every reload from scratch then waited for all outstanding memory loads.
+__device__ __forceinline__ int opaque_lane(int x)
+{
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
 // Stores and loads through a generic pointer that is known to address LDS (or global
 // memory): the explicit address space gives ds_write / global_load instructions instead of
 // flat ones (a flat access counts against both the LDS and the memory wait counters, so

@@ -380,7 +380,10 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void summary_kernel(FwdA
     if (a.cpb > 1)
         stage_load<T, D, MP, false, CC>(st1, nullptr, kbase + (first + GG::C) * ts, vbase + (first + GG::C) * ts, ts,
                                         GG::C, tid);
+    const int tid_ = tid, g_ = g, r_ = r;
     for (int n = 0; n < a.cpb; ++n) {
+        // lane indices re-derived per chunk (opaque_lane): addresses stay inside the loop
+        const int r = opaque_lane(r_), g = opaque_lane(g_), tid = opaque_lane(tid_);
         __syncthreads();
         stage_store<T, D, MP, false, CC>(st0, nullptr, Kt, Vt, GG::C, tid);
         st0 = st1;
@@ -428,6 +431,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
     T* lPh = ZvT + (size_t)D * GG::LDZ;  // anchored twiddle row conj(rho^P) of the chunk
 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
+    const int tid_ = tid, g_ = g, r_ = r;  // the chunk loop re-derives its own copies
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in a scalar register
     const int seg = blockIdx.x % a.nseg, bh = blockIdx.x / a.nseg, h = bh % a.H;
     const int ch0 = seg * a.cps;
@@ -568,6 +572,8 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
     const double rT = AN ? a.rperiod[h] : 0.0;
 
     for (int n = 0; n < nch; ++n) {
+        // lane indices re-derived per chunk (opaque_lane): addresses stay inside the loop
+        const int r = opaque_lane(r_), g = opaque_lane(g_), tid = opaque_lane(tid_);
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
         if constexpr (!P::TL) {
