@@ -304,6 +304,7 @@ void make_decay_plan(const bla_params* p, DecayPlan* dp)
 struct BwdPlan {
     Plan pl;
     int nseg, cps;
+    int nbk, cpb;  // summary blocks per sequence and chunks per block
     size_t off_fsum, off_asum, total;
 };
 
@@ -327,8 +328,8 @@ void make_bwd_plan(const bla_params* p, BwdPlan* bp)
     pl.upw = 1;
     const long long units = (long long)p->B * p->H;
     int nseg = 1;
+    const long long cus = device_cu_count();
     if (units > 0 && pl.nch > 1) {
-        const long long cus = device_cu_count();
         if (units < cus) {
             long long want = cus / units;
             if (want > pl.nch) want = pl.nch;
@@ -339,10 +340,25 @@ void make_bwd_plan(const bla_params* p, BwdPlan* bp)
     nseg = pl.nch > 0 ? (pl.nch + cps - 1) / cps : 1;
     bp->nseg = nseg;
     bp->cps = cps;
+    // Summary blocks (bf16 kernels): the adjoint summaries cover every segment but the first,
+    // (nseg - 1) units of work per sequence, so with few segments that pass would leave compute
+    // units idle.  Each segment is cut into bps blocks of cps / bps chunks (the forward and
+    // adjoint summaries are taken per block and combined block by block) until the pass has
+    // a workgroup per compute unit; the last, possibly shorter, segment must still reach its
+    // last block.  The float32 kernels take one block per segment.
+    int bps = 1;
+    if (p->io_dtype == BLA_BF16 && nseg > 1) {
+        const int last_len = pl.nch - (nseg - 1) * cps;  // chunks of the last segment
+        while (units * (nseg - 1) * bps < cus && cps % (2 * bps) == 0 &&
+               last_len > (2 * bps - 1) * (cps / (2 * bps)))
+            bps *= 2;
+    }
+    bp->nbk = nseg * bps;
+    bp->cpb = cps / bps;
     const size_t unit_bytes = (size_t)4 * pl.MP * pl.D * sizeof(float);
     bp->off_fsum = pl.off_summ;
-    bp->off_asum = align_up(bp->off_fsum + (size_t)units * nseg * unit_bytes);
-    bp->total = align_up(bp->off_asum + (size_t)units * nseg * unit_bytes);
+    bp->off_asum = align_up(bp->off_fsum + (size_t)units * bp->nbk * unit_bytes);
+    bp->total = align_up(bp->off_asum + (size_t)units * bp->nbk * unit_bytes);
 }
 
 }  // namespace
@@ -812,6 +828,8 @@ static bla_status backward_impl(const bla_params* p, const double* T, const void
     a.nch = pl.nch;
     a.nseg = bp.nseg;
     a.cps = bp.cps;
+    a.nbk = bp.nbk;
+    a.cpb = bp.cpb;
     a.t0 = p->t0;
     a.scale = pl.scale;
     void* ev3[3] = {events ? events[2] : nullptr, events ? events[3] : nullptr, events ? events[4] : nullptr};

@@ -941,6 +941,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kernel(BwdArgs a)
 template <typename T, int D, int MP, int SP>
 hipError_t launch_backward_shape(const BwdArgs& a, hipStream_t s, void* const* ev)
 {
+    if (a.nbk != a.nseg || a.cpb != a.cps) return hipErrorInvalidValue;  // one summary block per segment
     auto mark = [&](int i) -> hipError_t {
         return (ev && ev[i]) ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
     };

@@ -104,7 +104,7 @@ __device__ __forceinline__ const float* rho_row(const float* sRhoC, const float*
 }
 
 // ---------------------------------------------------------------------------------
-// Forward summaries (bf16): per (b, h, segment) the pre-rotated state after the segment's
+// Forward summaries (bf16): per (b, h, summary block) the pre-rotated state after the block's
 // tokens from zero, stored as [k|v][re|im][MP][D] (as bwd_fsum_kernel).
 template <int D, int MP>
 __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
@@ -118,8 +118,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
     bf16* sE = Vs + C * LDQ;
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int seg = blockIdx.x % a.nseg, bh = blockIdx.x / a.nseg, h = bh % a.H;
-    const int ch0 = seg * a.cps, nch = min(a.cps, a.nch - ch0);
+    const int blk = blockIdx.x % a.nbk, bh = blockIdx.x / a.nbk, h = bh % a.H;
+    const int ch0 = blk * a.cpb, nch = min(a.cpb, a.nch - ch0);
     const bf16* kb_ = (const bf16*)a.k + (size_t)bh * a.L * D;
     const bf16* vb = (const bf16*)a.v + (size_t)bh * a.L * D;
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
@@ -179,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
         rotate_dm<bf16, D, MP, false>(Zk, rc, w, r);
         rotate_dm<bf16, D, MP, false>(Zv, rc, w, r);
     }
-    float* S = a.fsum + ((size_t)bh * a.nseg + seg) * 4 * MP * D;
+    float* S = a.fsum + ((size_t)bh * a.nbk + blk) * 4 * MP * D;
 #pragma unroll
     for (int o = 0; o < OWN; ++o) {
         const int mt = w + NW * o;
@@ -226,9 +226,14 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nsu = SUM ? a.nseg - 1 : a.nseg;
-    const int seg = blockIdx.x % nsu + (SUM ? 1 : 0), bh = blockIdx.x / nsu, h = bh % a.H;
-    const int ch0 = seg * a.cps, nch = min(a.cps, a.nch - ch0);
+    // SUM: one summary block of a segment but the first; otherwise one segment.  last_blk:
+    // the last summary block the walk covers.
+    const int bps = a.nbk / a.nseg;
+    const int nsu = SUM ? a.nbk - bps : a.nseg;
+    const int seg = blockIdx.x % nsu + (SUM ? bps : 0), bh = blockIdx.x / nsu, h = bh % a.H;
+    const int cpu = SUM ? a.cpb : a.cps;  // chunks per walked unit (block or segment)
+    const int ch0 = seg * cpu, nch = min(cpu, a.nch - ch0);
+    const int last_blk = SUM ? seg : (seg + 1) * bps - 1;
     const bf16* qb = (const bf16*)a.q + (size_t)bh * a.L * D;
     const bf16* kb_ = (const bf16*)a.k + (size_t)bh * a.L * D;
     const bf16* vb = (const bf16*)a.v + (size_t)bh * a.L * D;
@@ -278,9 +283,9 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
             Zv[o][1][dt] = s1 * vr + c1 * vi;
         }
     }
-    for (int sg = 0; sg <= seg; ++sg) {
-        const long long len = (long long)min(a.cps * C, a.L - sg * a.cps * C);
-        const float* S = a.fsum + ((size_t)bh * a.nseg + sg) * 4 * MP * D;
+    for (int sg = 0; sg <= last_blk; ++sg) {
+        const long long len = (long long)min(a.cpb * C, a.L - sg * a.cpb * C);
+        const float* S = a.fsum + ((size_t)bh * a.nbk + sg) * 4 * MP * D;
 #pragma unroll
         for (int o = 0; o < OWN; ++o) {
             const int mt = w + NW * o;
@@ -346,9 +351,9 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
         }
     }
     if constexpr (!SUM) {
-        for (int sg = a.nseg - 1; sg > seg; --sg) {
-            const long long len = (long long)min(a.cps * C, a.L - sg * a.cps * C);
-            const float* S = a.asum + ((size_t)bh * a.nseg + sg) * 4 * MP * D;
+        for (int sg = a.nbk - 1; sg > last_blk; --sg) {
+            const long long len = (long long)min(a.cpb * C, a.L - sg * a.cpb * C);
+            const float* S = a.asum + ((size_t)bh * a.nbk + sg) * 4 * MP * D;
 #pragma unroll
             for (int od = 0; od < ODT; ++od) {
                 const int dt = w + NW * od;
@@ -774,7 +779,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
         const int dt = w + NW * od;
         if (dt >= NDT) continue;
         if constexpr (SUM) {
-            float* S = a.asum + ((size_t)bh * a.nseg + seg) * 4 * MP * D;
+            float* S = a.asum + ((size_t)bh * a.nbk + seg) * 4 * MP * D;
 #pragma unroll
             for (int p2 = 0; p2 < 2; ++p2)
 #pragma unroll
@@ -819,11 +824,12 @@ hipError_t launch_backward16_shape(const BwdArgs& a, hipStream_t s, void* const*
         return (ev && ev[i]) ? hipEventRecord((hipEvent_t)ev[i], s) : hipSuccess;
     };
     const unsigned units = (unsigned)(a.B * a.H);
-    hipLaunchKernelGGL((bwd16_fsum_kernel<D, MP>), dim3(units * a.nseg), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((bwd16_fsum_kernel<D, MP>), dim3(units * a.nbk), dim3(kThreads), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || (e = mark(0)) != hipSuccess) return e;
     if (a.nseg > 1) {
-        hipLaunchKernelGGL((bwd16_kernel<D, MP, SP, true>), dim3(units * (a.nseg - 1)), dim3(kThreads), 0, s, a);
+        const unsigned sum_blocks = (unsigned)(a.nbk - a.nbk / a.nseg);  // blocks of segments 1..nseg-1
+        hipLaunchKernelGGL((bwd16_kernel<D, MP, SP, true>), dim3(units * sum_blocks), dim3(kThreads), 0, s, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if ((e = mark(1)) != hipSuccess) return e;

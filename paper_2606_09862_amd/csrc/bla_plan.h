@@ -194,10 +194,11 @@ struct BwdArgs {
     const void* ABm;       // [2MP][SP]    (A | B) transposed
     const int* theta;      // [H][SP]
     const double* rperiod; // [H] 1 / T
-    float* fsum;           // [B*H][nseg][2][2][MP][D] forward summaries of the segments
-    float* asum;           // [B*H][nseg][2][2][MP][D] adjoint summaries (segment 0 unused)
+    float* fsum;           // [B*H][nbk][2][2][MP][D] forward summaries of the blocks
+    float* asum;           // [B*H][nbk][2][2][MP][D] adjoint summaries (blocks of segment 0 unused)
     int B, H, L, M;
     int nch, nseg, cps;    // chunks per sequence, segments, chunks per segment
+    int nbk, cpb;          // summary blocks per sequence (nseg times a power of two), chunks per block
     long long t0;
     float scale;
 };

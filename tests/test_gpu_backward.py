@@ -138,6 +138,20 @@ def test_backward_unsupported_shapes_are_rejected():
         bla.backward(q, q, q, q, [255.0], 128, 128)
 
 
+@pytest.mark.parametrize("d,M,S", [(64, 32, 64), (32, 16, 32)])
+def test_backward_summary_blocks(d, M, S):
+    """64 sequences of 8 chunks, the last one ragged: 4 segments of 2 chunks on the 256 compute
+    units of an MI355X, and the adjoint summaries split into 2 blocks per segment (8 blocks of one
+    chunk), so the forward states and the adjoint of every segment are Horner sums over blocks;
+    with input states, final-state gradients and a position offset.  The oracle checks four
+    sequences."""
+    B, H, L = 16, 4, 64 * 7 + 13
+    (q, k, v, g), (sk, sv, gk, gv) = tensors(91 + d, B, H, L, d, M, torch.bfloat16, with_states=True)
+    T = bi.periods(M, H)
+    run_bwd(q, k, v, g, T, M, S, torch.bfloat16, t0=5, sk=sk, sv=sv, gk=gk, gv=gv, label="summary blocks",
+            rows=[(0, 0), (5, 1), (10, 2), (15, 3)])
+
+
 def test_backward_workload3_sampled_rows():
     """The LM-layer workload at full size (B=8, H=16, L=4096, d=M=S=64, bf16) in the launch
     configuration the benchmark times; the oracle checks four whole sequences."""
