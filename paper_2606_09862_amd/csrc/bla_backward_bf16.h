@@ -225,6 +225,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
     float* sRhoC = reinterpret_cast<float*>(sTheta + SP);
 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
+    const int tid_ = tid, g_ = g, r_ = r;  // the chunk loop re-derives its own copies
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     // SUM: one summary block of a segment but the first; otherwise one segment.  last_blk:
     // the last summary block the walk covers.
@@ -389,6 +390,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
     __syncthreads();  // tables in LDS
 
     for (int n = nch - 1; n >= 0; --n) {
+        // lane indices re-derived per chunk (opaque_lane): addresses stay inside the loop
+        const int r = opaque_lane(r_), g = opaque_lane(g_), tid = opaque_lane(tid_);
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
         const float* rc = rho_row(sRhoC, E32h, c, MP);  // rho^c
