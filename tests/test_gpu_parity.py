@@ -166,6 +166,20 @@ def test_bf16_unit_layouts(B, H, L, d, M, S, T):
 
 
 @pytest.mark.parametrize("B,H,L,d,M,S,T", [
+    (8, 4, 64 * 8 + 5, 32, 16, 16, (31.0, 62.0, 31.0, 62.0)),     # d = 32: one 32-column summary slice
+    (4, 4, 64 * 6 + 17, 128, 32, 32, (63.0, 126.0, 63.0, 126.0)),  # d = 128: four slices, one unit per workgroup
+    (8, 4, 64 * 5 + 40, 64, 8, 15, (15.0, 30.0, 15.0, 30.0)),     # 16 modes: two-wave summary workgroups
+])
+def test_pair_summary_layouts(B, H, L, d, M, S, T):
+    """bf16 sequences numerous enough for the pair kernels (at least 16 units per workgroup slot)
+    yet split into several segments on 256 compute units, so that the summary kernel runs its
+    32-column slices (one per d/32), its mode-tile split and its XCD-grouped indexing at
+    d = 32, 128 and 16 modes (the LM-layer and recall workloads cover d = 64)."""
+    q, k, v = gauss(L + 3 * d + M, B, H, L, d, torch.bfloat16)
+    run_case(q, k, v, T[:H], M, S, torch.bfloat16, label=f"pair summaries {B}x{H}x{L}x{d} M={M}")
+
+
+@pytest.mark.parametrize("B,H,L,d,M,S,T", [
     (1, 2, 64 * 11 + 9, 128, 128, 128, (255.0, 510.0)),  # d = M = 128: eight waves, one mode tile each
     (2, 1, 300, 128, 100, 256, (199.0,)),                 # modes padded 100 -> 128, slots 256
 ])
