@@ -50,11 +50,16 @@ __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f};
 
 // A uniform pointer the optimiser cannot see through (no code is emitted).  Re-deriving a
 // table pointer this way once per loop iteration keeps the table's fragments from being
-// hoisted out of the loop into registers (which spills when the tables are large).
+// hoisted out of the loop into registers (which spills when the tables are large).  The
+// pointer itself is not passed through the asm statement, only a zero offset added to it:
+// the compiler still sees that it addresses global memory (a kernel argument) and emits
+// global loads, not flat ones (a flat load counts against the LDS wait counter as well, so
+// every wait for an LDS read would also wait for the table loads in flight).
 template <typename P> __device__ __forceinline__ const P* opaque(const P* p)
 {
-    asm volatile("" : "+s"(p));
-    return p;
+    int zero = 0;
+    asm volatile("" : "+s"(zero));
+    return p + zero;
 }
 
 // A lane value the optimiser cannot see through (no code is emitted).  Lane indices
