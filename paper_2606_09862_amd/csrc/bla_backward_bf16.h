@@ -44,7 +44,7 @@ template <int D, int MP, int SP> struct Bwd16 {
     static constexpr size_t E_ELEMS = (size_t)C * LE;
     static constexpr size_t S_ELEMS = (size_t)SP * LE;
     static constexpr size_t LDS_BYTES =
-        (A_ELEMS + G_ELEMS + B_ELEMS + Z_ELEMS + E_ELEMS + S_ELEMS) * 2 + (size_t)SP * 4 + (size_t)2 * MP * 4;
+        (A_ELEMS + G_ELEMS + B_ELEMS + Z_ELEMS + E_ELEMS + S_ELEMS) * 2 + (size_t)SP * 4 + (size_t)2 * 2 * MP * 4;
     static_assert(LDS_BYTES <= kBwdMaxLds, "backward tiles fit in LDS");
     static_assert((size_t)2 * C * LDH <= G_ELEMS, "H tiles fit in the Gram region");
 };
@@ -98,9 +98,22 @@ __device__ __forceinline__ void copy_conj_phase(bf16* dst, int ld, const bf16* s
 
 // cos | sin of m w c (float32, 2MP) for the chunk's length: the LDS row of rho^C, or the
 // workspace's phase table for a ragged chunk.
-__device__ __forceinline__ const float* rho_row(const float* sRhoC, const float* E32h, int c, int MP)
+__device__ __forceinline__ const float* rho_row(const float* sRho, int c, int MP)
 {
-    return c == kChunk ? sRhoC : E32h + (size_t)c * 2 * MP;
+    return c == kChunk ? sRho : sRho + 2 * MP;
+}
+
+// sRho[0 .. 2MP): rho^C; sRho[2MP .. 4MP): rho^c of the sequence's last chunk (c = L - (nch-1) C,
+// the only chunk that can be shorter).  Both rows live in LDS, so the selected row is read
+// with LDS loads (a row chosen between LDS and global memory would be read with flat loads,
+// which hold every LDS wait until they return).
+__device__ __forceinline__ void load_rho_rows(float* sRho, const float* E32h, const BwdArgs& a, int MP, int tid)
+{
+    const int c_last = a.L - (a.nch - 1) * kChunk;
+    for (int i = tid; i < 2 * MP; i += kThreads) {
+        sRho[i] = E32h[(size_t)kChunk * 2 * MP + i];
+        sRho[2 * MP + i] = E32h[(size_t)c_last * 2 * MP + i];
+    }
 }
 
 // ---------------------------------------------------------------------------------
@@ -112,7 +125,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
     using G = Bwd16<D, MP, 32>;
     constexpr int C = kChunk, NMT = G::NMT, NDT = G::NDT, OWN = G::OWN, NW = G::NW, LDQ = G::LDQ, LE = G::LE;
     __shared__ __attribute__((aligned(16))) bf16 lds[2 * C * LDQ + C * LE];
-    __shared__ __attribute__((aligned(16))) float sRhoC[2 * MP];
+    __shared__ __attribute__((aligned(16))) float sRhoC[2 * 2 * MP];
     bf16* Ks = lds;
     bf16* Vs = Ks + C * LDQ;
     bf16* sE = Vs + C * LDQ;
@@ -124,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
     const bf16* vb = (const bf16*)a.v + (size_t)bh * a.L * D;
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     copy_conj_phase<MP>(sE, LE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
-    for (int i = tid; i < 2 * MP; i += kThreads) sRhoC[i] = E32h[(size_t)C * 2 * MP + i];
+    load_rho_rows(sRhoC, E32h, a, MP, tid);
 
     StateTiles<bf16, D, MP> Zk, Zv;
 #pragma unroll
@@ -175,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
                 }
             }
         }
-        const float* rc = rho_row(sRhoC, E32h, c, MP);
+        const float* rc = rho_row(sRhoC, c, MP);
         rotate_dm<bf16, D, MP, false>(Zk, rc, w, r);
         rotate_dm<bf16, D, MP, false>(Zv, rc, w, r);
     }
@@ -255,7 +268,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
     copy_conj_phase<MP>(sE, LE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
     copy_table<bf16, SP, 2 * MP, LE>(sAB, (const bf16*)a.ABs, tid);
     for (int i = tid; i < SP; i += kThreads) sTheta[i] = a.theta[(size_t)h * SP + i];
-    for (int i = tid; i < 2 * MP; i += kThreads) sRhoC[i] = E32h[(size_t)C * 2 * MP + i];
+    load_rho_rows(sRhoC, E32h, a, MP, tid);
 
     // ---- forward state after the segment (pre-rotated, [d][m] tiles, mode tiles split)
     StateTiles<bf16, D, MP> Zk, Zv;
@@ -394,7 +407,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
         const int r = opaque_lane(r_), g = opaque_lane(g_), tid = opaque_lane(tid_);
         const int tok0 = (ch0 + n) * C;
         const int c = min(C, a.L - tok0);
-        const float* rc = rho_row(sRhoC, E32h, c, MP);  // rho^c
+        const float* rc = rho_row(sRhoC, c, MP);  // rho^c
         __syncthreads();  // previous chunk done with the token tiles and the weights
         {
             bf16* rows[4] = {Ks, Vs, Qs, dOs};

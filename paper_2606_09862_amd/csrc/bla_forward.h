@@ -118,7 +118,7 @@ template <typename T, int D, int MP, int SP, int CC = kChunk> struct Fwd : Geo<T
     static constexpr size_t TAB_ELEMS = (size_t)SP * LDAS + (size_t)2 * MP * LDAM + (size_t)G::C * LDE +
                                         (size_t)2 * 2 * MP * LDR;
     // float32 rows rho and rho^C, then the int32 mask thresholds
-    static constexpr size_t SMALL_BYTES = (size_t)2 * 2 * MP * 4 + (size_t)SP * 4;
+    static constexpr size_t SMALL_BYTES = (size_t)3 * 2 * MP * 4 + (size_t)SP * 4;
     static constexpr size_t BASE_BYTES = BASE_ELEMS * sizeof(T);
     static constexpr size_t FULL_BYTES = BASE_BYTES + TAB_ELEMS * sizeof(T) + SMALL_BYTES;
     static constexpr bool TL = FULL_BYTES <= kMaxLds;  // tables live in LDS
@@ -283,17 +283,20 @@ __device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP, CC>
 }
 
 // Step 10: Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i] on the wave's own mode tiles.
-// rhoC: the row rho^C (full chunks); E32 (row stride 2MP): phase table for a ragged c;
+// rhoC: the row rho^C (full chunks); rhoL: the row rho^c of the sequence's last chunk;
+// E32 (row stride 2MP): phase table for the ragged chunk's rho^{c-i} fragments;
 // Erev / ldR: the [2MP][C] table of rho^{C-i} (full chunks).
 template <typename T, int D, int MP, int CC = kChunk>
 __device__ __forceinline__ void advance_state(StateTiles<T, D, MP, CC>& Zk, StateTiles<T, D, MP, CC>& Zv,
                                               const T* Kt, const T* Vt, const float* rhoC,
-                                              const float* E32, const T* Erev, int ldR, int c, int w,
-                                              int g, int r)
+                                              const float* rhoL, const float* E32, const T* Erev, int ldR,
+                                              int c, int w, int g, int r)
 {
     using GG = Geo<T, D, MP, CC>;
     using F = typename Frag<T>::type;
-    const float* Ec = (c == GG::C) ? rhoC : E32 + (size_t)c * 2 * MP;
+    // rho^c: a chunk shorter than C is the sequence's last one, whose row is rhoL (held where
+    // rhoC is, so that the selected row is read with loads of one address space)
+    const float* Ec = (c == GG::C) ? rhoC : rhoL;
 #pragma unroll
     for (int o = 0; o < GG::OWN; ++o) {
         const int mt = w + GG::NW * o;
@@ -392,7 +395,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void summary_kernel(FwdA
             stage_load<T, D, MP, false, CC>(st1, nullptr, kbase + tok * ts, vbase + tok * ts, ts, GG::C, tid);
         }
         __syncthreads();
-        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, E32h, ErevTh, GG::C, GG::C, w, g, r);
+        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, rhoC, E32h, ErevTh, GG::C, GG::C, w, g, r);
     }
     float* S = a.summ + ((size_t)bh * a.nbs + blk) * 4 * MP * D;
 #pragma unroll
@@ -452,6 +455,8 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
     const T* tErev;      // [2MP][C] rho^{C-i} rows
     const float* rho1;   // rho   (float32, 2MP)
     const float* rhoC;   // rho^C (float32, 2MP)
+    const float* rhoL;   // rho^c of the sequence's last chunk (float32, 2MP)
+    const int c_last = a.L - (a.nch - 1) * C;  // length of the last chunk (the only short one)
     const int* tTheta;   // start-mask thresholds [SP]
     constexpr int sABs = P::TL ? P::LDAS : 2 * MP;
     constexpr int sABm = P::TL ? P::LDAM : SP;
@@ -467,7 +472,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         T* lEbar = lEtab + (size_t)C * P::LDE;
         T* lErev = lEbar + (size_t)2 * MP * P::LDR;
         float* lRho = reinterpret_cast<float*>(lErev + (size_t)2 * MP * P::LDR);
-        int* lTheta = reinterpret_cast<int*>(lRho + 4 * MP);
+        int* lTheta = reinterpret_cast<int*>(lRho + 6 * MP);
         copy_table<T, SP, 2 * MP, P::LDAS, GG::NTHR>(lABs, (const T*)a.ABs, tid);
         copy_table<T, 2 * MP, SP, P::LDAM, GG::NTHR>(lABm, (const T*)a.ABm, tid);
         copy_table<T, C, 2 * MP, P::LDE, GG::NTHR>(lEtab, gEtab, tid);
@@ -475,6 +480,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         copy_table<T, 2 * MP, C, P::LDR, GG::NTHR>(lErev, gErev, tid);
         copy_table<float, 1, 2 * MP, 2 * MP, GG::NTHR>(lRho, E32h + 2 * MP, tid);                    // rho
         copy_table<float, 1, 2 * MP, 2 * MP, GG::NTHR>(lRho + 2 * MP, E32h + (size_t)C * 2 * MP, tid);  // rho^C
+        copy_table<float, 1, 2 * MP, 2 * MP, GG::NTHR>(lRho + 4 * MP, E32h + (size_t)c_last * 2 * MP, tid);  // rho^c_last
         copy_table<int, 1, SP, SP, GG::NTHR>(lTheta, thh, tid);
         tABs = lABs;
         tABm = lABm;
@@ -483,6 +489,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         tErev = lErev;
         rho1 = lRho;
         rhoC = lRho + 2 * MP;
+        rhoL = lRho + 4 * MP;
         tTheta = lTheta;
     } else {
         tABs = (const T*)a.ABs;
@@ -492,6 +499,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         tErev = gErev;
         rho1 = E32h + 2 * MP;
         rhoC = E32h + (size_t)C * 2 * MP;
+        rhoL = E32h + (size_t)c_last * 2 * MP;
         tTheta = thh;
     }
 
@@ -822,7 +830,7 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         }
         __syncthreads();  // everyone done reading ZvT
 
-        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, E32h, tErev, sR, c, w, g, r);
+        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, rhoL, E32h, tErev, sR, c, w, g, r);
         write_zvt<T, D, MP, CC>(ZvT, Zv, w, g, r);
     }
 
