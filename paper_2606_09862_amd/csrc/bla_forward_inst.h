@@ -129,6 +129,14 @@ template <typename T, int D, int MP, int SP> constexpr int pair_units()
                 return hipGetLastError();                                                               \
             }                                                                                           \
         }                                                                                               \
+        if constexpr (sizeof(T) == 2) {                                                                 \
+            if (p.C == kChunk) { /* bf16, 64-token chunks: the sliced summary kernel */                 \
+                hipLaunchKernelGGL((summary_pair_kernel<D, MP, true>),                                  \
+                                   dim3((unsigned)summary_grid_x<D, MP>((long long)p.B * p.nbs), (unsigned)p.H),  \
+                                   dim3(summary_threads<D, MP>()), 0, s, a);                            \
+                return hipGetLastError();                                                               \
+            }                                                                                           \
+        }                                                                                               \
         switch (p.C) {                                                                                  \
         case 16: return launch_one_summary<T, D, MP, 16>(p, a, s);                                      \
         case 32: return launch_one_summary<T, D, MP, 32>(p, a, s);                                      \

@@ -126,8 +126,9 @@ __device__ __forceinline__ void pair_stage_store(const PStage<D, MP, SP>& st, bf
 
 // Copy a table of ROWS x COLS bf16 (source rows contiguous) into LDS rows of stride DST,
 // all loads of a thread in flight before its stores.  FO: store the rows fragment-ordered
-// (frag_col); SW: store them row-swizzled (swz_col).
-template <int ROWS, int COLS, int DST, int NTHR, bool FO = false, bool SW = false>
+// (frag_col); SW: store them row-swizzled (swz_col); NEG_HI: negate the upper half of every
+// row (columns COLS/2 ..), e.g. [cos | sin] -> [cos | -sin].
+template <int ROWS, int COLS, int DST, int NTHR, bool FO = false, bool SW = false, bool NEG_HI = false>
 __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
 {
     typedef int intx2 __attribute__((ext_vector_type(2)));
@@ -143,8 +144,9 @@ __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
         const int u = tid + i * NTHR;
         if (PIECES % NTHR == 0 || u < PIECES) {
             const int row = u / (COLS / 4), col = 4 * (u % (COLS / 4));
-            *reinterpret_cast<intx2*>(dst + (size_t)row * DST + (FO ? frag_col(col) : SW ? swz_col(row, col) : col)) =
-                buf[i];
+            intx2 x = buf[i];
+            if (NEG_HI && col >= COLS / 2) x ^= (int)0x80008000;  // the sign bits of four bf16
+            *reinterpret_cast<intx2*>(dst + (size_t)row * DST + (FO ? frag_col(col) : SW ? swz_col(row, col) : col)) = x;
         }
     }
 }
@@ -349,8 +351,10 @@ template <int D, int MP> constexpr long long summary_grid_x(long long jobs)
 
 // grid: summary_grid_x(B * nbs) x H workgroups of NTHR threads; every (b, summarised block)
 // pair has DS workgroups, one per 32-column slice of K and V; the block covers chunks
-// [blk * cpb, (blk + 1) * cpb).
-template <int D, int MP>
+// [blk * cpb, (blk + 1) * cpb).  PLAIN_E: the phase table holds [cos | sin] (the one-unit
+// kernels' tables) instead of conj(rho^i) = [cos | -sin]; its sine half is negated on the
+// copy into LDS.  The summaries are the same either way.
+template <int D, int MP, bool PLAIN_E = false>
 __global__ __launch_bounds__((SumPair<D, MP>::NTHR))
 __attribute__((amdgpu_waves_per_eu(SumPair<D, MP>::MINB * SumPair<D, MP>::NW / 4))) void summary_pair_kernel(FwdArgs a)
 {
@@ -380,7 +384,7 @@ __attribute__((amdgpu_waves_per_eu(SumPair<D, MP>::MINB * SumPair<D, MP>::NW / 4
     const bf16* vb = (const bf16*)a.v + fwd_in_base(a, bh) + first * ts + ds * P::DW;
 
     // tables first: their loads are then the oldest in flight when they are stored
-    pair_copy<C, 2 * MP, P::LE, P::NTHR>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
+    pair_copy<C, 2 * MP, P::LE, P::NTHR, false, false, PLAIN_E>(sE, (const bf16*)a.Etab + (size_t)h * C * 2 * MP, tid);
     const float* E32h = a.E32 + (size_t)h * (C + 1) * 2 * MP;
     for (int i = tid; i < 2 * MP; i += P::NTHR) sRhoC[i] = E32h[(size_t)C * 2 * MP + i];
 
