@@ -150,6 +150,15 @@ __device__ __forceinline__ bf16x8 ld_frag16(const bf16* row, int kb, int g)
     return *reinterpret_cast<const bf16x8*>(row + 32 * kb + 8 * g);
 }
 
+// ld_frag16's fragment (reduction order 32kb + 8g + e) from an LDS row that is only 8-byte
+// aligned: two 8-byte reads (the second volatile, as in ld_frag_2x8).
+__device__ __forceinline__ bf16x8 ld_frag16_2x8(const bf16* row, int kb, int g)
+{
+    typedef const __attribute__((address_space(3))) bf16x4 lds4;
+    lds4* a = (lds4*)(row + 32 * kb + 8 * g);
+    return join(*a, *(const volatile __attribute__((address_space(3))) bf16x4*)(a + 1));
+}
+
 // Fragment of a natural row for the accumulator order (32kb + 4g .. + 3, 32kb + 16 + 4g ..
 // + 3) as two separate 8-byte LDS reads.  The second read is volatile so that the two are not
 // merged into one ds_read2_b64, which gfx950 serves at a quarter to half of the rate of two

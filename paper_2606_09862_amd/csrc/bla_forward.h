@@ -122,9 +122,31 @@ template <typename T, int D, int MP, int SP, int CC = kChunk> struct Fwd : Geo<T
     static constexpr size_t BASE_BYTES = BASE_ELEMS * sizeof(T);
     static constexpr size_t FULL_BYTES = BASE_BYTES + TAB_ELEMS * sizeof(T) + SMALL_BYTES;
     static constexpr bool TL = FULL_BYTES <= kMaxLds;  // tables live in LDS
-    static constexpr size_t LDS_BYTES = TL ? FULL_BYTES : BASE_BYTES;
+    // Split chain (bf16, eight waves for four token tiles, tables outside LDS): the two waves
+    // of a token tile share steps (4)-(9) -- one half of the slots each for the scores, one
+    // half of the modes for the readout weights, one half of the head dims for the output.
+    // The unnormalised slot weights P~ ([C][LDP]) and the per-token (max, sum) of each slot
+    // half ([C][2][2] float32) pass through LDS after the per-chunk buffers.
+    static constexpr int LDP = SP + G::PAD;
+    static constexpr size_t SPLIT_BYTES = (size_t)G::C * LDP * sizeof(T) + (size_t)G::C * 4 * 4;
+    static constexpr bool SPLIT = sizeof(T) == 2 && G::NW == 2 * G::NT && SP % 64 == 0 && !TL &&
+                                  BASE_BYTES + SPLIT_BYTES <= kMaxLds;
+    static constexpr size_t LDS_BYTES = TL ? FULL_BYTES : BASE_BYTES + (SPLIT ? SPLIT_BYTES : 0);
     static_assert(SP % 32 == 0, "slot padding");
 };
+
+// Token tile of wave w in the split chain: waves w and w + 4 share a SIMD, and the tiles
+// {0, 3} and {1, 2} put one short and one long causal tile on every SIMD.
+__device__ __forceinline__ int split_tile(int w) { return (0x12032130 >> (4 * w)) & 15; }
+
+// An operand fragment times a per-lane factor (bf16 in, bf16 out, float32 product).
+__device__ __forceinline__ bf16x8 scale_frag(bf16x8 x, float f)
+{
+    bf16x8 y;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = (bf16)((float)x[e] * f);
+    return y;
+}
 
 // The wave's fp32 state tiles: [owned mode tile][Re, Im][head-dim tile].
 template <typename T, int D, int MP, int CC = kChunk> using StateTiles = floatx4[Geo<T, D, MP, CC>::OWN][2][D / 16];
@@ -432,6 +454,9 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
     T* GT = Qs + (size_t)C * P::LDQU;
     T* ZvT = GT + (size_t)C * P::LDG;
     T* lPh = ZvT + (size_t)D * GG::LDZ;  // anchored twiddle row conj(rho^P) of the chunk
+    // split chain: P~ rows and the per-token softmax statistics of the two slot halves
+    T* Pw = reinterpret_cast<T*>(lds_raw + P::BASE_BYTES);
+    float* sStat = reinterpret_cast<float*>(lds_raw + P::BASE_BYTES + (size_t)C * P::LDP * sizeof(T));
 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
     const int tid_ = tid, g_ = g, r_ = r;  // the chunk loop re-derives its own copies
@@ -705,8 +730,178 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         }
         __syncthreads();
 
+        // ---- per-token chain, split over the two waves of each token tile
+        if constexpr (P::SPLIT) {
+            const int tt = split_tile(w), hv = w / NT;  // token tile, half
+            const int j = 16 * tt + r;
+            const long long pos = a.t0 + tok0 + j;
+            constexpr int NSH = P::NST / 2, KSH = P::KBS / 2, MH = NMT / 2, DH = NDT / 2;
+            {
+                // (4)-(5) scores of slots [SP/2 hv, SP/2 (hv + 1)), masked, exponentiated
+                // against the half's own maximum.  The slot-matrix fragments come from global
+                // memory (L2): reduction block kb + 2 is requested before the products of block
+                // kb are issued (the scheduling barriers keep that order), so about two blocks
+                // are in flight instead of one fragment.  Reduction order 32kb + 8g + e on both
+                // operands (a 16-byte read of the table row).
+                F tb[2][NSH], ub[2];
+                auto ld_blk = [&](F (&t)[NSH], F& u, int kb) {
+#pragma unroll
+                    for (int s4 = 0; s4 < NSH; ++s4)
+                        t[s4] = ld_global<F>(tABs + (size_t)(16 * (NSH * hv + s4) + r) * sABs + 32 * kb + 8 * g);
+                    u = ld_frag16_2x8(UT + (size_t)j * P::LDQU, kb, g);  // rows 8-byte aligned
+                };
+                floatx4 sc[NSH];
+#pragma unroll
+                for (int s4 = 0; s4 < NSH; ++s4) sc[s4] = zero4();
+                ld_blk(tb[0], ub[0], 0);
+                ld_blk(tb[1], ub[1], 1);
+#pragma unroll
+                for (int kb = 0; kb < GG::KBM; ++kb) {
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int s4 = 0; s4 < NSH; ++s4) sc[s4] = mma(tb[kb & 1][s4], ub[kb & 1], sc[s4]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (kb + 2 < GG::KBM) ld_blk(tb[kb & 1], ub[kb & 1], kb + 2);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                float mx = -INFINITY;
+#pragma unroll
+                for (int s4 = 0; s4 < NSH; ++s4) {
+                    const intx4 th = *reinterpret_cast<const intx4*>(tTheta + 16 * (NSH * hv + s4) + 4 * g);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if (pos < (long long)th[e]) sc[s4][e] = -INFINITY;
+                        mx = fmaxf(mx, sc[s4][e]);
+                    }
+                }
+                mx = rows_max(mx);
+                // the upper half can be fully masked (its weights are then zero); the lower
+                // half holds slot 0, whose threshold is 0
+                const float mref = mx == -INFINITY ? 0.f : mx;
+                float sum = 0.f;
+#pragma unroll
+                for (int s4 = 0; s4 < NSH; ++s4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float ex = __expf(sc[s4][e] - mref);
+                        sc[s4][e] = ex;
+                        sum += ex;
+                    }
+                sum = rows_sum(sum);
+#pragma unroll
+                for (int s4 = 0; s4 < NSH; ++s4) st4<T>(Pw + (size_t)j * P::LDP + 16 * (NSH * hv + s4) + 4 * g, sc[s4]);
+                if (g == 0) {
+                    sStat[(j * 2 + hv) * 2 + 0] = mx;
+                    sStat[(j * 2 + hv) * 2 + 1] = sum;
+                }
+            }
+            __syncthreads();  // P~ and the statistics visible; U no longer read
+
+            {
+                // (6)-(7) readout weights of mode tiles [MH hv, MH (hv + 1)), published to
+                // LDS over U: [Re W'' | Im-part] rows in the order the output contraction reads
+                const float m0 = sStat[j * 4 + 0], s0 = sStat[j * 4 + 1];
+                const float m1 = sStat[j * 4 + 2], s1 = sStat[j * 4 + 3];
+                const float M = fmaxf(m0, m1);
+                const float e0 = __expf(m0 - M), e1 = __expf(m1 - M);
+                const float inv = __builtin_amdgcn_rcpf(e0 * s0 + e1 * s1);
+                const float f0 = e0 * inv, f1 = e1 * inv;
+                F pf[P::KBS];
+#pragma unroll
+                for (int kb = 0; kb < P::KBS; ++kb)
+                    pf[kb] = scale_frag(ld_frag16_2x8(Pw + (size_t)j * P::LDP, kb, g), kb < KSH ? f0 : f1);
+                // column tiles in the order (q, Re/Im p, u); tile i's KBS fragments of the
+                // transposed slot matrix are requested two tiles ahead of its products
+                constexpr int NG = 2 * MH;  // column tiles of the half
+                auto col_tile = [&](int i) { return ((i >> 1) & 1) * NMT + MH * hv + 2 * (i >> 2) + (i & 1); };
+                F ab[2][P::KBS];
+                auto ld_tile = [&](F (&t)[P::KBS], int i) {
+                    const T* row = tABm + (size_t)(16 * col_tile(i) + r) * sABm;
+#pragma unroll
+                    for (int ks = 0; ks < P::KBS; ++ks) t[ks] = ld_global<F>(row + 32 * ks + 8 * g);
+                };
+                ld_tile(ab[0], 0);
+                ld_tile(ab[1], 1);
+                floatx4 wa[2][2];  // [Re, Im][mode tile MH hv + 2q + u] of the current q
+#pragma unroll
+                for (int i = 0; i < NG; ++i) {
+                    const int pp = (i >> 1) & 1, u = i & 1;
+                    __builtin_amdgcn_sched_barrier(0);
+                    wa[pp][u] = zero4();
+#pragma unroll
+                    for (int ks = 0; ks < P::KBS; ++ks) wa[pp][u] = mma(ab[i & 1][ks], pf[ks], wa[pp][u]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (i + 2 < NG) ld_tile(ab[i & 1], i + 2);
+                    if ((i & 3) == 3) {
+                        // (7) twiddle the two mode tiles of this q and publish them
+#pragma unroll
+                        for (int v2 = 0; v2 < 2; ++v2) {
+                            const int mt = MH * hv + 2 * (i >> 2) + v2;
+                            floatx4 cs, sn;
+                            if constexpr (AN) {
+                                cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
+                                sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
+                            } else {
+                                cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
+                                sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                            }
+                            const floatx4 am = wa[0][v2], bm = wa[1][v2];
+                            st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, am * cs + bm * sn);
+                            st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * mt + 4 * g, am * sn - bm * cs);
+                        }
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __syncthreads();  // W'' rows visible
+
+            {
+                // (8)-(9) output head dims [16 DH hv, 16 DH (hv + 1)) of the tile's tokens
+                F wf[GG::KBM];
+#pragma unroll
+                for (int kb = 0; kb < GG::KBM; ++kb) wf[kb] = ld_frag<T>(UT + (size_t)j * P::LDQU, 32 * kb, g);
+                floatx4 oa[DH];
+#pragma unroll
+                for (int d2 = 0; d2 < DH; ++d2) {
+                    const int dt = DH * hv + d2;
+                    oa[d2] = zero4();
+#pragma unroll
+                    for (int kb = 0; kb < GG::KBM; ++kb)
+                        oa[d2] = mma(ld_frag<T>(ZvT + (size_t)(16 * dt + r) * GG::LDZ, 32 * kb, g), wf[kb], oa[d2]);
+                }
+                floatx4 hh[NT];
+#pragma unroll
+                for (int kt = 0; kt < NT; ++kt) {
+                    hh[kt] = zero4();
+                    if (kt <= tt) {
+#pragma unroll
+                        for (int kb = 0; kb < GG::KBM; ++kb)
+                            hh[kt] = mma(ld_frag<T>(tEtab + (size_t)(16 * kt + r) * sEtab, 32 * kb, g), wf[kb], hh[kt]);
+                        if (kt == tt) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (4 * g + e > r) hh[kt][e] = 0.f;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int kb = 0; kb < GG::KBC; ++kb) {
+                    if (2 * kb <= tt) {
+                        const F hf = frag_from_acc<T>(hh[2 * kb], hh[2 * kb + 1]);
+#pragma unroll
+                        for (int d2 = 0; d2 < DH; ++d2)
+                            oa[d2] = mma(ld_frag_c<T, CC>(Vt + (size_t)(16 * (DH * hv + d2) + r) * GG::LDK, kb, g), hf,
+                                         oa[d2]);
+                    }
+                }
+                if (j < c) {
+#pragma unroll
+                    for (int d2 = 0; d2 < DH; ++d2)
+                        st4<T>(ob + (size_t)(tok0 + j) * tso + 16 * (DH * hv + d2) + 4 * g, oa[d2]);
+                }
+            }
+        } else if (w < NT) {
         // ---- per-token chain on token tile w: scores, softmax, readout, output
-        if (w < NT) {
             const int j = 16 * w + r;
             const long long pos = a.t0 + tok0 + j;
             F uf[GG::KBM];

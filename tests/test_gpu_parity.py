@@ -182,10 +182,14 @@ def test_pair_summary_layouts(B, H, L, d, M, S, T):
 @pytest.mark.parametrize("B,H,L,d,M,S,T", [
     (1, 2, 64 * 11 + 9, 128, 128, 128, (255.0, 510.0)),  # d = M = 128: eight waves, one mode tile each
     (2, 1, 300, 128, 100, 256, (199.0,)),                 # modes padded 100 -> 128, slots 256
+    (1, 2, 64 * 6 + 23, 128, 128, 64, (127.0, 300.0)),     # 64 slots: 32 per wave of a token tile
 ])
 def test_wide_state_eight_waves(B, H, L, d, M, S, T):
-    """bf16, d = M = 128 runs eight waves per workgroup (the token chain on the first four);
-    float32 I/O at this size does not fit the LDS tiles and is rejected."""
+    """bf16, d = M = 128 runs eight waves per workgroup.  With 64 or 128 slots the two waves
+    of a token tile split the chain (slot halves, whose softmax statistics are combined; mode
+    halves; head-dim halves), the upper slot half fully masked at the first positions; with 256
+    slots the chain runs on the first four waves.  float32 I/O at this size does not fit the
+    LDS tiles and is rejected."""
     q, k, v = gauss(L + 5 * M + S, B, H, L, d, torch.bfloat16)
     run_case(q, k, v, T[:H], M, S, torch.bfloat16, label=f"eight waves {B}x{H}x{L}x{d} M={M} S={S}")
     bla = _bla()
