@@ -692,9 +692,59 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                 }
             }
         }
+        // Split chain (one owned mode tile): the conj(E) fragments and phase twiddles of phase
+        // B are the same for every token tile; they are requested here, before the barrier, so
+        // that their latency overlaps it (16-byte loads in the reduction order 32kb + 8g + e,
+        // matched by the Gram-tile reads below).
+        F ebh[P::SPLIT ? 2 : 1][P::SPLIT ? GG::KBC : 1];
+        typename Frag<T>::half twh[P::SPLIT && !AN ? NT : 1][2];
+        if constexpr (P::SPLIT) {
+            static_assert(OWN == 1 && !GG::HALF, "one owned mode tile, 32-token reduction blocks");
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+#pragma unroll
+                for (int kb = 0; kb < GG::KBC; ++kb)
+                    ebh[p][kb] = ld_global<F>(tEbar + (size_t)(16 * (p * NMT + w) + r) * sR + 32 * kb + 8 * g);
+            if constexpr (!AN) {
+#pragma unroll
+                for (int ct = 0; ct < NT; ++ct) {
+                    twh[ct][0] = ld4<T>(tEtab + (size_t)(16 * ct + r) * sEtab + 16 * w + 4 * g);
+                    twh[ct][1] = ld4<T>(tEtab + (size_t)(16 * ct + r) * sEtab + MP + 16 * w + 4 * g);
+                }
+            }
+        }
         __syncthreads();
 
         // ---- phase B: + G conj(E), twiddle by E, publish U to LDS
+        if constexpr (P::SPLIT) {
+            const int mt = w;
+#pragma unroll
+            for (int ct = 0; ct < NT; ++ct) {
+#pragma unroll
+                for (int kb = 0; kb < GG::KBC; ++kb) {
+                    if (2 * kb <= ct) {
+                        // keys 32kb + 8g + e; the half past the diagonal tile (g >= 2 when
+                        // 2kb + 1 > ct) is not written this chunk: zero
+                        F gf = ld_frag16_2x8(GT + (size_t)(16 * ct + r) * P::LDG, kb, g);
+                        if (2 * kb + 1 > ct && g >= 2) gf = zero_frag<T>();
+#pragma unroll
+                        for (int p = 0; p < 2; ++p) U[0][p][ct] = mma(ebh[p][kb], gf, U[0][p][ct]);
+                    }
+                }
+                const int j = 16 * ct + r;
+                floatx4 cs, sn;
+                if constexpr (AN) {
+                    cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
+                    sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
+                } else {
+                    cs = to_f4(twh[ct][0]);
+                    sn = to_f4(twh[ct][1]);
+                }
+                const floatx4 re = U[0][0][ct], im = U[0][1][ct];
+                st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, cs * re - sn * im);
+                st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * mt + 4 * g, sn * re + cs * im);
+            }
+        } else
 #pragma unroll
         for (int o = 0; o < OWN; ++o) {
             const int mt = w + NW * o;
@@ -855,11 +905,27 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
             }
             __syncthreads();  // W'' rows visible
 
+            // (8)-(9) output head dims [16 DH hv, 16 DH (hv + 1)) of the tile's tokens.  The
+            // readout weights, the Z'_v rows and the phase-table rows are all read in the
+            // natural reduction order (32kb + 8g + e), so each phase-table fragment is one
+            // 16-byte global load; those of the H tiles are requested in groups of KBM/4 two
+            // groups ahead of their products.  Every wave forms all NT key tiles of H (those
+            // above its diagonal are then zeroed): the same work and code on every wave, and no
+            // longer than the last token tile's causal share, which bounds the stage anyway.
             {
-                // (8)-(9) output head dims [16 DH hv, 16 DH (hv + 1)) of the tile's tokens
+                constexpr int TT = NT - 1;
+                constexpr int NPK = 4, GW = GG::KBM / NPK, NGR = NPK * NT;  // groups per key tile, their size
+                F eb[2][GW];
+                auto ld_e = [&](F (&t)[GW], int gi) {
+                    const T* row = tEtab + (size_t)(16 * (gi / NPK) + r) * sEtab + 32 * GW * (gi % NPK) + 8 * g;
+#pragma unroll
+                    for (int i = 0; i < GW; ++i) t[i] = ld_global<F>(row + 32 * i);
+                };
+                ld_e(eb[0], 0);
+                ld_e(eb[1], 1);
                 F wf[GG::KBM];
 #pragma unroll
-                for (int kb = 0; kb < GG::KBM; ++kb) wf[kb] = ld_frag<T>(UT + (size_t)j * P::LDQU, 32 * kb, g);
+                for (int kb = 0; kb < GG::KBM; ++kb) wf[kb] = ld_frag16_2x8(UT + (size_t)j * P::LDQU, kb, g);
                 floatx4 oa[DH];
 #pragma unroll
                 for (int d2 = 0; d2 < DH; ++d2) {
@@ -867,23 +933,25 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                     oa[d2] = zero4();
 #pragma unroll
                     for (int kb = 0; kb < GG::KBM; ++kb)
-                        oa[d2] = mma(ld_frag<T>(ZvT + (size_t)(16 * dt + r) * GG::LDZ, 32 * kb, g), wf[kb], oa[d2]);
+                        oa[d2] = mma(ld_frag16_2x8(ZvT + (size_t)(16 * dt + r) * GG::LDZ, kb, g), wf[kb], oa[d2]);
                 }
                 floatx4 hh[NT];
 #pragma unroll
-                for (int kt = 0; kt < NT; ++kt) {
-                    hh[kt] = zero4();
-                    if (kt <= tt) {
+                for (int kt = 0; kt < NT; ++kt) hh[kt] = zero4();
 #pragma unroll
-                        for (int kb = 0; kb < GG::KBM; ++kb)
-                            hh[kt] = mma(ld_frag<T>(tEtab + (size_t)(16 * kt + r) * sEtab, 32 * kb, g), wf[kb], hh[kt]);
-                        if (kt == tt) {
+                for (int gi = 0; gi < NGR; ++gi) {
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                if (4 * g + e > r) hh[kt][e] = 0.f;
-                        }
-                    }
+                    for (int i = 0; i < GW; ++i) hh[gi / NPK] = mma(eb[gi & 1][i], wf[GW * (gi % NPK) + i], hh[gi / NPK]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (gi + 2 < NGR) ld_e(eb[gi & 1], gi + 2);
                 }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int kt = 0; kt < NT; ++kt)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (kt > tt || (kt == tt && 4 * g + e > r)) hh[kt][e] = 0.f;
 #pragma unroll
                 for (int kb = 0; kb < GG::KBC; ++kb) {
                     if (2 * kb <= tt) {
