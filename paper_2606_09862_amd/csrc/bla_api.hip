@@ -194,6 +194,16 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
     pl->off_summ = off;   off = align_up(off + (size_t)units * pl->nbs * pl->unit_floats * 4);
     const size_t ncarry = pl->pair ? 0 : (size_t)(pl->nseg - 1);  // the pair kernel needs no carries
     pl->off_carry = off;  off = align_up(off + (size_t)units * ncarry * pl->unit_floats * 4);
+    // the bf16 d = M = 128 forward kernel with 64 or 128 slots reads its tables as fragments
+    pl->fragtab = !step && pl->bf16 && !pl->pair && pl->C == kChunk && pl->D == 128 && pl->MP == 128 &&
+                  (pl->SP == 64 || pl->SP == 128);
+    const size_t fab = pl->fragtab ? SP * MP2 * esz : 0, fh = pl->fragtab ? H * C * MP2 * esz : 0;
+    pl->off_fABs = off;   off = align_up(off + fab);
+    pl->off_fABm = off;   off = align_up(off + fab);
+    pl->off_fEtab = off;  off = align_up(off + fh);
+    pl->off_fEbar = off;  off = align_up(off + fh);
+    pl->off_fErev = off;  off = align_up(off + fh);
+    pl->off_fTw = off;    off = align_up(off + fh);
     pl->total = off;
 }
 
@@ -203,7 +213,7 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
 {
     // key: everything the tables' contents and layout depend on
     int32_t f[14] = {pl.H, pl.M, pl.S, pl.MP, pl.SP, pl.C, pl.bf16, pl.anchor, pl.pair, step ? 2 : pl.C + 1,
-                     pl.cpb * pl.C, 0, 0, 0};
+                     pl.cpb * pl.C, 0, step ? 0 : pl.fragtab, 0};
     const float tab_scale = pl.pair ? 1.f : pl.scale;
     memcpy(&f[11], &tab_scale, sizeof(float));
     uint64_t key = fnv_mix(1469598103934665603ull, f, sizeof(f));
@@ -246,6 +256,25 @@ bla_status build_tables(const Plan& pl, const double* T, char* ws, hipStream_t s
             a.T[i] = T[h0 + i] < tmin ? tmin : T[h0 + i];  // clamp, as Alg. 1 and Alg. 3 do
         }
         if (launch_tables(a, pl.bf16, s) != hipSuccess) return BLA_ERR_HIP;
+    }
+    if (!step && pl.fragtab) {
+        FragTabArgs fa;
+        fa.ABs = ws + pl.off_ABs;
+        fa.ABm = ws + pl.off_ABm;
+        fa.Etab = ws + pl.off_Etab;
+        fa.EbarT = ws + pl.off_EbarT;
+        fa.ErevT = ws + pl.off_ErevT;
+        fa.fABs = ws + pl.off_fABs;
+        fa.fABm = ws + pl.off_fABm;
+        fa.fEtab = ws + pl.off_fEtab;
+        fa.fEbar = ws + pl.off_fEbar;
+        fa.fErev = ws + pl.off_fErev;
+        fa.fTw = ws + pl.off_fTw;
+        fa.H = pl.H;
+        fa.C = pl.C;
+        fa.MP = pl.MP;
+        fa.SP = pl.SP;
+        if (launch_fragtab(fa, s) != hipSuccess) return BLA_ERR_HIP;
     }
     tables_record(dev, ws, key);
     return BLA_OK;
@@ -475,6 +504,14 @@ static bla_status forward_impl(const bla_params* p, const double* T, const void*
     a.Etab = ws + pl.off_Etab;
     a.ABs = ws + pl.off_ABs;
     a.ABm = ws + pl.off_ABm;
+    if (pl.fragtab) {
+        a.fABs = ws + pl.off_fABs;
+        a.fABm = ws + pl.off_fABm;
+        a.fEtab = ws + pl.off_fEtab;
+        a.fEbar = ws + pl.off_fEbar;
+        a.fErev = ws + pl.off_fErev;
+        a.fTw = ws + pl.off_fTw;
+    }
     a.theta = (const int*)(ws + pl.off_theta);
     a.summ = (float*)(ws + pl.off_summ);
     a.carry = (float*)(ws + pl.off_carry);

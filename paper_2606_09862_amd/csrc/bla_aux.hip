@@ -109,6 +109,59 @@ __global__ __launch_bounds__(kThreads) void tables_kernel(TableArgs a)
     }
 }
 
+// One thread per 16-byte piece of a fragment-ordered table (see FragTabArgs): the shared slot
+// matrices, each head's Etab, EbarT and ErevT, then the heads' twiddle tables.
+__global__ __launch_bounds__(kThreads) void fragtab_kernel(FragTabArgs a)
+{
+    const long long MP2 = 2 * a.MP;
+    const long long nab = (long long)a.SP * MP2 / 8, nh = (long long)a.C * MP2 / 8;
+    long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const bf16* src;
+    bf16* dst;
+    int K;  // columns of the source table
+    if (u < nab) {
+        src = (const bf16*)a.ABs, dst = (bf16*)a.fABs, K = (int)MP2;
+    } else if ((u -= nab) < nab) {
+        src = (const bf16*)a.ABm, dst = (bf16*)a.fABm, K = a.SP;
+    } else if ((u -= nab) >= 3 * nh * a.H) {
+        // twiddle pieces: (h, mt, ct, lane) -> cos | sin of the lane's token and four modes
+        u -= 3 * nh * a.H;
+        const int NMT = a.MP / 16, NT = a.C / 16;
+        const long long h = u / (nh);
+        if (h >= a.H) return;
+        const int l = (int)(u % 64), ct = (int)((u / 64) % NT), mt = (int)((u / (64 * NT)) % NMT);
+        const bf16* row = (const bf16*)a.Etab + (size_t)h * nh * 8 + (size_t)(16 * ct + (l & 15)) * MP2;
+        const int m = 16 * mt + 4 * (l >> 4);
+        bf16x8 x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            x[e] = row[m + e];
+            x[4 + e] = row[a.MP + m + e];
+        }
+        *reinterpret_cast<bf16x8*>((bf16*)a.fTw + (size_t)u * 8) = x;
+        return;
+    } else {
+        const long long h = u / (3 * nh);
+        if (h >= a.H) return;
+        const int which = (int)((u % (3 * nh)) / nh);
+        u %= nh;
+        const size_t off = (size_t)h * nh * 8;
+        K = which == 0 ? (int)MP2 : a.C;
+        src = (const bf16*)(which == 0 ? a.Etab : which == 1 ? a.EbarT : a.ErevT) + off;
+        dst = (bf16*)(which == 0 ? a.fEtab : which == 1 ? a.fEbar : a.fErev) + off;
+    }
+    const int l = (int)(u % 64), f = (int)(u / 64), kb = f % (K / 32), i = f / (K / 32);
+    const bf16x8 x = *reinterpret_cast<const bf16x8*>(src + (size_t)(16 * i + (l & 15)) * K + 32 * kb + 8 * (l >> 4));
+    *reinterpret_cast<bf16x8*>(dst + (size_t)u * 8) = x;
+}
+
+hipError_t launch_fragtab(const FragTabArgs& a, hipStream_t s)
+{
+    const long long n = 2ll * a.SP * 2 * a.MP / 8 + (long long)a.H * 4 * a.C * 2 * a.MP / 8;
+    hipLaunchKernelGGL(fragtab_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_tables(const TableArgs& a, int is_bf16, hipStream_t s)
 {
     const long long n = (long long)a.nh * a.jrows * a.MP + (long long)a.nh * (a.SP + a.MP) +

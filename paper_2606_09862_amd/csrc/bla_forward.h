@@ -79,7 +79,8 @@ template <typename T, int D, int MP, int CC = kChunk> struct Geo {
     static constexpr int LDZ = 2 * MP + PAD;    // ZvT: [D][LDZ]
     static constexpr size_t KT_ELEMS = (size_t)D * LDK;
     static constexpr size_t Q_ELEMS = (size_t)C * LDQ;
-    // staging units: Q rows in pieces of 8 elements, K/V in 4-token x 8-element blocks
+    // staging units: Q rows in pieces of 8 elements, K/V in 4-token x 8-element blocks (consecutive
+    // threads take consecutive 8-element pieces of the same four rows: coalesced global reads)
     static constexpr int QU = C * D / 8;
     static constexpr int KVU = 2 * (C / 4) * (D / 8);
     static constexpr int QPT = (QU + NTHR - 1) / NTHR;
@@ -182,7 +183,7 @@ __device__ __forceinline__ void stage_load(Stage<T, D, MP, CC>& st, const T* qc,
 #pragma unroll
     for (int i = 0; i < GG::KVPT; ++i) {
         const int u = tid + i * GG::NTHR;
-        const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
+        const int which = u / UNITS, uu = u % UNITS, dq = uu % (D / 8), tq = uu / (D / 8);
         const T* src = (which ? vc : kc) + 8 * dq;
         if (GG::KVU % GG::NTHR == 0 || u < GG::KVU) {
 #pragma unroll
@@ -217,7 +218,7 @@ __device__ __forceinline__ void stage_store(const Stage<T, D, MP, CC>& st, T* Qs
     for (int i = 0; i < GG::KVPT; ++i) {
         const int u = tid + i * GG::NTHR;
         if (GG::KVU % GG::NTHR == 0 || u < GG::KVU) {
-            const int which = u / UNITS, uu = u % UNITS, tq = uu % (GG::C / 4), dq = uu / (GG::C / 4);
+            const int which = u / UNITS, uu = u % UNITS, dq = uu % (D / 8), tq = uu / (D / 8);
             T* dst = (which ? Vt : Kt) + (8 * dq) * GG::LDK + 4 * tq;
             H x[4][2];
 #pragma unroll
@@ -302,6 +303,54 @@ __device__ __forceinline__ void write_zvt(T* ZvT, const StateTiles<T, D, MP, CC>
             }
         }
     }
+}
+
+// erev_frag in the reduction order 32kb + 8g + e (bf16).
+template <int MP>
+__device__ __forceinline__ bf16x8 erev_frag_nat(const float* E32, int ldE, int c, int p, int mt, int kb, int g, int r)
+{
+    bf16x8 f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int i = 32 * kb + 8 * g + e;
+        float val = 0.f;
+        if (i < c) val = E32[(size_t)(c - i) * ldE + p * MP + 16 * mt + r];
+        f[e] = (bf16)val;
+    }
+    return f;
+}
+
+// Step 10 for a wave that owns one mode tile, with the rho^{c-i} fragments ef[kb][Re, Im]
+// given in the reduction order 32kb + 8g + e (bf16), the rotation (cc, ss) of the lane's mode
+// row (Z'_k) and (cv, sv) of its four mode columns (Z'_v).
+template <typename T, int D, int MP, int CC = kChunk>
+__device__ __forceinline__ void advance_owned(StateTiles<T, D, MP, CC>& Zk, StateTiles<T, D, MP, CC>& Zv,
+                                              const T* Kt, const T* Vt, const bf16x8 (&ef)[Geo<T, D, MP, CC>::KBC][2],
+                                              float cc, float ss, floatx4 cv, floatx4 sv, int g, int r)
+{
+    using GG = Geo<T, D, MP, CC>;
+    static_assert(GG::OWN == 1 && sizeof(T) == 2 && !GG::HALF, "one owned mode tile, bf16, 32-token blocks");
+#pragma unroll
+    for (int dt = 0; dt < GG::NDT; ++dt) {
+        const floatx4 kr = Zk[0][0][dt], ki = Zk[0][1][dt];
+        Zk[0][0][dt] = cc * kr - ss * ki;
+        Zk[0][1][dt] = ss * kr + cc * ki;
+        const floatx4 vr = Zv[0][0][dt], vi = Zv[0][1][dt];
+        Zv[0][0][dt] = cv * vr - sv * vi;
+        Zv[0][1][dt] = sv * vr + cv * vi;
+    }
+#pragma unroll
+    for (int kb = 0; kb < GG::KBC; ++kb)
+#pragma unroll
+        for (int dt = 0; dt < GG::NDT; ++dt) {
+            const bf16x8 kf = ld_frag16_2x8((const bf16*)Kt + (size_t)(16 * dt + r) * GG::LDK, kb, g);
+            const bf16x8 vf = ld_frag16_2x8((const bf16*)Vt + (size_t)(16 * dt + r) * GG::LDK, kb, g);
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                Zk[0][p][dt] = mma(kf, ef[kb][p], Zk[0][p][dt]);
+                Zv[0][p][dt] = mma(ef[kb][p], vf, Zv[0][p][dt]);
+            }
+        }
 }
 
 // Step 10: Z' <- rho^c o Z' + sum_i rho^{c-i} [k_i | v_i] on the wave's own mode tiles.
@@ -490,6 +539,13 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
     const T* gEbar = (const T*)a.EbarT + (size_t)h * 2 * MP * C;
     const T* gErev = (const T*)a.ErevT + (size_t)h * 2 * MP * C;
     const T* gEtab = (const T*)a.Etab + (size_t)h * C * 2 * MP;
+    // fragment-ordered tables of the split chain (one contiguous 1 KB block per fragment)
+    const T* fABs = (const T*)a.fABs;
+    const T* fABm = (const T*)a.fABm;
+    const T* fEtab = (const T*)a.fEtab + (size_t)h * C * 2 * MP;
+    const T* fEbar = (const T*)a.fEbar + (size_t)h * C * 2 * MP;
+    const T* fErev = (const T*)a.fErev + (size_t)h * C * 2 * MP;
+    const T* fTw = (const T*)a.fTw + (size_t)h * C * 2 * MP;
     if constexpr (P::TL) {
         T* lABs = lPh + (size_t)2 * MP;
         T* lABm = lABs + (size_t)SP * P::LDAS;
@@ -616,6 +672,14 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
             tEtab = opaque(tEtab);
             tEbar = opaque(tEbar);
             tErev = opaque(tErev);
+            if constexpr (P::SPLIT) {
+                fABs = opaque(fABs);
+                fABm = opaque(fABm);
+                fEtab = opaque(fEtab);
+                fEbar = opaque(fEbar);
+                fErev = opaque(fErev);
+                fTw = opaque(fTw);
+            }
         }
         __syncthreads();  // previous chunk done with Qs / Kt / Vt and the twiddle row
         stage_store<T, D, MP, true, CC>(st, Qs, Kt, Vt, c, tid);
@@ -694,23 +758,20 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         }
         // Split chain (one owned mode tile): the conj(E) fragments and phase twiddles of phase
         // B are the same for every token tile; they are requested here, before the barrier, so
-        // that their latency overlaps it (16-byte loads in the reduction order 32kb + 8g + e,
+        // that their latency overlaps it (fragment-ordered table, reduction order 32kb + 8g + e,
         // matched by the Gram-tile reads below).
         F ebh[P::SPLIT ? 2 : 1][P::SPLIT ? GG::KBC : 1];
-        typename Frag<T>::half twh[P::SPLIT && !AN ? NT : 1][2];
+        F twh[P::SPLIT && !AN ? NT : 1];  // cos e = 0..3 | sin e = 0..3 of the lane's token, modes 16w + 4g + e
         if constexpr (P::SPLIT) {
             static_assert(OWN == 1 && !GG::HALF, "one owned mode tile, 32-token reduction blocks");
 #pragma unroll
             for (int p = 0; p < 2; ++p)
 #pragma unroll
                 for (int kb = 0; kb < GG::KBC; ++kb)
-                    ebh[p][kb] = ld_global<F>(tEbar + (size_t)(16 * (p * NMT + w) + r) * sR + 32 * kb + 8 * g);
+                    ebh[p][kb] = ld_global<F>(fEbar + ((size_t)((p * NMT + w) * GG::KBC + kb) * 64 + (tid & 63)) * 8);
             if constexpr (!AN) {
 #pragma unroll
-                for (int ct = 0; ct < NT; ++ct) {
-                    twh[ct][0] = ld4<T>(tEtab + (size_t)(16 * ct + r) * sEtab + 16 * w + 4 * g);
-                    twh[ct][1] = ld4<T>(tEtab + (size_t)(16 * ct + r) * sEtab + MP + 16 * w + 4 * g);
-                }
+                for (int ct = 0; ct < NT; ++ct) twh[ct] = ld_global<F>(fTw + ((size_t)(w * NT + ct) * 64 + (tid & 63)) * 8);
             }
         }
         __syncthreads();
@@ -737,8 +798,8 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                     cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
                     sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
                 } else {
-                    cs = to_f4(twh[ct][0]);
-                    sn = to_f4(twh[ct][1]);
+                    cs = to_f4(__builtin_shufflevector(twh[ct], twh[ct], 0, 1, 2, 3));
+                    sn = to_f4(__builtin_shufflevector(twh[ct], twh[ct], 4, 5, 6, 7));
                 }
                 const floatx4 re = U[0][0][ct], im = U[0][1][ct];
                 st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, cs * re - sn * im);
@@ -788,16 +849,16 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
             constexpr int NSH = P::NST / 2, KSH = P::KBS / 2, MH = NMT / 2, DH = NDT / 2;
             {
                 // (4)-(5) scores of slots [SP/2 hv, SP/2 (hv + 1)), masked, exponentiated
-                // against the half's own maximum.  The slot-matrix fragments come from global
-                // memory (L2): reduction block kb + 2 is requested before the products of block
-                // kb are issued (the scheduling barriers keep that order), so about two blocks
-                // are in flight instead of one fragment.  Reduction order 32kb + 8g + e on both
-                // operands (a 16-byte read of the table row).
+                // against the half's own maximum.  The slot-matrix fragments come from the
+                // fragment-ordered copy in global memory (L2; one coalesced 1 KB block each):
+                // reduction block kb + 2 is requested before the products of block kb are issued
+                // (the scheduling barriers keep that order), so about two blocks are in flight.
+                // Reduction order 32kb + 8g + e on both operands.
                 F tb[2][NSH], ub[2];
                 auto ld_blk = [&](F (&t)[NSH], F& u, int kb) {
 #pragma unroll
                     for (int s4 = 0; s4 < NSH; ++s4)
-                        t[s4] = ld_global<F>(tABs + (size_t)(16 * (NSH * hv + s4) + r) * sABs + 32 * kb + 8 * g);
+                        t[s4] = ld_global<F>(fABs + ((size_t)((NSH * hv + s4) * GG::KBM + kb) * 64 + (tid & 63)) * 8);
                     u = ld_frag16_2x8(UT + (size_t)j * P::LDQU, kb, g);  // rows 8-byte aligned
                 };
                 floatx4 sc[NSH];
@@ -866,9 +927,9 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                 auto col_tile = [&](int i) { return ((i >> 1) & 1) * NMT + MH * hv + 2 * (i >> 2) + (i & 1); };
                 F ab[2][P::KBS];
                 auto ld_tile = [&](F (&t)[P::KBS], int i) {
-                    const T* row = tABm + (size_t)(16 * col_tile(i) + r) * sABm;
+                    const T* fr = fABm + ((size_t)col_tile(i) * P::KBS * 64 + (tid & 63)) * 8;
 #pragma unroll
-                    for (int ks = 0; ks < P::KBS; ++ks) t[ks] = ld_global<F>(row + 32 * ks + 8 * g);
+                    for (int ks = 0; ks < P::KBS; ++ks) t[ks] = ld_global<F>(fr + (size_t)ks * 64 * 8);
                 };
                 ld_tile(ab[0], 0);
                 ld_tile(ab[1], 1);
@@ -892,8 +953,9 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                                 cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
                                 sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
                             } else {
-                                cs = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + 16 * mt + 4 * g));
-                                sn = to_f4(ld4<T>(tEtab + (size_t)j * sEtab + MP + 16 * mt + 4 * g));
+                                const F tw = ld_global<F>(fTw + ((size_t)(mt * NT + tt) * 64 + (tid & 63)) * 8);
+                                cs = to_f4(__builtin_shufflevector(tw, tw, 0, 1, 2, 3));
+                                sn = to_f4(__builtin_shufflevector(tw, tw, 4, 5, 6, 7));
                             }
                             const floatx4 am = wa[0][v2], bm = wa[1][v2];
                             st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, am * cs + bm * sn);
@@ -907,9 +969,9 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
 
             // (8)-(9) output head dims [16 DH hv, 16 DH (hv + 1)) of the tile's tokens.  The
             // readout weights, the Z'_v rows and the phase-table rows are all read in the
-            // natural reduction order (32kb + 8g + e), so each phase-table fragment is one
-            // 16-byte global load; those of the H tiles are requested in groups of KBM/4 two
-            // groups ahead of their products.  Every wave forms all NT key tiles of H (those
+            // natural reduction order (32kb + 8g + e); each phase-table fragment is one
+            // coalesced block of the fragment-ordered copy.  Those of the H tiles are requested
+            // in groups of KBM/4 two groups ahead of their products.  Every wave forms all NT key tiles of H (those
             // above its diagonal are then zeroed): the same work and code on every wave, and no
             // longer than the last token tile's causal share, which bounds the stage anyway.
             {
@@ -917,9 +979,9 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                 constexpr int NPK = 4, GW = GG::KBM / NPK, NGR = NPK * NT;  // groups per key tile, their size
                 F eb[2][GW];
                 auto ld_e = [&](F (&t)[GW], int gi) {
-                    const T* row = tEtab + (size_t)(16 * (gi / NPK) + r) * sEtab + 32 * GW * (gi % NPK) + 8 * g;
+                    const T* fr = fEtab + ((size_t)((gi / NPK) * GG::KBM + GW * (gi % NPK)) * 64 + (tid & 63)) * 8;
 #pragma unroll
-                    for (int i = 0; i < GW; ++i) t[i] = ld_global<F>(row + 32 * i);
+                    for (int i = 0; i < GW; ++i) t[i] = ld_global<F>(fr + (size_t)i * 64 * 8);
                 };
                 ld_e(eb[0], 0);
                 ld_e(eb[1], 1);
@@ -1093,7 +1155,22 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         }
         __syncthreads();  // everyone done reading ZvT
 
-        advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, rhoL, E32h, tErev, sR, c, w, g, r);
+        if constexpr (P::SPLIT) {
+            // step (10) with rho^{c-i} from the fragment-ordered table (reduction order 32kb +
+            // 8g + e, matched by the K and V reads); a ragged last chunk builds it from E32
+            F ef[GG::KBC][2];
+#pragma unroll
+            for (int kb = 0; kb < GG::KBC; ++kb)
+#pragma unroll
+                for (int p = 0; p < 2; ++p)
+                    ef[kb][p] = (c == C) ? ld_global<F>(fErev + ((size_t)((p * NMT + w) * GG::KBC + kb) * 64 + (tid & 63)) * 8)
+                                         : erev_frag_nat<MP>(E32h, 2 * MP, c, p, w, kb, g, r);
+            const float* Ec = (c == C) ? rhoC : rhoL;
+            advance_owned<T, D, MP, CC>(Zk, Zv, Kt, Vt, ef, Ec[16 * w + r], Ec[MP + 16 * w + r], ld4f(Ec + 16 * w + 4 * g),
+                                        ld4f(Ec + MP + 16 * w + 4 * g), g, r);
+        } else {
+            advance_state<T, D, MP, CC>(Zk, Zv, Kt, Vt, rhoC, rhoL, E32h, tErev, sR, c, w, g, r);
+        }
         write_zvt<T, D, MP, CC>(ZvT, Zv, w, g, r);
     }
 

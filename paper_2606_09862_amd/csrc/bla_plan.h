@@ -29,9 +29,35 @@ struct Plan {
     int anchor;          // 1: slots anchored at absolute phase 0 (Sec. 3.3), 0: at the current token
     int cpb, nbs;        // chunks per summarised block, summarised blocks per sequence
     size_t unit_floats;  // floats of one full (k and v) pre-rotated state: 4*MP*D
+    // 1: the tables read from global memory by the d = M = 128 forward kernel also exist in
+    // operand-fragment order (see FragTabArgs)
+    int fragtab;
     // workspace byte offsets
     size_t off_E32, off_EbarT, off_ErevT, off_Etab, off_ABs, off_ABm, off_theta,
-        off_rotblk, off_trig, off_rperiod, off_period, off_summ, off_carry, total;
+        off_rotblk, off_trig, off_rperiod, off_period, off_summ, off_carry,
+        off_fABs, off_fABm, off_fEtab, off_fEbar, off_fErev, off_fTw, total;
+};
+
+// Fragment-ordered copies of row-major bf16 tables M[R][K]: operand fragment (i, kb) of rows
+// 16i..16i+15 and reduction block kb (columns 32kb + 8g + e for lane 16g + r) is stored as
+// 64 consecutive 16-byte pieces, piece l = 16g + r holding M[16i + r][32kb + 8g .. + 7].  A
+// wave then loads a fragment as one contiguous 1 KB block (coalesced), where the row-major
+// table costs a separate 16-byte access per lane.
+struct FragTabArgs {
+    const void* ABs;   // [SP][2MP]
+    const void* ABm;   // [2MP][SP]
+    const void* Etab;  // [H][C][2MP]
+    const void* EbarT; // [H][2MP][C]
+    const void* ErevT; // [H][2MP][C]
+    void* fABs;
+    void* fABm;
+    void* fEtab;
+    void* fEbar;
+    void* fErev;
+    // phase twiddles in lane order: [H][MP/16 mode tiles][C/16 token tiles][64 lanes][8], lane
+    // 16g + r holding cos | sin of m w j for j = 16 ct + r, m = 16 mt + 4g .. + 3
+    void* fTw;
+    int H, C, MP, SP;
 };
 
 struct TableArgs {
@@ -69,6 +95,13 @@ struct FwdArgs {
     const void* Etab;
     const void* ABs;
     const void* ABm;
+    // fragment-ordered copies (FragTabArgs), when the plan has them
+    const void* fABs;
+    const void* fABm;
+    const void* fEtab;
+    const void* fEbar;
+    const void* fErev;
+    const void* fTw;
     const int* theta;
     float* summ;
     float* carry;
@@ -228,6 +261,7 @@ inline bool backward_supported(int bf16, int D, int MP, int SP)
 
 // Launchers (defined in the .hip translation units).  They return a HIP error.
 hipError_t launch_tables(const TableArgs& a, int bf16, hipStream_t s);
+hipError_t launch_fragtab(const FragTabArgs& a, hipStream_t s);
 hipError_t launch_summary(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_scan(const Plan& p, const FwdArgs& a, hipStream_t s);
 hipError_t launch_forward(const Plan& p, const FwdArgs& a, hipStream_t s);
