@@ -167,9 +167,11 @@ void make_plan(const bla_params* p, bool step, Plan* pl)
                 // Blocks per segment: enough summary workgroups to fill the device, within
                 // the scratch cap; always a divisor of cps.
                 // The pair kernel combines the summaries itself: one block per segment.
+                // bf16 64-token summaries run D/32 column-slice workgroups per block.
                 int bps = 1;
                 const size_t unit_bytes = pl->unit_floats * sizeof(float);
-                while (!pl->pair && units * (nseg - 1) * bps < 2 * cus && cps % (2 * bps) == 0 &&
+                const long long slices = pl->bf16 && pl->C == kChunk ? pl->D / 32 : 1;
+                while (!pl->pair && units * (nseg - 1) * bps * slices < 2 * cus && cps % (2 * bps) == 0 &&
                        (size_t)units * (nseg - 1) * (2 * bps) * unit_bytes <= kMaxSummaryBytes)
                     bps *= 2;
                 pl->cpb = cps / bps;
