@@ -123,22 +123,19 @@ template <typename T, int D, int MP, int SP, int CC = kChunk> struct Fwd : Geo<T
     static constexpr size_t BASE_BYTES = BASE_ELEMS * sizeof(T);
     static constexpr size_t FULL_BYTES = BASE_BYTES + TAB_ELEMS * sizeof(T) + SMALL_BYTES;
     static constexpr bool TL = FULL_BYTES <= kMaxLds;  // tables live in LDS
-    // Split chain (bf16, eight waves for four token tiles, tables outside LDS): the two waves
-    // of a token tile share steps (4)-(9) -- one half of the slots each for the scores, one
-    // half of the modes for the readout weights, one half of the head dims for the output.
-    // The unnormalised slot weights P~ ([C][LDP]) and the per-token (max, sum) of each slot
-    // half ([C][2][2] float32) pass through LDS after the per-chunk buffers.
+    // Split chain (bf16, eight waves, four token tiles, tables outside LDS): steps (4)-(9) are
+    // split by output columns -- each wave forms one slot tile of the scores, one mode tile of
+    // the readout weights and one head-dim tile of the output, for every token of the chunk,
+    // so that each table fragment it loads serves all four token tiles.  The unnormalised slot
+    // weights P~ ([C][LDP]) pass through LDS after the per-chunk buffers (later the H tiles);
+    // the per-token (max, sum) of each slot tile use the Gram buffer, free by then.
     static constexpr int LDP = SP + G::PAD;
-    static constexpr size_t SPLIT_BYTES = (size_t)G::C * LDP * sizeof(T) + (size_t)G::C * 4 * 4;
+    static constexpr size_t SPLIT_BYTES = (size_t)G::C * LDP * sizeof(T);
     static constexpr bool SPLIT = sizeof(T) == 2 && G::NW == 2 * G::NT && SP % 64 == 0 && !TL &&
                                   BASE_BYTES + SPLIT_BYTES <= kMaxLds;
     static constexpr size_t LDS_BYTES = TL ? FULL_BYTES : BASE_BYTES + (SPLIT ? SPLIT_BYTES : 0);
     static_assert(SP % 32 == 0, "slot padding");
 };
-
-// Token tile of wave w in the split chain: waves w and w + 4 share a SIMD, and the tiles
-// {0, 3} and {1, 2} put one short and one long causal tile on every SIMD.
-__device__ __forceinline__ int split_tile(int w) { return (0x12032130 >> (4 * w)) & 15; }
 
 // An operand fragment times a per-lane factor (bf16 in, bf16 out, float32 product).
 __device__ __forceinline__ bf16x8 scale_frag(bf16x8 x, float f)
@@ -503,9 +500,10 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
     T* GT = Qs + (size_t)C * P::LDQU;
     T* ZvT = GT + (size_t)C * P::LDG;
     T* lPh = ZvT + (size_t)D * GG::LDZ;  // anchored twiddle row conj(rho^P) of the chunk
-    // split chain: P~ rows and the per-token softmax statistics of the two slot halves
+    // split chain: P~ rows (then the H tiles) and the per-token (max, sum) of every slot tile
     T* Pw = reinterpret_cast<T*>(lds_raw + P::BASE_BYTES);
-    float* sStat = reinterpret_cast<float*>(lds_raw + P::BASE_BYTES + (size_t)C * P::LDP * sizeof(T));
+    float* sStat = reinterpret_cast<float*>(GT);
+    static_assert(!P::SPLIT || (size_t)C * P::NST * 2 * 4 <= (size_t)C * P::LDG * sizeof(T), "statistics fit");
 
     const int tid = threadIdx.x, g = (tid & 63) >> 4, r = tid & 15;
     const int tid_ = tid, g_ = g, r_ = r;  // the chunk loop re-derives its own copies
@@ -841,193 +839,188 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
         }
         __syncthreads();
 
-        // ---- per-token chain, split over the two waves of each token tile
+        // ---- per-token chain, split by output columns over the eight waves
         if constexpr (P::SPLIT) {
-            const int tt = split_tile(w), hv = w / NT;  // token tile, half
-            const int j = 16 * tt + r;
-            const long long pos = a.t0 + tok0 + j;
-            constexpr int NSH = P::NST / 2, KSH = P::KBS / 2, MH = NMT / 2, DH = NDT / 2;
+            static_assert(NT == 4 && NW == 8 && NMT == NW && NDT == NW, "eight waves, four token tiles");
+            constexpr int NST = P::NST, NTT = NT * NST / NW;  // slot tiles; token tiles per wave
+            const int lane = tid & 63;
             {
-                // (4)-(5) scores of slots [SP/2 hv, SP/2 (hv + 1)), masked, exponentiated
-                // against the half's own maximum.  The slot-matrix fragments come from the
-                // fragment-ordered copy in global memory (L2; one coalesced 1 KB block each):
-                // reduction block kb + 2 is requested before the products of block kb are issued
-                // (the scheduling barriers keep that order), so about two blocks are in flight.
-                // Reduction order 32kb + 8g + e on both operands.
-                F tb[2][NSH], ub[2];
-                auto ld_blk = [&](F (&t)[NSH], F& u, int kb) {
-#pragma unroll
-                    for (int s4 = 0; s4 < NSH; ++s4)
-                        t[s4] = ld_global<F>(fABs + ((size_t)((NSH * hv + s4) * GG::KBM + kb) * 64 + (tid & 63)) * 8);
-                    u = ld_frag16_2x8(UT + (size_t)j * P::LDQU, kb, g);  // rows 8-byte aligned
+                // (4)-(5) scores of slot tile st for token tiles tt0 .. tt0 + NTT - 1, masked and
+                // exponentiated against the tile's own maximum.  The slot-matrix fragment of
+                // reduction block kb (fragment-ordered: one coalesced 1 KB load) is requested two
+                // blocks ahead and serves every token tile of the wave.
+                const int st = w % NST, tt0 = (w / NST) * NTT;
+                F ab[2];
+                auto ld_ab = [&](F& t, int kb) {
+                    t = ld_global<F>(fABs + ((size_t)(st * GG::KBM + kb) * 64 + lane) * 8);
                 };
-                floatx4 sc[NSH];
+                floatx4 sc[NTT];
 #pragma unroll
-                for (int s4 = 0; s4 < NSH; ++s4) sc[s4] = zero4();
-                ld_blk(tb[0], ub[0], 0);
-                ld_blk(tb[1], ub[1], 1);
+                for (int i = 0; i < NTT; ++i) sc[i] = zero4();
+                ld_ab(ab[0], 0);
+                ld_ab(ab[1], 1);
 #pragma unroll
                 for (int kb = 0; kb < GG::KBM; ++kb) {
+                    F uf[NTT];
+#pragma unroll
+                    for (int i = 0; i < NTT; ++i)
+                        uf[i] = ld_frag16_2x8(UT + (size_t)(16 * (tt0 + i) + r) * P::LDQU, kb, g);
                     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                    for (int s4 = 0; s4 < NSH; ++s4) sc[s4] = mma(tb[kb & 1][s4], ub[kb & 1], sc[s4]);
+                    for (int i = 0; i < NTT; ++i) sc[i] = mma(ab[kb & 1], uf[i], sc[i]);
                     __builtin_amdgcn_sched_barrier(0);
-                    if (kb + 2 < GG::KBM) ld_blk(tb[kb & 1], ub[kb & 1], kb + 2);
+                    if (kb + 2 < GG::KBM) ld_ab(ab[kb & 1], kb + 2);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                float mx = -INFINITY;
+                const intx4 th = *reinterpret_cast<const intx4*>(tTheta + 16 * st + 4 * g);
 #pragma unroll
-                for (int s4 = 0; s4 < NSH; ++s4) {
-                    const intx4 th = *reinterpret_cast<const intx4*>(tTheta + 16 * (NSH * hv + s4) + 4 * g);
+                for (int i = 0; i < NTT; ++i) {
+                    const int j = 16 * (tt0 + i) + r;
+                    const long long pos = a.t0 + tok0 + j;
+                    float mx = -INFINITY;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        if (pos < (long long)th[e]) sc[s4][e] = -INFINITY;
-                        mx = fmaxf(mx, sc[s4][e]);
+                        if (pos < (long long)th[e]) sc[i][e] = -INFINITY;
+                        mx = fmaxf(mx, sc[i][e]);
                     }
-                }
-                mx = rows_max(mx);
-                // the upper half can be fully masked (its weights are then zero); the lower
-                // half holds slot 0, whose threshold is 0
-                const float mref = mx == -INFINITY ? 0.f : mx;
-                float sum = 0.f;
-#pragma unroll
-                for (int s4 = 0; s4 < NSH; ++s4)
+                    mx = rows_max(mx);
+                    // a slot tile can be fully masked (its weights are then zero); tile 0 holds
+                    // slot 0, whose threshold is 0
+                    const float mref = mx == -INFINITY ? 0.f : mx;
+                    float sum = 0.f;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float ex = __expf(sc[s4][e] - mref);
-                        sc[s4][e] = ex;
+                        const float ex = __expf(sc[i][e] - mref);
+                        sc[i][e] = ex;
                         sum += ex;
                     }
-                sum = rows_sum(sum);
-#pragma unroll
-                for (int s4 = 0; s4 < NSH; ++s4) st4<T>(Pw + (size_t)j * P::LDP + 16 * (NSH * hv + s4) + 4 * g, sc[s4]);
-                if (g == 0) {
-                    sStat[(j * 2 + hv) * 2 + 0] = mx;
-                    sStat[(j * 2 + hv) * 2 + 1] = sum;
+                    sum = rows_sum(sum);
+                    st4<T>(Pw + (size_t)j * P::LDP + 16 * st + 4 * g, sc[i]);
+                    if (g == 0) {
+                        sStat[(j * NST + st) * 2 + 0] = mx;
+                        sStat[(j * NST + st) * 2 + 1] = sum;
+                    }
                 }
             }
             __syncthreads();  // P~ and the statistics visible; U no longer read
 
             {
-                // (6)-(7) readout weights of mode tiles [MH hv, MH (hv + 1)), published to
-                // LDS over U: [Re W'' | Im-part] rows in the order the output contraction reads
-                const float m0 = sStat[j * 4 + 0], s0 = sStat[j * 4 + 1];
-                const float m1 = sStat[j * 4 + 2], s1 = sStat[j * 4 + 3];
-                const float M = fmaxf(m0, m1);
-                const float e0 = __expf(m0 - M), e1 = __expf(m1 - M);
-                const float inv = __builtin_amdgcn_rcpf(e0 * s0 + e1 * s1);
-                const float f0 = e0 * inv, f1 = e1 * inv;
-                F pf[P::KBS];
+                // (6)-(7) readout weights of mode tile w ([Re | Im] column tiles w, NMT + w) for
+                // every token tile; the transposed slot-matrix fragments (fragment-ordered) are
+                // loaded once and serve all four token tiles, the P~ fragments are scaled by the
+                // normalisation of their slot tile (natural order: lanes g < 2 hold slot tile 2ks,
+                // lanes g >= 2 tile 2ks + 1)
+                F am[2][P::KBS];
 #pragma unroll
-                for (int kb = 0; kb < P::KBS; ++kb)
-                    pf[kb] = scale_frag(ld_frag16_2x8(Pw + (size_t)j * P::LDP, kb, g), kb < KSH ? f0 : f1);
-                // column tiles in the order (q, Re/Im p, u); tile i's KBS fragments of the
-                // transposed slot matrix are requested two tiles ahead of its products
-                constexpr int NG = 2 * MH;  // column tiles of the half
-                auto col_tile = [&](int i) { return ((i >> 1) & 1) * NMT + MH * hv + 2 * (i >> 2) + (i & 1); };
-                F ab[2][P::KBS];
-                auto ld_tile = [&](F (&t)[P::KBS], int i) {
-                    const T* fr = fABm + ((size_t)col_tile(i) * P::KBS * 64 + (tid & 63)) * 8;
+                for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
-                    for (int ks = 0; ks < P::KBS; ++ks) t[ks] = ld_global<F>(fr + (size_t)ks * 64 * 8);
+                    for (int ks = 0; ks < P::KBS; ++ks)
+                        am[pp][ks] = ld_global<F>(fABm + ((size_t)((pp * NMT + w) * P::KBS + ks) * 64 + lane) * 8);
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt) {
+                    const int j = 16 * tt + r;
+                    float mt_[NST], st_[NST];
+                    float M = -INFINITY;
+#pragma unroll
+                    for (int q = 0; q < NST; ++q) {
+                        mt_[q] = sStat[(j * NST + q) * 2 + 0];
+                        st_[q] = sStat[(j * NST + q) * 2 + 1];
+                        M = fmaxf(M, mt_[q]);
+                    }
+                    float tot = 0.f;
+#pragma unroll
+                    for (int q = 0; q < NST; ++q) {
+                        mt_[q] = __expf(mt_[q] - M);  // 0 for a fully masked tile
+                        tot += mt_[q] * st_[q];
+                    }
+                    const float inv = __builtin_amdgcn_rcpf(tot);
+                    F pf[P::KBS];
+#pragma unroll
+                    for (int ks = 0; ks < P::KBS; ++ks)
+                        pf[ks] = scale_frag(ld_frag16_2x8(Pw + (size_t)j * P::LDP, ks, g),
+                                            (g < 2 ? mt_[2 * ks] : mt_[2 * ks + 1]) * inv);
+                    floatx4 wa[2];
+#pragma unroll
+                    for (int pp = 0; pp < 2; ++pp) {
+                        wa[pp] = zero4();
+#pragma unroll
+                        for (int ks = 0; ks < P::KBS; ++ks) wa[pp] = mma(am[pp][ks], pf[ks], wa[pp]);
+                    }
+                    floatx4 cs, sn;
+                    if constexpr (AN) {
+                        cs = to_f4(ld4_lds<T>(lPh + 16 * w + 4 * g));
+                        sn = to_f4(ld4_lds<T>(lPh + MP + 16 * w + 4 * g));
+                    } else {
+                        const F tw = ld_global<F>(fTw + ((size_t)(w * NT + tt) * 64 + lane) * 8);
+                        cs = to_f4(__builtin_shufflevector(tw, tw, 0, 1, 2, 3));
+                        sn = to_f4(__builtin_shufflevector(tw, tw, 4, 5, 6, 7));
+                    }
+                    const floatx4 a0 = wa[0], b0 = wa[1];
+                    st4<T>(UT + (size_t)j * P::LDQU + 16 * w + 4 * g, a0 * cs + b0 * sn);
+                    st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * w + 4 * g, a0 * sn - b0 * cs);
+                }
+            }
+            __syncthreads();  // W'' rows visible; P~ no longer read
+
+            {
+                // (8)-(9) output head-dim tile w of every token tile.  The causal H tiles
+                // (key tile kt <= token tile tt, ten of them) are shared out over the waves and
+                // published to LDS over P~ as [token][key] rows (the tiles just past the
+                // diagonal, which the 32-key blocks of the H V products also read, as zeros).
+                T* Hs = Pw;
+                auto h_tile = [&](int q, int& tt, int& kt) {
+                    // q = 0..9 over (tt, kt), kt <= tt, in the order (0,0) (1,0) (1,1) (2,0) ...
+                    tt = q < 1 ? 0 : q < 3 ? 1 : q < 6 ? 2 : 3;
+                    kt = q - tt * (tt + 1) / 2;
                 };
-                ld_tile(ab[0], 0);
-                ld_tile(ab[1], 1);
-                floatx4 wa[2][2];  // [Re, Im][mode tile MH hv + 2q + u] of the current q
 #pragma unroll
-                for (int i = 0; i < NG; ++i) {
-                    const int pp = (i >> 1) & 1, u = i & 1;
-                    __builtin_amdgcn_sched_barrier(0);
-                    wa[pp][u] = zero4();
+                for (int u2 = 0; u2 < 2; ++u2) {
+                    const int q = w + NW * u2;
+                    if (q < 10) {
+                        int tt, kt;
+                        h_tile(q, tt, kt);
+                        floatx4 hh = zero4();
+                        const T* fe = fEtab + ((size_t)kt * GG::KBM * 64 + lane) * 8;
+                        F ef[GG::KBM];
 #pragma unroll
-                    for (int ks = 0; ks < P::KBS; ++ks) wa[pp][u] = mma(ab[i & 1][ks], pf[ks], wa[pp][u]);
-                    __builtin_amdgcn_sched_barrier(0);
-                    if (i + 2 < NG) ld_tile(ab[i & 1], i + 2);
-                    if ((i & 3) == 3) {
-                        // (7) twiddle the two mode tiles of this q and publish them
+                        for (int kb = 0; kb < GG::KBM; ++kb) ef[kb] = ld_global<F>(fe + (size_t)kb * 64 * 8);
 #pragma unroll
-                        for (int v2 = 0; v2 < 2; ++v2) {
-                            const int mt = MH * hv + 2 * (i >> 2) + v2;
-                            floatx4 cs, sn;
-                            if constexpr (AN) {
-                                cs = to_f4(ld4_lds<T>(lPh + 16 * mt + 4 * g));
-                                sn = to_f4(ld4_lds<T>(lPh + MP + 16 * mt + 4 * g));
-                            } else {
-                                const F tw = ld_global<F>(fTw + ((size_t)(mt * NT + tt) * 64 + (tid & 63)) * 8);
-                                cs = to_f4(__builtin_shufflevector(tw, tw, 0, 1, 2, 3));
-                                sn = to_f4(__builtin_shufflevector(tw, tw, 4, 5, 6, 7));
-                            }
-                            const floatx4 am = wa[0][v2], bm = wa[1][v2];
-                            st4<T>(UT + (size_t)j * P::LDQU + 16 * mt + 4 * g, am * cs + bm * sn);
-                            st4<T>(UT + (size_t)j * P::LDQU + MP + 16 * mt + 4 * g, am * sn - bm * cs);
+                        for (int kb = 0; kb < GG::KBM; ++kb)
+                            hh = mma(ef[kb], ld_frag16_2x8(UT + (size_t)(16 * tt + r) * P::LDQU, kb, g), hh);
+                        if (kt == tt) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (4 * g + e > r) hh[e] = 0.f;
                         }
+                        st4<T>(Hs + (size_t)(16 * tt + r) * P::LDP + 16 * kt + 4 * g, hh);
+                    } else if (q < 12) {
+                        const int tt = 2 * (q - 10);  // tiles (0, 1) and (2, 3)
+                        st4<T>(Hs + (size_t)(16 * tt + r) * P::LDP + 16 * (tt + 1) + 4 * g, zero4());
                     }
                 }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            __syncthreads();  // W'' rows visible
-
-            // (8)-(9) output head dims [16 DH hv, 16 DH (hv + 1)) of the tile's tokens.  The
-            // readout weights, the Z'_v rows and the phase-table rows are all read in the
-            // natural reduction order (32kb + 8g + e); each phase-table fragment is one
-            // coalesced block of the fragment-ordered copy.  Those of the H tiles are requested
-            // in groups of KBM/4 two groups ahead of their products.  Every wave forms all NT key tiles of H (those
-            // above its diagonal are then zeroed): the same work and code on every wave, and no
-            // longer than the last token tile's causal share, which bounds the stage anyway.
-            {
-                constexpr int TT = NT - 1;
-                constexpr int NPK = 4, GW = GG::KBM / NPK, NGR = NPK * NT;  // groups per key tile, their size
-                F eb[2][GW];
-                auto ld_e = [&](F (&t)[GW], int gi) {
-                    const T* fr = fEtab + ((size_t)((gi / NPK) * GG::KBM + GW * (gi % NPK)) * 64 + (tid & 63)) * 8;
+                // O^T tile (head dims 16w .., tokens of tile tt) = Re(W'' Z'_v) over the modes
+                F zf[GG::KBM];
 #pragma unroll
-                    for (int i = 0; i < GW; ++i) t[i] = ld_global<F>(fr + (size_t)i * 64 * 8);
-                };
-                ld_e(eb[0], 0);
-                ld_e(eb[1], 1);
-                F wf[GG::KBM];
+                for (int kb = 0; kb < GG::KBM; ++kb) zf[kb] = ld_frag16_2x8(ZvT + (size_t)(16 * w + r) * GG::LDZ, kb, g);
+                floatx4 oa[NT];
 #pragma unroll
-                for (int kb = 0; kb < GG::KBM; ++kb) wf[kb] = ld_frag16_2x8(UT + (size_t)j * P::LDQU, kb, g);
-                floatx4 oa[DH];
-#pragma unroll
-                for (int d2 = 0; d2 < DH; ++d2) {
-                    const int dt = DH * hv + d2;
-                    oa[d2] = zero4();
+                for (int tt = 0; tt < NT; ++tt) {
+                    oa[tt] = zero4();
 #pragma unroll
                     for (int kb = 0; kb < GG::KBM; ++kb)
-                        oa[d2] = mma(ld_frag16_2x8(ZvT + (size_t)(16 * dt + r) * GG::LDZ, kb, g), wf[kb], oa[d2]);
+                        oa[tt] = mma(zf[kb], ld_frag16_2x8(UT + (size_t)(16 * tt + r) * P::LDQU, kb, g), oa[tt]);
                 }
-                floatx4 hh[NT];
+                __syncthreads();  // H tiles visible
 #pragma unroll
-                for (int kt = 0; kt < NT; ++kt) hh[kt] = zero4();
+                for (int tt = 0; tt < NT; ++tt) {
 #pragma unroll
-                for (int gi = 0; gi < NGR; ++gi) {
-                    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                    for (int i = 0; i < GW; ++i) hh[gi / NPK] = mma(eb[gi & 1][i], wf[GW * (gi % NPK) + i], hh[gi / NPK]);
-                    __builtin_amdgcn_sched_barrier(0);
-                    if (gi + 2 < NGR) ld_e(eb[gi & 1], gi + 2);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int kt = 0; kt < NT; ++kt)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (kt > tt || (kt == tt && 4 * g + e > r)) hh[kt][e] = 0.f;
-#pragma unroll
-                for (int kb = 0; kb < GG::KBC; ++kb) {
-                    if (2 * kb <= tt) {
-                        const F hf = frag_from_acc<T>(hh[2 * kb], hh[2 * kb + 1]);
-#pragma unroll
-                        for (int d2 = 0; d2 < DH; ++d2)
-                            oa[d2] = mma(ld_frag_c<T, CC>(Vt + (size_t)(16 * (DH * hv + d2) + r) * GG::LDK, kb, g), hf,
-                                         oa[d2]);
+                    for (int kb = 0; kb < GG::KBC; ++kb) {
+                        if (2 * kb <= tt)
+                            oa[tt] = mma(ld_frag16_2x8(Vt + (size_t)(16 * w + r) * GG::LDK, kb, g),
+                                         ld_frag16_2x8(Hs + (size_t)(16 * tt + r) * P::LDP, kb, g), oa[tt]);
                     }
-                }
-                if (j < c) {
-#pragma unroll
-                    for (int d2 = 0; d2 < DH; ++d2)
-                        st4<T>(ob + (size_t)(tok0 + j) * tso + 16 * (DH * hv + d2) + 4 * g, oa[d2]);
+                    const int j = 16 * tt + r;
+                    if (j < c) st4<T>(ob + (size_t)(tok0 + j) * tso + 16 * w + 4 * g, oa[tt]);
                 }
             }
         } else if (w < NT) {
