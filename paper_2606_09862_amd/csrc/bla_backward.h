@@ -66,6 +66,8 @@ template <typename T, int D, int MP, int SP> struct Bwd : Geo<T, D, MP> {
 // Staging of NTEN token tensors of one chunk (tensor 0 = K, 1 = V, 2 = Q, 3 = dO) in units
 // of 4 tokens x 8 elements: registers first (issued a chunk ahead), then LDS, transposed
 // ([D][LDK], tokens contiguous) and, with ROW, row-major ([C][LDQ]).  Rows past c are zero.
+// Consecutive threads take consecutive 8-element pieces of the same four rows, so the global
+// reads are coalesced.
 template <typename T, int D, int NTEN> struct BStage {
     static constexpr int UPT = (kChunk / 4) * (D / 8);   // units per tensor
     static constexpr int PT = (NTEN * UPT + kThreads - 1) / kThreads;
@@ -80,7 +82,7 @@ __device__ __forceinline__ void bstage_load(BStage<T, D, NTEN>& st, const T* con
     for (int i = 0; i < S::PT; ++i) {
         const int u = tid + i * kThreads;
         if ((NTEN * S::UPT) % kThreads == 0 || u < NTEN * S::UPT) {
-            const int ten = u / S::UPT, uu = u % S::UPT, tq = uu % (kChunk / 4), dq = uu / (kChunk / 4);
+            const int ten = u / S::UPT, uu = u % S::UPT, dq = uu % (D / 8), tq = uu / (D / 8);
             const T* base = src[ten] + 8 * dq;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
@@ -103,7 +105,7 @@ __device__ __forceinline__ void bstage_store(const BStage<T, D, NTEN>& st, T* co
     for (int i = 0; i < S::PT; ++i) {
         const int u = tid + i * kThreads;
         if ((NTEN * S::UPT) % kThreads == 0 || u < NTEN * S::UPT) {
-            const int ten = u / S::UPT, uu = u % S::UPT, tq = uu % (kChunk / 4), dq = uu / (kChunk / 4);
+            const int ten = u / S::UPT, uu = u % S::UPT, dq = uu % (D / 8), tq = uu / (D / 8);
             H x[4][2];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {

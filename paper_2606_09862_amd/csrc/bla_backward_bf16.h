@@ -69,7 +69,7 @@ __device__ __forceinline__ void bstage_store_rows(const BStage<bf16, D, NTEN>& s
     for (int i = 0; i < S::PT; ++i) {
         const int u = tid + i * kThreads;
         if ((NTEN * S::UPT) % kThreads == 0 || u < NTEN * S::UPT) {
-            const int ten = u / S::UPT, uu = u % S::UPT, tq = uu % (kChunk / 4), dq = uu / (kChunk / 4);
+            const int ten = u / S::UPT, uu = u % S::UPT, dq = uu % (D / 8), tq = uu / (D / 8);
             bf16* rd = dst[ten] + 8 * dq;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
