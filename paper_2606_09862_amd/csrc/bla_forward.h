@@ -976,26 +976,28 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
 #pragma unroll
                 for (int u2 = 0; u2 < 2; ++u2) {
                     const int q = w + NW * u2;
-                    if (q < 10) {
+                    if (q < 12) {
                         int tt, kt;
-                        h_tile(q, tt, kt);
                         floatx4 hh = zero4();
-                        const T* fe = fEtab + ((size_t)kt * GG::KBM * 64 + lane) * 8;
-                        F ef[GG::KBM];
+                        if (q < 10) {
+                            h_tile(q, tt, kt);
+                            const T* fe = fEtab + ((size_t)kt * GG::KBM * 64 + lane) * 8;
+                            F ef[GG::KBM];
 #pragma unroll
-                        for (int kb = 0; kb < GG::KBM; ++kb) ef[kb] = ld_global<F>(fe + (size_t)kb * 64 * 8);
+                            for (int kb = 0; kb < GG::KBM; ++kb) ef[kb] = ld_global<F>(fe + (size_t)kb * 64 * 8);
 #pragma unroll
-                        for (int kb = 0; kb < GG::KBM; ++kb)
-                            hh = mma(ef[kb], ld_frag16_2x8(UT + (size_t)(16 * tt + r) * P::LDQU, kb, g), hh);
-                        if (kt == tt) {
+                            for (int kb = 0; kb < GG::KBM; ++kb)
+                                hh = mma(ef[kb], ld_frag16_2x8(UT + (size_t)(16 * tt + r) * P::LDQU, kb, g), hh);
+                            if (kt == tt) {
 #pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                if (4 * g + e > r) hh[e] = 0.f;
+                                for (int e = 0; e < 4; ++e)
+                                    if (4 * g + e > r) hh[e] = 0.f;
+                            }
+                        } else {
+                            tt = 2 * (q - 10);  // the zero tiles (0, 1) and (2, 3)
+                            kt = tt + 1;
                         }
                         st4<T>(Hs + (size_t)(16 * tt + r) * P::LDP + 16 * kt + 4 * g, hh);
-                    } else if (q < 12) {
-                        const int tt = 2 * (q - 10);  // tiles (0, 1) and (2, 3)
-                        st4<T>(Hs + (size_t)(16 * tt + r) * P::LDP + 16 * (tt + 1) + 4 * g, zero4());
                     }
                 }
                 // O^T tile (head dims 16w .., tokens of tile tt) = Re(W'' Z'_v) over the modes
