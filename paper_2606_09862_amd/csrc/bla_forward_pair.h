@@ -38,6 +38,18 @@
 
 namespace bla {
 
+// Lane-ordered segment summaries of the pair path: part p (Re Z_k, Im Z_k, Re Z_v, Im Z_v) of
+// mode tile mt and head-dim tile dt is one accumulator tile, stored as 64 consecutive 16-byte
+// pieces (lane l's four floats at 4 l), so that the summary kernel writes and the forward
+// prologue reads it as one contiguous 1 KB block.  Lane (g, r) holds Z_k[16mt + r][16dt + 4g
+// .. + 3] and Z_v[16dt + r][16mt + 4g .. + 3] (the two kernels' tile layouts).  The one-unit
+// plans keep the row-major [4][..] layout that their scan reads.
+template <int D, int MP>
+__host__ __device__ constexpr size_t sum_tile(int p, int mt, int dt)
+{
+    return (((size_t)p * (MP / 16) + mt) * (D / 16) + dt) * 256;
+}
+
 template <int D, int MP, int SP> struct Pair {
     static constexpr int C = kChunk, NT = C / 16, WPU = 4;
     static constexpr int NMT = MP / 16, NDT = D / 16, NST = SP / 16;
@@ -502,9 +514,14 @@ __attribute__((amdgpu_waves_per_eu(SumPair<D, MP>::MINB * SumPair<D, MP>::NW / 4
             const int dt = ds * P::NDT + wd + WD * i;
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
-                st4f(S + ((size_t)q * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[j][i][q]);
-                st4f(S + (size_t)2 * MP * D + ((size_t)q * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
-                     Zv[j][i][q]);
+                if constexpr (PLAIN_E) {  // one-unit plans: the scan's row-major layout
+                    st4f(S + ((size_t)q * MP + 16 * mt + r) * D + 16 * dt + 4 * g, Zk[j][i][q]);
+                    st4f(S + (size_t)2 * MP * D + ((size_t)q * D + 16 * dt + r) * MP + 16 * mt + 4 * g,
+                         Zv[j][i][q]);
+                } else {  // pair plans: lane order (sum_tile)
+                    st4f(S + sum_tile<D, MP>(q, mt, dt) + 4 * (tid & 63), Zk[j][i][q]);
+                    st4f(S + sum_tile<D, MP>(2 + q, mt, dt) + 4 * (tid & 63), Zv[j][i][q]);
+                }
             }
         }
     }
@@ -669,12 +686,9 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
             for (int o = 0; o < OWN; ++o) {
                 const int mt = min(wl + P::WPU * o, NMT - 1);
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    dst[o][dt][0] = ld4f(Sj + ((size_t)0 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
-                    dst[o][dt][1] = ld4f(Sj + ((size_t)1 * MP + 16 * mt + r) * D + 16 * dt + 4 * g);
-                    dst[o][dt][2] = ld4f(Sj + (size_t)2 * MP * D + ((size_t)0 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
-                    dst[o][dt][3] = ld4f(Sj + (size_t)2 * MP * D + ((size_t)1 * D + 16 * dt + r) * MP + 16 * mt + 4 * g);
-                }
+                for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                    for (int pp = 0; pp < 4; ++pp) dst[o][dt][pp] = ld4f(Sj + sum_tile<D, MP>(pp, mt, dt) + 4 * (tid & 63));
             }
         };
         auto combine = [&](const floatx4 (&src)[OWN][NDT][4]) {
