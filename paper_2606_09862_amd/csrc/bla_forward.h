@@ -137,15 +137,6 @@ template <typename T, int D, int MP, int SP, int CC = kChunk> struct Fwd : Geo<T
     static_assert(SP % 32 == 0, "slot padding");
 };
 
-// An operand fragment times a per-lane factor (bf16 in, bf16 out, float32 product).
-__device__ __forceinline__ bf16x8 scale_frag(bf16x8 x, float f)
-{
-    bf16x8 y;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) y[e] = (bf16)((float)x[e] * f);
-    return y;
-}
-
 // The wave's fp32 state tiles: [owned mode tile][Re, Im][head-dim tile].
 template <typename T, int D, int MP, int CC = kChunk> using StateTiles = floatx4[Geo<T, D, MP, CC>::OWN][2][D / 16];
 // ---------------------------------------------------------------------------------
@@ -903,13 +894,36 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
                 }
             }
             __syncthreads();  // P~ and the statistics visible; U no longer read
+            {
+                // (5) normalisation in place: wave w rescales the P~ rows of tokens 8w .. 8w + 7,
+                // eight lanes per token, each lane SP/8 consecutive slots (within one slot tile):
+                // P = P~ exp(m_tile - M) / sum_tiles exp(m_tile - M) s_tile, M the token's maximum
+                constexpr int SPL = SP / 8;  // slots per lane
+                static_assert(SPL == 8 || SPL == 16, "a lane's slots lie in one slot tile");
+                const int jn = 8 * w + (lane >> 3), s0 = SPL * (lane & 7);
+                float M = -INFINITY, mine = 0.f, tot = 0.f;
+#pragma unroll
+                for (int q = 0; q < NST; ++q) M = fmaxf(M, sStat[(jn * NST + q) * 2]);
+#pragma unroll
+                for (int q = 0; q < NST; ++q) {
+                    const float e = __expf(sStat[(jn * NST + q) * 2] - M);  // 0 for a fully masked tile
+                    tot += e * sStat[(jn * NST + q) * 2 + 1];
+                    if (q == s0 / 16) mine = e;
+                }
+                const float f = mine * __builtin_amdgcn_rcpf(tot);
+                T* prow = Pw + (size_t)jn * P::LDP + s0;
+#pragma unroll
+                for (int i = 0; i < SPL; i += 4) {
+                    const typename Frag<T>::half x = ld4_lds<T>(prow + i);
+                    st4<T>(prow + i, to_f4(x) * f);
+                }
+            }
+            __syncthreads();  // P normalised
 
             {
                 // (6)-(7) readout weights of mode tile w ([Re | Im] column tiles w, NMT + w) for
                 // every token tile; the transposed slot-matrix fragments (fragment-ordered) are
-                // loaded once and serve all four token tiles, the P~ fragments are scaled by the
-                // normalisation of their slot tile (natural order: lanes g < 2 hold slot tile 2ks,
-                // lanes g >= 2 tile 2ks + 1)
+                // loaded once and serve all four token tiles
                 F am[2][P::KBS];
 #pragma unroll
                 for (int pp = 0; pp < 2; ++pp)
@@ -919,26 +933,9 @@ __global__ __launch_bounds__((Geo<T, D, MP, CC>::NTHR)) void forward_kernel(FwdA
 #pragma unroll
                 for (int tt = 0; tt < NT; ++tt) {
                     const int j = 16 * tt + r;
-                    float mt_[NST], st_[NST];
-                    float M = -INFINITY;
-#pragma unroll
-                    for (int q = 0; q < NST; ++q) {
-                        mt_[q] = sStat[(j * NST + q) * 2 + 0];
-                        st_[q] = sStat[(j * NST + q) * 2 + 1];
-                        M = fmaxf(M, mt_[q]);
-                    }
-                    float tot = 0.f;
-#pragma unroll
-                    for (int q = 0; q < NST; ++q) {
-                        mt_[q] = __expf(mt_[q] - M);  // 0 for a fully masked tile
-                        tot += mt_[q] * st_[q];
-                    }
-                    const float inv = __builtin_amdgcn_rcpf(tot);
                     F pf[P::KBS];
 #pragma unroll
-                    for (int ks = 0; ks < P::KBS; ++ks)
-                        pf[ks] = scale_frag(ld_frag16_2x8(Pw + (size_t)j * P::LDP, ks, g),
-                                            (g < 2 ? mt_[2 * ks] : mt_[2 * ks + 1]) * inv);
+                    for (int ks = 0; ks < P::KBS; ++ks) pf[ks] = ld_frag16_2x8(Pw + (size_t)j * P::LDP, ks, g);
                     floatx4 wa[2];
 #pragma unroll
                     for (int pp = 0; pp < 2; ++pp) {
