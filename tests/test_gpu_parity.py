@@ -196,6 +196,21 @@ def test_wide_state_eight_waves(B, H, L, d, M, S, T):
     assert bla.supported(bla.make_params(B, H, L, d, M, S, torch.float32)) != 0
 
 
+@pytest.mark.parametrize("S", [128, 64])
+def test_wide_state_in_offset_segments(S):
+    """d = M = 128 (eight waves, the column-split chain and its fragment-ordered tables) with
+    input states, t0 > 0 and a ragged tail, cut into many segments: the carries from the block
+    summaries and the scan enter every segment but the first."""
+    B, H, L, d, M, T = 1, 2, 64 * 13 + 29, 128, 128, (300.0, 511.0)
+    q, k, v = gauss(31 + S, B, H, L, d, torch.bfloat16)
+    rng = np.random.default_rng(32)
+    sk = rng.standard_normal((B, H, 2, M, d)).astype(np.float32) * 0.1
+    sv = rng.standard_normal((B, H, 2, M, d)).astype(np.float32) * 0.1
+    sk[:, :, 1, 0] = 0.0
+    sv[:, :, 1, 0] = 0.0
+    run_case(q, k, v, T, M, S, torch.bfloat16, t0=777, sk=sk, sv=sv, label=f"wide continuation S={S}")
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_state_in_and_offset(dtype):
     """Continue a sequence: state_in from the oracle, t0 > 0 (start mask at absolute positions)."""

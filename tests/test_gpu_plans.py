@@ -63,6 +63,32 @@ def test_reuse_tables():
         assert torch.equal(a, b)
 
 
+def test_reuse_tables_wide():
+    """The d = M = 128 plan keeps fragment-ordered copies of its tables next to the row-major
+    ones: kept with the tables, rebuilt with them when the periods change."""
+    bla = _bla()
+    B, H, L, d, M, S = 1, 2, 64 * 5 + 11, 128, 128, 128
+    T1, T2 = (255.0, 300.0), (400.0, 260.5)
+    q, k, v = gauss(41, B, H, L, d, torch.bfloat16)
+    tq, tk, tv = (to_dev(x, torch.bfloat16) for x in (q, k, v))
+    p = bla.make_params(B, H, L, d, M, S, torch.bfloat16)
+    ws = torch.empty(bla.workspace_size(p), dtype=torch.uint8, device="cuda")
+    ref1 = bla.forward(tq, tk, tv, T1, M, S, workspace=ws)
+    again = bla.forward(tq, tk, tv, T1, M, S, workspace=ws, reuse_tables=True)
+    torch.cuda.synchronize()
+    for a, b in zip(ref1, again):
+        assert torch.equal(a, b)
+    got2 = bla.forward(tq, tk, tv, T2, M, S, workspace=ws, reuse_tables=True)
+    torch.cuda.synchronize()
+    ro, rk, rv = oracle.forward(q, k, v, T2, M, S)
+    assert_close(got2[0].float().cpu().numpy(), ro, 2e-2, "O, new periods")
+    assert_close(got2[2].cpu().numpy(), rv, 2e-2, "state_v, new periods")
+    got1 = bla.forward(tq, tk, tv, T1, M, S, workspace=ws, reuse_tables=True)
+    torch.cuda.synchronize()
+    for a, b in zip(ref1, got1):
+        assert torch.equal(a, b)
+
+
 def test_out_buffer_is_checked():
     bla = _bla()
     q, k, v = (to_dev(x, torch.bfloat16) for x in gauss(3, 1, 2, 70, 32, torch.bfloat16))
