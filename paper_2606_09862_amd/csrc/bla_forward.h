@@ -20,7 +20,10 @@
 // tiles, and the per-token chain (4-9) by token tiles, so that the chain passes
 // its intermediates in registers (see bla_device.h).  The fp32 state of the
 // wave's own mode tiles lives in registers for the whole segment; its bf16 copy
-// of Z'_v goes through LDS for (7).
+// of Z'_v goes through LDS for (7).  The bf16 d = M = 128 shape with 64 or 128 slots
+// splits (4)-(9) by output columns instead (Fwd::SPLIT: slot, mode and head-dim tiles
+// per wave, the intermediates through LDS) and reads its tables as fragment-ordered
+// copies in global memory (FragTabArgs).
 //
 // Data movement: the next chunk's Q, K, V are loaded into registers while the
 // current chunk computes, and written to LDS (Q row-major, K and V transposed)
@@ -57,7 +60,8 @@ template <typename T, int D, int MP, int CC = kChunk> struct Geo {
     // Threads per workgroup: 4 waves, or 8 for d = M = 128, where four waves would each hold
     // two mode tiles of both states (256 registers) and spill, and for 128-token chunks (one
     // token tile per wave); the token chain runs on waves 0..NT-1 and the other waves take
-    // part in the mode-tile phases only.
+    // part in the mode-tile phases only, except in the split chain (Fwd::SPLIT), where every
+    // wave takes a share of steps (4)-(9).
     static constexpr int NTHR = ((D == 128 && MP == 128) || NT > 4) ? 2 * kThreads : kThreads;
     static constexpr int NW = NTHR / 64;        // waves
     static constexpr int NMT = MP / 16;         // mode tiles
