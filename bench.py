@@ -241,6 +241,8 @@ def bench_forward(args, hip, inputs, form, cid=3):
     if decay:
         spans = {"tables_and_schedule": (0, 1), "summaries_and_scan": (1, 3), "forward": (3, 4)}
     phase_ms = {ph: float(np.mean([hip.elapsed_ms(e[a], e[b]) for e in evs])) for ph, (a, b) in spans.items()}
+    # per-call durations of the same pass (first to last event of a call): their median
+    call_ms = float(np.median([hip.elapsed_ms(e[0], e[4]) for e in evs]))
     tokens = w.B * w.L
     if decay:
         flops = decay_flops_per_token_head(w.d, w.S) * w.B * w.H * w.L
@@ -283,6 +285,7 @@ def bench_forward(args, hip, inputs, form, cid=3):
         "forward_kernel_hbm_gbs": round(nbytes / t_fwd / 1e9, 1),
         "phase_us": {k2: round(v2 * 1e3, 2) for k2, v2 in phase_ms.items()},
         "ideal_us": round(max(t_mfma, t_hbm) * 1e6, 2),
+        "median_call_us_with_events": round(call_ms * 1e3, 2),
         "kernel_sources_sha": digest,
     }
     del tq, tk, tv, o, sk, sv, ws
