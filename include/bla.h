@@ -71,7 +71,7 @@ extern "C" {
 typedef enum {
     BLA_OK = 0,
     BLA_ERR_INVALID_ARG = 1, /* a null/misaligned pointer, a negative size, a bad period */
-    BLA_ERR_UNSUPPORTED = 2, /* a valid shape this build has no kernel for            */
+    BLA_ERR_UNSUPPORTED = 2, /* a valid shape the library has no kernel for           */
     BLA_ERR_WORKSPACE = 3,   /* workspace pointer null or smaller than required       */
     BLA_ERR_HIP = 4          /* the HIP runtime reported an error while launching     */
 } bla_status;
@@ -108,7 +108,7 @@ typedef struct {
 /* Human-readable name of a status code (static string, never NULL). */
 const char* bla_status_string(bla_status s);
 
-/* BLA_OK if the shape in *p has a kernel in this build, else the error it would get. */
+/* BLA_OK if the shape in *p has a kernel in the library, else the error it would get. */
 bla_status bla_supported(const bla_params* p);
 
 /*

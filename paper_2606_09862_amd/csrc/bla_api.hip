@@ -401,7 +401,7 @@ const char* bla_status_string(bla_status s)
     switch (s) {
     case BLA_OK: return "BLA_OK";
     case BLA_ERR_INVALID_ARG: return "BLA_ERR_INVALID_ARG: invalid argument";
-    case BLA_ERR_UNSUPPORTED: return "BLA_ERR_UNSUPPORTED: shape not supported by this build";
+    case BLA_ERR_UNSUPPORTED: return "BLA_ERR_UNSUPPORTED: shape not supported by the library";
     case BLA_ERR_WORKSPACE: return "BLA_ERR_WORKSPACE: workspace missing or too small";
     case BLA_ERR_HIP: return "BLA_ERR_HIP: HIP runtime error";
     }
