@@ -188,6 +188,22 @@ __device__ __forceinline__ bf16x8 ld_frag_2x8_sw(const bf16* row, int kb, int g,
     return join(*a, *(const volatile __attribute__((address_space(3))) bf16x4*)(a + 4));
 }
 
+// Row swizzle keyed on bit 2 of the row, for a table written as 16 x 16 accumulator tiles
+// (8-byte pieces, one row per lane of a 16-lane group) and read as 16-byte row fragments.  An
+// 8-byte LDS write serves 16 lanes per cycle over 32 banks, so at a row stride of 8 (mod 32)
+// dwords the 16 rows of a tile fall on 4 bank groups (4-way conflicts); flipping bit 3 of the
+// column in rows 4-7 and 12-15 of every 16 halves that, and unlike the bit-3 swizzle it keeps
+// the 16-byte row-fragment reads of such a table conflict-free (both measured with the LDS
+// bank-conflict counter on gfx950).
+__host__ __device__ constexpr int swz4_col(int row, int col) { return col ^ (((row >> 2) & 1) << 3); }
+
+// ld_frag16 on a swz4_col table; row points at table row 16i + r.  The lane's 8-element block
+// 8g moves to 8(g ^ 1) in the rows the swizzle flips and stays one 16-byte read.
+__device__ __forceinline__ bf16x8 ld_frag16_sw4(const bf16* row, int kb, int g, int r)
+{
+    return *reinterpret_cast<const bf16x8*>(row + 32 * kb + ((8 * g) ^ (((r >> 2) & 1) << 3)));
+}
+
 // ld_frag_tr on a swizzled table (rows 32kb + 4g + r/4 and 16 below: bit 3 is bit 1 of g;
 // x0 is a multiple of 16).
 __device__ __forceinline__ bf16x8 ld_frag_tr_sw(const bf16* M, int ld, int x0, int kb, int g, int r)
