@@ -66,14 +66,15 @@ template <int D, int MP, int SP> struct Pair {
     // at this stride, and their row fragments are two separate 8-byte reads.  The published
     // state is row-swizzled as well: every wave writes its owned tiles there once per chunk
     // as 8-byte pieces (16 rows x 4 consecutive pieces per instruction), which at these
-    // strides put 4 rows on the same banks; the swizzles leave 2.  Z'_k (swz4_col) is read as
-    // 16-byte fragments (ld_frag16_sw4), Z'_v (swz_col), read against accumulator-derived
-    // fragments, as two 8-byte pieces (ld_frag_2x8_sw), both without conflicts.
+    // strides put 4 rows on the same banks; swz4_col leaves 2.  Z'_k is read as 16-byte
+    // fragments; Z'_v, read against accumulator-derived fragments, is stored fragment-ordered
+    // (frag_col) under the same swizzle, so its fragments are 16-byte reads as well
+    // (ld_frag16_sw4 for both, without conflicts).
     static constexpr int LAB = 2 * MP + 16;  // [A|B]:     [SP][LAB]
     static constexpr int LE = 2 * MP + 16;   // phase tab: [C][LE]
     static constexpr int LK = D + 16;        // K, V:      [C][LK]
     static constexpr int LZK = D + 16;       // Z'_k:      [2MP][LZK]  (Re rows, then Im rows)
-    static constexpr int LZ = 2 * MP + 16;   // Z'_v:      [D][LZ]     (Re | Im along the row)
+    static constexpr int LZ = 2 * MP + 16;   // Z'_v:      [D][LZ]     (Re | Im along the row, fragment-ordered)
     // per unit, after Z'_v: the anchored twiddle row [cos | sin](m w P) of the chunk, [2MP]
     // (the queries do not pass through LDS: each lane loads its own token's fragments)
     static constexpr size_t AB_ELEMS = (size_t)SP * LAB;
@@ -168,7 +169,7 @@ __device__ __forceinline__ void pair_copy(bf16* dst, const bf16* src, int tid)
 
 // Publish the owned mode tiles of the state as bf16 operands: Z'_k as [2MP][LZK] rows
 // (mode m, head-dim along the row, swz4_col) and Z'_v as [D][LZ] rows (head-dim d, modes along
-// the row, swz_col).
+// the row, fragment-ordered and swz4_col).
 template <int D, int MP, int SP>
 __device__ __forceinline__ void pair_write_zk(bf16* ZkT, const PState<D, MP, SP>& Zk, int wl, int g, int r)
 {
@@ -196,8 +197,8 @@ __device__ __forceinline__ void pair_write_zv(bf16* ZvT, const PState<D, MP, SP>
         if (mt < P::NMT) {
 #pragma unroll
             for (int dt = 0; dt < P::NDT; ++dt) {
-                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + swz_col(r, 16 * mt + 4 * g), Zv[o][0][dt]);
-                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + swz_col(r, MP + 16 * mt + 4 * g), Zv[o][1][dt]);
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + swz4_col(r, frag_col(16 * mt + 4 * g)), Zv[o][0][dt]);
+                st4<bf16>(ZvT + (size_t)(16 * dt + r) * P::LZ + swz4_col(r, frag_col(MP + 16 * mt + 4 * g)), Zv[o][1][dt]);
             }
         }
     }
@@ -903,7 +904,7 @@ __global__ __launch_bounds__((256 * Pair<D, MP, SP>::U)) void forward_pair_kerne
                 oa[dt] = zero4();
 #pragma unroll
                 for (int kb = 0; kb < P::KBM; ++kb)
-                    oa[dt] = mma(ld_frag_2x8_sw(ZvT + (size_t)(16 * dt + r) * P::LZ, kb, g, r), wf[kb], oa[dt]);
+                    oa[dt] = mma(ld_frag16_sw4(ZvT + (size_t)(16 * dt + r) * P::LZ, kb, g, r), wf[kb], oa[dt]);
             }
             floatx4 hh[NT];
 #pragma unroll
