@@ -33,10 +33,28 @@ template <int D, int MP, int SP> struct Bwd16 {
     static constexpr int LDU = 2 * MP + 4;            // U, Y [C][LDU]
     static constexpr int LE = 2 * MP + 12;            // phase table [C][LE]; slot matrix [SP][LE]
     // Tiles written row-major by the wave that produces them (8-byte stores) and read
-    // transposed (ds_read_b64_tr_b16):
-    static constexpr int LDH = C + 4;                 // H tiles [query][key]
-    static constexpr int LDW = 2 * MP + 4;            // readout weights [token][Re m | Im m]
-    static constexpr int LDZ = D + 4;                 // Z'_k [Re m | Im m][d]
+    // transposed (ds_read_b64_tr_b16).  Where the LDS allows it without costing a workgroup
+    // per compute unit (PS), they are piece-swizzled (pswz_col) at row strides of 8 x odd
+    // (mod 64) dwords, so that neither the stores nor the transposed reads meet bank conflicts;
+    // otherwise a stride of 2 (mod 32) dwords keeps the stores conflict-free.
+    static constexpr size_t lds_bytes(int tp)
+    {
+        const int ldh = C + tp, ldw = 2 * MP + tp, ldz = D + tp;
+        return ((size_t)4 * C * LDQ + (size_t)2 * C * (ldh > LDK ? ldh : LDK) +
+                (size_t)2 * C * (ldw > LDU ? ldw : LDU) + (size_t)2 * MP * ldz + (size_t)C * LE + (size_t)SP * LE) * 2 +
+               (size_t)SP * 4 + (size_t)2 * 2 * MP * 4;
+    }
+    static constexpr bool PS =
+        lds_bytes(16) <= kBwdMaxLds && (2 * lds_bytes(16) <= kBwdMaxLds || 2 * lds_bytes(4) > kBwdMaxLds);
+    static constexpr int TP = PS ? 16 : 4;
+    static constexpr int LDH = C + TP;                // H tiles [query][key]
+    static constexpr int LDW = 2 * MP + TP;           // readout weights [token][Re m | Im m]
+    static constexpr int LDZ = D + TP;                // Z'_k [Re m | Im m][d]
+    __device__ static int tcol(int row, int col) { return PS ? pswz_col(row, col) : col; }
+    __device__ static bf16x8 ld_t(const bf16* M, int ld, int x0, int kb, int g, int r)
+    {
+        return PS ? ld_frag_tr_ps(M, ld, x0, kb, g, r) : ld_frag_tr(M, ld, x0, kb, g, r);
+    }
     static constexpr size_t A_ELEMS = (size_t)4 * C * LDQ;
     static constexpr size_t G_ELEMS = (size_t)2 * C * (LDH > LDK ? LDH : LDK);
     static constexpr size_t B_ELEMS = (size_t)2 * C * (LDW > LDU ? LDW : LDU);
@@ -456,7 +474,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
                         for (int p = 0; p < 2; ++p)
-                            st_lds<bf16x4>(ZkT + (size_t)(p * MP + 16 * mt + r) * P::LDZ + 16 * dt + 4 * g,
+                            st_lds<bf16x4>(ZkT + (size_t)(p * MP + 16 * mt + r) * P::LDZ + P::tcol(p * MP + 16 * mt + r, 16 * dt + 4 * g),
                                            cvt4(Zk[o][p][dt], bf16()));
                 }
             }
@@ -628,8 +646,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     const floatx4 am = wa[mt], bm = wa[NMT + mt];
                     wa[mt] = am * cs - bm * ns;
                     wa[NMT + mt] = am * ns + bm * cs;
-                    st_lds<bf16x4>(WvT + (size_t)j * P::LDW + 16 * mt + 4 * g, cvt4(wa[mt], bf16()));
-                    st_lds<bf16x4>(WvT + (size_t)j * P::LDW + MP + 16 * mt + 4 * g, cvt4(wa[NMT + mt], bf16()));
+                    st_lds<bf16x4>(WvT + (size_t)j * P::LDW + P::tcol(j, 16 * mt + 4 * g), cvt4(wa[mt], bf16()));
+                    st_lds<bf16x4>(WvT + (size_t)j * P::LDW + P::tcol(j, MP + 16 * mt + 4 * g), cvt4(wa[NMT + mt], bf16()));
                 }
                 if constexpr (!SUM) {
                     F wf[KBM];
@@ -648,7 +666,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                                     if (4 * g + e > r) hv[e] = 0.f;
                             }
                         }
-                        st_lds<bf16x4>(HvT + (size_t)j * P::LDH + 16 * kt + 4 * g, cvt4(hv, bf16()));
+                        st_lds<bf16x4>(HvT + (size_t)j * P::LDH + P::tcol(j, 16 * kt + 4 * g), cvt4(hv, bf16()));
                     }
                 }
             }
@@ -668,8 +686,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     const floatx4 am = wq[mt], bm = wq[NMT + mt];
                     wq[mt] = am * cs - bm * ns;
                     wq[NMT + mt] = am * ns + bm * cs;
-                    st_lds<bf16x4>(WqT + (size_t)j * P::LDW + 16 * mt + 4 * g, cvt4(wq[mt], bf16()));
-                    st_lds<bf16x4>(WqT + (size_t)j * P::LDW + MP + 16 * mt + 4 * g, cvt4(wq[NMT + mt], bf16()));
+                    st_lds<bf16x4>(WqT + (size_t)j * P::LDW + P::tcol(j, 16 * mt + 4 * g), cvt4(wq[mt], bf16()));
+                    st_lds<bf16x4>(WqT + (size_t)j * P::LDW + P::tcol(j, MP + 16 * mt + 4 * g), cvt4(wq[NMT + mt], bf16()));
                 }
                 if constexpr (!SUM) {
                     F qf2[KBM];
@@ -681,7 +699,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                         oa[dt] = zero4();
 #pragma unroll
                         for (int kb = 0; kb < KBM; ++kb)
-                            oa[dt] = mma(ld_frag_tr(ZkT, P::LDZ, 16 * dt, kb, g, r), qf2[kb], oa[dt]);
+                            oa[dt] = mma(P::ld_t(ZkT, P::LDZ, 16 * dt, kb, g, r), qf2[kb], oa[dt]);
                     }
                     floatx4 hq[NT];
 #pragma unroll
@@ -697,7 +715,7 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                                     if (4 * g + e > r) hq[kt][e] = 0.f;
                             }
                         }
-                        st_lds<bf16x4>(HqT + (size_t)j * P::LDH + 16 * kt + 4 * g, cvt4(hq[kt], bf16()));
+                        st_lds<bf16x4>(HqT + (size_t)j * P::LDH + P::tcol(j, 16 * kt + 4 * g), cvt4(hq[kt], bf16()));
                     }
 #pragma unroll
                     for (int kb = 0; kb < KBC; ++kb) {
@@ -757,8 +775,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                     floatx4 ka = zero4(), va = zero4();
 #pragma unroll
                     for (int kb = 0; kb < KBC; ++kb) {
-                        ka = mma(qtf[kb], ld_frag_tr(HqT, P::LDH, 16 * kt, kb, g, r), ka);
-                        va = mma(otf[kb], ld_frag_tr(HvT, P::LDH, 16 * kt, kb, g, r), va);
+                        ka = mma(qtf[kb], P::ld_t(HqT, P::LDH, 16 * kt, kb, g, r), ka);
+                        va = mma(otf[kb], P::ld_t(HvT, P::LDH, 16 * kt, kb, g, r), va);
                     }
 #pragma unroll
                     for (int kb = 0; kb < KBM; ++kb) {
@@ -782,8 +800,8 @@ __global__ __launch_bounds__(kThreads) void bwd16_kernel(BwdArgs a)
                 for (int p = 0; p < 2; ++p)
 #pragma unroll
                     for (int mt = 0; mt < NMT; ++mt) {
-                        Gk[od][p][mt] = mma(ld_frag_tr(WqT, P::LDW, p * MP + 16 * mt, kb, g, r), qtf, Gk[od][p][mt]);
-                        Gv[od][p][mt] = mma(ld_frag_tr(WvT, P::LDW, p * MP + 16 * mt, kb, g, r), otf, Gv[od][p][mt]);
+                        Gk[od][p][mt] = mma(P::ld_t(WqT, P::LDW, p * MP + 16 * mt, kb, g, r), qtf, Gk[od][p][mt]);
+                        Gv[od][p][mt] = mma(P::ld_t(WvT, P::LDW, p * MP + 16 * mt, kb, g, r), otf, Gv[od][p][mt]);
                     }
             }
         }

@@ -212,6 +212,22 @@ __device__ __forceinline__ bf16x8 ld_frag_tr_sw(const bf16* M, int ld, int x0, i
     return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
 }
 
+// Piece swizzle for tiles written as 16 x 16 accumulator tiles with 8-byte stores (one row per
+// lane of a 16-lane group, 16 lanes per store cycle over 32 banks) and read only transposed
+// (ld_tr: 8 rows of 32 bytes per half wave).  At a row stride of 8 x odd (mod 64) dwords the
+// transposed reads are conflict-free, but the 16 rows of a store fall on 4 bank groups;
+// XOR-ing the 4-element piece index inside each 16-column group with bits 2-3 of the row
+// spreads them over all 32 banks, while each row keeps its 4 pieces in the same 32 bytes.
+__host__ __device__ constexpr int pswz_col(int row, int col) { return col ^ (((row >> 2) & 3) << 2); }
+
+// ld_frag_tr on a pswz_col table (x0 a multiple of 16): the rows 32kb + 4g + r/4 and 16 below
+// have bits 2-3 equal to g.
+__device__ __forceinline__ bf16x8 ld_frag_tr_ps(const bf16* M, int ld, int x0, int kb, int g, int r)
+{
+    const bf16* p = M + (size_t)(32 * kb + 4 * g + (r >> 2)) * ld + x0 + 4 * ((r & 3) ^ g);
+    return join(ld_tr(p), ld_tr(p + (size_t)16 * ld));
+}
+
 // ld_frag_tr on a tile whose columns are fragment-ordered (4-column groups stay contiguous,
 // so each lane's 4 consecutive elements are still one 8-byte read).
 __device__ __forceinline__ bf16x8 ld_frag_tr_fo(const bf16* M, int ld, int x0, int kb, int g, int r)
