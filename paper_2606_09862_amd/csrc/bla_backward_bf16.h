@@ -141,7 +141,10 @@ template <int D, int MP>
 __global__ __launch_bounds__(kThreads) void bwd16_fsum_kernel(BwdArgs a)
 {
     using G = Bwd16<D, MP, 32>;
-    constexpr int C = kChunk, NMT = G::NMT, NDT = G::NDT, OWN = G::OWN, NW = G::NW, LDQ = G::LDQ, LE = G::LE;
+    constexpr int C = kChunk, NMT = G::NMT, NDT = G::NDT, OWN = G::OWN, NW = G::NW;
+    // K, V and the phase table are read only transposed here: row strides of 8 x odd (mod 64)
+    // dwords keep those reads free of bank conflicts
+    constexpr int LDQ = D + 16, LE = 2 * MP + 16;
     __shared__ __attribute__((aligned(16))) bf16 lds[2 * C * LDQ + C * LE];
     __shared__ __attribute__((aligned(16))) float sRhoC[2 * 2 * MP];
     bf16* Ks = lds;
